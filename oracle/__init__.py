@@ -1,0 +1,27 @@
+"""CPU oracle for the streamFFN routed-expert path.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import anything from this package.  The
+HIP library never calls it, and it shares no code with the library: no
+kernels, headers, helpers, tables or pre/post-processing.  Its inputs come
+from the seeded workload generator (which holds none of the method's
+arithmetic) or from the tests themselves.
+
+Modules (each function cites the passage of the paper it follows):
+
+* ``fp8``     -- OCP e4m3fn decode/encode written from the format definition,
+                 plus 1x128 activation block quantisation.
+* ``routing`` -- per-batch expert histogram, exclusive scan, tile-aligned
+                 offsets, stable permutation and inverse map (Appendix C,
+                 "Grouped FFN invocations").
+* ``policy``  -- streamFFN batch composition: launch threshold theta and the
+                 final flush (Section 3.2, "Launch threshold"), plus the
+                 synchronous (wait-for-all) and per-chunk baselines (Section
+                 4.3, ablation).
+* ``ffn``     -- the routed-expert output: expert FFN = GEMM, activation,
+                 GEMM (Appendix C), each routed contribution weighted by its
+                 routing coefficient exactly once and summed at the source
+                 token (Appendix C, "Output return and combine").  float64.
+
+Precision readings (the paper fixes none of them) are stated per function.
+"""
