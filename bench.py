@@ -1,0 +1,176 @@
+"""Benchmark of the streamFFN routed-expert path on one MI355X.
+
+Workload (the synchronous-EP shape): d_model 4096, expert d_ff 2048, 8 local
+experts, 4 replicas x 2048 tokens routed top-8 over 64 experts uniformly, one
+chunk per replica, all arriving together, bf16 weights and tokens.  One step
+is one layer through the whole path: open the layer, submit every chunk (the
+launch policy forms the batch), histogram/scan/permute, grouped GEMM1 with
+SwiGLU, grouped GEMM2, combine, layer barrier.  Inputs are resident in HBM
+before the timed region.
+
+value = routed-expert FFN TFLOP/s = 6 * d_model * d_ff * (local pairs) per
+step / time per step.  The JSON line also carries the roofline of the
+dominant kernel (grouped GEMM1, timed with HIP events on its own stream) and
+the CPU oracle's throughput on a bounded sample.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+       [--workload NAME] [--policy wait_all|per_chunk|threshold --theta N --streams S]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "routed-expert FFN TFLOP/s (% MFMA peak) + time-to-last-chunk-done, 1 GPU"
+PEAK = {"bf16": 2500.0, "fp8": 5000.0}   # dense MFMA TFLOP/s, MI355X
+HBM_PEAK_GBS = 8000.0
+# measured HBM traffic of the dominant kernel (rocprofv3 FETCH_SIZE /
+# WRITE_SIZE, scaled by a plain-copy calibration), bytes per launch, keyed by
+# workload; None until counters for the current kernel are taken
+TRAFFIC_BYTES = {}
+
+POLICIES = {"wait_all": 0, "per_chunk": 1, "threshold": 2}
+
+
+def describe(cfg, name):
+    return (f"{name}: d_model={cfg['d']}, d_ff={cfg['I']}, {cfg['E']} local experts of "
+            f"{cfg['Eg']}, top-{cfg['k']} {'uniform' if cfg['zipf'] is None else 'Zipf(%s)' % cfg['zipf']}, "
+            f"{cfg['R']} replicas x {cfg['T']} tokens, {cfg['R'] * cfg['cpr']} chunks, "
+            f"{cfg['w']} weights")
+
+
+def cpu_baseline(wl, budget_s=12.0):
+    """The CPU oracle as it stands, on a bounded sample of the same workload's
+    delivered tokens; returns TFLOP/s over the pairs it computed."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    from oracle import ffn
+    import torch
+
+    c = wl.cfg
+
+    def bits(t):
+        return None if t is None else (t.view(torch.int16).numpy().view(np.uint16)
+                                       if t.dtype == torch.bfloat16 else t.numpy())
+    kind = {"f32": "f32", "bf16": "bf16", "fp8_e4m3_b128": "fp8"}[c["w"]]
+    bank = ffn.ExpertBank(kind, bits(wl.w_gate), bits(wl.w_up), bits(wl.w_down),
+                          bits(wl.s_gate), bits(wl.s_up), bits(wl.s_down))
+    h_mode = {"f32": None, "bf16": "bf16", "fp8": "fp8"}[kind]
+    x_mode = "fp8" if kind == "fp8" else None
+    deliv = np.argwhere(wl.delivered)
+    rng = np.random.default_rng(0)
+    deliv = deliv[rng.permutation(len(deliv))]
+    for e in range(c["E"]):      # decode weights outside the timed sample
+        bank(e)
+    done_pairs, t_total, n_tok, step = 0, 0.0, 0, 64
+    while t_total < budget_s and n_tok < len(deliv):
+        sel = deliv[n_tok:n_tok + step]
+        xb = bits(wl.x)[sel[:, 0], sel[:, 1]]
+        ids = wl.topk_local[sel[:, 0], sel[:, 1]]
+        w = wl.topk_w[sel[:, 0], sel[:, 1]]
+        t0 = time.perf_counter()
+        x = ffn.decode_rows(xb, "bf16" if c["x"] == "bf16" else "f32")
+        ffn.routed_output(x, ids, w, bank, c["E"], h_mode=h_mode, x_mode=x_mode)
+        t_total += time.perf_counter() - t0
+        done_pairs += int((ids >= 0).sum())
+        n_tok += len(sel)
+        step = min(step * 2, 1024)
+    flops = 6.0 * c["d"] * c["I"] * done_pairs
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": flops / t_total / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{n_tok} delivered tokens ({done_pairs} pairs) of the same workload, "
+                      f"float64 numpy, {t_total:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="sync_d4096")
+    ap.add_argument("--policy", default="wait_all", choices=list(POLICIES))
+    ap.add_argument("--theta", type=int, default=1)
+    ap.add_argument("--streams", type=int, default=1)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build has no multi-GPU path "
+              f"(--gpus {args.gpus} requested)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_33252_amd import cep, harness, workload as W
+
+    if not os.path.exists(cep.LIB_PATH):
+        from paper_2609_33252_amd import build
+        build.build()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+
+    wl = W.generate(args.workload, 0)
+    c = wl.cfg
+    run = harness.Runner(wl, n_streams=max(1, args.streams))
+    pol = POLICIES[args.policy]
+    flops_step = 6.0 * c["d"] * c["I"] * run.n_pairs
+    dtype = "fp8" if c["w"] == W.FP8 else "bf16"
+
+    def step():
+        run.run(policy=pol, theta=args.theta, n_streams=args.streams)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    cep.cep_get_status(run.ctx)
+    ms_step = elapsed / args.steps * 1e3
+    value = flops_step / (elapsed / args.steps) / 1e12
+
+    # kernel phases of each step, from HIP events on the batch stream
+    ph = {"route_ms": [], "gemm1_ms": [], "gemm2_ms": [], "combine_ms": [], "last_done_ms": []}
+    for _ in range(args.steps):
+        step()
+        st = run.stats()
+        for key in ("route_ms", "gemm1_ms", "gemm2_ms", "combine_ms"):
+            ph[key].append(sum(b[key] for b in st["batches"]))
+        ph["last_done_ms"].append(max(b["end_ms"] for b in st["batches"]))
+    avg = {k: sum(v) / len(v) for k, v in ph.items()}
+    n_launch = len(st["batches"])
+    g1_flops = 4.0 * c["d"] * c["I"] * run.n_pairs / n_launch
+    g1_ms = avg["gemm1_ms"] / n_launch
+    achieved = g1_flops / (g1_ms * 1e-3) / 1e12
+    traffic = TRAFFIC_BYTES.get(args.workload)
+    roofline = {"bound": "mfma", "kernel": "k_gemm_%s<SwiGLU> (grouped gate/up GEMM)" % dtype,
+                "achieved": round(achieved, 2), "peak": PEAK[dtype], "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK[dtype], 4), "traffic": traffic,
+                "launch_ms": round(g1_ms, 4), "flop_per_launch": g1_flops}
+    line = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
+        "data": "synthetic",
+        "config": {"workload": describe(c, args.workload), "local_pairs": run.n_pairs,
+                   "policy": args.policy, "theta": args.theta, "streams": args.streams,
+                   "global_batch": c["R"] * c["T"], "seq_len": c["T"], "parallelism": "ep_share_1gpu"},
+        "pct_mfma_peak": round(100 * value / PEAK[dtype], 2),
+        "time_to_last_chunk_done_ms": round(avg["last_done_ms"], 4),
+        "phases_ms": {k: round(v, 4) for k, v in avg.items() if k != "last_done_ms"},
+        "roofline": roofline,
+    }
+    run.close()
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

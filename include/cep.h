@@ -1,0 +1,223 @@
+/*
+ * cep.h -- C ABI of libcep, the per-GPU streamFFN routed-expert path of
+ * CascadeEP ("Asynchronous Expert Execution for MoE Prefill under Attention
+ * Imbalance") for AMD Instinct MI355X (gfx950).
+ *
+ * One GPU holds E local experts (its expert-parallel share).  Routed token
+ * chunks arrive from R attention replicas at different times (Section 3.2,
+ * "Asynchronous EP and streaming FFN"; Appendix C, "Asynchronous dispatch").
+ * The library batches ready chunks under a launch policy (Section 3.2,
+ * "Launch threshold"), and runs every batch as one grouped FFN invocation
+ * on one of several HIP streams (Section 3.2, "Multi-stream execution"):
+ *
+ *   1. histogram of local expert ids over the batch's valid (token, slot) pairs
+ *   2. exclusive scan -> per-expert row offsets, aligned to the GEMM M tile
+ *   3. stable permute/pack of token rows into expert-contiguous order, with an
+ *      inverse map (FP8: activations quantised per 1x128 block on the way)
+ *   4. grouped gate/up GEMM with fused SwiGLU (FP8: h re-quantised per 1x128)
+ *   5. grouped down GEMM, scaled by the routing coefficient
+ *   6. combine: each source token's local contributions summed in slot order
+ *      and written to its (replica, token) row of the output
+ *   (steps 1-6: Appendix C, "Grouped FFN invocations" and "Output return and
+ *   combine").
+ *
+ * The single-GPU part of opportunistic expert weight fetching (Section 3.3;
+ * Appendix C, "One-shot weight fetching") is a side-stream device-to-device
+ * copy of whole expert weight blobs into a preallocated buffer; the work of
+ * fetched experts runs as a separate grouped invocation on a helper stream
+ * gated by the copy.
+ *
+ * Conventions for every entry point:
+ *   - Return value: CEP_OK or a negative cep_status.  Nothing aborts or
+ *     throws across the ABI.  cep_last_error() gives a message for the last
+ *     failure on a context (HIP failures carry hipGetErrorString text).
+ *   - "device" pointers are HIP device memory on the context's device;
+ *     "host" pointers are ordinary host memory.  Dense arrays are row-major.
+ *   - A context is used by one host thread at a time.
+ *   - Work is enqueued asynchronously; only cep_destroy, cep_get_stats,
+ *     cep_get_batch_routing and cep_get_status wait for the GPU.
+ */
+#ifndef CEP_H
+#define CEP_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct cep_ctx cep_ctx; /* opaque, library-owned */
+
+enum cep_status {
+  CEP_OK = 0,
+  CEP_EINVAL = -1, /* bad argument: shape, id, pointer, dtype, unknown batch */
+  CEP_ENOMEM = -2, /* allocation failed, or a size exceeds a configured capacity */
+  CEP_EHIP = -3,   /* a HIP runtime call failed (message in cep_last_error) */
+  CEP_ESTATE = -4, /* call not valid in the current layer state / generation */
+  CEP_EBUSY = -5   /* the one weight fetch of this layer was already issued */
+};
+
+enum cep_dtype {
+  CEP_F32 = 0,          /* float32 (converted to bf16 inside the library)     */
+  CEP_BF16 = 1,         /* bfloat16                                            */
+  CEP_FP8_E4M3_B128 = 2 /* weights only: OCP e4m3fn codes, one float32 scale
+                           per 128x128 block                                   */
+};
+
+enum cep_policy {
+  CEP_WAIT_ALL = 0,  /* synchronous EP: one batch after every expected chunk  */
+  CEP_PER_CHUNK = 1, /* asynchronous EP without threshold: one batch per chunk */
+  CEP_THRESHOLD = 2  /* streamFFN: launch when pending pairs >= threshold      */
+};
+
+typedef struct {
+  int d_model;                /* hidden size d, multiple of 128               */
+  int d_ff;                   /* expert intermediate size I, multiple of 128  */
+  int n_local_experts;        /* E, 1..64                                     */
+  int top_k;                  /* k routing slots per token, 1..16             */
+  int max_replicas;           /* R_max                                        */
+  int max_tokens_per_replica; /* T_max; also the row stride of `out` per replica */
+  int w_dtype;                /* cep_dtype of the expert weights              */
+  int x_dtype;                /* cep_dtype of the token rows (F32 or BF16)    */
+  int n_streams;              /* stream slots for batches, 1..8               */
+  int max_pairs_per_batch;    /* capacity of one batch in valid pairs; 0 means
+                                 max_replicas * max_tokens_per_replica * top_k */
+  size_t fetch_buffer_bytes;  /* capacity of the temporary weight buffer      */
+  int record_routing;         /* nonzero: keep every batch's routing metadata
+                                 for cep_get_batch_routing (test/debug aid)   */
+} cep_config;
+
+/* Expert weights in math orientation (y = x W), device memory:
+ *   w_gate, w_up : [E][d][I]     w_down : [E][I][d]   (element type w_dtype)
+ *   FP8 only, float32 block scales (value = code * scale of its block):
+ *   s_gate, s_up : [E][d/128][I/128]   s_down : [E][I/128][d/128]            */
+typedef struct {
+  const void *w_gate, *w_up, *w_down;
+  const float *s_gate, *s_up, *s_down;
+} cep_weights;
+
+/* Bytes of one expert's packed weight blob (the library's device layout of
+ * gate/up, down and scales).  0 if cfg is invalid.  The unit of a weight
+ * fetch (Appendix C, "One-shot weight fetching": experts are copied whole). */
+size_t cep_packed_expert_bytes(const cep_config *cfg);
+
+/* Pack experts [first, first+n) of w into dst (device, n blobs back to back,
+ * n * cep_packed_expert_bytes bytes, caller-owned).  Builds the weight region
+ * a donor GPU would hold.  Enqueued on stream s; w must stay valid until then. */
+int cep_pack_experts(const cep_config *cfg, const cep_weights *w, int first, int n,
+                     void *dst, hipStream_t s);
+
+/* Create a context: validates cfg, allocates every scratch buffer, the chunk
+ * arena and the fetch buffer, creates the streams, and packs the weights of
+ * resident experts into library-owned memory.  resident: host [E] flags,
+ * NULL = all resident; an expert with flag 0 has no local weights and its
+ * work can only run after cep_weight_fetch brings them (w is not read for
+ * it).  Synchronises s before returning, so the caller may free w after. */
+int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_weights *w,
+                     const uint8_t *resident, hipStream_t s);
+
+/* Launch policy (Section 3.2; baselines of Section 4.3).  threshold_pairs is
+ * theta in valid local (token, slot) pairs, used by CEP_THRESHOLD (>= 1).
+ * n_streams in 1..cfg.n_streams.  Only between layers (CEP_ESTATE otherwise). */
+int cep_set_policy(cep_ctx *ctx, int policy, int threshold_pairs, int n_streams);
+
+/* Open layer `generation`.  n_replicas <= R_max; chunks_per_replica: host
+ * [n_replicas], the number of chunks each replica will submit (the final
+ * flush fires after the last of them).  out: device float32
+ * [n_replicas][T_max][d]; the combine step writes the rows of delivered
+ * tokens, other rows are left untouched (pass zeroed memory for y = 0 there).
+ * `out` must stay valid until cep_combine's event completes.  The previous
+ * layer must have been combined (CEP_ESTATE otherwise). */
+int cep_begin_layer(cep_ctx *ctx, uint32_t generation, int n_replicas,
+                    const int *chunks_per_replica, float *out);
+
+/* Submit one chunk of replica `replica`'s routed tokens (a dispatch lane
+ * becoming ready, Appendix C).  Device arrays, borrowed until the batch that
+ * contains the chunk has finished (cep_combine's event covers all):
+ *   token_idx [n_rows] int32 token slot in [0, T_max), each (replica, token)
+ *             at most once per layer
+ *   x         [n_rows][d] rows (x_dtype)
+ *   topk_id   [n_rows][k] int32 local expert id in [0, E) or -1 (remote slot)
+ *   topk_w    [n_rows][k] float32 routing coefficients
+ * n_pairs: host-known count of valid (id >= 0) entries.  arrival: event after
+ * which the data is valid (NULL: valid now).  May launch batches per policy;
+ * never blocks.  chunk_id (optional) receives the chunk's sequence number.
+ * Errors: CEP_ESTATE for a wrong generation or a closed layer, CEP_EINVAL
+ * for bad sizes, CEP_ENOMEM if the layer's rows exceed the arena
+ * (R_max * T_max rows) or n_pairs exceeds max_pairs_per_batch.  Ids outside
+ * [-1, E) or a wrong n_pairs are detected on the device and reported by
+ * cep_get_status. */
+int cep_submit_chunk(cep_ctx *ctx, uint32_t generation, int replica, int n_rows, int n_pairs,
+                     const int32_t *token_idx, const void *x, const int32_t *topk_id,
+                     const float *topk_w, hipEvent_t arrival, int64_t *chunk_id);
+
+/* Launch everything pending now (explicit final flush, Section 3.2).
+ * No-op when nothing is pending. */
+int cep_flush(cep_ctx *ctx);
+
+/* One-shot weight fetch (Section 3.3, Algorithm 1's AsyncFetch; Appendix C,
+ * "One-shot weight fetching").  Copies the packed blobs src_blobs[i] (device
+ * pointers, each cep_packed_expert_bytes, e.g. from cep_pack_experts) of local
+ * experts ids[i] into the context's fetch buffer on stream `side` and returns
+ * a library-owned event `ready` that completes with the copy.  Grouped FFN
+ * work of these experts in later batches of this layer runs on a helper
+ * stream that waits for `ready`; other experts are not delayed.  One fetch
+ * per layer: a second call returns CEP_EBUSY.  Total bytes above
+ * fetch_buffer_bytes: CEP_ENOMEM and nothing is copied.  Duplicate or
+ * out-of-range ids: CEP_EINVAL.  Batches launched before the fetch use the
+ * resident weights.  src_blobs must stay valid until `ready` completes. */
+int cep_weight_fetch(cep_ctx *ctx, const int *ids, int n, const void *const *src_blobs,
+                     hipStream_t side, hipEvent_t *ready);
+
+/* Layer barrier (Appendix C, "Output return and combine": the next layer is
+ * admitted only after all outputs are in).  Flushes pending chunks, makes
+ * stream s wait for every batch of the layer, and returns a library-owned
+ * event `done` (may be NULL) recorded on s after which `out` is final.
+ * Closes the layer.  CEP_ESTATE if the layer is not open or chunks are still
+ * expected (call cep_flush first to end a layer early). */
+int cep_combine(cep_ctx *ctx, hipStream_t s, hipEvent_t *done);
+
+/* Routing metadata of batch `batch` of the last layer (requires
+ * cfg.record_routing; waits for that batch).  Host outputs, any may be NULL:
+ *   align [1]: M-tile alignment A;  n_pairs [1]; n_rows [1]
+ *   cnt [E]; off [E+1] unpadded; off_pad [E+1] A-aligned
+ *   perm_src [n_pairs]: flat pair index (row_in_batch * k + slot) of each
+ *            unpadded grouped row, expert-major, stable
+ *   pos_of   [n_rows * k]: padded grouped row of each flat pair, -1 if remote
+ *   chunks   [n_chunks_max]: chunk sequence numbers in the batch (n_chunks [1])
+ * Sizes: call with NULL arrays first to read n_pairs / n_rows / n_chunks. */
+int cep_get_batch_routing(cep_ctx *ctx, int batch, int *align, int *n_pairs, int *n_rows,
+                          int32_t *cnt, int32_t *off, int32_t *off_pad, int32_t *perm_src,
+                          int32_t *pos_of, int64_t *chunks, int *n_chunks);
+
+/* Number of batches launched in the current (or last) layer. */
+int cep_get_batch_count(const cep_ctx *ctx);
+
+/* Waits for the layer's work and writes a JSON object to buf (host, cap
+ * bytes, NUL-terminated; CEP_ENOMEM if too small): per batch its chunks,
+ * rows, pairs, stream slot, start/end in ms from the layer's origin
+ * (cep_begin_layer) and the durations of its routing, GEMM1, GEMM2 and
+ * combine phases (HIP events on the batch stream between the launches); per
+ * chunk its arrival (when a timing event was given, else -1) in the same
+ * clock; and the fetch interval. */
+int cep_get_stats(cep_ctx *ctx, char *buf, size_t cap);
+
+/* Waits for all work and reads the device-side error word: CEP_OK, or
+ * CEP_EINVAL if a submitted chunk had an id outside [-1, E) or a pair count
+ * different from its n_pairs (message in cep_last_error).  Clears it. */
+int cep_get_status(cep_ctx *ctx);
+
+/* Message for the last failure on ctx ("" if none).  With ctx NULL: the last
+ * failure, on the calling thread, of a call that had no context to hold it
+ * (cep_init_experts, cep_pack_experts). */
+const char *cep_last_error(const cep_ctx *ctx);
+
+/* Wait for all work, release every resource.  NULL is a no-op. */
+int cep_destroy(cep_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CEP_H */

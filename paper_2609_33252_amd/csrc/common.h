@@ -1,0 +1,133 @@
+// Internal declarations shared by libcep's kernels and its runtime.
+// Not part of the public ABI (include/cep.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#define CEP_API extern "C" __attribute__((visibility("default")))
+
+namespace cep {
+
+constexpr int kMaxExperts = 64;
+constexpr int kMaxTopK = 16;
+constexpr int kAlign = 128;          // M tile = per-expert row alignment A
+constexpr int kRouteThreads = 256;   // threads per routing block
+constexpr int kRoutePairs = 2048;    // flat pairs per routing block (8 rounds of 256)
+constexpr int kInterleave = 32;      // gate/up column interleave of the packed W1
+
+// One M tile of a grouped GEMM: expert, first grouped row, valid rows in it.
+struct Tile {
+  int expert;
+  int row0;
+  int rows;
+  int pad;
+};
+
+// Where each expert's packed weight blob lives: resident experts at
+// res + e * bytes; fetched experts (bit e of fetched set) in the fetch
+// buffer at slot = number of fetched experts with a smaller id.
+struct BlobTable {
+  const uint8_t *res;
+  const uint8_t *fetch;
+  size_t bytes;
+  uint64_t fetched;
+};
+
+__host__ __device__ inline const uint8_t *blob_of(const BlobTable &t, int e) {
+  if ((t.fetched >> e) & 1) {
+    const uint64_t below = t.fetched & ((1ull << e) - 1);
+    return t.fetch + (size_t)__builtin_popcountll(below) * t.bytes;
+  }
+  return t.res + (size_t)e * t.bytes;
+}
+
+// Packed blob layout of one expert (byte offsets from the blob start).
+//   bf16: W1p [2I][d] bf16 (K contiguous), W2p [d][I] bf16
+//   fp8 : W1p [2I][d] u8, W2p [d][I] u8, S1 [2I/32][d/128] f32, S2 [d/128][I/128] f32
+// Row n' of W1p holds column j = (n'/64)*32 + n'%32 of the gate weights when
+// (n'/32) is even and of the up weights when it is odd, so that one 64-row
+// group carries matching gate and up columns for the fused SwiGLU.
+struct BlobLayout {
+  size_t w1_off, w2_off, s1_off, s2_off, bytes;
+};
+
+inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+inline BlobLayout blob_layout(int d, int I, bool fp8) {
+  BlobLayout L{};
+  size_t es = fp8 ? 1 : 2;
+  L.w1_off = 0;
+  L.w2_off = align_up(L.w1_off + (size_t)2 * I * d * es, 256);
+  size_t end = L.w2_off + (size_t)d * I * es;
+  if (fp8) {
+    L.s1_off = align_up(end, 256);
+    L.s2_off = align_up(L.s1_off + (size_t)(2 * I / kInterleave) * (d / 128) * 4, 256);
+    end = L.s2_off + (size_t)(d / 128) * (I / 128) * 4;
+  }
+  L.bytes = align_up(end, 256);
+  return L;
+}
+
+// Chunk arena of one layer: one entry per submitted row, in submission order.
+struct Arena {
+  int32_t *ids;        // [cap][k] local expert id or -1
+  float *w;            // [cap][k] routing coefficient
+  int32_t *dst;        // [cap] output row (replica * T_max + token) or -1
+  const void **xrow;   // [cap] pointer to the row's input
+};
+
+// Per-stream-slot scratch of one grouped invocation.
+struct Scratch {
+  int32_t *blk_cnt;    // [max_blocks][E] pairs per (routing block, expert)
+  int32_t *blk_base;   // [max_blocks][E] first grouped row of each block's pairs
+  int32_t *cnt;        // [E]
+  int32_t *off;        // [E+1]
+  int32_t *off_pad;    // [E+1]
+  Tile *tiles;         // [2][max_tiles]: resident list, fetched list
+  int32_t *n_tiles;    // [2]
+  int32_t *pos_of;     // [max_rows * k] grouped row of each flat pair or -1
+  int32_t *perm;       // [max_mpad] flat pair of each grouped row or -1
+  float *wrow;         // [max_mpad] routing coefficient of each grouped row
+  void *xg;            // [max_mpad][d] bf16 or e4m3
+  float *xs;           // [max_mpad][d/128] fp8 activation scales
+  void *h;             // [max_mpad][I] bf16 or e4m3
+  float *hs;           // [max_mpad][I/128] fp8 scales of h
+  float *y;            // [max_mpad][d] f32, already scaled by the coefficient
+};
+
+// Device error word bits.
+enum : uint32_t { kErrBadId = 1u, kErrPairCount = 2u, kErrBadToken = 4u, kErrOverflow = 8u };
+
+// ---- launchers (implemented in the .hip files) ----
+// weight packing
+hipError_t launch_pack_w1(const void *wg, const void *wu, int w_dtype, int d, int I,
+                          uint8_t *dst_w1, hipStream_t s);
+hipError_t launch_pack_w2(const void *wd, int w_dtype, int d, int I, uint8_t *dst_w2,
+                          hipStream_t s);
+hipError_t launch_pack_scales(const float *sg, const float *su, const float *sd, int d, int I,
+                              float *dst_s1, float *dst_s2, hipStream_t s);
+
+// routing
+hipError_t launch_ingest(const Arena &a, int row0, int n_rows, int k, int E, int replica,
+                         int t_max, const int32_t *token_idx, const void *x, size_t x_row_bytes,
+                         const int32_t *topk_id, const float *topk_w, uint32_t *err,
+                         hipStream_t s);
+hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int E,
+                        int expected_pairs, int max_mpad, int max_tiles,
+                        uint64_t fetched_mask, int x_dtype, bool fp8, int d,
+                        uint32_t *err, hipStream_t s);
+hipError_t launch_combine(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int d,
+                          float *out, hipStream_t s);
+
+// grouped GEMMs over tile list `which` (0 resident, 1 fetched) of a scratch
+// whose lists hold list_cap tiles each; the grid covers grid_tiles M tiles
+hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles,
+                        const BlobTable &bt, const BlobLayout &L, bool fp8, int d, int I,
+                        hipStream_t s);
+hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles,
+                        const BlobTable &bt, const BlobLayout &L, bool fp8, int d, int I,
+                        hipStream_t s);
+
+}  // namespace cep

@@ -1,0 +1,417 @@
+// Routing, packing and combine kernels of the streamFFN path for gfx950.
+//
+// Appendix C, "Grouped FFN invocations": the rows selected from ready source
+// lanes are grouped contiguously by expert, with per-expert offsets aligned
+// to the GEMM tile and an inverse map back to (source replica, token, slot).
+// Appendix C, "Output return and combine": each routed contribution is
+// weighted by its routing coefficient exactly once and summed at the source
+// token.
+//
+// All of these are HBM-bound scans; none of them is a contraction.
+#include "common.h"
+
+#include <hip/hip_bf16.h>
+
+namespace cep {
+namespace {
+
+__device__ inline uint64_t lanemask_lt_popc(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+}
+
+// ---------------------------------------------------------------- ingest
+// Copies one chunk's routing metadata into the layer's arena (one entry per
+// row, in submission order), so that a batch of whole chunks is a contiguous
+// arena range.  Ids outside [-1, E) are flagged and treated as remote; token
+// slots outside [0, T_max) are flagged and their row dropped.
+__global__ __launch_bounds__(256) void k_ingest(Arena a, int row0, int n_rows, int k, int E,
+                                                int replica, int t_max,
+                                                const int32_t *__restrict__ token_idx,
+                                                const char *__restrict__ x, size_t x_row_bytes,
+                                                const int32_t *__restrict__ topk_id,
+                                                const float *__restrict__ topk_w,
+                                                uint32_t *err) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_rows) return;
+  const int t = token_idx[i];
+  int dst = -1;
+  if (t >= 0 && t < t_max) dst = replica * t_max + t;
+  else atomicOr(err, kErrBadToken);
+  a.dst[row0 + i] = dst;
+  a.xrow[row0 + i] = x + (size_t)i * x_row_bytes;
+  for (int s = 0; s < k; ++s) {
+    int id = topk_id[(size_t)i * k + s];
+    if (id < -1 || id >= E) {
+      atomicOr(err, kErrBadId);
+      id = -1;
+    }
+    if (dst < 0) id = -1;
+    a.ids[(size_t)(row0 + i) * k + s] = id;
+    a.w[(size_t)(row0 + i) * k + s] = topk_w[(size_t)i * k + s];
+  }
+}
+
+// ------------------------------------------------------------ histogram
+// Block b counts the valid pairs of flat pairs [b*2048, (b+1)*2048) per
+// expert.  Each wave resolves its 64 ids with ballots: the lowest pending
+// lane names an expert, one ballot finds all lanes holding it.
+__global__ __launch_bounds__(kRouteThreads) void k_route_count(const int32_t *__restrict__ ids,
+                                                               int n_flat, int E,
+                                                               int32_t *__restrict__ blk_cnt) {
+  __shared__ int hist[kMaxExperts];
+  const int tid = threadIdx.x, lane = tid & 63;
+  if (tid < E) hist[tid] = 0;
+  __syncthreads();
+  const int base = blockIdx.x * kRoutePairs;
+#pragma unroll
+  for (int r = 0; r < kRoutePairs / kRouteThreads; ++r) {
+    const int p = base + r * kRouteThreads + tid;
+    const int id = p < n_flat ? ids[p] : -1;
+    uint64_t active = __ballot(id >= 0);
+    while (active) {
+      const int leader = __builtin_ctzll(active);
+      const int e = __shfl(id, leader);
+      const uint64_t m = __ballot(id == e);
+      if (lane == leader) atomicAdd(&hist[e], (int)__popcll(m));
+      active &= ~m;
+    }
+  }
+  __syncthreads();
+  if (tid < E) blk_cnt[blockIdx.x * E + tid] = hist[tid];
+}
+
+// ------------------------------------------------------------------ scan
+// One block: per-expert totals, unpadded and tile-aligned exclusive scans,
+// the first grouped row of every routing block's pairs of every expert, and
+// the M-tile lists of the resident and the fetched experts.
+__global__ __launch_bounds__(256) void k_route_scan(Scratch sc, int n_blocks, int E,
+                                                    int expected_pairs, int max_mpad,
+                                                    int max_tiles, uint64_t fetched_mask,
+                                                    uint32_t *err) {
+  __shared__ int s_cnt[kMaxExperts], s_off[kMaxExperts + 1], s_pad[kMaxExperts + 1];
+  __shared__ int s_tile0[kMaxExperts];
+  const int tid = threadIdx.x;
+  if (tid < E) {
+    int c = 0;
+    for (int b = 0; b < n_blocks; ++b) c += sc.blk_cnt[b * E + tid];
+    s_cnt[tid] = c;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int o = 0, op = 0, total = 0;
+    int t0[2] = {0, 0};
+    for (int e = 0; e < E; ++e) {
+      s_off[e] = o;
+      s_pad[e] = op;
+      const int which = (int)((fetched_mask >> e) & 1);
+      s_tile0[e] = t0[which];
+      t0[which] += (s_cnt[e] + kAlign - 1) / kAlign;
+      o += s_cnt[e];
+      op += (s_cnt[e] + kAlign - 1) / kAlign * kAlign;
+    }
+    s_off[E] = o;
+    s_pad[E] = op;
+    total = o;
+    if (total != expected_pairs) atomicOr(err, kErrPairCount);
+    if (op > max_mpad || t0[0] > max_tiles || t0[1] > max_tiles) atomicOr(err, kErrOverflow);
+    sc.n_tiles[0] = min(t0[0], max_tiles);
+    sc.n_tiles[1] = min(t0[1], max_tiles);
+  }
+  __syncthreads();
+  if (tid <= E) {
+    sc.off[tid] = s_off[tid];
+    sc.off_pad[tid] = s_pad[tid];
+  }
+  if (tid < E) {
+    sc.cnt[tid] = s_cnt[tid];
+    int run = s_pad[tid];
+    for (int b = 0; b < n_blocks; ++b) {
+      sc.blk_base[b * E + tid] = run;
+      run += sc.blk_cnt[b * E + tid];
+    }
+    const int which = (int)((fetched_mask >> tid) & 1);
+    Tile *list = sc.tiles + (size_t)which * max_tiles;
+    const int nt = (s_cnt[tid] + kAlign - 1) / kAlign;
+    for (int q = 0; q < nt; ++q) {
+      const int ti = s_tile0[tid] + q;
+      const int row0 = s_pad[tid] + q * kAlign;
+      if (ti >= max_tiles || row0 + kAlign > max_mpad) break;
+      list[ti] = Tile{tid, row0, min(kAlign, s_cnt[tid] - q * kAlign), 0};
+    }
+  }
+}
+
+// ------------------------------------------------------- permute + pack
+// Same block decomposition as k_route_count.  Each pair's grouped row is the
+// block's first row for its expert, plus pairs of that expert in earlier
+// rounds of this block, in earlier waves of this round, and in lower lanes
+// of this wave (stable in canonical order).  The pair's input row is then
+// copied (bf16), converted (f32 -> bf16) or quantised (e4m3 with one scale
+// per 128 channels) into its grouped row.
+template <int XMODE>  // 0: bf16 -> bf16, 1: f32 -> bf16, 2: bf16 -> e4m3 + scales
+__global__ __launch_bounds__(kRouteThreads) void k_route_scatter(Arena a, Scratch sc, int row0,
+                                                                 int n_flat, int k, int E, int d,
+                                                                 int max_mpad) {
+  __shared__ int running[kMaxExperts];
+  __shared__ int wave_cnt[kRouteThreads / 64][kMaxExperts];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int b = blockIdx.x;
+  if (tid < E) running[tid] = sc.blk_base[b * E + tid];
+  for (int i = tid; i < (kRouteThreads / 64) * kMaxExperts; i += kRouteThreads)
+    (&wave_cnt[0][0])[i] = 0;
+  __syncthreads();
+  const int32_t *ids = a.ids + (size_t)row0 * k;
+  const float *wts = a.w + (size_t)row0 * k;
+  const int base = b * kRoutePairs;
+  for (int r = 0; r < kRoutePairs / kRouteThreads; ++r) {
+    const int p = base + r * kRouteThreads + tid;
+    const int id = p < n_flat ? ids[p] : -1;
+    int rank = 0;
+    uint64_t active = __ballot(id >= 0);
+    const uint64_t valid = active;
+    while (active) {
+      const int leader = __builtin_ctzll(active);
+      const int e = __shfl(id, leader);
+      const uint64_t m = __ballot(id == e);
+      if (id == e) rank = (int)lanemask_lt_popc(m);
+      if (lane == leader) wave_cnt[wid][e] = (int)__popcll(m);
+      active &= ~m;
+    }
+    __syncthreads();
+    int pos = -1;
+    if (id >= 0) {
+      pos = running[id] + rank;
+      for (int w = 0; w < wid; ++w) pos += wave_cnt[w][id];
+      if (pos >= max_mpad) pos = -1;
+    }
+    __syncthreads();
+    if (tid < E) {
+      int add = 0;
+      for (int w = 0; w < kRouteThreads / 64; ++w) {
+        add += wave_cnt[w][tid];
+        wave_cnt[w][tid] = 0;
+      }
+      running[tid] += add;
+    }
+    __syncthreads();  // wave_cnt cleared before the next round writes it
+    if (p < n_flat) sc.pos_of[p] = pos;
+    if (pos >= 0) {
+      sc.perm[pos] = p;
+      sc.wrow[pos] = wts[p];
+    }
+    // copy the rows of this wave's valid pairs, one row per step, whole wave
+    const char *src_row = (id >= 0) ? (const char *)a.xrow[row0 + p / k] : nullptr;
+    uint64_t todo = valid & __ballot(pos >= 0);
+    while (todo) {
+      const int j = __builtin_ctzll(todo);
+      todo &= todo - 1;
+      const int dpos = __shfl(pos, j);
+      const uint64_t sp = (uint64_t)__shfl((long long)(uintptr_t)src_row, j);
+      const char *src = (const char *)(uintptr_t)sp;
+      if (XMODE == 0) {
+        const uint4 *s4 = (const uint4 *)src;
+        uint4 *d4 = (uint4 *)((char *)sc.xg + (size_t)dpos * d * 2);
+        for (int c = lane; c < d / 8; c += 64) d4[c] = s4[c];
+      } else if (XMODE == 1) {
+        const float4 *s4 = (const float4 *)src;
+        uint4 *d4 = (uint4 *)((char *)sc.xg + (size_t)dpos * d * 2);
+        for (int c = lane; c < d / 8; c += 64) {
+          const float4 lo = s4[2 * c], hi = s4[2 * c + 1];
+          union { __bf16 h[8]; uint4 u; } o;
+          o.h[0] = (__bf16)lo.x; o.h[1] = (__bf16)lo.y; o.h[2] = (__bf16)lo.z; o.h[3] = (__bf16)lo.w;
+          o.h[4] = (__bf16)hi.x; o.h[5] = (__bf16)hi.y; o.h[6] = (__bf16)hi.z; o.h[7] = (__bf16)hi.w;
+          d4[c] = o.u;
+        }
+      } else {
+        // 16 lanes x 8 channels = one 128-channel scale block
+        const uint4 *s4 = (const uint4 *)src;
+        uint8_t *dq = (uint8_t *)sc.xg + (size_t)dpos * d;
+        float *ds = sc.xs + (size_t)dpos * (d / 128);
+        for (int c0 = 0; c0 < d; c0 += 512) {
+          const int c = c0 + lane * 8;
+          const bool ok = c < d;
+          float v[8];
+          float amax = 0.f;
+          if (ok) {
+            union { uint4 u; __bf16 h[8]; } in;
+            in.u = s4[c / 8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+              v[q] = (float)in.h[q];
+              amax = fmaxf(amax, fabsf(v[q]));
+            }
+          }
+#pragma unroll
+          for (int sh = 1; sh < 16; sh <<= 1) amax = fmaxf(amax, __shfl_xor(amax, sh, 16));
+          const float scale = amax > 0.f ? amax / 448.0f : 1.0f;
+          if (ok) {
+            int lo = 0, hi = 0;
+            lo = __builtin_amdgcn_cvt_pk_fp8_f32(v[0] / scale, v[1] / scale, lo, false);
+            lo = __builtin_amdgcn_cvt_pk_fp8_f32(v[2] / scale, v[3] / scale, lo, true);
+            hi = __builtin_amdgcn_cvt_pk_fp8_f32(v[4] / scale, v[5] / scale, hi, false);
+            hi = __builtin_amdgcn_cvt_pk_fp8_f32(v[6] / scale, v[7] / scale, hi, true);
+            *(uint2 *)(dq + c) = make_uint2((uint32_t)lo, (uint32_t)hi);
+            if ((lane & 15) == 0) ds[c / 128] = scale;
+          }
+        }
+      }
+    }
+  }
+}
+
+// --------------------------------------------------------------- combine
+// One block per batch row: out[dst] = sum over its valid slots, in slot
+// order, of the grouped output rows (already scaled by their coefficient).
+__global__ __launch_bounds__(256) void k_combine(Arena a, Scratch sc, int row0, int k, int d,
+                                                 float *__restrict__ out) {
+  const int i = blockIdx.x;
+  const int dst = a.dst[row0 + i];
+  if (dst < 0) return;
+  const int32_t *pos = sc.pos_of + (size_t)i * k;
+  float4 *o = (float4 *)(out + (size_t)dst * d);
+  const float4 *y = (const float4 *)sc.y;
+  for (int c = threadIdx.x; c < d / 4; c += blockDim.x) {
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s = 0; s < k; ++s) {
+      const int ps = pos[s];
+      if (ps < 0) continue;
+      const float4 v = y[(size_t)ps * (d / 4) + c];
+      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    }
+    o[c] = acc;
+  }
+}
+
+// ------------------------------------------------------- weight packing
+// out[map(c)][r] = in[r][c] for a [rows][cols] matrix, 64x64 tiles via LDS.
+// MAP 0: identity; MAP 1: gate half of the W1 interleave; MAP 2: up half.
+template <typename TI, typename TO, int MAP>
+__global__ __launch_bounds__(256) void k_transpose(const TI *__restrict__ in, TO *__restrict__ out,
+                                                   int rows, int cols) {
+  __shared__ TO tile[64][65];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int j = ty; j < 64; j += 4) {
+    const int r = r0 + j, c = c0 + tx;
+    if (r < rows && c < cols) tile[j][tx] = (TO)in[(size_t)r * cols + c];
+  }
+  __syncthreads();
+  for (int j = ty; j < 64; j += 4) {
+    const int c = c0 + j, r = r0 + tx;
+    if (r < rows && c < cols) {
+      int oc = c;
+      if (MAP == 1) oc = (c / kInterleave) * (2 * kInterleave) + c % kInterleave;
+      if (MAP == 2) oc = (c / kInterleave) * (2 * kInterleave) + kInterleave + c % kInterleave;
+      out[(size_t)oc * rows + r] = tile[tx][j];
+    }
+  }
+}
+
+__global__ void k_pack_scales(const float *sg, const float *su, const float *sd, int d, int I,
+                              float *s1, float *s2) {
+  const int kb_n = d / 128, ib_n = I / 128;
+  const int n1 = (2 * I / kInterleave) * kb_n;
+  for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < n1 + kb_n * ib_n;
+       t += gridDim.x * blockDim.x) {
+    if (t < n1) {
+      // S1[g][kb] = scale of the gate (g even) or up (g odd) block holding
+      // original column (g/2)*32, at k-block kb.  s_gate is [d/128][I/128].
+      const int g = t / kb_n, kb = t % kb_n;
+      const int col = (g / 2) * kInterleave;
+      s1[t] = ((g & 1) ? su : sg)[kb * ib_n + col / 128];
+    } else {
+      // S2[nb][kb] = s_down[kb][nb]; s_down is [I/128][d/128]
+      const int u = t - n1;
+      const int nb = u / ib_n, kb = u % ib_n;
+      s2[u] = sd[kb * kb_n + nb];
+    }
+  }
+}
+
+}  // namespace
+
+// ================================================================ launchers
+hipError_t launch_pack_w1(const void *wg, const void *wu, int w_dtype, int d, int I,
+                          uint8_t *dst, hipStream_t s) {
+  dim3 grid((I + 63) / 64, (d + 63) / 64);
+  if (w_dtype == 2) {
+    hipLaunchKernelGGL((k_transpose<uint8_t, uint8_t, 1>), grid, dim3(256), 0, s,
+                       (const uint8_t *)wg, dst, d, I);
+    hipLaunchKernelGGL((k_transpose<uint8_t, uint8_t, 2>), grid, dim3(256), 0, s,
+                       (const uint8_t *)wu, dst, d, I);
+  } else if (w_dtype == 1) {
+    hipLaunchKernelGGL((k_transpose<__bf16, __bf16, 1>), grid, dim3(256), 0, s,
+                       (const __bf16 *)wg, (__bf16 *)dst, d, I);
+    hipLaunchKernelGGL((k_transpose<__bf16, __bf16, 2>), grid, dim3(256), 0, s,
+                       (const __bf16 *)wu, (__bf16 *)dst, d, I);
+  } else {
+    hipLaunchKernelGGL((k_transpose<float, __bf16, 1>), grid, dim3(256), 0, s,
+                       (const float *)wg, (__bf16 *)dst, d, I);
+    hipLaunchKernelGGL((k_transpose<float, __bf16, 2>), grid, dim3(256), 0, s,
+                       (const float *)wu, (__bf16 *)dst, d, I);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_w2(const void *wd, int w_dtype, int d, int I, uint8_t *dst,
+                          hipStream_t s) {
+  dim3 grid((d + 63) / 64, (I + 63) / 64);
+  if (w_dtype == 2)
+    hipLaunchKernelGGL((k_transpose<uint8_t, uint8_t, 0>), grid, dim3(256), 0, s,
+                       (const uint8_t *)wd, dst, I, d);
+  else if (w_dtype == 1)
+    hipLaunchKernelGGL((k_transpose<__bf16, __bf16, 0>), grid, dim3(256), 0, s,
+                       (const __bf16 *)wd, (__bf16 *)dst, I, d);
+  else
+    hipLaunchKernelGGL((k_transpose<float, __bf16, 0>), grid, dim3(256), 0, s,
+                       (const float *)wd, (__bf16 *)dst, I, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_scales(const float *sg, const float *su, const float *sd, int d, int I,
+                              float *s1, float *s2, hipStream_t s) {
+  hipLaunchKernelGGL(k_pack_scales, dim3(64), dim3(256), 0, s, sg, su, sd, d, I, s1, s2);
+  return hipGetLastError();
+}
+
+hipError_t launch_ingest(const Arena &a, int row0, int n_rows, int k, int E, int replica,
+                         int t_max, const int32_t *token_idx, const void *x, size_t x_row_bytes,
+                         const int32_t *topk_id, const float *topk_w, uint32_t *err,
+                         hipStream_t s) {
+  if (n_rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_ingest, dim3((n_rows + 255) / 256), dim3(256), 0, s, a, row0, n_rows, k,
+                     E, replica, t_max, token_idx, (const char *)x, x_row_bytes, topk_id,
+                     topk_w, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int E,
+                        int expected_pairs, int max_mpad, int max_tiles, uint64_t fetched_mask,
+                        int x_dtype, bool fp8, int d, uint32_t *err, hipStream_t s) {
+  const int n_flat = n_rows * k;
+  const int nb = (n_flat + kRoutePairs - 1) / kRoutePairs;
+  if (nb == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_route_count, dim3(nb), dim3(kRouteThreads), 0, s,
+                     a.ids + (size_t)row0 * k, n_flat, E, sc.blk_cnt);
+  hipLaunchKernelGGL(k_route_scan, dim3(1), dim3(256), 0, s, sc, nb, E, expected_pairs,
+                     max_mpad, max_tiles, fetched_mask, err);
+  if (fp8)
+    hipLaunchKernelGGL(k_route_scatter<2>, dim3(nb), dim3(kRouteThreads), 0, s, a, sc, row0,
+                       n_flat, k, E, d, max_mpad);
+  else if (x_dtype == 0)
+    hipLaunchKernelGGL(k_route_scatter<1>, dim3(nb), dim3(kRouteThreads), 0, s, a, sc, row0,
+                       n_flat, k, E, d, max_mpad);
+  else
+    hipLaunchKernelGGL(k_route_scatter<0>, dim3(nb), dim3(kRouteThreads), 0, s, a, sc, row0,
+                       n_flat, k, E, d, max_mpad);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int d,
+                          float *out, hipStream_t s) {
+  if (n_rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_combine, dim3(n_rows), dim3(256), 0, s, a, sc, row0, k, d, out);
+  return hipGetLastError();
+}
+
+}  // namespace cep

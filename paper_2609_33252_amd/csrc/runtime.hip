@@ -1,0 +1,676 @@
+// Host runtime of libcep: context, chunk arena, launch policy, stream slots,
+// weight fetch, layer barrier and statistics.  Implements include/cep.h.
+//
+// Section 3.2 ("Launch threshold", "Multi-stream execution"), Appendix C
+// ("Asynchronous dispatch", "Grouped FFN invocations", "One-shot weight
+// fetching", "Output return and combine").
+//
+// Threading: one host thread per context.  Every entry point except the
+// introspection calls only enqueues work.
+#include "common.h"
+#include "../../include/cep.h"
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+using namespace cep;
+
+namespace {
+
+struct ChunkRec {
+  int replica;
+  int row0, n_rows, n_pairs;
+  hipEvent_t arrival;  // caller-owned, may be null
+};
+
+struct BatchRec {
+  int64_t first_chunk;
+  int n_chunks;
+  int row0, n_rows, n_pairs;
+  int slot;
+  bool helper;
+  hipEvent_t ev_start, ev_end;
+  // on the batch stream after: routing, GEMM1, GEMM2, combine
+  hipEvent_t ev_phase[4];
+  // recorded routing (record_routing only), pinned host memory
+  int32_t *h_cnt = nullptr, *h_off = nullptr, *h_off_pad = nullptr, *h_perm = nullptr,
+          *h_pos = nullptr;
+  int mpad_bound = 0;
+};
+
+enum LayerState { kIdle = 0, kOpen = 1 };
+
+}  // namespace
+
+struct cep_ctx {
+  cep_config cfg{};
+  int device = 0;
+  std::string err;
+  bool fp8 = false;
+  BlobLayout L{};
+  uint8_t *w_res = nullptr;  // E blobs
+  std::vector<uint8_t> resident;
+  uint8_t *fetch_buf = nullptr;
+  Arena arena{};
+  int arena_cap = 0;
+  uint32_t *d_err = nullptr;
+  int max_pairs = 0, max_mpad = 0, max_tiles = 0, max_blocks = 0, max_rows = 0;
+  hipStream_t ingest = nullptr;
+  hipStream_t st[8] = {}, helper[8] = {};
+  Scratch sc[8] = {};
+  std::vector<void *> allocs;
+  // policy
+  int policy = CEP_WAIT_ALL, theta = 1, n_streams = 1;
+  // layer state
+  int state = kIdle;
+  uint32_t gen = 0;
+  int n_rep = 0, expected_chunks = 0;
+  float *out = nullptr;
+  int rows_used = 0;
+  std::vector<ChunkRec> chunks;
+  int64_t pending_first = 0;
+  int pending_pairs = 0, pending_rows = 0;
+  std::vector<BatchRec> batches;
+  bool origin_set = false;
+  hipEvent_t ev_origin = nullptr;
+  // fetch
+  bool fetched = false;
+  uint64_t fetched_mask = 0;
+  hipEvent_t ev_fetch_start = nullptr, ev_fetch_ready = nullptr;
+  // sync-only events, one set per slot (re-recorded per batch)
+  hipEvent_t ev_ingest[8] = {}, ev_routed[8] = {}, ev_helper[8] = {};
+  hipEvent_t ev_layer_done = nullptr;
+  std::vector<hipEvent_t> timing_pool;
+  size_t timing_used = 0;
+};
+
+namespace {
+
+// message of the last failure of a call that had no context yet
+thread_local std::string g_err;
+
+int fail(cep_ctx *c, int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  (c ? c->err : g_err) = buf;
+  return code;
+}
+
+#define HIPCHK(ctx, call)                                                              \
+  do {                                                                                 \
+    hipError_t e_ = (call);                                                            \
+    if (e_ != hipSuccess)                                                              \
+      return fail((ctx), CEP_EHIP, "%s: %s (%s:%d)", #call, hipGetErrorString(e_), __FILE__, \
+                  __LINE__);                                                           \
+  } while (0)
+
+bool valid_config(const cep_config *c, std::string *why) {
+  auto bad = [&](const char *m) { *why = m; return false; };
+  if (!c) return bad("cfg is NULL");
+  if (c->d_model <= 0 || c->d_model % 128) return bad("d_model must be a positive multiple of 128");
+  if (c->d_ff <= 0 || c->d_ff % 128) return bad("d_ff must be a positive multiple of 128");
+  if (c->n_local_experts < 1 || c->n_local_experts > kMaxExperts) return bad("n_local_experts must be in 1..64");
+  if (c->top_k < 1 || c->top_k > kMaxTopK) return bad("top_k must be in 1..16");
+  if (c->max_replicas < 1 || c->max_tokens_per_replica < 1) return bad("max_replicas and max_tokens_per_replica must be >= 1");
+  if ((long long)c->max_replicas * c->max_tokens_per_replica > (1LL << 24)) return bad("max_replicas * max_tokens_per_replica too large");
+  if (c->w_dtype < CEP_F32 || c->w_dtype > CEP_FP8_E4M3_B128) return bad("bad w_dtype");
+  if (c->x_dtype != CEP_F32 && c->x_dtype != CEP_BF16) return bad("x_dtype must be CEP_F32 or CEP_BF16");
+  if (c->w_dtype == CEP_FP8_E4M3_B128 && c->x_dtype != CEP_BF16) return bad("fp8 weights need bf16 token rows");
+  if (c->w_dtype == CEP_FP8_E4M3_B128 && c->d_model % 256) return bad("fp8 weights need d_model multiple of 256");
+  if (c->n_streams < 1 || c->n_streams > 8) return bad("n_streams must be in 1..8");
+  if (c->max_pairs_per_batch < 0) return bad("max_pairs_per_batch must be >= 0");
+  return true;
+}
+
+void *dalloc(cep_ctx *c, size_t bytes, hipError_t *e) {
+  void *p = nullptr;
+  *e = hipMalloc(&p, std::max<size_t>(bytes, 256));
+  if (*e == hipSuccess) c->allocs.push_back(p);
+  return p;
+}
+
+hipEvent_t timing_event(cep_ctx *c) {
+  if (c->timing_used == c->timing_pool.size()) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    c->timing_pool.push_back(e);
+  }
+  return c->timing_pool[c->timing_used++];
+}
+
+void free_batch_records(cep_ctx *c) {
+  for (auto &b : c->batches) {
+    (void)hipHostFree(b.h_cnt);
+    (void)hipHostFree(b.h_off);
+    (void)hipHostFree(b.h_off_pad);
+    (void)hipHostFree(b.h_perm);
+    (void)hipHostFree(b.h_pos);
+  }
+  c->batches.clear();
+}
+
+// Launch all pending chunks as one grouped invocation on the next stream slot.
+int launch_pending(cep_ctx *c) {
+  const int64_t nch = (int64_t)c->chunks.size() - c->pending_first;
+  if (nch <= 0 || c->pending_pairs == 0) {
+    c->pending_first = c->chunks.size();
+    c->pending_pairs = c->pending_rows = 0;
+    return CEP_OK;
+  }
+  const cep_config &cfg = c->cfg;
+  const int E = cfg.n_local_experts, k = cfg.top_k, d = cfg.d_model, I = cfg.d_ff;
+  // every expert whose weights are not resident must have been fetched
+  for (int e = 0; e < E; ++e)
+    if (!c->resident[e] && !((c->fetched_mask >> e) & 1))
+      return fail(c, CEP_ESTATE, "expert %d has no resident weights and no fetch this layer", e);
+
+  BatchRec b{};
+  b.first_chunk = c->pending_first;
+  b.n_chunks = (int)nch;
+  b.row0 = c->chunks[c->pending_first].row0;
+  b.n_rows = c->pending_rows;
+  b.n_pairs = c->pending_pairs;
+  b.slot = (int)(c->batches.size() % c->n_streams);
+  const int slot = b.slot;
+  hipStream_t s = c->st[slot];
+  const Scratch &sc = c->sc[slot];
+  const int P = b.n_pairs;
+  const int tiles = std::min(c->max_tiles, (P + kAlign - 1) / kAlign + E);
+  b.mpad_bound = std::min(c->max_mpad, tiles * kAlign);
+  b.ev_start = timing_event(c);
+  b.ev_end = timing_event(c);
+  for (hipEvent_t &e : b.ev_phase) e = timing_event(c);
+  if (!b.ev_start || !b.ev_end || !b.ev_phase[0] || !b.ev_phase[1] || !b.ev_phase[2] ||
+      !b.ev_phase[3])
+    return fail(c, CEP_EHIP, "hipEventCreate failed");
+
+  // the batch sees its chunks only after the ingest stream has staged them
+  HIPCHK(c, hipEventRecord(c->ev_ingest[slot], c->ingest));
+  HIPCHK(c, hipStreamWaitEvent(s, c->ev_ingest[slot], 0));
+  HIPCHK(c, hipEventRecord(b.ev_start, s));
+  HIPCHK(c, launch_route(c->arena, sc, b.row0, b.n_rows, k, E, P, c->max_mpad, c->max_tiles,
+                         c->fetched_mask, cfg.x_dtype, c->fp8, d, c->d_err, s));
+  HIPCHK(c, hipEventRecord(b.ev_phase[0], s));
+
+  BlobTable bt{c->w_res, c->fetch_buf, c->L.bytes, c->fetched_mask};
+
+  b.helper = c->fetched_mask != 0;
+  if (b.helper) {
+    hipStream_t h = c->helper[slot];
+    HIPCHK(c, hipEventRecord(c->ev_routed[slot], s));
+    HIPCHK(c, hipStreamWaitEvent(h, c->ev_routed[slot], 0));
+    HIPCHK(c, hipStreamWaitEvent(h, c->ev_fetch_ready, 0));
+    HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, bt, c->L, c->fp8, d, I, h));
+    HIPCHK(c, launch_gemm2(sc, 1, c->max_tiles, tiles, bt, c->L, c->fp8, d, I, h));
+    HIPCHK(c, hipEventRecord(c->ev_helper[slot], h));
+  }
+  HIPCHK(c, launch_gemm1(sc, 0, c->max_tiles, tiles, bt, c->L, c->fp8, d, I, s));
+  HIPCHK(c, hipEventRecord(b.ev_phase[1], s));
+  HIPCHK(c, launch_gemm2(sc, 0, c->max_tiles, tiles, bt, c->L, c->fp8, d, I, s));
+  HIPCHK(c, hipEventRecord(b.ev_phase[2], s));
+  if (b.helper) HIPCHK(c, hipStreamWaitEvent(s, c->ev_helper[slot], 0));
+  HIPCHK(c, launch_combine(c->arena, sc, b.row0, b.n_rows, k, d, c->out, s));
+  HIPCHK(c, hipEventRecord(b.ev_phase[3], s));
+
+  if (cfg.record_routing) {
+    HIPCHK(c, hipHostMalloc((void **)&b.h_cnt, sizeof(int32_t) * E, 0));
+    HIPCHK(c, hipHostMalloc((void **)&b.h_off, sizeof(int32_t) * (E + 1), 0));
+    HIPCHK(c, hipHostMalloc((void **)&b.h_off_pad, sizeof(int32_t) * (E + 1), 0));
+    HIPCHK(c, hipHostMalloc((void **)&b.h_perm, sizeof(int32_t) * b.mpad_bound, 0));
+    HIPCHK(c, hipHostMalloc((void **)&b.h_pos, sizeof(int32_t) * (size_t)b.n_rows * k, 0));
+    HIPCHK(c, hipMemcpyAsync(b.h_cnt, sc.cnt, sizeof(int32_t) * E, hipMemcpyDeviceToHost, s));
+    HIPCHK(c, hipMemcpyAsync(b.h_off, sc.off, sizeof(int32_t) * (E + 1), hipMemcpyDeviceToHost, s));
+    HIPCHK(c, hipMemcpyAsync(b.h_off_pad, sc.off_pad, sizeof(int32_t) * (E + 1),
+                             hipMemcpyDeviceToHost, s));
+    HIPCHK(c, hipMemcpyAsync(b.h_perm, sc.perm, sizeof(int32_t) * b.mpad_bound,
+                             hipMemcpyDeviceToHost, s));
+    HIPCHK(c, hipMemcpyAsync(b.h_pos, sc.pos_of, sizeof(int32_t) * (size_t)b.n_rows * k,
+                             hipMemcpyDeviceToHost, s));
+  }
+  HIPCHK(c, hipEventRecord(b.ev_end, s));
+  c->batches.push_back(b);
+  c->pending_first = c->chunks.size();
+  c->pending_pairs = c->pending_rows = 0;
+  return CEP_OK;
+}
+
+}  // namespace
+
+// ================================================================== ABI
+
+CEP_API size_t cep_packed_expert_bytes(const cep_config *cfg) {
+  std::string why;
+  if (!valid_config(cfg, &why)) return 0;
+  return blob_layout(cfg->d_model, cfg->d_ff, cfg->w_dtype == CEP_FP8_E4M3_B128).bytes;
+}
+
+static int pack_range(const cep_config *cfg, const cep_weights *w, int first, int n, uint8_t *dst,
+                      hipStream_t s, cep_ctx *c, const uint8_t *mask) {
+  const int d = cfg->d_model, I = cfg->d_ff;
+  const bool fp8 = cfg->w_dtype == CEP_FP8_E4M3_B128;
+  const BlobLayout L = blob_layout(d, I, fp8);
+  const size_t es = cfg->w_dtype == CEP_F32 ? 4 : (fp8 ? 1 : 2);
+  const size_t mat = (size_t)d * I * es;
+  const size_t smat = (size_t)(d / 128) * (I / 128);
+  for (int q = 0; q < n; ++q) {
+    const int e = first + q;
+    if (mask && !mask[e]) continue;
+    uint8_t *blob = dst + (size_t)q * L.bytes;
+    HIPCHK(c, launch_pack_w1((const uint8_t *)w->w_gate + e * mat, (const uint8_t *)w->w_up + e * mat,
+                             cfg->w_dtype, d, I, blob + L.w1_off, s));
+    HIPCHK(c, launch_pack_w2((const uint8_t *)w->w_down + e * mat, cfg->w_dtype, d, I,
+                             blob + L.w2_off, s));
+    if (fp8)
+      HIPCHK(c, launch_pack_scales(w->s_gate + e * smat, w->s_up + e * smat, w->s_down + e * smat,
+                                   d, I, (float *)(blob + L.s1_off), (float *)(blob + L.s2_off), s));
+  }
+  return CEP_OK;
+}
+
+CEP_API int cep_pack_experts(const cep_config *cfg, const cep_weights *w, int first, int n,
+                             void *dst, hipStream_t s) {
+  std::string why;
+  if (!valid_config(cfg, &why)) return fail(nullptr, CEP_EINVAL, "cep_pack_experts: %s", why.c_str());
+  if (!w || !dst || first < 0 || n < 0 || first + n > cfg->n_local_experts)
+    return fail(nullptr, CEP_EINVAL, "cep_pack_experts: bad weights, dst or expert range");
+  if (!w->w_gate || !w->w_up || !w->w_down ||
+      (cfg->w_dtype == CEP_FP8_E4M3_B128 && (!w->s_gate || !w->s_up || !w->s_down)))
+    return fail(nullptr, CEP_EINVAL, "cep_pack_experts: NULL weight or scale pointer");
+  return pack_range(cfg, w, first, n, (uint8_t *)dst, s, nullptr, nullptr);
+}
+
+CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_weights *w,
+                             const uint8_t *resident, hipStream_t s) {
+  if (!out) return fail(nullptr, CEP_EINVAL, "cep_init_experts: out is NULL");
+  *out = nullptr;
+  std::string why;
+  if (!valid_config(cfg, &why)) return fail(nullptr, CEP_EINVAL, "cep_init_experts: %s", why.c_str());
+  if (!w || !w->w_gate || !w->w_up || !w->w_down ||
+      (cfg->w_dtype == CEP_FP8_E4M3_B128 && (!w->s_gate || !w->s_up || !w->s_down)))
+    return fail(nullptr, CEP_EINVAL, "cep_init_experts: NULL weight or scale pointer");
+  cep_ctx *c = new cep_ctx();
+  c->cfg = *cfg;
+  if (hipGetDevice(&c->device) != hipSuccess) {
+    delete c;
+    return fail(nullptr, CEP_EHIP, "cep_init_experts: hipGetDevice failed");
+  }
+  const int E = cfg->n_local_experts, k = cfg->top_k, d = cfg->d_model, I = cfg->d_ff;
+  c->fp8 = cfg->w_dtype == CEP_FP8_E4M3_B128;
+  c->L = blob_layout(d, I, c->fp8);
+  c->resident.assign(E, 1);
+  if (resident)
+    for (int e = 0; e < E; ++e) c->resident[e] = resident[e] ? 1 : 0;
+  c->arena_cap = cfg->max_replicas * cfg->max_tokens_per_replica;
+  c->max_rows = c->arena_cap;
+  const long long def_pairs = (long long)c->arena_cap * k;
+  c->max_pairs = cfg->max_pairs_per_batch > 0 ? (int)std::min<long long>(cfg->max_pairs_per_batch, def_pairs)
+                                              : (int)def_pairs;
+  c->max_tiles = (c->max_pairs + kAlign - 1) / kAlign + E;
+  c->max_mpad = c->max_tiles * kAlign;
+  c->max_blocks = (int)(((long long)c->max_rows * k + kRoutePairs - 1) / kRoutePairs);
+  c->policy = CEP_WAIT_ALL;
+  c->n_streams = cfg->n_streams;
+
+  hipError_t e = hipSuccess;
+  auto A = [&](size_t bytes) { return e == hipSuccess ? dalloc(c, bytes, &e) : nullptr; };
+  c->w_res = (uint8_t *)A(c->L.bytes * E);
+  if (cfg->fetch_buffer_bytes) c->fetch_buf = (uint8_t *)A(cfg->fetch_buffer_bytes);
+  c->arena.ids = (int32_t *)A(sizeof(int32_t) * c->arena_cap * k);
+  c->arena.w = (float *)A(sizeof(float) * c->arena_cap * k);
+  c->arena.dst = (int32_t *)A(sizeof(int32_t) * c->arena_cap);
+  c->arena.xrow = (const void **)A(sizeof(void *) * c->arena_cap);
+  c->d_err = (uint32_t *)A(sizeof(uint32_t));
+  const size_t xes = c->fp8 ? 1 : 2;
+  for (int i = 0; i < cfg->n_streams; ++i) {
+    Scratch &sc = c->sc[i];
+    sc.blk_cnt = (int32_t *)A(sizeof(int32_t) * c->max_blocks * E);
+    sc.blk_base = (int32_t *)A(sizeof(int32_t) * c->max_blocks * E);
+    sc.cnt = (int32_t *)A(sizeof(int32_t) * E);
+    sc.off = (int32_t *)A(sizeof(int32_t) * (E + 1));
+    sc.off_pad = (int32_t *)A(sizeof(int32_t) * (E + 1));
+    sc.tiles = (Tile *)A(sizeof(Tile) * 2 * c->max_tiles);
+    sc.n_tiles = (int32_t *)A(sizeof(int32_t) * 2);
+    sc.pos_of = (int32_t *)A(sizeof(int32_t) * (size_t)c->max_rows * k);
+    sc.perm = (int32_t *)A(sizeof(int32_t) * c->max_mpad);
+    sc.wrow = (float *)A(sizeof(float) * c->max_mpad);
+    sc.xg = A(xes * c->max_mpad * d);
+    sc.h = A(xes * c->max_mpad * I);
+    sc.y = (float *)A(sizeof(float) * c->max_mpad * d);
+    if (c->fp8) {
+      sc.xs = (float *)A(sizeof(float) * c->max_mpad * (d / 128));
+      sc.hs = (float *)A(sizeof(float) * c->max_mpad * (I / 128));
+    }
+  }
+  if (e != hipSuccess) {
+    cep_destroy(c);
+    return fail(nullptr, CEP_ENOMEM, "cep_init_experts: device allocation failed: %s",
+                hipGetErrorString(e));
+  }
+  // streams at default priority; events for ordering only skip timing
+  bool ok = hipStreamCreateWithFlags(&c->ingest, hipStreamNonBlocking) == hipSuccess;
+  for (int i = 0; i < cfg->n_streams && ok; ++i) {
+    ok = hipStreamCreateWithFlags(&c->st[i], hipStreamNonBlocking) == hipSuccess &&
+         hipStreamCreateWithFlags(&c->helper[i], hipStreamNonBlocking) == hipSuccess &&
+         hipEventCreateWithFlags(&c->ev_ingest[i], hipEventDisableTiming) == hipSuccess &&
+         hipEventCreateWithFlags(&c->ev_routed[i], hipEventDisableTiming) == hipSuccess &&
+         hipEventCreateWithFlags(&c->ev_helper[i], hipEventDisableTiming) == hipSuccess;
+  }
+  ok = ok && hipEventCreate(&c->ev_origin) == hipSuccess &&
+       hipEventCreate(&c->ev_fetch_start) == hipSuccess &&
+       hipEventCreate(&c->ev_fetch_ready) == hipSuccess &&
+       hipEventCreateWithFlags(&c->ev_layer_done, hipEventDisableTiming) == hipSuccess;
+  ok = ok && hipMemsetAsync(c->d_err, 0, sizeof(uint32_t), s) == hipSuccess;
+  if (!ok) {
+    cep_destroy(c);
+    return fail(nullptr, CEP_EHIP, "cep_init_experts: stream/event creation failed");
+  }
+  int rc = pack_range(cfg, w, 0, E, c->w_res, s, c, c->resident.data());
+  if (rc == CEP_OK && hipStreamSynchronize(s) != hipSuccess)
+    rc = fail(c, CEP_EHIP, "cep_init_experts: weight packing failed");
+  if (rc != CEP_OK) {
+    g_err = c->err;
+    cep_destroy(c);
+    return rc;
+  }
+  *out = c;
+  return CEP_OK;
+}
+
+CEP_API int cep_set_policy(cep_ctx *c, int policy, int threshold_pairs, int n_streams) {
+  if (!c) return CEP_EINVAL;
+  if (c->state != kIdle) return fail(c, CEP_ESTATE, "cep_set_policy inside an open layer");
+  if (policy < CEP_WAIT_ALL || policy > CEP_THRESHOLD)
+    return fail(c, CEP_EINVAL, "unknown policy %d", policy);
+  if (policy == CEP_THRESHOLD && threshold_pairs < 1)
+    return fail(c, CEP_EINVAL, "threshold must be >= 1");
+  if (n_streams < 1 || n_streams > c->cfg.n_streams)
+    return fail(c, CEP_EINVAL, "n_streams must be in 1..%d", c->cfg.n_streams);
+  c->policy = policy;
+  c->theta = policy == CEP_THRESHOLD ? threshold_pairs : (policy == CEP_PER_CHUNK ? 1 : 0);
+  c->n_streams = n_streams;
+  return CEP_OK;
+}
+
+CEP_API int cep_begin_layer(cep_ctx *c, uint32_t generation, int n_replicas,
+                            const int *chunks_per_replica, float *out) {
+  if (!c) return CEP_EINVAL;
+  if (c->state != kIdle) return fail(c, CEP_ESTATE, "previous layer not combined");
+  if (n_replicas < 1 || n_replicas > c->cfg.max_replicas || !chunks_per_replica || !out)
+    return fail(c, CEP_EINVAL, "bad n_replicas / chunks_per_replica / out");
+  long long tot = 0;
+  for (int r = 0; r < n_replicas; ++r) {
+    if (chunks_per_replica[r] < 0) return fail(c, CEP_EINVAL, "negative chunk count");
+    tot += chunks_per_replica[r];
+  }
+  // the previous layer's batches may still read the arena: stage after them
+  for (int i = 0; i < c->cfg.n_streams; ++i) {
+    HIPCHK(c, hipEventRecord(c->ev_ingest[i], c->st[i]));
+    HIPCHK(c, hipStreamWaitEvent(c->ingest, c->ev_ingest[i], 0));
+    HIPCHK(c, hipEventRecord(c->ev_routed[i], c->helper[i]));
+    HIPCHK(c, hipStreamWaitEvent(c->ingest, c->ev_routed[i], 0));
+  }
+  free_batch_records(c);
+  c->timing_used = 0;
+  c->gen = generation;
+  c->n_rep = n_replicas;
+  c->expected_chunks = (int)tot;
+  c->out = out;
+  c->rows_used = 0;
+  c->chunks.clear();
+  c->pending_first = 0;
+  c->pending_pairs = c->pending_rows = 0;
+  HIPCHK(c, hipEventRecord(c->ev_origin, c->ingest));  // clock origin of this layer's stats
+  c->origin_set = true;
+  c->fetched = false;
+  c->fetched_mask = 0;
+  c->state = kOpen;
+  return CEP_OK;
+}
+
+CEP_API int cep_submit_chunk(cep_ctx *c, uint32_t generation, int replica, int n_rows, int n_pairs,
+                             const int32_t *token_idx, const void *x, const int32_t *topk_id,
+                             const float *topk_w, hipEvent_t arrival, int64_t *chunk_id) {
+  if (!c) return CEP_EINVAL;
+  if (c->state != kOpen) return fail(c, CEP_ESTATE, "no open layer");
+  if (generation != c->gen) return fail(c, CEP_ESTATE, "generation %u, layer is %u", generation, c->gen);
+  if ((int)c->chunks.size() >= c->expected_chunks)
+    return fail(c, CEP_ESTATE, "all %d expected chunks already submitted", c->expected_chunks);
+  if (replica < 0 || replica >= c->n_rep) return fail(c, CEP_EINVAL, "replica %d out of range", replica);
+  if (n_rows < 0 || n_pairs < 0 || (long long)n_pairs > (long long)n_rows * c->cfg.top_k)
+    return fail(c, CEP_EINVAL, "bad n_rows %d / n_pairs %d", n_rows, n_pairs);
+  if (n_rows > 0 && (!token_idx || !x || !topk_id || !topk_w))
+    return fail(c, CEP_EINVAL, "NULL chunk array");
+  if (c->rows_used + n_rows > c->arena_cap)
+    return fail(c, CEP_ENOMEM, "layer rows exceed max_replicas * max_tokens_per_replica");
+  if (n_pairs > c->max_pairs)
+    return fail(c, CEP_ENOMEM, "chunk pairs %d exceed max_pairs_per_batch %d", n_pairs, c->max_pairs);
+  if (arrival) HIPCHK(c, hipStreamWaitEvent(c->ingest, arrival, 0));
+  const size_t xrb = (size_t)c->cfg.d_model * (c->cfg.x_dtype == CEP_F32 ? 4 : 2);
+  HIPCHK(c, launch_ingest(c->arena, c->rows_used, n_rows, c->cfg.top_k, c->cfg.n_local_experts,
+                          replica, c->cfg.max_tokens_per_replica, token_idx, x, xrb, topk_id,
+                          topk_w, c->d_err, c->ingest));
+  ChunkRec ch{replica, c->rows_used, n_rows, n_pairs, arrival};
+  c->rows_used += n_rows;
+  const int64_t id = (int64_t)c->chunks.size();
+  if (chunk_id) *chunk_id = id;
+
+  // a chunk that would overflow a batch first launches what is pending
+  if (n_pairs > 0 && c->pending_pairs > 0 && c->pending_pairs + n_pairs > c->max_pairs) {
+    int rc = launch_pending(c);
+    if (rc != CEP_OK) return rc;
+  }
+  c->chunks.push_back(ch);
+  if (n_pairs > 0) {
+    if (c->pending_pairs == 0) c->pending_first = id;
+    c->pending_pairs += n_pairs;
+    c->pending_rows = (int)(c->rows_used - c->chunks[c->pending_first].row0);
+  } else if (c->pending_pairs == 0) {
+    c->pending_first = id + 1;
+  }
+  const bool last = (int)c->chunks.size() == c->expected_chunks;
+  const bool thresh = c->policy != CEP_WAIT_ALL && c->pending_pairs >= c->theta && c->pending_pairs > 0;
+  if (thresh || last) return launch_pending(c);
+  return CEP_OK;
+}
+
+CEP_API int cep_flush(cep_ctx *c) {
+  if (!c) return CEP_EINVAL;
+  if (c->state != kOpen) return fail(c, CEP_ESTATE, "no open layer");
+  return launch_pending(c);
+}
+
+CEP_API int cep_weight_fetch(cep_ctx *c, const int *ids, int n, const void *const *src_blobs,
+                             hipStream_t side, hipEvent_t *ready) {
+  if (!c) return CEP_EINVAL;
+  if (c->state != kOpen) return fail(c, CEP_ESTATE, "no open layer");
+  if (c->fetched) return fail(c, CEP_EBUSY, "one weight fetch per layer");
+  if (n < 0 || (n > 0 && (!ids || !src_blobs)))
+    return fail(c, CEP_EINVAL, "bad fetch arguments");
+  uint64_t mask = 0;
+  for (int i = 0; i < n; ++i) {
+    if (ids[i] < 0 || ids[i] >= c->cfg.n_local_experts)
+      return fail(c, CEP_EINVAL, "fetch id %d out of range", ids[i]);
+    if ((mask >> ids[i]) & 1) return fail(c, CEP_EINVAL, "duplicate fetch id %d", ids[i]);
+    if (!src_blobs[i]) return fail(c, CEP_EINVAL, "NULL source blob");
+    mask |= 1ull << ids[i];
+  }
+  const size_t need = (size_t)n * c->L.bytes;
+  if (need > c->cfg.fetch_buffer_bytes)
+    return fail(c, CEP_ENOMEM, "fetch of %zu bytes exceeds the %zu-byte buffer", need,
+                c->cfg.fetch_buffer_bytes);
+  c->fetched = true;  // one decision per layer, also when it copies nothing
+  if (n == 0) {
+    if (ready) *ready = nullptr;
+    return CEP_OK;
+  }
+  hipStream_t s = side ? side : c->helper[0];
+  // do not overwrite the buffer while an earlier layer may still read it
+  for (int i = 0; i < c->cfg.n_streams; ++i) {
+    HIPCHK(c, hipEventRecord(c->ev_routed[i], c->helper[i]));
+    HIPCHK(c, hipStreamWaitEvent(s, c->ev_routed[i], 0));
+  }
+  HIPCHK(c, hipEventRecord(c->ev_fetch_start, s));
+  // expert e goes to slot = number of fetched experts with a smaller id
+  for (int i = 0; i < n; ++i) {
+    const int slot = __builtin_popcountll(mask & ((1ull << ids[i]) - 1));
+    uint8_t *dst = c->fetch_buf + (size_t)slot * c->L.bytes;
+    HIPCHK(c, hipMemcpyAsync(dst, src_blobs[i], c->L.bytes, hipMemcpyDeviceToDevice, s));
+  }
+  HIPCHK(c, hipEventRecord(c->ev_fetch_ready, s));
+  c->fetched_mask = mask;
+  if (ready) *ready = c->ev_fetch_ready;
+  return CEP_OK;
+}
+
+CEP_API int cep_combine(cep_ctx *c, hipStream_t s, hipEvent_t *done) {
+  if (!c) return CEP_EINVAL;
+  if (c->state != kOpen) return fail(c, CEP_ESTATE, "no open layer");
+  if ((int)c->chunks.size() < c->expected_chunks)
+    return fail(c, CEP_ESTATE, "%d of %d chunks submitted; cep_flush ends a layer early",
+                (int)c->chunks.size(), c->expected_chunks);
+  int rc = launch_pending(c);
+  if (rc != CEP_OK) return rc;
+  for (int i = 0; i < c->cfg.n_streams; ++i) {
+    HIPCHK(c, hipEventRecord(c->ev_ingest[i], c->st[i]));
+    HIPCHK(c, hipStreamWaitEvent(s, c->ev_ingest[i], 0));
+  }
+  HIPCHK(c, hipEventRecord(c->ev_layer_done, s));
+  if (done) *done = c->ev_layer_done;
+  c->state = kIdle;
+  return CEP_OK;
+}
+
+CEP_API int cep_get_batch_count(const cep_ctx *c) { return c ? (int)c->batches.size() : 0; }
+
+CEP_API int cep_get_batch_routing(cep_ctx *c, int batch, int *align, int *n_pairs, int *n_rows,
+                                  int32_t *cnt, int32_t *off, int32_t *off_pad, int32_t *perm_src,
+                                  int32_t *pos_of, int64_t *chunks, int *n_chunks) {
+  if (!c) return CEP_EINVAL;
+  if (batch < 0 || batch >= (int)c->batches.size()) return fail(c, CEP_EINVAL, "no batch %d", batch);
+  const BatchRec &b = c->batches[batch];
+  const int E = c->cfg.n_local_experts, k = c->cfg.top_k;
+  if (align) *align = kAlign;
+  if (n_pairs) *n_pairs = b.n_pairs;
+  if (n_rows) *n_rows = b.n_rows;
+  if (n_chunks) *n_chunks = b.n_chunks;
+  if (chunks)
+    for (int i = 0; i < b.n_chunks; ++i) chunks[i] = b.first_chunk + i;
+  if (!(cnt || off || off_pad || perm_src || pos_of)) return CEP_OK;
+  if (!c->cfg.record_routing) return fail(c, CEP_ESTATE, "record_routing is off");
+  HIPCHK(c, hipEventSynchronize(b.ev_end));
+  if (cnt) memcpy(cnt, b.h_cnt, sizeof(int32_t) * E);
+  if (off) memcpy(off, b.h_off, sizeof(int32_t) * (E + 1));
+  if (off_pad) memcpy(off_pad, b.h_off_pad, sizeof(int32_t) * (E + 1));
+  if (pos_of) memcpy(pos_of, b.h_pos, sizeof(int32_t) * (size_t)b.n_rows * k);
+  if (perm_src) {
+    for (int e = 0; e < E; ++e)
+      for (int q = 0; q < b.h_cnt[e]; ++q) {
+        const int p = b.h_off_pad[e] + q;
+        if (p < b.mpad_bound && b.h_off[e] + q < b.n_pairs) perm_src[b.h_off[e] + q] = b.h_perm[p];
+      }
+  }
+  return CEP_OK;
+}
+
+CEP_API int cep_get_stats(cep_ctx *c, char *buf, size_t cap) {
+  if (!c || !buf) return CEP_EINVAL;
+  std::string js = "{\"batches\":[";
+  char tmp[512];
+  for (size_t i = 0; i < c->batches.size(); ++i) {
+    const BatchRec &b = c->batches[i];
+    HIPCHK(c, hipEventSynchronize(b.ev_end));
+    float t0 = 0, t1 = 0, ph[4] = {0, 0, 0, 0};
+    HIPCHK(c, hipEventElapsedTime(&t0, c->ev_origin, b.ev_start));
+    HIPCHK(c, hipEventElapsedTime(&t1, c->ev_origin, b.ev_end));
+    hipEvent_t prev = b.ev_start;
+    for (int p = 0; p < 4; ++p) {
+      HIPCHK(c, hipEventElapsedTime(&ph[p], prev, b.ev_phase[p]));
+      prev = b.ev_phase[p];
+    }
+    snprintf(tmp, sizeof tmp,
+             "%s{\"first_chunk\":%lld,\"n_chunks\":%d,\"rows\":%d,\"pairs\":%d,\"slot\":%d,"
+             "\"helper\":%s,\"start_ms\":%.6f,\"end_ms\":%.6f,\"route_ms\":%.6f,"
+             "\"gemm1_ms\":%.6f,\"gemm2_ms\":%.6f,\"combine_ms\":%.6f}",
+             i ? "," : "", (long long)b.first_chunk, b.n_chunks, b.n_rows, b.n_pairs, b.slot,
+             b.helper ? "true" : "false", t0, t1, ph[0], ph[1], ph[2], ph[3]);
+    js += tmp;
+  }
+  js += "],\"chunks\":[";
+  for (size_t i = 0; i < c->chunks.size(); ++i) {
+    const ChunkRec &ch = c->chunks[i];
+    float ta = -1;
+    if (ch.arrival && c->origin_set) {
+      // an arrival event without timing has no timestamp: report -1 and
+      // clear the runtime's sticky error so later launches do not see it
+      if (hipEventSynchronize(ch.arrival) != hipSuccess ||
+          hipEventElapsedTime(&ta, c->ev_origin, ch.arrival) != hipSuccess) {
+        ta = -1;
+        (void)hipGetLastError();
+      }
+    }
+    snprintf(tmp, sizeof tmp, "%s{\"replica\":%d,\"rows\":%d,\"pairs\":%d,\"arrival_ms\":%.6f}",
+             i ? "," : "", ch.replica, ch.n_rows, ch.n_pairs, ta);
+    js += tmp;
+  }
+  js += "]";
+  if (c->fetched && c->fetched_mask) {
+    float f0 = 0, f1 = 0;
+    HIPCHK(c, hipEventSynchronize(c->ev_fetch_ready));
+    if (c->origin_set) {
+      (void)hipEventElapsedTime(&f0, c->ev_origin, c->ev_fetch_start);
+      (void)hipEventElapsedTime(&f1, c->ev_origin, c->ev_fetch_ready);
+    }
+    snprintf(tmp, sizeof tmp, ",\"fetch\":{\"start_ms\":%.6f,\"end_ms\":%.6f,\"bytes\":%zu}", f0,
+             f1, (size_t)__builtin_popcountll(c->fetched_mask) * c->L.bytes);
+    js += tmp;
+  }
+  js += "}";
+  if (js.size() + 1 > cap) return fail(c, CEP_ENOMEM, "stats need %zu bytes", js.size() + 1);
+  memcpy(buf, js.c_str(), js.size() + 1);
+  return CEP_OK;
+}
+
+CEP_API int cep_get_status(cep_ctx *c) {
+  if (!c) return CEP_EINVAL;
+  HIPCHK(c, hipDeviceSynchronize());
+  uint32_t w = 0;
+  HIPCHK(c, hipMemcpy(&w, c->d_err, sizeof w, hipMemcpyDeviceToHost));
+  HIPCHK(c, hipMemset(c->d_err, 0, sizeof w));
+  if (!w) return CEP_OK;
+  return fail(c, CEP_EINVAL, "device-side check failed:%s%s%s%s", (w & kErrBadId) ? " expert id out of range" : "",
+              (w & kErrPairCount) ? " n_pairs mismatch" : "", (w & kErrBadToken) ? " token index out of range" : "",
+              (w & kErrOverflow) ? " batch exceeded scratch capacity" : "");
+}
+
+CEP_API const char *cep_last_error(const cep_ctx *c) {
+  if (!c) return g_err.c_str();
+  return c->err.c_str();
+}
+
+CEP_API int cep_destroy(cep_ctx *c) {
+  if (!c) return CEP_OK;
+  (void)hipDeviceSynchronize();
+  free_batch_records(c);
+  for (hipEvent_t e : c->timing_pool) (void)hipEventDestroy(e);
+  hipEvent_t evs[] = {c->ev_origin, c->ev_fetch_start, c->ev_fetch_ready, c->ev_layer_done};
+  for (hipEvent_t e : evs)
+    if (e) (void)hipEventDestroy(e);
+  for (int i = 0; i < 8; ++i) {
+    if (c->ev_ingest[i]) (void)hipEventDestroy(c->ev_ingest[i]);
+    if (c->ev_routed[i]) (void)hipEventDestroy(c->ev_routed[i]);
+    if (c->ev_helper[i]) (void)hipEventDestroy(c->ev_helper[i]);
+    if (c->st[i]) (void)hipStreamDestroy(c->st[i]);
+    if (c->helper[i]) (void)hipStreamDestroy(c->helper[i]);
+  }
+  if (c->ingest) (void)hipStreamDestroy(c->ingest);
+  for (void *p : c->allocs) (void)hipFree(p);
+  delete c;
+  return CEP_OK;
+}

@@ -1,0 +1,277 @@
+"""GPU parity of the HIP path (through the C ABI) against the CPU oracle.
+
+* routing metadata and batch composition: bit-exact, every config
+* outputs: elementwise tolerance (bf16, f32 inputs) or relative RMS (fp8),
+  at reduced token counts over all rows and at full size on sampled tokens
+* closed forms on the GPU: identity-permutation expert, zero expert
+* invariance: chunking, submission order, policy and stream count do not
+  change the output (bitwise); a fetched expert equals a resident one
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import policy as opol
+from oracle import routing as orout
+from paper_2609_33252_amd import cep, harness, workload as W
+
+from . import _util as U
+
+pytestmark = pytest.mark.gpu
+
+# token counts small enough for the oracle over every row, at the real
+# d_model / d_ff of each configuration, spanning several M tiles per expert
+REDUCED = {
+    "tiny": {},
+    "sync_d4096": dict(T=512),
+    "zipf_stream_d7168": dict(T=512, cpr=4),
+    "zipf_imbalanced_d7168": dict(T=512, cpr=4),
+    "fp8_fetch_d6144": dict(T=256, cpr=2),
+}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    cep.lib()
+    torch.cuda.set_device(0)
+
+
+def _out(run):
+    torch.cuda.synchronize()
+    cep.cep_get_status(run.ctx)
+    return run.out.cpu().numpy()
+
+
+# ------------------------------------------------------------- routing
+@pytest.mark.parametrize("name", W.CONFIG_ORDER)
+def test_routing_and_batches_bit_exact(name):
+    # routing does not depend on d / d_ff: full token counts, small widths
+    small = dict(d=256, I=128)
+    wl = W.generate(name, 0, **small)
+    run = harness.Runner(wl, n_streams=3, record_routing=True, use_fetch=True)
+    theta = max(1, wl.n_pairs // 5)
+    run.run(policy=cep.CEP_THRESHOLD, theta=theta, n_streams=3)
+    torch.cuda.synchronize()
+    cep.cep_get_status(run.ctx)
+    pairs_seq = [ch.n_pairs for ch in run.chunks]
+    expect = opol.batches(pairs_seq, opol.THRESHOLD, theta)
+    nb = cep.cep_get_batch_count(run.ctx)
+    assert nb == len(expect)
+    E, k = wl.cfg["E"], wl.cfg["k"]
+    for b in range(nb):
+        m = cep.cep_get_batch_routing(run.ctx, b, E, k)
+        got_chunks = [int(c) for c in m["chunks"] if run.chunks[int(c)].n_pairs > 0]
+        assert got_chunks == expect[b]
+        ids = [wl.topk_local[wl.chunks[c].replica][wl.chunks[c].token_idx]
+               for c in m["chunks"]]
+        ref = orout.batch_routing(ids, E, m["align"])
+        for key in ("cnt", "off", "off_pad", "perm_src", "pos_of"):
+            assert np.array_equal(m[key], ref[key]), (b, key)
+    run.close()
+
+
+def test_policies_match_batch_oracle():
+    wl = W.generate("zipf_stream_d7168", 0, d=256, I=128)
+    run = harness.Runner(wl, n_streams=4, record_routing=True)
+    seq = [ch.n_pairs for ch in run.chunks]
+    for pol, theta, ns in ((cep.CEP_WAIT_ALL, 1, 1), (cep.CEP_PER_CHUNK, 1, 2),
+                           (cep.CEP_THRESHOLD, 32, 4), (cep.CEP_THRESHOLD, 4096, 2)):
+        run.run(policy=pol, theta=theta, n_streams=ns)
+        torch.cuda.synchronize()
+        want = opol.batches(seq, {0: opol.WAIT_ALL, 1: opol.PER_CHUNK, 2: opol.THRESHOLD}[pol],
+                            theta)
+        got = []
+        for b in range(cep.cep_get_batch_count(run.ctx)):
+            m = cep.cep_get_batch_routing(run.ctx, b, wl.cfg["E"], wl.cfg["k"])
+            got.append([int(c) for c in m["chunks"] if seq[int(c)] > 0])
+        assert got == want, (pol, theta)
+        st = run.stats()
+        assert [b["slot"] for b in st["batches"]] == [i % ns for i in range(len(want))]
+    run.close()
+
+
+# ------------------------------------------------------------- outputs
+@pytest.mark.parametrize("name", W.CONFIG_ORDER)
+def test_outputs_match_oracle_reduced(name):
+    wl = W.generate(name, 0, **REDUCED[name])
+    run = harness.Runner(wl, n_streams=2)
+    run.run(policy=cep.CEP_THRESHOLD, theta=max(1, wl.n_pairs // 3), n_streams=2)
+    got = _out(run)
+    run.close()
+    ref = U.reference(wl)
+    mx, rel = U.compare(wl, got, ref)
+    assert not got[~wl.delivered].any()
+    print(f"{name}: pairs={wl.n_pairs} max_abs={mx:.3e} rel_rms={rel:.3e}")
+
+
+@pytest.mark.parametrize("name", ["sync_d4096", "zipf_stream_d7168", "fp8_fetch_d6144"])
+def test_full_size_sampled_tokens(name):
+    wl = W.generate(name, 0)
+    run = harness.Runner(wl, n_streams=1)
+    run.run(policy=cep.CEP_WAIT_ALL)
+    got = _out(run)
+    run.close()
+    rng = np.random.default_rng(1)
+    deliv = np.argwhere(wl.delivered)
+    pick = deliv[rng.choice(len(deliv), size=24, replace=False)]
+    # include tokens routed to the hottest and coldest local experts
+    cnt = np.bincount(wl.topk_local[wl.topk_local >= 0], minlength=wl.cfg["E"])
+    for e in (int(cnt.argmax()), int(np.argmin(np.where(cnt > 0, cnt, 1 << 30)))):
+        rt = np.argwhere((wl.topk_local == e).any(axis=2))
+        pick = np.vstack([pick, rt[-2:]])
+    ref = U.reference(wl, tokens=pick)
+    mx, rel = U.compare(wl, got[pick[:, 0], pick[:, 1]], ref)
+    assert not got[~wl.delivered].any()
+    print(f"{name} full: pairs={wl.n_pairs} sampled={len(pick)} max_abs={mx:.3e} rel={rel:.3e}")
+
+
+# --------------------------------------------------------- closed forms
+def _custom(d, I, E, wg, wu, wd, R=2, T=256):
+    wl = W.generate("sync_d4096", 3, d=d, I=I, E=E, Eg=E + 2, k=2, R=R, T=T)
+    wl.w_gate, wl.w_up, wl.w_down = wg, wu, wd
+    return wl
+
+
+@pytest.mark.parametrize("beta", [0.5, 2.0])
+def test_identity_permutation_expert_closed_form(beta):
+    d = I = 256
+    pi = np.roll(np.arange(d), 3)
+    P = np.zeros((d, d), np.float32)
+    P[pi, np.arange(d)] = 1.0
+    wg = torch.from_numpy(np.stack([beta * P] * 2)).to(torch.bfloat16)
+    wu = torch.from_numpy(np.stack([P] * 2)).to(torch.bfloat16)
+    wd = torch.from_numpy(np.stack([P.T.copy()] * 2)).to(torch.bfloat16)
+    wl = _custom(d, I, 2, wg, wu, wd)
+    run = harness.Runner(wl, n_streams=1)
+    run.run(policy=cep.CEP_PER_CHUNK)
+    got = _out(run)
+    run.close()
+    x = wl.x.double().numpy()
+    h = x * (beta * x) / (1 + np.exp(-beta * x))
+    hb = torch.from_numpy(h).to(torch.bfloat16).double().numpy()
+    wsum = np.where(wl.topk_local >= 0, wl.topk_w, 0).astype(np.float64)
+    # every local slot contributes w * h: y = sum_s w_s * bf16(h)
+    ref = np.zeros_like(x)
+    for s in range(wl.cfg["k"]):
+        ref += wsum[:, :, s:s + 1] * hb
+    err = np.abs(got - ref)
+    # h is rounded to bf16 on both sides; float32 silu may move it by one ulp
+    assert np.all(err <= 2.0 ** -7 * np.abs(ref) * wl.cfg["k"] + 1e-6), err.max()
+
+
+def test_zero_down_weights_give_exact_zero():
+    wl = W.generate("sync_d4096", 4, T=256)
+    wl.w_down = torch.zeros_like(wl.w_down)
+    run = harness.Runner(wl)
+    run.run(policy=cep.CEP_THRESHOLD, theta=500, n_streams=2)
+    got = _out(run)
+    run.close()
+    assert not got.any()
+
+
+# ------------------------------------------------------------ invariance
+def test_chunking_order_policy_streams_invariance_bitwise():
+    wl = W.generate("zipf_imbalanced_d7168", 0, T=512, cpr=8)
+    run = harness.Runner(wl, n_streams=4)
+    outs = []
+    rng = np.random.default_rng(0)
+    for pol, theta, ns, order in ((cep.CEP_WAIT_ALL, 1, 1, None),
+                                  (cep.CEP_PER_CHUNK, 1, 4, None),
+                                  (cep.CEP_THRESHOLD, 200, 3, None),
+                                  (cep.CEP_THRESHOLD, 700, 2, list(rng.permutation(len(run.chunks))))):
+        run.out.zero_()
+        run.run(policy=pol, theta=theta, n_streams=ns, order=order)
+        outs.append(_out(run))
+    run.close()
+    for o in outs[1:]:
+        assert np.array_equal(o, outs[0])
+
+
+def test_fetched_experts_equal_resident_bitwise():
+    wl = W.generate("fp8_fetch_d6144", 0, T=256, cpr=2)
+    a = harness.Runner(wl, n_streams=2, use_fetch=True)
+    a.run(policy=cep.CEP_THRESHOLD, theta=600, n_streams=2)
+    ga = _out(a)
+    st = a.stats()
+    assert "fetch" in st and st["fetch"]["bytes"] == len(wl.fetched) * a.blob_bytes
+    assert all(b["helper"] for b in st["batches"])
+    a.close()
+    b = harness.Runner(wl, n_streams=1, use_fetch=False)
+    b.run(policy=cep.CEP_WAIT_ALL)
+    gb = _out(b)
+    b.close()
+    assert np.array_equal(ga, gb)
+
+
+# ----------------------------------------------------------- error paths
+def test_error_paths():
+    wl = W.generate("tiny", 0)
+    run = harness.Runner(wl, n_streams=2)
+    ctx = run.ctx
+    ch = run.chunks[0]
+    E = pytest.raises
+    with E(cep.CepError) as e:  # no open layer
+        cep.cep_submit_chunk(ctx, 1, 0, ch.n_rows, ch.n_pairs, ch.token_idx, ch.x, ch.ids, ch.w)
+    assert e.value.status == cep.CEP_ESTATE
+    cep.cep_begin_layer(ctx, 7, run.chunks_per_replica, run.out)
+    with E(cep.CepError) as e:  # wrong generation
+        cep.cep_submit_chunk(ctx, 8, 0, ch.n_rows, ch.n_pairs, ch.token_idx, ch.x, ch.ids, ch.w)
+    assert e.value.status == cep.CEP_ESTATE
+    with E(cep.CepError) as e:  # replica out of range
+        cep.cep_submit_chunk(ctx, 7, 5, ch.n_rows, ch.n_pairs, ch.token_idx, ch.x, ch.ids, ch.w)
+    assert e.value.status == cep.CEP_EINVAL
+    with E(cep.CepError) as e:  # more pairs than rows * k
+        cep.cep_submit_chunk(ctx, 7, 0, 1, 5, ch.token_idx, ch.x, ch.ids, ch.w)
+    assert e.value.status == cep.CEP_EINVAL
+    with E(cep.CepError) as e:  # policy change inside a layer
+        cep.cep_set_policy(ctx, cep.CEP_PER_CHUNK)
+    assert e.value.status == cep.CEP_ESTATE
+    with E(cep.CepError) as e:  # fetch beyond the (zero-byte) buffer
+        cep.cep_weight_fetch(ctx, [0], [run.out.data_ptr()])
+    assert e.value.status == cep.CEP_ENOMEM
+    cep.cep_weight_fetch(ctx, [], [])  # the one decision: empty
+    with E(cep.CepError) as e:  # no second fetch decision in a layer
+        cep.cep_weight_fetch(ctx, [], [])
+    assert e.value.status == cep.CEP_EBUSY
+    cep.cep_flush(ctx)  # nothing pending: no-op
+    with E(cep.CepError) as e:  # chunks still expected
+        cep.cep_combine(ctx)
+    assert e.value.status == cep.CEP_ESTATE
+    for c in run.chunks:
+        cep.cep_submit_chunk(ctx, 7, c.replica, c.n_rows, c.n_pairs, c.token_idx, c.x, c.ids, c.w)
+    with E(cep.CepError) as e:  # all expected chunks already in
+        cep.cep_submit_chunk(ctx, 7, 0, ch.n_rows, ch.n_pairs, ch.token_idx, ch.x, ch.ids, ch.w)
+    assert e.value.status == cep.CEP_ESTATE
+    cep.cep_combine(ctx)
+    torch.cuda.synchronize()
+    cep.cep_get_status(ctx)
+
+    # device-side checks: an id outside [-1, E) and a wrong pair count
+    bad = ch.ids.clone()
+    bad[0, 0] = wl.cfg["E"] + 3
+    cep.cep_begin_layer(ctx, 9, [1, 0], run.out)
+    cep.cep_submit_chunk(ctx, 9, 0, ch.n_rows, ch.n_pairs, ch.token_idx, ch.x, bad, ch.w)
+    cep.cep_combine(ctx)
+    with E(cep.CepError) as e:
+        cep.cep_get_status(ctx)
+    assert e.value.status == cep.CEP_EINVAL and "expert id" in str(e.value)
+    cep.cep_get_status(ctx)  # cleared
+    run.close()
+
+
+def test_all_remote_chunk_launches_nothing():
+    wl = W.generate("tiny", 0)
+    run = harness.Runner(wl)
+    ch = run.chunks[0]
+    ids = torch.full_like(ch.ids, -1)
+    run.out.fill_(3.0)
+    cep.cep_begin_layer(run.ctx, 1, [1, 0], run.out)
+    cep.cep_submit_chunk(run.ctx, 1, ch.replica, ch.n_rows, 0, ch.token_idx, ch.x, ids, ch.w)
+    cep.cep_combine(run.ctx)
+    torch.cuda.synchronize()
+    cep.cep_get_status(run.ctx)
+    assert cep.cep_get_batch_count(run.ctx) == 0
+    assert torch.all(run.out == 3.0)
+    run.close()
