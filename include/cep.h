@@ -73,7 +73,7 @@ enum cep_policy {
 };
 
 typedef struct {
-  int d_model;                /* hidden size d, multiple of 128               */
+  int d_model;                /* hidden size d, multiple of 256               */
   int d_ff;                   /* expert intermediate size I, multiple of 128  */
   int n_local_experts;        /* E, 1..64                                     */
   int top_k;                  /* k routing slots per token, 1..16             */

@@ -12,7 +12,9 @@ namespace cep {
 
 constexpr int kMaxExperts = 64;
 constexpr int kMaxTopK = 16;
-constexpr int kAlign = 128;          // M tile = per-expert row alignment A
+constexpr int kBf16TileM = 256;      // bf16 grouped GEMM tile
+constexpr int kBf16TileN = 256;
+constexpr int kFp8TileM = 128;       // e4m3 grouped GEMM tile
 constexpr int kRouteThreads = 256;   // threads per routing block
 constexpr int kRoutePairs = 2048;    // flat pairs per routing block (8 rounds of 256)
 constexpr int kInterleave = 32;      // gate/up column interleave of the packed W1
@@ -54,6 +56,9 @@ struct BlobLayout {
 };
 
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Per-expert row alignment A of the grouped layout = M tile of the GEMMs.
+inline int gemm_align(bool fp8) { return fp8 ? kFp8TileM : kBf16TileM; }
 
 inline BlobLayout blob_layout(int d, int I, bool fp8) {
   BlobLayout L{};
@@ -115,9 +120,9 @@ hipError_t launch_ingest(const Arena &a, int row0, int n_rows, int k, int E, int
                          const int32_t *topk_id, const float *topk_w, uint32_t *err,
                          hipStream_t s);
 hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int E,
-                        int expected_pairs, int max_mpad, int max_tiles,
-                        uint64_t fetched_mask, int x_dtype, bool fp8, int d,
-                        uint32_t *err, hipStream_t s);
+                        int align, int expected_pairs, int max_mpad, int max_tiles,
+                        uint64_t fetched_mask, int x_dtype, bool fp8, int d, uint32_t *err,
+                        hipStream_t s);
 hipError_t launch_combine(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int d,
                           float *out, hipStream_t s);
 

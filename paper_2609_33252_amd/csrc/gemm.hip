@@ -51,13 +51,213 @@ __device__ inline int xcd_remap(int bid, int G) {
 
 __device__ inline float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
 
+// Grouped tile order: GM consecutive M tiles x all N tiles form a group, M
+// fastest inside it, so the blocks an XCD runs together share GM row panels
+// of A and the weight panels of their N tiles in that XCD's L2.
+template <int GM>
+__device__ inline void tile_of(int L, int n_tiles_n, int *mt, int *nt) {
+  const int grp = L / (GM * n_tiles_n), idx = L % (GM * n_tiles_n);
+  *mt = grp * GM + idx % GM;
+  *nt = idx / GM;
+}
+
+// Work item of this workgroup, balanced over the XCDs.  The grid covers the
+// host's upper bound on M tiles; the live count is on the device.  The live
+// work W (whole groups) is cut into 8 contiguous shares, one per XCD
+// (workgroup ids are dispatched round-robin over the XCDs), so the surplus
+// workgroups of the bound never leave an XCD idle while another holds the
+// tail.  Returns false for a surplus workgroup.
+template <int GM>
+__device__ inline bool balanced_tile(int n_live, int n_tiles_n, int *mt, int *nt) {
+  const int W = (n_live + GM - 1) / GM * GM * n_tiles_n;
+  const int C = (W + 7) / 8;
+  const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
+  const int L = x * C + j;
+  if (j >= C || L >= W) return false;
+  tile_of<GM>(L, n_tiles_n, mt, nt);
+  return *mt < n_live;
+}
+
+// Grid for balanced_tile: at least the bound's work, a multiple of 8.
+inline int balanced_grid(int grid_tiles, int gm, int n_tiles_n) {
+  return ((grid_tiles + gm - 1) / gm * gm * n_tiles_n + 7) / 8 * 8;
+}
+constexpr int kGroupM = 8;
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// One direct global->LDS load of 16 bytes per lane: lane l's bytes land at
+// LDS byte offset lds_seg + 16*l.  Issued as inline assembly so that the
+// compiler does not order later LDS reads behind it; the caller synchronises
+// with wait_vmcnt and a barrier.  m0 holds the LDS base; it is reserved to
+// the compiler, so its value is saved and restored around the load (one wait
+// state after writing m0 before the load reads it).
+__device__ inline void dma16(const void *gptr, uint32_t lds_seg) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(gptr), "s"(lds_seg)
+      : "memory");
+}
+
+__device__ inline uint32_t lds_offset(const void *p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+
+// s_waitcnt immediate that waits until at most N vector-memory operations of
+// this wave are outstanding (gfx9 encoding: vmcnt in bits [3:0] and [15:14];
+// expcnt 7 and lgkmcnt 15 mean "do not wait" on those counters).
+template <int N>
+__device__ inline void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// ------------------------------------------------------- bf16, LDS DMA
+// BM x BN output tile (256 x 256), 4 waves as 2x2, each wave (BM/2) x (BN/2)
+// built from v_mfma_f32_32x32x16_bf16 fragments.  K advances in steps of 32
+// through a ring of STAGES LDS buffers filled by direct global->LDS loads
+// (global_load_lds_dwordx4, no staging registers) issued STAGES-1 steps
+// ahead, one barrier per step.  An LDS row is 32 bf16 = four 16-byte chunks;
+// chunk c of row r lives at slot c ^ ((r >> 2) & 3): sixteen consecutive
+// rows read at one chunk (what one LDS cycle serves of an MFMA operand read)
+// then cover all sixteen 16-byte slots of a 256-byte bank window, so the
+// reads are conflict-free (a (r >> 1) swizzle measured 50% bank-conflict
+// cycles).  A load instruction fills 64 consecutive slots, so each lane
+// fetches the global chunk that belongs in its slot.
+template <int BM, int BN, bool SWIGLU>
+__global__ __launch_bounds__(256, 1) void k_gemm_bf16_dma(GemmArgs g) {
+  constexpr int BK = 32, STAGES = 4;
+  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int FM = WM / 32, FN = WN / 32;
+  constexpr int A_SEG = BM * BK * 2 / 1024, B_SEG = BN * BK * 2 / 1024;  // 1 KB segments
+  constexpr int A_LD = A_SEG / 4, B_LD = B_SEG / 4;                      // per wave
+  int mt, nt;
+  if (!balanced_tile<kGroupM>(*g.n_tiles, g.N / BN, &mt, &nt)) return;
+  const Tile t = g.tiles[mt];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wid >> 1, wn = wid & 1;
+  const int K = g.K, nk = K / BK;
+  const char *Ag = (const char *)(g.A + (size_t)t.row0 * K * 2);
+  const char *Bg = (const char *)(blob_of(g.bt, t.expert) + g.b_off + (size_t)nt * BN * K * 2);
+
+  __shared__ u32x4 sA[STAGES][BM * 4];
+  __shared__ u32x4 sB[STAGES][BN * 4];
+
+  // this lane's source chunk inside a 1 KB segment (16 rows x 4 chunks)
+  const int seg_row = lane >> 2;
+  const int src_chunk = (lane & 3) ^ ((seg_row >> 2) & 3);
+  const uint32_t lane_off = (uint32_t)seg_row * K * 2 + src_chunk * 16;
+
+#define CEP_DMA_STAGE(kt)                                                              \
+  {                                                                                    \
+    const int buf_ = (kt) % STAGES;                                                    \
+    _Pragma("unroll") for (int i = 0; i < A_LD; ++i) {                                 \
+      const int seg = wid * A_LD + i;                                                  \
+      dma16(Ag + (size_t)seg * 16 * K * 2 + (size_t)(kt) * BK * 2 + lane_off,          \
+            __builtin_amdgcn_readfirstlane(lds_offset(&sA[buf_][seg * 64])));          \
+    }                                                                                  \
+    _Pragma("unroll") for (int i = 0; i < B_LD; ++i) {                                 \
+      const int seg = wid * B_LD + i;                                                  \
+      dma16(Bg + (size_t)seg * 16 * K * 2 + (size_t)(kt) * BK * 2 + lane_off,          \
+            __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf_][seg * 64])));          \
+    }                                                                                  \
+  }
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x16{};
+
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nk) CEP_DMA_STAGE(s);
+
+  // operand slot offsets: row r = (wave base) + i*32 + lane%32 has
+  // (r >> 2) & 3 == ((lane & 31) >> 2) & 3 for every fragment
+  const int rsw = ((lane & 31) >> 2) & 3;
+  for (int kt = 0; kt < nk; ++kt) {
+    // this thread's loads of step kt are done when at most the loads of the
+    // steps issued after it are still outstanding
+    static_assert(STAGES == 4, "the waits below assume two later steps in flight");
+    if (kt + 2 < nk)
+      wait_vmcnt<2 * (A_LD + B_LD)>();
+    else if (kt + 1 < nk)
+      wait_vmcnt<A_LD + B_LD>();
+    else
+      wait_vmcnt<0>();
+    // every wave's loads of step kt landed; step kt-1 fully consumed.  A bare
+    // barrier: __syncthreads() would also drain the later steps' loads.
+    __builtin_amdgcn_s_barrier();
+    if (kt + STAGES - 1 < nk) CEP_DMA_STAGE(kt + STAGES - 1);
+    const int cur = kt % STAGES;
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int slot = (kk * 2 + (lane >> 5)) ^ rsw;
+      bf16x8 a[FM], b[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        a[i] = __builtin_bit_cast(bf16x8, sA[cur][(wm * WM + i * 32 + (lane & 31)) * 4 + slot]);
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        b[j] = __builtin_bit_cast(bf16x8, sB[cur][(wn * WN + j * 32 + (lane & 31)) * 4 + slot]);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  }
+#undef CEP_DMA_STAGE
+
+  // 32x32 accumulator layout: lane l, element r -> column l%32,
+  // row 8*(r/4) + 4*(l/32) + r%4.
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rt = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      if (rt >= t.rows) continue;
+      const size_t row = (size_t)t.row0 + rt;
+      if (SWIGLU) {
+        __bf16 *H = (__bf16 *)g.out;
+        const size_t hbase = row * (g.N / 2) + (nt * BN + wn * WN) / 2 + (lane & 31);
+#pragma unroll
+        for (int j2 = 0; j2 < FN / 2; ++j2)
+          H[hbase + j2 * 32] = (__bf16)silu_mul(acc[i][2 * j2][r], acc[i][2 * j2 + 1][r]);
+      } else {
+        const float w = g.wrow[row];
+        float *Y = (float *)g.out;
+        const size_t ybase = row * g.N + nt * BN + wn * WN + (lane & 31);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) Y[ybase + j * 32] = acc[i][j][r] * w;
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- bf16
-// 128x128 output tile, K step 64, 4 waves as 2x2, each wave 64x64 built from
-// 2x2 v_mfma_f32_32x32x16_bf16.  LDS rows are 64 bf16 (eight 16-byte chunks),
-// chunk c of row r stored at c ^ (r & 7) so both the global->LDS stores and
-// the MFMA operand reads (32 rows, one chunk each) are conflict-free.
-template <bool SWIGLU>
-__global__ __launch_bounds__(256) void k_gemm_bf16(GemmArgs g) {
+// BM x BN output tile (256 x 256), K step 64, 4 waves as 2x2, each wave
+// (BM/2) x (BN/2) built from v_mfma_f32_32x32x16_bf16 fragments, so each
+// 16-byte LDS read feeds BM/64 (or BN/64) MFMAs.  LDS holds two K steps of
+// A and B (double buffer, one barrier per step); the next step's tiles are
+// fetched into registers while the current step computes, then written to
+// the other buffer.  LDS rows are 64 bf16 (eight 16-byte chunks), chunk c of
+// row r stored at c ^ (r & 7): the global->LDS stores and the MFMA operand
+// reads (32 rows, one chunk each) are conflict-free.
+template <int BM, int BN, bool SWIGLU>
+__global__ __launch_bounds__(256, 1) void k_gemm_bf16(GemmArgs g) {
+  constexpr int BK = 64;
+  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int FM = WM / 32, FN = WN / 32;
+  constexpr int AV = BM * BK / 8 / 256, BV = BN * BK / 8 / 256;  // 16-byte loads per thread
   const int L = xcd_remap(blockIdx.x, gridDim.x);
   const int mt = L % g.max_tiles, nt = L / g.max_tiles;
   if (mt >= *g.n_tiles) return;
@@ -65,80 +265,97 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(GemmArgs g) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wid >> 1, wn = wid & 1;
-  const int K = g.K, kv = K / 8;
+  const int K = g.K, kv = K / 8, nk = K / BK;
   const u32x4 *Ag = (const u32x4 *)(g.A + (size_t)t.row0 * K * 2);
-  const u32x4 *Bg = (const u32x4 *)(blob_of(g.bt, t.expert) + g.b_off + (size_t)nt * 128 * K * 2);
+  const u32x4 *Bg = (const u32x4 *)(blob_of(g.bt, t.expert) + g.b_off + (size_t)nt * BN * K * 2);
 
-  __shared__ u32x4 sA[128 * 8];
-  __shared__ u32x4 sB[128 * 8];
-  u32x4 ra[4], rb[4];
-#define CEP_BF16_GLOAD(k0)                                   \
-  _Pragma("unroll") for (int i = 0; i < 4; ++i) {            \
-    const int v = tid + 256 * i, row = v >> 3, ch = v & 7;   \
-    ra[i] = Ag[(size_t)row * kv + ((k0) >> 3) + ch];         \
-    rb[i] = Bg[(size_t)row * kv + ((k0) >> 3) + ch];         \
+  __shared__ u32x4 sA[2][BM * 8];
+  __shared__ u32x4 sB[2][BN * 8];
+  u32x4 ra[AV], rb[BV];
+#define CEP_BF16_GLOAD(kt)                                              \
+  _Pragma("unroll") for (int i = 0; i < AV; ++i) {                      \
+    const int v = tid + 256 * i, row = v >> 3, ch = v & 7;              \
+    ra[i] = Ag[(size_t)row * kv + (kt) * 8 + ch];                       \
+  }                                                                     \
+  _Pragma("unroll") for (int i = 0; i < BV; ++i) {                      \
+    const int v = tid + 256 * i, row = v >> 3, ch = v & 7;              \
+    rb[i] = Bg[(size_t)row * kv + (kt) * 8 + ch];                       \
   }
-  f32x16 acc[2][2];
+#define CEP_BF16_LSTORE(buf)                                            \
+  _Pragma("unroll") for (int i = 0; i < AV; ++i) {                      \
+    const int v = tid + 256 * i, row = v >> 3, ch = v & 7;              \
+    sA[buf][row * 8 + (ch ^ (row & 7))] = ra[i];                        \
+  }                                                                     \
+  _Pragma("unroll") for (int i = 0; i < BV; ++i) {                      \
+    const int v = tid + 256 * i, row = v >> 3, ch = v & 7;              \
+    sB[buf][row * 8 + (ch ^ (row & 7))] = rb[i];                        \
+  }
+
+  f32x16 acc[FM][FN];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x16{};
 
   CEP_BF16_GLOAD(0);
-  for (int k0 = 0; k0 < K; k0 += 64) {
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int v = tid + 256 * i, row = v >> 3, ch = v & 7;
-      sA[row * 8 + (ch ^ (row & 7))] = ra[i];
-      sB[row * 8 + (ch ^ (row & 7))] = rb[i];
-    }
-    __syncthreads();
-    if (k0 + 64 < K) {
-      CEP_BF16_GLOAD(k0 + 64);
+  CEP_BF16_LSTORE(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) {
+      CEP_BF16_GLOAD(kt + 1);
     }
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      bf16x8 a[2], b[2];
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      bf16x8 a[FM], b[FN];
       const int ch = kk * 2 + (lane >> 5);
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int row = wm * 64 + i * 32 + (lane & 31);
-        a[i] = __builtin_bit_cast(bf16x8, sA[row * 8 + (ch ^ (row & 7))]);
+      for (int i = 0; i < FM; ++i) {
+        const int row = wm * WM + i * 32 + (lane & 31);
+        a[i] = __builtin_bit_cast(bf16x8, sA[cur][row * 8 + (ch ^ (row & 7))]);
       }
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int row = wn * 64 + j * 32 + (lane & 31);
-        b[j] = __builtin_bit_cast(bf16x8, sB[row * 8 + (ch ^ (row & 7))]);
+      for (int j = 0; j < FN; ++j) {
+        const int row = wn * WN + j * 32 + (lane & 31);
+        b[j] = __builtin_bit_cast(bf16x8, sB[cur][row * 8 + (ch ^ (row & 7))]);
       }
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
+    if (kt + 1 < nk) {
+      CEP_BF16_LSTORE(cur ^ 1);
+    }
+    __syncthreads();
   }
+#undef CEP_BF16_GLOAD
+#undef CEP_BF16_LSTORE
 
   // 32x32 accumulator layout: lane l, element r -> column l%32,
   // row 8*(r/4) + 4*(l/32) + r%4.
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < FM; ++i) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int rt = wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      const int rt = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
       if (rt >= t.rows) continue;
       const size_t row = (size_t)t.row0 + rt;
       if (SWIGLU) {
-        // wave columns: [gate 32 | up 32] of h columns nt*64 + wn*32 + [0, 32)
-        const float h = silu_mul(acc[i][0][r], acc[i][1][r]);
+        // fragment pairs (2*j2, 2*j2+1) are the gate and up columns of h
+        // columns (nt*BN + wn*WN)/2 + j2*32 + [0, 32)
         __bf16 *H = (__bf16 *)g.out;
-        H[row * (g.N / 2) + nt * 64 + wn * 32 + (lane & 31)] = (__bf16)h;
+        const size_t hbase = row * (g.N / 2) + (nt * BN + wn * WN) / 2 + (lane & 31);
+#pragma unroll
+        for (int j2 = 0; j2 < FN / 2; ++j2)
+          H[hbase + j2 * 32] = (__bf16)silu_mul(acc[i][2 * j2][r], acc[i][2 * j2 + 1][r]);
       } else {
         const float w = g.wrow[row];
         float *Y = (float *)g.out;
+        const size_t ybase = row * g.N + nt * BN + wn * WN + (lane & 31);
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-          Y[row * g.N + nt * 128 + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r] * w;
+        for (int j = 0; j < FN; ++j) Y[ybase + j * 32] = acc[i][j][r] * w;
       }
     }
   }
@@ -337,8 +554,9 @@ hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_til
     const int grid = grid_tiles * (g.N / 256);
     hipLaunchKernelGGL(k_gemm_fp8<true>, dim3(grid), dim3(256), 0, s, g);
   } else {
-    const int grid = grid_tiles * (g.N / 128);
-    hipLaunchKernelGGL(k_gemm_bf16<true>, dim3(grid), dim3(256), 0, s, g);
+    const int grid = balanced_grid(grid_tiles, kGroupM, g.N / kBf16TileN);
+    hipLaunchKernelGGL((k_gemm_bf16_dma<kBf16TileM, kBf16TileN, true>), dim3(grid), dim3(256), 0,
+                       s, g);
   }
   return hipGetLastError();
 }
@@ -360,8 +578,9 @@ hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_til
     const int grid = grid_tiles * (g.N / 256);
     hipLaunchKernelGGL(k_gemm_fp8<false>, dim3(grid), dim3(256), 0, s, g);
   } else {
-    const int grid = grid_tiles * (g.N / 128);
-    hipLaunchKernelGGL(k_gemm_bf16<false>, dim3(grid), dim3(256), 0, s, g);
+    const int grid = balanced_grid(grid_tiles, kGroupM, g.N / kBf16TileN);
+    hipLaunchKernelGGL((k_gemm_bf16_dma<kBf16TileM, kBf16TileN, false>), dim3(grid), dim3(256), 0,
+                       s, g);
   }
   return hipGetLastError();
 }

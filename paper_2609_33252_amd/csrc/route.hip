@@ -12,6 +12,8 @@
 
 #include <hip/hip_bf16.h>
 
+#include <algorithm>
+
 namespace cep {
 namespace {
 
@@ -84,7 +86,7 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_count(const int32_t *__
 // One block: per-expert totals, unpadded and tile-aligned exclusive scans,
 // the first grouped row of every routing block's pairs of every expert, and
 // the M-tile lists of the resident and the fetched experts.
-__global__ __launch_bounds__(256) void k_route_scan(Scratch sc, int n_blocks, int E,
+__global__ __launch_bounds__(256) void k_route_scan(Scratch sc, int n_blocks, int E, int align,
                                                     int expected_pairs, int max_mpad,
                                                     int max_tiles, uint64_t fetched_mask,
                                                     uint32_t *err) {
@@ -105,9 +107,9 @@ __global__ __launch_bounds__(256) void k_route_scan(Scratch sc, int n_blocks, in
       s_pad[e] = op;
       const int which = (int)((fetched_mask >> e) & 1);
       s_tile0[e] = t0[which];
-      t0[which] += (s_cnt[e] + kAlign - 1) / kAlign;
+      t0[which] += (s_cnt[e] + align - 1) / align;
       o += s_cnt[e];
-      op += (s_cnt[e] + kAlign - 1) / kAlign * kAlign;
+      op += (s_cnt[e] + align - 1) / align * align;
     }
     s_off[E] = o;
     s_pad[E] = op;
@@ -129,28 +131,29 @@ __global__ __launch_bounds__(256) void k_route_scan(Scratch sc, int n_blocks, in
       sc.blk_base[b * E + tid] = run;
       run += sc.blk_cnt[b * E + tid];
     }
+    // padding rows of this expert's last tile carry no pair
+    for (int r = s_pad[tid] + s_cnt[tid]; r < s_pad[tid + 1] && r < max_mpad; ++r) sc.perm[r] = -1;
     const int which = (int)((fetched_mask >> tid) & 1);
     Tile *list = sc.tiles + (size_t)which * max_tiles;
-    const int nt = (s_cnt[tid] + kAlign - 1) / kAlign;
+    const int nt = (s_cnt[tid] + align - 1) / align;
     for (int q = 0; q < nt; ++q) {
       const int ti = s_tile0[tid] + q;
-      const int row0 = s_pad[tid] + q * kAlign;
-      if (ti >= max_tiles || row0 + kAlign > max_mpad) break;
-      list[ti] = Tile{tid, row0, min(kAlign, s_cnt[tid] - q * kAlign), 0};
+      const int row0 = s_pad[tid] + q * align;
+      if (ti >= max_tiles || row0 + align > max_mpad) break;
+      list[ti] = Tile{tid, row0, min(align, s_cnt[tid] - q * align), 0};
     }
   }
 }
 
-// ------------------------------------------------------- permute + pack
+// -------------------------------------------------------------- permute
 // Same block decomposition as k_route_count.  Each pair's grouped row is the
 // block's first row for its expert, plus pairs of that expert in earlier
 // rounds of this block, in earlier waves of this round, and in lower lanes
-// of this wave (stable in canonical order).  The pair's input row is then
-// copied (bf16), converted (f32 -> bf16) or quantised (e4m3 with one scale
-// per 128 channels) into its grouped row.
-template <int XMODE>  // 0: bf16 -> bf16, 1: f32 -> bf16, 2: bf16 -> e4m3 + scales
+// of this wave (stable in canonical order).  Writes the inverse map (grouped
+// row of each pair), the permutation (pair of each grouped row) and the
+// routing coefficient of each grouped row.
 __global__ __launch_bounds__(kRouteThreads) void k_route_scatter(Arena a, Scratch sc, int row0,
-                                                                 int n_flat, int k, int E, int d,
+                                                                 int n_flat, int k, int E,
                                                                  int max_mpad) {
   __shared__ int running[kMaxExperts];
   __shared__ int wave_cnt[kRouteThreads / 64][kMaxExperts];
@@ -168,7 +171,6 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_scatter(Arena a, Scratc
     const int id = p < n_flat ? ids[p] : -1;
     int rank = 0;
     uint64_t active = __ballot(id >= 0);
-    const uint64_t valid = active;
     while (active) {
       const int leader = __builtin_ctzll(active);
       const int e = __shfl(id, leader);
@@ -199,60 +201,70 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_scatter(Arena a, Scratc
       sc.perm[pos] = p;
       sc.wrow[pos] = wts[p];
     }
-    // copy the rows of this wave's valid pairs, one row per step, whole wave
-    const char *src_row = (id >= 0) ? (const char *)a.xrow[row0 + p / k] : nullptr;
-    uint64_t todo = valid & __ballot(pos >= 0);
-    while (todo) {
-      const int j = __builtin_ctzll(todo);
-      todo &= todo - 1;
-      const int dpos = __shfl(pos, j);
-      const uint64_t sp = (uint64_t)__shfl((long long)(uintptr_t)src_row, j);
-      const char *src = (const char *)(uintptr_t)sp;
-      if (XMODE == 0) {
-        const uint4 *s4 = (const uint4 *)src;
-        uint4 *d4 = (uint4 *)((char *)sc.xg + (size_t)dpos * d * 2);
-        for (int c = lane; c < d / 8; c += 64) d4[c] = s4[c];
-      } else if (XMODE == 1) {
-        const float4 *s4 = (const float4 *)src;
-        uint4 *d4 = (uint4 *)((char *)sc.xg + (size_t)dpos * d * 2);
-        for (int c = lane; c < d / 8; c += 64) {
-          const float4 lo = s4[2 * c], hi = s4[2 * c + 1];
-          union { __bf16 h[8]; uint4 u; } o;
-          o.h[0] = (__bf16)lo.x; o.h[1] = (__bf16)lo.y; o.h[2] = (__bf16)lo.z; o.h[3] = (__bf16)lo.w;
-          o.h[4] = (__bf16)hi.x; o.h[5] = (__bf16)hi.y; o.h[6] = (__bf16)hi.z; o.h[7] = (__bf16)hi.w;
-          d4[c] = o.u;
+  }
+}
+
+// ----------------------------------------------------------------- pack
+// One wave per grouped row (kPackRows rows per block): the pair's input row
+// is copied (bf16), converted (f32 -> bf16) or quantised (e4m3, one scale per
+// 128 channels) into its grouped row.  Padding rows (no pair) are skipped.
+constexpr int kPackRows = 8;
+
+template <int XMODE>  // 0: bf16 -> bf16, 1: f32 -> bf16, 2: bf16 -> e4m3 + scales
+__global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0, int k, int E,
+                                                   int d, int n_rows_pad) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int end = min(n_rows_pad, sc.off_pad[E]);
+  for (int q = 0; q < kPackRows / 4; ++q) {
+    const int pos = blockIdx.x * kPackRows + q * 4 + wid;
+    if (pos >= end) return;
+    const int p = sc.perm[pos];
+    if (p < 0) continue;
+    const char *src = (const char *)a.xrow[row0 + p / k];
+    if (XMODE == 0) {
+      const uint4 *s4 = (const uint4 *)src;
+      uint4 *d4 = (uint4 *)((char *)sc.xg + (size_t)pos * d * 2);
+      for (int c = lane; c < d / 8; c += 64) d4[c] = s4[c];
+    } else if (XMODE == 1) {
+      const float4 *s4 = (const float4 *)src;
+      uint4 *d4 = (uint4 *)((char *)sc.xg + (size_t)pos * d * 2);
+      for (int c = lane; c < d / 8; c += 64) {
+        const float4 lo = s4[2 * c], hi = s4[2 * c + 1];
+        union { __bf16 h[8]; uint4 u; } o;
+        o.h[0] = (__bf16)lo.x; o.h[1] = (__bf16)lo.y; o.h[2] = (__bf16)lo.z; o.h[3] = (__bf16)lo.w;
+        o.h[4] = (__bf16)hi.x; o.h[5] = (__bf16)hi.y; o.h[6] = (__bf16)hi.z; o.h[7] = (__bf16)hi.w;
+        d4[c] = o.u;
+      }
+    } else {
+      // 16 lanes x 8 channels = one 128-channel scale block
+      const uint4 *s4 = (const uint4 *)src;
+      uint8_t *dq = (uint8_t *)sc.xg + (size_t)pos * d;
+      float *ds = sc.xs + (size_t)pos * (d / 128);
+      for (int c0 = 0; c0 < d; c0 += 512) {
+        const int c = c0 + lane * 8;
+        const bool ok = c < d;
+        float v[8];
+        float amax = 0.f;
+        if (ok) {
+          union { uint4 u; __bf16 h[8]; } in;
+          in.u = s4[c / 8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            v[j] = (float)in.h[j];
+            amax = fmaxf(amax, fabsf(v[j]));
+          }
         }
-      } else {
-        // 16 lanes x 8 channels = one 128-channel scale block
-        const uint4 *s4 = (const uint4 *)src;
-        uint8_t *dq = (uint8_t *)sc.xg + (size_t)dpos * d;
-        float *ds = sc.xs + (size_t)dpos * (d / 128);
-        for (int c0 = 0; c0 < d; c0 += 512) {
-          const int c = c0 + lane * 8;
-          const bool ok = c < d;
-          float v[8];
-          float amax = 0.f;
-          if (ok) {
-            union { uint4 u; __bf16 h[8]; } in;
-            in.u = s4[c / 8];
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
-              v[q] = (float)in.h[q];
-              amax = fmaxf(amax, fabsf(v[q]));
-            }
-          }
-#pragma unroll
-          for (int sh = 1; sh < 16; sh <<= 1) amax = fmaxf(amax, __shfl_xor(amax, sh, 16));
-          const float scale = amax > 0.f ? amax / 448.0f : 1.0f;
-          if (ok) {
-            int lo = 0, hi = 0;
-            lo = __builtin_amdgcn_cvt_pk_fp8_f32(v[0] / scale, v[1] / scale, lo, false);
-            lo = __builtin_amdgcn_cvt_pk_fp8_f32(v[2] / scale, v[3] / scale, lo, true);
-            hi = __builtin_amdgcn_cvt_pk_fp8_f32(v[4] / scale, v[5] / scale, hi, false);
-            hi = __builtin_amdgcn_cvt_pk_fp8_f32(v[6] / scale, v[7] / scale, hi, true);
-            *(uint2 *)(dq + c) = make_uint2((uint32_t)lo, (uint32_t)hi);
-            if ((lane & 15) == 0) ds[c / 128] = scale;
-          }
+        for (int sh = 1; sh < 16; sh <<= 1) amax = fmaxf(amax, __shfl_xor(amax, sh, 16));
+        const float scale = amax > 0.f ? amax / 448.0f : 1.0f;
+        if (ok) {
+          int lo = 0, hi = 0;
+          lo = __builtin_amdgcn_cvt_pk_fp8_f32(v[0] / scale, v[1] / scale, lo, false);
+          lo = __builtin_amdgcn_cvt_pk_fp8_f32(v[2] / scale, v[3] / scale, lo, true);
+          hi = __builtin_amdgcn_cvt_pk_fp8_f32(v[4] / scale, v[5] / scale, hi, false);
+          hi = __builtin_amdgcn_cvt_pk_fp8_f32(v[6] / scale, v[7] / scale, hi, true);
+          *(uint2 *)(dq + c) = make_uint2((uint32_t)lo, (uint32_t)hi);
+          if ((lane & 15) == 0) ds[c / 128] = scale;
         }
       }
     }
@@ -386,24 +398,28 @@ hipError_t launch_ingest(const Arena &a, int row0, int n_rows, int k, int E, int
 }
 
 hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int E,
-                        int expected_pairs, int max_mpad, int max_tiles, uint64_t fetched_mask,
-                        int x_dtype, bool fp8, int d, uint32_t *err, hipStream_t s) {
+                        int align, int expected_pairs, int max_mpad, int max_tiles,
+                        uint64_t fetched_mask, int x_dtype, bool fp8, int d, uint32_t *err,
+                        hipStream_t s) {
   const int n_flat = n_rows * k;
   const int nb = (n_flat + kRoutePairs - 1) / kRoutePairs;
   if (nb == 0) return hipSuccess;
   hipLaunchKernelGGL(k_route_count, dim3(nb), dim3(kRouteThreads), 0, s,
                      a.ids + (size_t)row0 * k, n_flat, E, sc.blk_cnt);
-  hipLaunchKernelGGL(k_route_scan, dim3(1), dim3(256), 0, s, sc, nb, E, expected_pairs,
+  hipLaunchKernelGGL(k_route_scan, dim3(1), dim3(256), 0, s, sc, nb, E, align, expected_pairs,
                      max_mpad, max_tiles, fetched_mask, err);
+  hipLaunchKernelGGL(k_route_scatter, dim3(nb), dim3(kRouteThreads), 0, s, a, sc, row0, n_flat,
+                     k, E, max_mpad);
+  // grouped rows: at most every pair plus one partial tile per expert
+  const long long bound = ((long long)(expected_pairs + align - 1) / align + E) * align;
+  const int n_pad = (int)std::min<long long>(bound, max_mpad);
+  const dim3 pgrid((n_pad + kPackRows - 1) / kPackRows);
   if (fp8)
-    hipLaunchKernelGGL(k_route_scatter<2>, dim3(nb), dim3(kRouteThreads), 0, s, a, sc, row0,
-                       n_flat, k, E, d, max_mpad);
+    hipLaunchKernelGGL(k_pack_rows<2>, pgrid, dim3(256), 0, s, a, sc, row0, k, E, d, n_pad);
   else if (x_dtype == 0)
-    hipLaunchKernelGGL(k_route_scatter<1>, dim3(nb), dim3(kRouteThreads), 0, s, a, sc, row0,
-                       n_flat, k, E, d, max_mpad);
+    hipLaunchKernelGGL(k_pack_rows<1>, pgrid, dim3(256), 0, s, a, sc, row0, k, E, d, n_pad);
   else
-    hipLaunchKernelGGL(k_route_scatter<0>, dim3(nb), dim3(kRouteThreads), 0, s, a, sc, row0,
-                       n_flat, k, E, d, max_mpad);
+    hipLaunchKernelGGL(k_pack_rows<0>, pgrid, dim3(256), 0, s, a, sc, row0, k, E, d, n_pad);
   return hipGetLastError();
 }
 

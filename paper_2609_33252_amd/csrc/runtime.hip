@@ -58,6 +58,7 @@ struct cep_ctx {
   Arena arena{};
   int arena_cap = 0;
   uint32_t *d_err = nullptr;
+  int align = 0;  // per-expert row alignment of the grouped layout (GEMM M tile)
   int max_pairs = 0, max_mpad = 0, max_tiles = 0, max_blocks = 0, max_rows = 0;
   hipStream_t ingest = nullptr;
   hipStream_t st[8] = {}, helper[8] = {};
@@ -114,7 +115,7 @@ int fail(cep_ctx *c, int code, const char *fmt, ...) {
 bool valid_config(const cep_config *c, std::string *why) {
   auto bad = [&](const char *m) { *why = m; return false; };
   if (!c) return bad("cfg is NULL");
-  if (c->d_model <= 0 || c->d_model % 128) return bad("d_model must be a positive multiple of 128");
+  if (c->d_model <= 0 || c->d_model % 256) return bad("d_model must be a positive multiple of 256");
   if (c->d_ff <= 0 || c->d_ff % 128) return bad("d_ff must be a positive multiple of 128");
   if (c->n_local_experts < 1 || c->n_local_experts > kMaxExperts) return bad("n_local_experts must be in 1..64");
   if (c->top_k < 1 || c->top_k > kMaxTopK) return bad("top_k must be in 1..16");
@@ -182,8 +183,9 @@ int launch_pending(cep_ctx *c) {
   hipStream_t s = c->st[slot];
   const Scratch &sc = c->sc[slot];
   const int P = b.n_pairs;
-  const int tiles = std::min(c->max_tiles, (P + kAlign - 1) / kAlign + E);
-  b.mpad_bound = std::min(c->max_mpad, tiles * kAlign);
+  const int A = c->align;
+  const int tiles = std::min(c->max_tiles, (P + A - 1) / A + E);
+  b.mpad_bound = std::min(c->max_mpad, tiles * A);
   b.ev_start = timing_event(c);
   b.ev_end = timing_event(c);
   for (hipEvent_t &e : b.ev_phase) e = timing_event(c);
@@ -195,7 +197,7 @@ int launch_pending(cep_ctx *c) {
   HIPCHK(c, hipEventRecord(c->ev_ingest[slot], c->ingest));
   HIPCHK(c, hipStreamWaitEvent(s, c->ev_ingest[slot], 0));
   HIPCHK(c, hipEventRecord(b.ev_start, s));
-  HIPCHK(c, launch_route(c->arena, sc, b.row0, b.n_rows, k, E, P, c->max_mpad, c->max_tiles,
+  HIPCHK(c, launch_route(c->arena, sc, b.row0, b.n_rows, k, E, A, P, c->max_mpad, c->max_tiles,
                          c->fetched_mask, cfg.x_dtype, c->fp8, d, c->d_err, s));
   HIPCHK(c, hipEventRecord(b.ev_phase[0], s));
 
@@ -312,8 +314,9 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
   const long long def_pairs = (long long)c->arena_cap * k;
   c->max_pairs = cfg->max_pairs_per_batch > 0 ? (int)std::min<long long>(cfg->max_pairs_per_batch, def_pairs)
                                               : (int)def_pairs;
-  c->max_tiles = (c->max_pairs + kAlign - 1) / kAlign + E;
-  c->max_mpad = c->max_tiles * kAlign;
+  c->align = gemm_align(c->fp8);
+  c->max_tiles = (c->max_pairs + c->align - 1) / c->align + E;
+  c->max_mpad = c->max_tiles * c->align;
   c->max_blocks = (int)(((long long)c->max_rows * k + kRoutePairs - 1) / kRoutePairs);
   c->policy = CEP_WAIT_ALL;
   c->n_streams = cfg->n_streams;
@@ -556,7 +559,7 @@ CEP_API int cep_get_batch_routing(cep_ctx *c, int batch, int *align, int *n_pair
   if (batch < 0 || batch >= (int)c->batches.size()) return fail(c, CEP_EINVAL, "no batch %d", batch);
   const BatchRec &b = c->batches[batch];
   const int E = c->cfg.n_local_experts, k = c->cfg.top_k;
-  if (align) *align = kAlign;
+  if (align) *align = c->align;
   if (n_pairs) *n_pairs = b.n_pairs;
   if (n_rows) *n_rows = b.n_rows;
   if (n_chunks) *n_chunks = b.n_chunks;
