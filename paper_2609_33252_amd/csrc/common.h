@@ -57,8 +57,19 @@ struct BlobLayout {
 
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
-// Per-expert row alignment A of the grouped layout = M tile of the GEMMs.
-inline int gemm_align(bool fp8) { return fp8 ? kFp8TileM : kBf16TileM; }
+constexpr int kBf16SmallTileM = 64;  // bf16 tile for batches with few rows per expert
+
+// Per-expert row alignment A of one batch's grouped layout = M tile of the
+// GEMMs that run it.  bf16 batches with fewer than one large tile of rows
+// per local expert on average use the small tile: the GEMMs then stream the
+// weights with four times as many workgroups.  Both bf16 tiles accumulate K
+// in the same order with the same MFMA, so results do not depend on it.
+inline int batch_align(bool fp8, int pairs, int n_experts) {
+  if (fp8) return kFp8TileM;
+  return pairs >= kBf16TileM * n_experts ? kBf16TileM : kBf16SmallTileM;
+}
+constexpr int kMinAlign = 64;
+constexpr int kMaxAlign = 256;
 
 inline BlobLayout blob_layout(int d, int I, bool fp8) {
   BlobLayout L{};
@@ -128,10 +139,11 @@ hipError_t launch_combine(const Arena &a, const Scratch &sc, int row0, int n_row
 
 // grouped GEMMs over tile list `which` (0 resident, 1 fetched) of a scratch
 // whose lists hold list_cap tiles each; the grid covers grid_tiles M tiles
-hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles,
+// with M tile `align` (the batch's row alignment)
+hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles, int align,
                         const BlobTable &bt, const BlobLayout &L, bool fp8, int d, int I,
                         hipStream_t s);
-hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles,
+hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles, int align,
                         const BlobTable &bt, const BlobLayout &L, bool fp8, int d, int I,
                         hipStream_t s);
 

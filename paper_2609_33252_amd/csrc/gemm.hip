@@ -537,7 +537,27 @@ GemmArgs base_args(const Scratch &sc, int which, int list_cap, int grid_tiles,
 
 }  // namespace
 
-hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles,
+template <bool SWIGLU>
+hipError_t launch_any(const GemmArgs &g, int grid_tiles, int align, bool fp8, hipStream_t s) {
+  if (fp8) {
+    if (align != kFp8TileM) return hipErrorInvalidValue;
+    const int grid = grid_tiles * (g.N / 256);
+    hipLaunchKernelGGL(k_gemm_fp8<SWIGLU>, dim3(grid), dim3(256), 0, s, g);
+  } else if (align == kBf16TileM) {
+    const int grid = balanced_grid(grid_tiles, kGroupM, g.N / kBf16TileN);
+    hipLaunchKernelGGL((k_gemm_bf16_dma<kBf16TileM, kBf16TileN, SWIGLU>), dim3(grid), dim3(256),
+                       0, s, g);
+  } else if (align == kBf16SmallTileM) {
+    const int grid = balanced_grid(grid_tiles, kGroupM, g.N / kBf16TileN);
+    hipLaunchKernelGGL((k_gemm_bf16_dma<kBf16SmallTileM, kBf16TileN, SWIGLU>), dim3(grid),
+                       dim3(256), 0, s, g);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles, int align,
                         const BlobTable &bt, const BlobLayout &L, bool fp8, int d, int I,
                         hipStream_t s) {
   if (grid_tiles <= 0) return hipSuccess;
@@ -550,18 +570,10 @@ hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_til
   g.bs_off = L.s1_off;
   g.out = sc.h;
   g.out_s = sc.hs;
-  if (fp8) {
-    const int grid = grid_tiles * (g.N / 256);
-    hipLaunchKernelGGL(k_gemm_fp8<true>, dim3(grid), dim3(256), 0, s, g);
-  } else {
-    const int grid = balanced_grid(grid_tiles, kGroupM, g.N / kBf16TileN);
-    hipLaunchKernelGGL((k_gemm_bf16_dma<kBf16TileM, kBf16TileN, true>), dim3(grid), dim3(256), 0,
-                       s, g);
-  }
-  return hipGetLastError();
+  return launch_any<true>(g, grid_tiles, align, fp8, s);
 }
 
-hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles,
+hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles, int align,
                         const BlobTable &bt, const BlobLayout &L, bool fp8, int d, int I,
                         hipStream_t s) {
   if (grid_tiles <= 0) return hipSuccess;
@@ -574,15 +586,7 @@ hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_til
   g.bs_off = L.s2_off;
   g.out = sc.y;
   g.wrow = sc.wrow;
-  if (fp8) {
-    const int grid = grid_tiles * (g.N / 256);
-    hipLaunchKernelGGL(k_gemm_fp8<false>, dim3(grid), dim3(256), 0, s, g);
-  } else {
-    const int grid = balanced_grid(grid_tiles, kGroupM, g.N / kBf16TileN);
-    hipLaunchKernelGGL((k_gemm_bf16_dma<kBf16TileM, kBf16TileN, false>), dim3(grid), dim3(256), 0,
-                       s, g);
-  }
-  return hipGetLastError();
+  return launch_any<false>(g, grid_tiles, align, fp8, s);
 }
 
 }  // namespace cep

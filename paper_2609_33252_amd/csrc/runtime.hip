@@ -32,6 +32,7 @@ struct BatchRec {
   int n_chunks;
   int row0, n_rows, n_pairs;
   int slot;
+  int align;  // per-expert row alignment of the grouped layout (GEMM M tile)
   bool helper;
   hipEvent_t ev_start, ev_end;
   // on the batch stream after: routing, GEMM1, GEMM2, combine
@@ -58,7 +59,6 @@ struct cep_ctx {
   Arena arena{};
   int arena_cap = 0;
   uint32_t *d_err = nullptr;
-  int align = 0;  // per-expert row alignment of the grouped layout (GEMM M tile)
   int max_pairs = 0, max_mpad = 0, max_tiles = 0, max_blocks = 0, max_rows = 0;
   hipStream_t ingest = nullptr;
   hipStream_t st[8] = {}, helper[8] = {};
@@ -183,7 +183,8 @@ int launch_pending(cep_ctx *c) {
   hipStream_t s = c->st[slot];
   const Scratch &sc = c->sc[slot];
   const int P = b.n_pairs;
-  const int A = c->align;
+  const int A = batch_align(c->fp8, b.n_pairs, E);
+  b.align = A;
   const int tiles = std::min(c->max_tiles, (P + A - 1) / A + E);
   b.mpad_bound = std::min(c->max_mpad, tiles * A);
   b.ev_start = timing_event(c);
@@ -209,13 +210,13 @@ int launch_pending(cep_ctx *c) {
     HIPCHK(c, hipEventRecord(c->ev_routed[slot], s));
     HIPCHK(c, hipStreamWaitEvent(h, c->ev_routed[slot], 0));
     HIPCHK(c, hipStreamWaitEvent(h, c->ev_fetch_ready, 0));
-    HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, bt, c->L, c->fp8, d, I, h));
-    HIPCHK(c, launch_gemm2(sc, 1, c->max_tiles, tiles, bt, c->L, c->fp8, d, I, h));
+    HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, A, bt, c->L, c->fp8, d, I, h));
+    HIPCHK(c, launch_gemm2(sc, 1, c->max_tiles, tiles, A, bt, c->L, c->fp8, d, I, h));
     HIPCHK(c, hipEventRecord(c->ev_helper[slot], h));
   }
-  HIPCHK(c, launch_gemm1(sc, 0, c->max_tiles, tiles, bt, c->L, c->fp8, d, I, s));
+  HIPCHK(c, launch_gemm1(sc, 0, c->max_tiles, tiles, A, bt, c->L, c->fp8, d, I, s));
   HIPCHK(c, hipEventRecord(b.ev_phase[1], s));
-  HIPCHK(c, launch_gemm2(sc, 0, c->max_tiles, tiles, bt, c->L, c->fp8, d, I, s));
+  HIPCHK(c, launch_gemm2(sc, 0, c->max_tiles, tiles, A, bt, c->L, c->fp8, d, I, s));
   HIPCHK(c, hipEventRecord(b.ev_phase[2], s));
   if (b.helper) HIPCHK(c, hipStreamWaitEvent(s, c->ev_helper[slot], 0));
   HIPCHK(c, launch_combine(c->arena, sc, b.row0, b.n_rows, k, d, c->out, s));
@@ -314,9 +315,10 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
   const long long def_pairs = (long long)c->arena_cap * k;
   c->max_pairs = cfg->max_pairs_per_batch > 0 ? (int)std::min<long long>(cfg->max_pairs_per_batch, def_pairs)
                                               : (int)def_pairs;
-  c->align = gemm_align(c->fp8);
-  c->max_tiles = (c->max_pairs + c->align - 1) / c->align + E;
-  c->max_mpad = c->max_tiles * c->align;
+  // capacities cover every batch alignment: most tiles with the smallest,
+  // most padded rows with the largest
+  c->max_tiles = (c->max_pairs + kMinAlign - 1) / kMinAlign + E;
+  c->max_mpad = (int)align_up((size_t)c->max_pairs, kMaxAlign) + kMaxAlign * (E + 1);
   c->max_blocks = (int)(((long long)c->max_rows * k + kRoutePairs - 1) / kRoutePairs);
   c->policy = CEP_WAIT_ALL;
   c->n_streams = cfg->n_streams;
@@ -559,7 +561,7 @@ CEP_API int cep_get_batch_routing(cep_ctx *c, int batch, int *align, int *n_pair
   if (batch < 0 || batch >= (int)c->batches.size()) return fail(c, CEP_EINVAL, "no batch %d", batch);
   const BatchRec &b = c->batches[batch];
   const int E = c->cfg.n_local_experts, k = c->cfg.top_k;
-  if (align) *align = c->align;
+  if (align) *align = b.align;
   if (n_pairs) *n_pairs = b.n_pairs;
   if (n_rows) *n_rows = b.n_rows;
   if (n_chunks) *n_chunks = b.n_chunks;

@@ -189,6 +189,27 @@ def test_chunking_order_policy_streams_invariance_bitwise():
         assert np.array_equal(o, outs[0])
 
 
+def test_large_and_small_m_tiles_agree_bitwise():
+    # one wait-all batch has >= 256 rows per expert (256-row M tile); single
+    # chunks have ~125 (64-row M tile): same K order, same bits
+    wl = W.generate("sync_d4096", 1, T=1024)
+    assert wl.n_pairs >= 256 * wl.cfg["E"]
+    assert max(wl.chunk_pairs(c) for c in wl.chunks) < 256 * wl.cfg["E"]
+    run = harness.Runner(wl, n_streams=2, record_routing=True)
+    run.run(policy=cep.CEP_WAIT_ALL)
+    a = _out(run)
+    m = cep.cep_get_batch_routing(run.ctx, 0, wl.cfg["E"], wl.cfg["k"])
+    assert m["align"] == 256
+    run.out.zero_()
+    run.run(policy=cep.CEP_PER_CHUNK, n_streams=2)
+    b = _out(run)
+    m = cep.cep_get_batch_routing(run.ctx, 0, wl.cfg["E"], wl.cfg["k"])
+    assert m["align"] == 64
+    run.close()
+    assert np.array_equal(a, b)
+    U.compare(wl, a, U.reference(wl))
+
+
 def test_fetched_experts_equal_resident_bitwise():
     wl = W.generate("fp8_fetch_d6144", 0, T=256, cpr=2)
     a = harness.Runner(wl, n_streams=2, use_fetch=True)
