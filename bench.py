@@ -88,6 +88,42 @@ def cpu_baseline(wl, budget_s=12.0):
                       f"float64 numpy, {t_total:.1f} s"}
 
 
+def sweep(args):
+    """Timed replay of a streaming workload under each launch policy: one
+    JSON line per policy (mean over --steps layers after --warmup)."""
+    import torch
+    from paper_2609_33252_amd import cep, harness, streaming, workload as W
+
+    wl = W.generate(args.workload, 0)
+    c = wl.cfg
+    run = harness.Runner(wl, n_streams=4)
+    flops = 6.0 * c["d"] * c["I"] * run.n_pairs
+    plan = [("wait_all", 1, 1), ("per_chunk", 1, 1), ("per_chunk", 1, 4)]
+    thetas = [int(t) for t in args.thetas.split(",")]
+    plan += [("threshold", t, s) for t in thetas for s in (1, 4)]
+    base = None
+    for name, theta, streams in plan:
+        pol = POLICIES[name]
+        res = []
+        for i in range(args.warmup + args.steps):
+            run.run(policy=pol, theta=theta, n_streams=streams, timed=True,
+                    time_scale=args.time_scale)
+            torch.cuda.synchronize()
+            if i >= args.warmup:
+                res.append(streaming.layer_metrics(run.stats(), flops))
+        m = streaming.mean_metrics(res)
+        if name == "wait_all":
+            base = m
+        line = {"workload": args.workload, "policy": name, "theta": theta, "streams": streams,
+                "time_scale": args.time_scale, "local_pairs": run.n_pairs, **m}
+        if base and m.get("busy_tflops") and base.get("busy_tflops"):
+            line["ffn_efficiency_vs_wait_all"] = m["busy_tflops"] / base["busy_tflops"]
+            line["exposed_tail_vs_wait_all"] = m["exposed_tail_ms"] / base["exposed_tail_ms"]
+        print(json.dumps(line), flush=True)
+    cep.cep_get_status(run.ctx)
+    run.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -100,7 +136,20 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run device-to-device copies of MIB MiB (counter calibration)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="timed-arrival replay under every launch policy (one JSON line each)")
+    ap.add_argument("--thetas", default="32,64,128,256,512,1024,2048,4096")
+    ap.add_argument("--time-scale", type=float, default=1.0,
+                    help="scale of the arrival schedule in --sweep (1 = as generated)")
     args = ap.parse_args()
+    if args.sweep:
+        if args.gpus != 1:
+            print("bench.py runs on one GPU only", file=sys.stderr)
+            sys.exit(2)
+        if args.workload == "sync_d4096":
+            args.workload = "zipf_imbalanced_d7168"
+        sweep(args)
+        return
     if args.calibrate_copy:
         import torch
         n = args.calibrate_copy << 20

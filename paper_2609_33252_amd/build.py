@@ -18,7 +18,7 @@ OUT = os.path.join(HERE, "libcep.so")
 OBJ = os.path.join(HERE, "_build")
 ARCH = "gfx950"
 
-SOURCES = ["route.hip", "gemm.hip", "runtime.hip"]
+SOURCES = ["route.hip", "gemm.hip", "gemm_bf16.hip", "gemm_fp8.hip", "runtime.hip"]
 
 # -packed-fp32-ops: keep the compiler from forming v_pk_{add,mul,fma}_f32.
 CFLAGS = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", f"--offload-arch={ARCH}",

@@ -1,0 +1,180 @@
+// bf16 grouped expert GEMMs for gfx950 (CDNA4) MFMA.
+//
+// Appendix C, "Grouped FFN invocations": within an invocation the two expert
+// GEMMs and the intervening activation run in stream order.  GEMM1 computes
+// the gate and up projections of every grouped row against its expert's
+// weights and applies SwiGLU in the epilogue; GEMM2 computes the down
+// projection and scales each row by its routing coefficient (the one place
+// the coefficient is applied).
+//
+// One kernel template, two instantiations:
+//   large batches: 256 x 256 tile, K steps of 32 through 4 LDS stages, one
+//     workgroup per CU -- MFMA-bound, each 16-byte LDS read feeds 4 MFMAs;
+//   small batches (few rows per expert): 64 x 128 tile, K steps of 64 through
+//     3 stages, two workgroups per CU -- weight-streaming (HBM) bound, sized
+//     for many weight bytes in flight per CU.
+// Both accumulate each output over K in the same order (ascending 16-wide
+// steps of v_mfma_f32_32x32x16_bf16), so a row's result does not depend on
+// which tile its batch used.
+#include "gemm_common.h"
+
+namespace cep {
+namespace {
+
+// BM x BN output tile, 4 waves as 2x2, each wave (BM/2) x (BN/2) built from
+// 32x32 MFMA fragments.  K advances in steps of BK through a ring of STAGES
+// LDS buffers filled by direct global->LDS loads (no staging registers)
+// issued STAGES-1 steps ahead, one barrier per step.  An LDS row holds BK
+// bf16 = CH 16-byte chunks; chunk c of row r lives at slot c ^ swz(r), with
+// swz chosen so that sixteen consecutive rows read at one chunk (what one LDS
+// cycle serves of an MFMA operand read) cover all sixteen 16-byte slots of a
+// 256-byte bank window.  A load instruction fills 64 consecutive slots, so
+// each lane fetches the global chunk that belongs in its slot.
+template <int BM, int BN, int BK, int STAGES, int OCC, bool SWIGLU>
+__global__ __launch_bounds__(256, OCC) void k_gemm_bf16(GemmArgs g) {
+  static_assert(BK == 32 || BK == 64, "LDS swizzle covers 4 or 8 chunks per row");
+  static_assert(STAGES == 3 || STAGES == 4, "wait counts below");
+  constexpr int CH = BK / 8;                  // 16-byte chunks per LDS row
+  constexpr int RPS = 1024 / (BK * 2);        // rows per 1 KB load segment
+  constexpr int SH = CH == 4 ? 2 : 1;         // swz(r) = (r >> SH) & (CH - 1)
+  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int FM = WM / 32, FN = WN / 32;
+  constexpr int A_LD = BM * BK * 2 / 1024 / 4, B_LD = BN * BK * 2 / 1024 / 4;  // per wave
+  constexpr int PER = A_LD + B_LD;            // loads per thread per step
+  int mt, nt;
+  if (!balanced_tile<kGroupM>(*g.n_tiles, g.N / BN, &mt, &nt)) return;
+  const Tile t = g.tiles[mt];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wid >> 1, wn = wid & 1;
+  const int K = g.K, nk = K / BK;
+  const char *Ag = (const char *)(g.A + (size_t)t.row0 * K * 2);
+  const char *Bg = (const char *)(blob_of(g.bt, t.expert) + g.b_off + (size_t)nt * BN * K * 2);
+
+  __shared__ u32x4 sA[STAGES][BM * CH];
+  __shared__ u32x4 sB[STAGES][BN * CH];
+
+  // Lane l of a load fills slot l of a 1 KB segment (RPS rows x CH chunks):
+  // row seg*RPS + l/CH, slot l%CH, which holds chunk (l%CH) ^ swz(row).  The
+  // swizzle uses the full row index (with 8 chunks per row, swz depends on
+  // the segment's position too).
+  const int seg_row = lane / CH;
+#define CEP_LANE_OFF(seg)                                                           \
+  ((uint32_t)((seg) * RPS + seg_row) * K * 2 +                                      \
+   (uint32_t)(((lane % CH) ^ ((((seg) * RPS + seg_row) >> SH) & (CH - 1))) * 16))
+#define CEP_DMA_STAGE(kt)                                                           \
+  {                                                                                 \
+    const int buf_ = (kt) % STAGES;                                                 \
+    _Pragma("unroll") for (int i = 0; i < A_LD; ++i) {                              \
+      const int seg = wid * A_LD + i;                                               \
+      dma16(Ag + (size_t)(kt) * BK * 2 + CEP_LANE_OFF(seg),                         \
+            __builtin_amdgcn_readfirstlane(lds_offset(&sA[buf_][seg * 64])));       \
+    }                                                                               \
+    _Pragma("unroll") for (int i = 0; i < B_LD; ++i) {                              \
+      const int seg = wid * B_LD + i;                                               \
+      dma16(Bg + (size_t)(kt) * BK * 2 + CEP_LANE_OFF(seg),                         \
+            __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf_][seg * 64])));       \
+    }                                                                               \
+  }
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x16{};
+
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nk) CEP_DMA_STAGE(s);
+
+  // every fragment row r = (wave base) + i*32 + lane%32 has
+  // swz(r) == swz(lane % 32) because the bases are multiples of 32
+  const int rsw = ((lane & 31) >> SH) & (CH - 1);
+  for (int kt = 0; kt < nk; ++kt) {
+    // this thread's loads of step kt are done when at most the loads of the
+    // steps issued after it are still outstanding
+    if (STAGES == 4 && kt + 2 < nk)
+      wait_vmcnt<(STAGES == 4 ? 2 : 1) * PER>();
+    else if (kt + 1 < nk)
+      wait_vmcnt<PER>();
+    else
+      wait_vmcnt<0>();
+    // every wave's loads of step kt landed; step kt-1 fully consumed.  A bare
+    // barrier: __syncthreads() would also drain the later steps' loads.
+    __builtin_amdgcn_s_barrier();
+    if (kt + STAGES - 1 < nk) CEP_DMA_STAGE(kt + STAGES - 1);
+    const int cur = kt % STAGES;
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int slot = (kk * 2 + (lane >> 5)) ^ rsw;
+      bf16x8 a[FM], b[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        a[i] = __builtin_bit_cast(bf16x8, sA[cur][(wm * WM + i * 32 + (lane & 31)) * CH + slot]);
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        b[j] = __builtin_bit_cast(bf16x8, sB[cur][(wn * WN + j * 32 + (lane & 31)) * CH + slot]);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  }
+#undef CEP_DMA_STAGE
+#undef CEP_LANE_OFF
+
+  // 32x32 accumulator layout: lane l, element r -> column l%32,
+  // row 8*(r/4) + 4*(l/32) + r%4.
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rt = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      if (rt >= t.rows) continue;
+      const size_t row = (size_t)t.row0 + rt;
+      if (SWIGLU) {
+        // fragment pairs (2*j2, 2*j2+1) are the gate and up columns of h
+        // columns (nt*BN + wn*WN)/2 + j2*32 + [0, 32)
+        __bf16 *H = (__bf16 *)g.out;
+        const size_t hbase = row * (g.N / 2) + (nt * BN + wn * WN) / 2 + (lane & 31);
+#pragma unroll
+        for (int j2 = 0; j2 < FN / 2; ++j2)
+          H[hbase + j2 * 32] = (__bf16)silu_mul(acc[i][2 * j2][r], acc[i][2 * j2 + 1][r]);
+      } else {
+        const float w = g.wrow[row];
+        float *Y = (float *)g.out;
+        const size_t ybase = row * g.N + nt * BN + wn * WN + (lane & 31);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) Y[ybase + j * 32] = acc[i][j][r] * w;
+      }
+    }
+  }
+}
+
+}  // namespace
+
+template <bool SWIGLU>
+hipError_t launch_bf16(const GemmArgs &g, int grid_tiles, int align, hipStream_t s) {
+  if (align == kBf16TileM) {
+    constexpr int BN = 256;
+    if (g.N % BN) return hipErrorInvalidValue;
+    const int grid = balanced_grid(grid_tiles, kGroupM, g.N / BN);
+    hipLaunchKernelGGL((k_gemm_bf16<kBf16TileM, BN, 32, 4, 1, SWIGLU>), dim3(grid), dim3(256), 0,
+                       s, g);
+  } else if (align == kBf16SmallTileM) {
+    constexpr int BN = 128;
+    if (g.N % BN || g.K % 64) return hipErrorInvalidValue;
+    const int grid = balanced_grid(grid_tiles, kGroupM, g.N / BN);
+    hipLaunchKernelGGL((k_gemm_bf16<kBf16SmallTileM, BN, 64, 3, 2, SWIGLU>), dim3(grid),
+                       dim3(256), 0, s, g);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template hipError_t launch_bf16<true>(const GemmArgs &, int, int, hipStream_t);
+template hipError_t launch_bf16<false>(const GemmArgs &, int, int, hipStream_t);
+
+}  // namespace cep

@@ -1,0 +1,108 @@
+// Device helpers shared by the grouped GEMM kernels (bf16 and e4m3).
+// Internal to libcep.
+#pragma once
+
+#include "common.h"
+
+#include <hip/hip_bf16.h>
+
+namespace cep {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Arguments of one grouped GEMM launch.  Both GEMMs are "NT" products:
+// A = grouped rows [M][K], B = packed weights [N][K], K contiguous in both,
+// so every MFMA operand is a contiguous run of K.  Work is a device tile
+// list (expert, first row, valid rows) built by the routing scan.
+struct GemmArgs {
+  const uint8_t *A;       // grouped rows [mpad][K] (bf16 or e4m3)
+  const float *As;        // e4m3: [mpad][K/128] row scales
+  const Tile *tiles;      // tile list
+  const int32_t *n_tiles; // live tiles in the list
+  int max_tiles;          // grid extent in M tiles (host upper bound)
+  int K, N;               // contraction length, packed output columns
+  size_t b_off, bs_off;   // offsets of B and its scales in each blob
+  BlobTable bt;
+  void *out;              // H [mpad][N/2] (GEMM1) or Y [mpad][N] f32 (GEMM2)
+  float *out_s;           // e4m3 GEMM1: h scales [mpad][N/256]
+  const float *wrow;      // GEMM2: routing coefficient per grouped row
+};
+
+__device__ inline float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
+
+// Grouped tile order: GM consecutive M tiles x all N tiles form a group, M
+// fastest inside it, so the workgroups an XCD runs together share GM row
+// panels of A and the weight panels of their N tiles in that XCD's L2.
+template <int GM>
+__device__ inline void tile_of(int L, int n_tiles_n, int *mt, int *nt) {
+  const int grp = L / (GM * n_tiles_n), idx = L % (GM * n_tiles_n);
+  *mt = grp * GM + idx % GM;
+  *nt = idx / GM;
+}
+
+// Work item of this workgroup, balanced over the XCDs.  The grid covers the
+// host's upper bound on M tiles; the live count is on the device.  The live
+// work W (whole groups) is cut into 8 contiguous shares, one per XCD
+// (workgroup ids are dispatched round-robin over the XCDs), so the surplus
+// workgroups of the bound never leave an XCD idle while another holds the
+// tail.  Returns false for a surplus workgroup.
+template <int GM>
+__device__ inline bool balanced_tile(int n_live, int n_tiles_n, int *mt, int *nt) {
+  const int W = (n_live + GM - 1) / GM * GM * n_tiles_n;
+  const int C = (W + 7) / 8;
+  const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
+  const int L = x * C + j;
+  if (j >= C || L >= W) return false;
+  tile_of<GM>(L, n_tiles_n, mt, nt);
+  return *mt < n_live;
+}
+
+// Grid for balanced_tile: at least the bound's work, a multiple of 8.
+inline int balanced_grid(int grid_tiles, int gm, int n_tiles_n) {
+  return ((grid_tiles + gm - 1) / gm * gm * n_tiles_n + 7) / 8 * 8;
+}
+constexpr int kGroupM = 8;
+
+// One direct global->LDS load of 16 bytes per lane: lane l's bytes land at
+// LDS byte offset lds_seg + 16*l.  Issued as inline assembly so that the
+// compiler does not order later LDS reads behind it; the caller synchronises
+// with wait_vmcnt and a barrier.  m0 holds the LDS base; it is reserved to
+// the compiler, so its value is saved and restored around the load (one wait
+// state after writing m0 before the load reads it).
+__device__ inline void dma16(const void *gptr, uint32_t lds_seg) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(gptr), "s"(lds_seg)
+      : "memory");
+}
+
+__device__ inline uint32_t lds_offset(const void *p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+
+// s_waitcnt immediate that waits until at most N vector-memory operations of
+// this wave are outstanding (gfx9 encoding: vmcnt in bits [3:0] and [15:14];
+// expcnt 7 and lgkmcnt 15 mean "do not wait" on those counters).
+template <int N>
+__device__ inline void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Launchers of the two kernel families (grid from the tile bound).
+template <bool SWIGLU>
+hipError_t launch_bf16(const GemmArgs &g, int grid_tiles, int align, hipStream_t s);
+template <bool SWIGLU>
+hipError_t launch_fp8(const GemmArgs &g, int grid_tiles, hipStream_t s);
+
+}  // namespace cep
