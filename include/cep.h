@@ -73,8 +73,8 @@ enum cep_policy {
 };
 
 typedef struct {
-  int d_model;                /* hidden size d, multiple of 256               */
-  int d_ff;                   /* expert intermediate size I, multiple of 128  */
+  int d_model;                /* hidden size d, multiple of 256, <= 32768     */
+  int d_ff;                   /* expert intermediate size I, mult. of 128, <= 32768 */
   int n_local_experts;        /* E, 1..64                                     */
   int top_k;                  /* k routing slots per token, 1..16             */
   int max_replicas;           /* R_max                                        */

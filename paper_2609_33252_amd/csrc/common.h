@@ -12,6 +12,7 @@ namespace cep {
 
 constexpr int kMaxExperts = 64;
 constexpr int kMaxTopK = 16;
+constexpr int kMaxDim = 32768;  // largest d_model and d_ff (fp8 GEMM keeps K/128 weight scales per row in LDS)
 constexpr int kBf16TileM = 256;      // bf16 grouped GEMM tile
 constexpr int kBf16TileN = 256;
 constexpr int kFp8TileM = 128;       // e4m3 grouped GEMM tile
@@ -107,9 +108,10 @@ struct Scratch {
   int32_t *perm;       // [max_mpad] flat pair of each grouped row or -1
   float *wrow;         // [max_mpad] routing coefficient of each grouped row
   void *xg;            // [max_mpad][d] bf16 or e4m3
-  float *xs;           // [max_mpad][d/128] fp8 activation scales
+  float *xs;           // [d/128][s_ld] e4m3 activation scales, k-block major
   void *h;             // [max_mpad][I] bf16 or e4m3
-  float *hs;           // [max_mpad][I/128] fp8 scales of h
+  float *hs;           // [I/128][s_ld] e4m3 scales of h, k-block major
+  int s_ld;            // row stride of xs / hs (= max_mpad, a multiple of 256)
   float *y;            // [max_mpad][d] f32, already scaled by the coefficient
 };
 

@@ -15,6 +15,7 @@ GemmArgs base_args(const Scratch &sc, int which, int list_cap, int grid_tiles,
   g.n_tiles = sc.n_tiles + which;
   g.max_tiles = grid_tiles;
   g.bt = bt;
+  g.s_ld = sc.s_ld;
   return g;
 }
 

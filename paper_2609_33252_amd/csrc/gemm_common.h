@@ -20,7 +20,8 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // list (expert, first row, valid rows) built by the routing scan.
 struct GemmArgs {
   const uint8_t *A;       // grouped rows [mpad][K] (bf16 or e4m3)
-  const float *As;        // e4m3: [mpad][K/128] row scales
+  const float *As;        // e4m3: [K/128][s_ld] row scales, k-block major
+  int s_ld;               // e4m3: row stride of the scale matrices
   const Tile *tiles;      // tile list
   const int32_t *n_tiles; // live tiles in the list
   int max_tiles;          // grid extent in M tiles (host upper bound)
@@ -28,7 +29,7 @@ struct GemmArgs {
   size_t b_off, bs_off;   // offsets of B and its scales in each blob
   BlobTable bt;
   void *out;              // H [mpad][N/2] (GEMM1) or Y [mpad][N] f32 (GEMM2)
-  float *out_s;           // e4m3 GEMM1: h scales [mpad][N/256]
+  float *out_s;           // e4m3 GEMM1: h scales [N/256][s_ld]
   const float *wrow;      // GEMM2: routing coefficient per grouped row
 };
 

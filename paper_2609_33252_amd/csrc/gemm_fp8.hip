@@ -13,174 +13,201 @@
 namespace cep {
 namespace {
 
-// 128x256 output tile, K step 128 (one scale block), 4 waves as 2x2, each
-// wave 64x128 built from 4x8 v_mfma_scale_f32_16x16x128_f8f6f4 with unit
-// hardware scales.  Each instruction covers one whole 128-wide K block, so
-// its result is promoted into the float32 accumulator with the product of
-// the row's activation scale and the weight block's scale.
+// 128x256 output tile, K step 128 (one scale block), 4 waves side by side,
+// each owning all 128 rows x 64 columns, built from 8x4
+// v_mfma_scale_f32_16x16x128_f8f6f4 with unit hardware scales.  Every
+// instruction covers one whole K block, so its result is promoted into the
+// float32 accumulator with the product of the row's activation scale and the
+// weight block's scale: two VALU operations per output element and K block,
+// which is why each wave holds few column scale blocks (GEMM1: the gate and
+// the up block of its 32 h columns; GEMM2: one) and few rows per lane.
+//
+// Operands stream through a ring of 3 LDS stages filled by direct
+// global->LDS loads issued two steps ahead (48 KB of codes + 512 B of row
+// scales per stage).  An LDS row is 128 codes = eight 16-byte chunks; chunk c
+// of row r lives at slot c ^ ((r >> 1) & 7), so the operand reads (sixteen
+// rows at one chunk per LDS cycle) are conflict-free.
 //
 // GEMM1 epilogue: h = silu(gate) * up over the tile's 128 h columns, one
-// amax per row (lanes, then the two column waves via LDS), scale =
-// amax / 448, e4m3 codes of h / scale.
+// amax per row (lanes, then the four waves via LDS), scale = amax / 448,
+// e4m3 codes of h / scale.
 template <bool SWIGLU>
-__global__ __launch_bounds__(256) void k_gemm_fp8(GemmArgs g) {
+__global__ __launch_bounds__(256, 1) void k_gemm_fp8(GemmArgs g) {
+  constexpr int BM = 128, BN = 256, BK = 128, STAGES = 3, WN = BN / 4;
+  constexpr int A_LD = BM * BK / 1024 / 4, B_LD = BN * BK / 1024 / 4;  // loads per wave
+  constexpr int PER = A_LD + B_LD;  // per thread per step; wave 0 adds one (row scales)
   int mt, nt;
-  if (!balanced_tile<kGroupM>(*g.n_tiles, g.N / 256, &mt, &nt)) return;
+  if (!balanced_tile<kGroupM>(*g.n_tiles, g.N / BN, &mt, &nt)) return;
   const Tile t = g.tiles[mt];
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wid >> 1, wn = wid & 1;
-  const int K = g.K, kv = K / 16, nkb = K / 128;
+  const int wn = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int K = g.K, nkb = K / BK;
   const uint8_t *blob = blob_of(g.bt, t.expert);
-  const u32x4 *Ag = (const u32x4 *)(g.A + (size_t)t.row0 * K);
-  const u32x4 *Bg = (const u32x4 *)(blob + g.b_off + (size_t)nt * 256 * K);
-  const float *Asg = g.As + (size_t)t.row0 * nkb;
+  const char *Ag = (const char *)(g.A + (size_t)t.row0 * K);
+  const char *Bg = (const char *)(blob + g.b_off + (size_t)nt * BN * K);
+  const char *Asg = (const char *)(g.As + t.row0);  // k-block kb at + kb * s_ld floats
   const float *Bs = (const float *)(blob + g.bs_off);
 
-  __shared__ u32x4 sA[128 * 8];
-  __shared__ u32x4 sB[256 * 8];
-  __shared__ float sAs[128];
-  __shared__ float red[2][128];
-  u32x4 ra[4], rb[8];
-  float ras = 0.f;
-#define CEP_FP8_GLOAD(kb)                                    \
-  _Pragma("unroll") for (int i = 0; i < 4; ++i) {            \
-    const int v = tid + 256 * i, row = v >> 3, ch = v & 7;   \
-    ra[i] = Ag[(size_t)row * kv + (kb) * 8 + ch];            \
-  }                                                          \
-  _Pragma("unroll") for (int i = 0; i < 8; ++i) {            \
-    const int v = tid + 256 * i, row = v >> 3, ch = v & 7;   \
-    rb[i] = Bg[(size_t)row * kv + (kb) * 8 + ch];            \
-  }                                                          \
-  if (tid < 128) ras = Asg[(size_t)tid * nkb + (kb)];
-  f32x4 acc[4][8];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{};
+  __shared__ u32x4 sA[STAGES][BM * 8];
+  __shared__ u32x4 sB[STAGES][BN * 8];
+  __shared__ float sAs[STAGES][BM];
+  __shared__ float red[4][BM];
+  __shared__ float sBs[8 * (kMaxDim / BK)];
 
-  CEP_FP8_GLOAD(0);
+  // lane l of a load fills slot l of a 1 KB segment (8 rows x 8 chunks)
+  const int seg_row = lane >> 3;
+#define CEP_F8_OFF(seg)                                                            \
+  ((uint32_t)((seg) * 8 + seg_row) * K +                                           \
+   (uint32_t)(((lane & 7) ^ ((((seg) * 8 + seg_row) >> 1) & 7)) * 16))
+#define CEP_F8_STAGE(kb)                                                           \
+  {                                                                                \
+    const int buf_ = (kb) % STAGES;                                                \
+    _Pragma("unroll") for (int i = 0; i < A_LD; ++i) {                             \
+      const int seg = wn * A_LD + i;                                               \
+      dma16(Ag + (size_t)(kb) * BK + CEP_F8_OFF(seg),                              \
+            __builtin_amdgcn_readfirstlane(lds_offset(&sA[buf_][seg * 64])));      \
+    }                                                                              \
+    _Pragma("unroll") for (int i = 0; i < B_LD; ++i) {                             \
+      const int seg = wn * B_LD + i;                                               \
+      dma16(Bg + (size_t)(kb) * BK + CEP_F8_OFF(seg),                              \
+            __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf_][seg * 64])));      \
+    }                                                                              \
+    if (wn == 0 && lane < 32)                                                      \
+      dma16(Asg + (size_t)(kb) * g.s_ld * 4 + lane * 16,                           \
+            __builtin_amdgcn_readfirstlane(lds_offset(&sAs[buf_][0])));            \
+  }
+
+  f32x4 acc[8][4];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{};
+
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nkb) CEP_F8_STAGE(s);
+
+  // The weight block scales of the tile's columns (8 consecutive rows of
+  // [N/32][nkb] for GEMM1, 2 of [N/128][nkb] for GEMM2) go to LDS once, so
+  // the main loop issues no vector loads besides the ring's.
+  {
+    const int nbs = (SWIGLU ? BN / kInterleave : BN / 128) * nkb;
+    const float *src = Bs + (size_t)nt * nbs;
+    for (int i = tid; i < nbs; i += 256) sBs[i] = src[i];
+  }
+  __syncthreads();
+
+  const int rsw = ((lane & 15) >> 1) & 7;  // swizzle of every operand row this lane reads
+  const int c0 = (lane >> 4) * 2;          // this lane's two chunks: K bytes [c0*16, c0*16+32)
+  // scale rows of this wave's column blocks: GEMM1 blocks j = 0,1 (gate) use
+  // row 2*wn, j = 2,3 (up) row 2*wn + 1; GEMM2's 64 columns lie in row wn/2
+  const float *sb_row0 = &sBs[(SWIGLU ? 2 * wn : wn / 2) * nkb];
+  const float *sb_row1 = &sBs[(SWIGLU ? 2 * wn + 1 : wn / 2) * nkb];
   for (int kb = 0; kb < nkb; ++kb) {
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int v = tid + 256 * i, row = v >> 3, ch = v & 7;
-      sA[row * 8 + (ch ^ (row & 7))] = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int v = tid + 256 * i, row = v >> 3, ch = v & 7;
-      sB[row * 8 + (ch ^ (row & 7))] = rb[i];
-    }
-    if (tid < 128) sAs[tid] = ras;
-    __syncthreads();
     if (kb + 1 < nkb) {
-      CEP_FP8_GLOAD(kb + 1);
+      if (wn == 0)
+        wait_vmcnt<PER + 1>();
+      else
+        wait_vmcnt<PER>();
+    } else {
+      wait_vmcnt<0>();
     }
+    __builtin_amdgcn_s_barrier();
+    if (kb + STAGES - 1 < nkb) CEP_F8_STAGE(kb + STAGES - 1);
+    const int cur = kb % STAGES;
+    const float sb0 = sb_row0[kb], sb1 = sb_row1[kb];
 
-    // weight block scales of this wave's columns at k-block kb
-    float sb[8];
+    i32x8 b[4];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int col = nt * 256 + wn * 128 + j * 16;
-      sb[j] = SWIGLU ? Bs[(size_t)(col / kInterleave) * nkb + kb]
-                     : Bs[(size_t)(col / 128) * nkb + kb];
-    }
-    i32x8 b[8];
-    const int c0 = (lane >> 4) * 2;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int row = wn * 128 + j * 16 + (lane & 15);
-      const u32x4 lo = sB[row * 8 + (c0 ^ (row & 7))];
-      const u32x4 hi = sB[row * 8 + ((c0 + 1) ^ (row & 7))];
+    for (int j = 0; j < 4; ++j) {
+      const int row = wn * WN + j * 16 + (lane & 15);
+      const u32x4 lo = sB[cur][row * 8 + (c0 ^ rsw)];
+      const u32x4 hi = sB[cur][row * 8 + ((c0 + 1) ^ rsw)];
       b[j] = __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = wm * 64 + i * 16 + (lane & 15);
-      const u32x4 lo = sA[row * 8 + (c0 ^ (row & 7))];
-      const u32x4 hi = sA[row * 8 + ((c0 + 1) ^ (row & 7))];
+    for (int i = 0; i < 8; ++i) {
+      const int row = i * 16 + (lane & 15);
+      const u32x4 lo = sA[cur][row * 8 + (c0 ^ rsw)];
+      const u32x4 hi = sA[cur][row * 8 + ((c0 + 1) ^ rsw)];
       const i32x8 a =
           __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-      const f32x4 sa = *(const f32x4 *)&sAs[wm * 64 + i * 16 + 4 * (lane >> 4)];
+      f32x4 p[4];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const f32x4 p = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
-            a, b[j], f32x4{}, 0, 0, 0, 127, 0, 127);
+      for (int j = 0; j < 4; ++j)
+        p[j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b[j], f32x4{}, 0, 0, 0, 127,
+                                                               0, 127);
+      const f32x4 sa = *(const f32x4 *)&sAs[cur][i * 16 + 4 * (lane >> 4)];
+      const f32x4 s0 = sa * sb0, s1 = sa * sb1;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[i][j][r] += p[r] * (sa[r] * sb[j]);
-      }
+      for (int j = 0; j < 4; ++j) acc[i][j] += p[j] * (j < 2 ? s0 : s1);
     }
   }
+#undef CEP_F8_STAGE
+#undef CEP_F8_OFF
 
   // 16x16 accumulator layout: lane l, element r -> column l%16,
   // row 4*(l/16) + r.
   if (SWIGLU) {
-    // h for jj in 0..3: gate block j = (jj/2)*4 + jj%2, up block j + 2;
-    // h column nt*128 + wn*64 + (jj/2)*32 + (jj%2)*16 + l%16
-    float h[4][4][4];
+    // h column nt*128 + wn*32 + jj*16 + l%16 = silu(gate block jj) * up block jj+2
+    float h[8][2][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const int j = (jj >> 1) * 4 + (jj & 1);
+      for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) h[i][jj][r] = silu_mul(acc[i][j][r], acc[i][j + 2][r]);
-      }
+        for (int r = 0; r < 4; ++r) h[i][jj][r] = silu_mul(acc[i][jj][r], acc[i][jj + 2][r]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        float m = 0.f;
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) m = fmaxf(m, fabsf(h[i][jj][r]));
+        float m = fmaxf(fabsf(h[i][0][r]), fabsf(h[i][1][r]));
 #pragma unroll
         for (int sh = 1; sh < 16; sh <<= 1) m = fmaxf(m, __shfl_xor(m, sh, 16));
-        if ((lane & 15) == 0) red[wn][wm * 64 + i * 16 + 4 * (lane >> 4) + r] = m;
+        if ((lane & 15) == 0) red[wn][i * 16 + 4 * (lane >> 4) + r] = m;
       }
     __syncthreads();
     uint8_t *H = (uint8_t *)g.out;
     const int I = g.N / 2;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int rt = wm * 64 + i * 16 + 4 * (lane >> 4) + r;
+        const int rt = i * 16 + 4 * (lane >> 4) + r;
         if (rt >= t.rows) continue;
-        const float amax = fmaxf(red[0][rt], red[1][rt]);
+        const float amax = fmaxf(fmaxf(red[0][rt], red[1][rt]), fmaxf(red[2][rt], red[3][rt]));
         const float scale = amax > 0.f ? amax / 448.0f : 1.0f;
         const size_t row = (size_t)t.row0 + rt;
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          const int col = nt * 128 + wn * 64 + (jj >> 1) * 32 + (jj & 1) * 16 + (lane & 15);
+        for (int jj = 0; jj < 2; ++jj) {
+          const int col = nt * 128 + wn * 32 + jj * 16 + (lane & 15);
           const int q = __builtin_amdgcn_cvt_pk_fp8_f32(h[i][jj][r] / scale, 0.f, 0, false);
           H[row * I + col] = (uint8_t)(q & 0xff);
         }
-        if (wn == 0 && (lane & 15) == 0) g.out_s[row * (I / 128) + nt] = scale;
+        if (wn == 0 && (lane & 15) == 0) g.out_s[(size_t)nt * g.s_ld + row] = scale;
       }
   } else {
     float *Y = (float *)g.out;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int rt = wm * 64 + i * 16 + 4 * (lane >> 4) + r;
+        const int rt = i * 16 + 4 * (lane >> 4) + r;
         if (rt >= t.rows) continue;
         const size_t row = (size_t)t.row0 + rt;
         const float w = g.wrow[row];
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          Y[row * g.N + nt * 256 + wn * 128 + j * 16 + (lane & 15)] = acc[i][j][r] * w;
+        for (int j = 0; j < 4; ++j)
+          Y[row * g.N + nt * BN + wn * WN + j * 16 + (lane & 15)] = acc[i][j][r] * w;
       }
   }
 }
-
 
 }  // namespace
 
 template <bool SWIGLU>
 hipError_t launch_fp8(const GemmArgs &g, int grid_tiles, hipStream_t s) {
-  if (g.N % 256 || g.K % 128) return hipErrorInvalidValue;
+  if (g.N % 256 || g.K % 128 || g.K > kMaxDim || g.s_ld % 4) return hipErrorInvalidValue;
   const int grid = balanced_grid(grid_tiles, kGroupM, g.N / 256);
   hipLaunchKernelGGL(k_gemm_fp8<SWIGLU>, dim3(grid), dim3(256), 0, s, g);
   return hipGetLastError();

@@ -239,7 +239,7 @@ __global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0
       // 16 lanes x 8 channels = one 128-channel scale block
       const uint4 *s4 = (const uint4 *)src;
       uint8_t *dq = (uint8_t *)sc.xg + (size_t)pos * d;
-      float *ds = sc.xs + (size_t)pos * (d / 128);
+      float *ds = sc.xs + pos;  // k-block major: block b at ds[b * s_ld]
       for (int c0 = 0; c0 < d; c0 += 512) {
         const int c = c0 + lane * 8;
         const bool ok = c < d;
@@ -264,7 +264,7 @@ __global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0
           hi = __builtin_amdgcn_cvt_pk_fp8_f32(v[4] / scale, v[5] / scale, hi, false);
           hi = __builtin_amdgcn_cvt_pk_fp8_f32(v[6] / scale, v[7] / scale, hi, true);
           *(uint2 *)(dq + c) = make_uint2((uint32_t)lo, (uint32_t)hi);
-          if ((lane & 15) == 0) ds[c / 128] = scale;
+          if ((lane & 15) == 0) ds[(size_t)(c / 128) * sc.s_ld] = scale;
         }
       }
     }

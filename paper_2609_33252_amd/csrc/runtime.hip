@@ -115,8 +115,10 @@ int fail(cep_ctx *c, int code, const char *fmt, ...) {
 bool valid_config(const cep_config *c, std::string *why) {
   auto bad = [&](const char *m) { *why = m; return false; };
   if (!c) return bad("cfg is NULL");
-  if (c->d_model <= 0 || c->d_model % 256) return bad("d_model must be a positive multiple of 256");
-  if (c->d_ff <= 0 || c->d_ff % 128) return bad("d_ff must be a positive multiple of 128");
+  if (c->d_model <= 0 || c->d_model % 256 || c->d_model > kMaxDim)
+    return bad("d_model must be a positive multiple of 256, at most 32768");
+  if (c->d_ff <= 0 || c->d_ff % 128 || c->d_ff > kMaxDim)
+    return bad("d_ff must be a positive multiple of 128, at most 32768");
   if (c->n_local_experts < 1 || c->n_local_experts > kMaxExperts) return bad("n_local_experts must be in 1..64");
   if (c->top_k < 1 || c->top_k > kMaxTopK) return bad("top_k must be in 1..16");
   if (c->max_replicas < 1 || c->max_tokens_per_replica < 1) return bad("max_replicas and max_tokens_per_replica must be >= 1");
@@ -351,6 +353,7 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
     if (c->fp8) {
       sc.xs = (float *)A(sizeof(float) * c->max_mpad * (d / 128));
       sc.hs = (float *)A(sizeof(float) * c->max_mpad * (I / 128));
+      sc.s_ld = c->max_mpad;
     }
   }
   if (e != hipSuccess) {
