@@ -23,17 +23,23 @@ namespace {
 
 // BM x BN output tile, 4 waves as 2x2, each wave (BM/2) x (BN/2) built from
 // 32x32 MFMA fragments.  K advances in steps of BK through a ring of STAGES
-// LDS buffers filled by direct global->LDS loads (no staging registers)
-// issued STAGES-1 steps ahead, one barrier per step.  An LDS row holds BK
-// bf16 = CH 16-byte chunks; chunk c of row r lives at slot c ^ swz(r), with
-// swz chosen so that sixteen consecutive rows read at one chunk (what one LDS
-// cycle serves of an MFMA operand read) cover all sixteen 16-byte slots of a
-// 256-byte bank window.  A load instruction fills 64 consecutive slots, so
-// each lane fetches the global chunk that belongs in its slot.
-template <int BM, int BN, int BK, int STAGES, int OCC, bool SWIGLU>
+// LDS buffers filled by direct global->LDS loads (no staging registers), one
+// barrier per step.  An LDS row holds BK bf16 = CH 16-byte chunks; chunk c of
+// row r lives at slot c ^ swz(r), with swz chosen so that sixteen consecutive
+// rows read at one chunk (what one LDS cycle serves of an MFMA operand read)
+// cover all sixteen 16-byte slots of a 256-byte bank window.  A load
+// instruction fills 64 consecutive slots, so each lane fetches the global
+// chunk that belongs in its slot.
+//
+// Two schedules.  PIPE (MFMA-bound tile): each 16-wide sub-step multiplies
+// fragments read during the previous sub-step, so LDS latency hides behind
+// the MFMAs; loads run STAGES-2 steps ahead.  Otherwise (weight-streaming
+// tile): fragments are read right before their MFMAs and loads run STAGES-1
+// steps ahead, which keeps more weight bytes in flight per LDS byte.
+template <int BM, int BN, int BK, int STAGES, int OCC, bool PIPE, bool SWIGLU>
 __global__ __launch_bounds__(256, OCC) void k_gemm_bf16(GemmArgs g) {
   static_assert(BK == 32 || BK == 64, "LDS swizzle covers 4 or 8 chunks per row");
-  static_assert(STAGES == 3 || STAGES == 4, "wait counts below");
+  static_assert(STAGES >= 3 && STAGES <= 5, "wait counts below");
   constexpr int CH = BK / 8;                  // 16-byte chunks per LDS row
   constexpr int RPS = 1024 / (BK * 2);        // rows per 1 KB load segment
   constexpr int SH = CH == 4 ? 2 : 1;         // swz(r) = (r >> SH) & (CH - 1)
@@ -83,44 +89,91 @@ __global__ __launch_bounds__(256, OCC) void k_gemm_bf16(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x16{};
 
-#pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
-    if (s < nk) CEP_DMA_STAGE(s);
-
   // every fragment row r = (wave base) + i*32 + lane%32 has
   // swz(r) == swz(lane % 32) because the bases are multiples of 32
   const int rsw = ((lane & 31) >> SH) & (CH - 1);
-  for (int kt = 0; kt < nk; ++kt) {
-    // this thread's loads of step kt are done when at most the loads of the
-    // steps issued after it are still outstanding
-    if (STAGES == 4 && kt + 2 < nk)
-      wait_vmcnt<(STAGES == 4 ? 2 : 1) * PER>();
-    else if (kt + 1 < nk)
-      wait_vmcnt<PER>();
-    else
-      wait_vmcnt<0>();
-    // every wave's loads of step kt landed; step kt-1 fully consumed.  A bare
-    // barrier: __syncthreads() would also drain the later steps' loads.
+#define CEP_LOAD_FRAG(fa_, fb_, buf_, kk_)                                          \
+  {                                                                                 \
+    const int slot_ = ((kk_) * 2 + (lane >> 5)) ^ rsw;                              \
+    _Pragma("unroll") for (int i = 0; i < FM; ++i) fa_[i] = __builtin_bit_cast(     \
+        bf16x8, sA[buf_][(wm * WM + i * 32 + (lane & 31)) * CH + slot_]);           \
+    _Pragma("unroll") for (int j = 0; j < FN; ++j) fb_[j] = __builtin_bit_cast(     \
+        bf16x8, sB[buf_][(wn * WN + j * 32 + (lane & 31)) * CH + slot_]);           \
+  }
+
+  constexpr int KK = BK / 16;
+  static_assert(!PIPE || KK % 2 == 0, "fragment double buffer alternates per sub-step");
+  if constexpr (PIPE) {
+    // Stage s is issued at the barrier of step s - STAGES + 1 (the prologue
+    // issues stages 0 .. STAGES-2), into the buffer of stage s - STAGES,
+    // whose last fragment reads completed before the MFMAs of step
+    // s - STAGES.
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+      if (s < nk) CEP_DMA_STAGE(s);
+    // stage 0 landed when at most the later prologue stages are outstanding
+    wait_stages<PER, STAGES - 2>(min(nk - 1, STAGES - 2));
     __builtin_amdgcn_s_barrier();
-    if (kt + STAGES - 1 < nk) CEP_DMA_STAGE(kt + STAGES - 1);
-    const int cur = kt % STAGES;
+
+    // The last sub-step of step kt first waits for stage kt+1, issues the
+    // loads of stage kt+STAGES-1 and reads the first fragments of kt+1.
+    bf16x8 fa[2][FM], fb[2][FN];
+    CEP_LOAD_FRAG(fa[0], fb[0], 0, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+      const int cur = kt % STAGES;
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      const int slot = (kk * 2 + (lane >> 5)) ^ rsw;
-      bf16x8 a[FM], b[FN];
+      for (int kk = 0; kk < KK; ++kk) {
+        const int p = kk & 1, q = p ^ 1;
+        if (kk + 1 < KK) {
+          CEP_LOAD_FRAG(fa[q], fb[q], cur, kk + 1);
+        } else if (kt + 1 < nk) {
+          // this thread's loads of stage kt+1 are done when at most the
+          // loads of the stages issued after it (up to kt+STAGES-2) are
+          // outstanding
+          wait_stages<PER, STAGES - 3>(min(nk - 1, kt + STAGES - 2) - (kt + 1));
+          __builtin_amdgcn_s_barrier();
+          if (kt + STAGES - 1 < nk) CEP_DMA_STAGE(kt + STAGES - 1);
+          CEP_LOAD_FRAG(fa[q], fb[q], (kt + 1) % STAGES, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
-        a[i] = __builtin_bit_cast(bf16x8, sA[cur][(wm * WM + i * 32 + (lane & 31)) * CH + slot]);
+        for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
-        b[j] = __builtin_bit_cast(bf16x8, sB[cur][(wn * WN + j * 32 + (lane & 31)) * CH + slot]);
+          for (int j = 0; j < FN; ++j)
+            acc[i][j] =
+                __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[p][i], fb[p][j], acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  } else {
+    // Stage s is issued at the top of step s - STAGES + 1, into the buffer
+    // of stage s - STAGES, which every wave finished reading in step
+    // s - STAGES (before this step's barrier).
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+    for (int s = 0; s < STAGES - 1; ++s)
+      if (s < nk) CEP_DMA_STAGE(s);
+    for (int kt = 0; kt < nk; ++kt) {
+      // this thread's loads of step kt are done when at most the loads of
+      // the steps issued after it are outstanding
+      wait_stages<PER, STAGES - 2>(min(nk - 1, kt + STAGES - 2) - kt);
+      // every wave's loads of step kt landed; step kt-1 fully consumed.  A
+      // bare barrier: __syncthreads() would also drain the later loads.
+      __builtin_amdgcn_s_barrier();
+      if (kt + STAGES - 1 < nk) CEP_DMA_STAGE(kt + STAGES - 1);
+      const int cur = kt % STAGES;
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+      for (int kk = 0; kk < KK; ++kk) {
+        bf16x8 fa[FM], fb[FN];
+        CEP_LOAD_FRAG(fa, fb, cur, kk);
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+      }
     }
   }
+#undef CEP_LOAD_FRAG
 #undef CEP_DMA_STAGE
 #undef CEP_LANE_OFF
 
@@ -160,13 +213,13 @@ hipError_t launch_bf16(const GemmArgs &g, int grid_tiles, int align, hipStream_t
     constexpr int BN = 256;
     if (g.N % BN) return hipErrorInvalidValue;
     const int grid = balanced_grid(grid_tiles, kGroupM, g.N / BN);
-    hipLaunchKernelGGL((k_gemm_bf16<kBf16TileM, BN, 32, 4, 1, SWIGLU>), dim3(grid), dim3(256), 0,
+    hipLaunchKernelGGL((k_gemm_bf16<kBf16TileM, BN, 32, 4, 1, true, SWIGLU>), dim3(grid), dim3(256), 0,
                        s, g);
   } else if (align == kBf16SmallTileM) {
     constexpr int BN = 128;
     if (g.N % BN || g.K % 64) return hipErrorInvalidValue;
     const int grid = balanced_grid(grid_tiles, kGroupM, g.N / BN);
-    hipLaunchKernelGGL((k_gemm_bf16<kBf16SmallTileM, BN, 64, 3, 2, SWIGLU>), dim3(grid),
+    hipLaunchKernelGGL((k_gemm_bf16<kBf16SmallTileM, BN, 64, 3, 2, false, SWIGLU>), dim3(grid),
                        dim3(256), 0, s, g);
   } else {
     return hipErrorInvalidValue;

@@ -100,6 +100,22 @@ __device__ inline void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
+// Waits until at most r (0 <= r <= R) groups of PER vector-memory operations
+// of this wave are outstanding.
+template <int PER, int R>
+__device__ inline void wait_stages(int r) {
+  if constexpr (R >= 3) {
+    if (r >= 3) return wait_vmcnt<3 * PER>();
+  }
+  if constexpr (R >= 2) {
+    if (r >= 2) return wait_vmcnt<2 * PER>();
+  }
+  if constexpr (R >= 1) {
+    if (r >= 1) return wait_vmcnt<PER>();
+  }
+  wait_vmcnt<0>();
+}
+
 // Launchers of the two kernel families (grid from the tile bound).
 template <bool SWIGLU>
 hipError_t launch_bf16(const GemmArgs &g, int grid_tiles, int align, hipStream_t s);

@@ -65,10 +65,16 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_count(const int32_t *__
   if (tid < E) hist[tid] = 0;
   __syncthreads();
   const int base = blockIdx.x * kRoutePairs;
+  constexpr int R = kRoutePairs / kRouteThreads;
+  int idv[R];  // all loads first: one memory latency per block, not one per round
 #pragma unroll
-  for (int r = 0; r < kRoutePairs / kRouteThreads; ++r) {
+  for (int r = 0; r < R; ++r) {
     const int p = base + r * kRouteThreads + tid;
-    const int id = p < n_flat ? ids[p] : -1;
+    idv[r] = p < n_flat ? ids[p] : -1;
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int id = idv[r];
     uint64_t active = __ballot(id >= 0);
     while (active) {
       const int leader = __builtin_ctzll(active);
@@ -85,36 +91,52 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_count(const int32_t *__
 // ------------------------------------------------------------------ scan
 // One block: per-expert totals, unpadded and tile-aligned exclusive scans,
 // the first grouped row of every routing block's pairs of every expert, and
-// the M-tile lists of the resident and the fetched experts.
+// the M-tile lists of the resident and the fetched experts.  Thread t serves
+// expert t % E over a contiguous range of routing blocks (group t / E), so
+// the block counts are read in parallel and scanned in LDS.
 __global__ __launch_bounds__(256) void k_route_scan(Scratch sc, int n_blocks, int E, int align,
                                                     int expected_pairs, int max_mpad,
                                                     int max_tiles, uint64_t fetched_mask,
                                                     uint32_t *err) {
+  __shared__ int s_part[256];  // [group][expert]: range sum, then exclusive prefix
   __shared__ int s_cnt[kMaxExperts], s_off[kMaxExperts + 1], s_pad[kMaxExperts + 1];
   __shared__ int s_tile0[kMaxExperts];
   const int tid = threadIdx.x;
+  const int G = 256 / E, e = tid % E, grp = tid / E;
+  const bool mine = grp < G;
+  const int span = (n_blocks + G - 1) / G;
+  const int b0 = min(grp * span, n_blocks), b1 = min(b0 + span, n_blocks);
+  if (mine) {
+    int part = 0;
+    for (int b = b0; b < b1; ++b) part += sc.blk_cnt[b * E + e];
+    s_part[grp * E + e] = part;
+  }
+  __syncthreads();
   if (tid < E) {
-    int c = 0;
-    for (int b = 0; b < n_blocks; ++b) c += sc.blk_cnt[b * E + tid];
-    s_cnt[tid] = c;
+    int run = 0;
+    for (int q = 0; q < G; ++q) {
+      const int v = s_part[q * E + tid];
+      s_part[q * E + tid] = run;
+      run += v;
+    }
+    s_cnt[tid] = run;
   }
   __syncthreads();
   if (tid == 0) {
-    int o = 0, op = 0, total = 0;
+    int o = 0, op = 0;
     int t0[2] = {0, 0};
-    for (int e = 0; e < E; ++e) {
-      s_off[e] = o;
-      s_pad[e] = op;
-      const int which = (int)((fetched_mask >> e) & 1);
-      s_tile0[e] = t0[which];
-      t0[which] += (s_cnt[e] + align - 1) / align;
-      o += s_cnt[e];
-      op += (s_cnt[e] + align - 1) / align * align;
+    for (int x = 0; x < E; ++x) {
+      s_off[x] = o;
+      s_pad[x] = op;
+      const int which = (int)((fetched_mask >> x) & 1);
+      s_tile0[x] = t0[which];
+      t0[which] += (s_cnt[x] + align - 1) / align;
+      o += s_cnt[x];
+      op += (s_cnt[x] + align - 1) / align * align;
     }
     s_off[E] = o;
     s_pad[E] = op;
-    total = o;
-    if (total != expected_pairs) atomicOr(err, kErrPairCount);
+    if (o != expected_pairs) atomicOr(err, kErrPairCount);
     if (op > max_mpad || t0[0] > max_tiles || t0[1] > max_tiles) atomicOr(err, kErrOverflow);
     sc.n_tiles[0] = min(t0[0], max_tiles);
     sc.n_tiles[1] = min(t0[1], max_tiles);
@@ -124,15 +146,20 @@ __global__ __launch_bounds__(256) void k_route_scan(Scratch sc, int n_blocks, in
     sc.off[tid] = s_off[tid];
     sc.off_pad[tid] = s_pad[tid];
   }
-  if (tid < E) {
-    sc.cnt[tid] = s_cnt[tid];
-    int run = s_pad[tid];
-    for (int b = 0; b < n_blocks; ++b) {
-      sc.blk_base[b * E + tid] = run;
-      run += sc.blk_cnt[b * E + tid];
+  if (tid < E) sc.cnt[tid] = s_cnt[tid];
+  if (mine) {
+    int run = s_pad[e] + s_part[grp * E + e];
+    for (int b = b0; b < b1; ++b) {
+      sc.blk_base[b * E + e] = run;
+      run += sc.blk_cnt[b * E + e];
     }
-    // padding rows of this expert's last tile carry no pair
-    for (int r = s_pad[tid] + s_cnt[tid]; r < s_pad[tid + 1] && r < max_mpad; ++r) sc.perm[r] = -1;
+  }
+  // padding rows of each expert's last tile carry no pair
+  for (int i = tid; i < E * align; i += 256) {
+    const int x = i / align, r = s_pad[x] + s_cnt[x] + i % align;
+    if (r < s_pad[x + 1] && r < max_mpad) sc.perm[r] = -1;
+  }
+  if (tid < E) {
     const int which = (int)((fetched_mask >> tid) & 1);
     Tile *list = sc.tiles + (size_t)which * max_tiles;
     const int nt = (s_cnt[tid] + align - 1) / align;
@@ -166,9 +193,19 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_scatter(Arena a, Scratc
   const int32_t *ids = a.ids + (size_t)row0 * k;
   const float *wts = a.w + (size_t)row0 * k;
   const int base = b * kRoutePairs;
-  for (int r = 0; r < kRoutePairs / kRouteThreads; ++r) {
+  constexpr int R = kRoutePairs / kRouteThreads;
+  int idv[R];  // all loads first: one memory latency per block, not one per round
+  float wv[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
     const int p = base + r * kRouteThreads + tid;
-    const int id = p < n_flat ? ids[p] : -1;
+    idv[r] = p < n_flat ? ids[p] : -1;
+    wv[r] = p < n_flat ? wts[p] : 0.f;
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int p = base + r * kRouteThreads + tid;
+    const int id = idv[r];
     int rank = 0;
     uint64_t active = __ballot(id >= 0);
     while (active) {
@@ -199,7 +236,7 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_scatter(Arena a, Scratc
     if (p < n_flat) sc.pos_of[p] = pos;
     if (pos >= 0) {
       sc.perm[pos] = p;
-      sc.wrow[pos] = wts[p];
+      sc.wrow[pos] = wv[r];
     }
   }
 }

@@ -62,6 +62,9 @@ struct cep_ctx {
   int max_pairs = 0, max_mpad = 0, max_tiles = 0, max_blocks = 0, max_rows = 0;
   hipStream_t ingest = nullptr;
   hipStream_t st[8] = {}, helper[8] = {};
+  // slot streams and helper streams that ran batches since the last layer
+  // barrier; the next layer's staging waits for exactly these
+  unsigned used_st = 0, used_helper = 0;
   Scratch sc[8] = {};
   std::vector<void *> allocs;
   // policy
@@ -84,9 +87,9 @@ struct cep_ctx {
   hipEvent_t ev_fetch_start = nullptr, ev_fetch_ready = nullptr;
   // sync-only events, one set per slot (re-recorded per batch)
   hipEvent_t ev_ingest[8] = {}, ev_routed[8] = {}, ev_helper[8] = {};
-  hipEvent_t ev_layer_done = nullptr;
-  std::vector<hipEvent_t> timing_pool;
-  size_t timing_used = 0;
+  hipEvent_t ev_layer_done = nullptr, ev_layer_ingest = nullptr;
+  std::vector<hipEvent_t> timing_pool[2];  // [fenced]
+  size_t timing_used[2] = {0, 0};
 };
 
 namespace {
@@ -139,13 +142,24 @@ void *dalloc(cep_ctx *c, size_t bytes, hipError_t *e) {
   return p;
 }
 
-hipEvent_t timing_event(cep_ctx *c) {
-  if (c->timing_used == c->timing_pool.size()) {
+// Timing events from per-layer pools.  Phase markers only measure time, so
+// they skip the system-scope fence (an L2 writeback and invalidate between
+// the phases); a batch's end event keeps it, because the host reads the
+// batch's routing copies after synchronising on it.
+// Events that only order streams of this device: a device-scope release.
+constexpr unsigned kDepEvent = hipEventDisableTiming | hipEventReleaseToDevice;
+
+hipEvent_t timing_event(cep_ctx *c, bool fenced) {
+  std::vector<hipEvent_t> &pool = c->timing_pool[fenced];
+  size_t &used = c->timing_used[fenced];
+  if (used == pool.size()) {
     hipEvent_t e = nullptr;
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
-    c->timing_pool.push_back(e);
+    if (hipEventCreateWithFlags(&e, fenced ? hipEventDefault : hipEventDisableSystemFence) !=
+        hipSuccess)
+      return nullptr;
+    pool.push_back(e);
   }
-  return c->timing_pool[c->timing_used++];
+  return pool[used++];
 }
 
 void free_batch_records(cep_ctx *c) {
@@ -182,23 +196,28 @@ int launch_pending(cep_ctx *c) {
   b.n_pairs = c->pending_pairs;
   b.slot = (int)(c->batches.size() % c->n_streams);
   const int slot = b.slot;
-  hipStream_t s = c->st[slot];
+  // one stream: batches run on the ingest stream itself, in submission
+  // order after their chunks' staging, without a cross-stream hop
+  hipStream_t s = c->n_streams == 1 ? c->ingest : c->st[slot];
+  if (s != c->ingest) c->used_st |= 1u << slot;
   const Scratch &sc = c->sc[slot];
   const int P = b.n_pairs;
   const int A = batch_align(c->fp8, b.n_pairs, E);
   b.align = A;
   const int tiles = std::min(c->max_tiles, (P + A - 1) / A + E);
   b.mpad_bound = std::min(c->max_mpad, tiles * A);
-  b.ev_start = timing_event(c);
-  b.ev_end = timing_event(c);
-  for (hipEvent_t &e : b.ev_phase) e = timing_event(c);
+  b.ev_start = timing_event(c, false);
+  b.ev_end = timing_event(c, true);
+  for (hipEvent_t &e : b.ev_phase) e = timing_event(c, false);
   if (!b.ev_start || !b.ev_end || !b.ev_phase[0] || !b.ev_phase[1] || !b.ev_phase[2] ||
       !b.ev_phase[3])
     return fail(c, CEP_EHIP, "hipEventCreate failed");
 
   // the batch sees its chunks only after the ingest stream has staged them
-  HIPCHK(c, hipEventRecord(c->ev_ingest[slot], c->ingest));
-  HIPCHK(c, hipStreamWaitEvent(s, c->ev_ingest[slot], 0));
+  if (s != c->ingest) {
+    HIPCHK(c, hipEventRecord(c->ev_ingest[slot], c->ingest));
+    HIPCHK(c, hipStreamWaitEvent(s, c->ev_ingest[slot], 0));
+  }
   HIPCHK(c, hipEventRecord(b.ev_start, s));
   HIPCHK(c, launch_route(c->arena, sc, b.row0, b.n_rows, k, E, A, P, c->max_mpad, c->max_tiles,
                          c->fetched_mask, cfg.x_dtype, c->fp8, d, c->d_err, s));
@@ -209,6 +228,7 @@ int launch_pending(cep_ctx *c) {
   b.helper = c->fetched_mask != 0;
   if (b.helper) {
     hipStream_t h = c->helper[slot];
+    c->used_helper |= 1u << slot;
     HIPCHK(c, hipEventRecord(c->ev_routed[slot], s));
     HIPCHK(c, hipStreamWaitEvent(h, c->ev_routed[slot], 0));
     HIPCHK(c, hipStreamWaitEvent(h, c->ev_fetch_ready, 0));
@@ -366,14 +386,15 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
   for (int i = 0; i < cfg->n_streams && ok; ++i) {
     ok = hipStreamCreateWithFlags(&c->st[i], hipStreamNonBlocking) == hipSuccess &&
          hipStreamCreateWithFlags(&c->helper[i], hipStreamNonBlocking) == hipSuccess &&
-         hipEventCreateWithFlags(&c->ev_ingest[i], hipEventDisableTiming) == hipSuccess &&
-         hipEventCreateWithFlags(&c->ev_routed[i], hipEventDisableTiming) == hipSuccess &&
-         hipEventCreateWithFlags(&c->ev_helper[i], hipEventDisableTiming) == hipSuccess;
+         hipEventCreateWithFlags(&c->ev_ingest[i], kDepEvent) == hipSuccess &&
+         hipEventCreateWithFlags(&c->ev_routed[i], kDepEvent) == hipSuccess &&
+         hipEventCreateWithFlags(&c->ev_helper[i], kDepEvent) == hipSuccess;
   }
-  ok = ok && hipEventCreate(&c->ev_origin) == hipSuccess &&
-       hipEventCreate(&c->ev_fetch_start) == hipSuccess &&
+  ok = ok && hipEventCreateWithFlags(&c->ev_origin, hipEventDisableSystemFence) == hipSuccess &&
+       hipEventCreateWithFlags(&c->ev_fetch_start, hipEventDisableSystemFence) == hipSuccess &&
        hipEventCreate(&c->ev_fetch_ready) == hipSuccess &&
-       hipEventCreateWithFlags(&c->ev_layer_done, hipEventDisableTiming) == hipSuccess;
+       hipEventCreateWithFlags(&c->ev_layer_done, hipEventDisableTiming) == hipSuccess &&
+       hipEventCreateWithFlags(&c->ev_layer_ingest, kDepEvent) == hipSuccess;
   ok = ok && hipMemsetAsync(c->d_err, 0, sizeof(uint32_t), s) == hipSuccess;
   if (!ok) {
     cep_destroy(c);
@@ -419,13 +440,18 @@ CEP_API int cep_begin_layer(cep_ctx *c, uint32_t generation, int n_replicas,
   }
   // the previous layer's batches may still read the arena: stage after them
   for (int i = 0; i < c->cfg.n_streams; ++i) {
-    HIPCHK(c, hipEventRecord(c->ev_ingest[i], c->st[i]));
-    HIPCHK(c, hipStreamWaitEvent(c->ingest, c->ev_ingest[i], 0));
-    HIPCHK(c, hipEventRecord(c->ev_routed[i], c->helper[i]));
-    HIPCHK(c, hipStreamWaitEvent(c->ingest, c->ev_routed[i], 0));
+    if ((c->used_st >> i) & 1) {
+      HIPCHK(c, hipEventRecord(c->ev_ingest[i], c->st[i]));
+      HIPCHK(c, hipStreamWaitEvent(c->ingest, c->ev_ingest[i], 0));
+    }
+    if ((c->used_helper >> i) & 1) {
+      HIPCHK(c, hipEventRecord(c->ev_routed[i], c->helper[i]));
+      HIPCHK(c, hipStreamWaitEvent(c->ingest, c->ev_routed[i], 0));
+    }
   }
+  c->used_st = c->used_helper = 0;
   free_batch_records(c);
-  c->timing_used = 0;
+  c->timing_used[0] = c->timing_used[1] = 0;
   c->gen = generation;
   c->n_rep = n_replicas;
   c->expected_chunks = (int)tot;
@@ -545,9 +571,17 @@ CEP_API int cep_combine(cep_ctx *c, hipStream_t s, hipEvent_t *done) {
                 (int)c->chunks.size(), c->expected_chunks);
   int rc = launch_pending(c);
   if (rc != CEP_OK) return rc;
+  // every batch of the layer ran on a used slot stream or on the ingest
+  // stream (which also staged every chunk)
   for (int i = 0; i < c->cfg.n_streams; ++i) {
-    HIPCHK(c, hipEventRecord(c->ev_ingest[i], c->st[i]));
-    HIPCHK(c, hipStreamWaitEvent(s, c->ev_ingest[i], 0));
+    if ((c->used_st >> i) & 1) {
+      HIPCHK(c, hipEventRecord(c->ev_ingest[i], c->st[i]));
+      HIPCHK(c, hipStreamWaitEvent(s, c->ev_ingest[i], 0));
+    }
+  }
+  if (s != c->ingest) {
+    HIPCHK(c, hipEventRecord(c->ev_layer_ingest, c->ingest));
+    HIPCHK(c, hipStreamWaitEvent(s, c->ev_layer_ingest, 0));
   }
   HIPCHK(c, hipEventRecord(c->ev_layer_done, s));
   if (done) *done = c->ev_layer_done;
@@ -666,8 +700,10 @@ CEP_API int cep_destroy(cep_ctx *c) {
   if (!c) return CEP_OK;
   (void)hipDeviceSynchronize();
   free_batch_records(c);
-  for (hipEvent_t e : c->timing_pool) (void)hipEventDestroy(e);
-  hipEvent_t evs[] = {c->ev_origin, c->ev_fetch_start, c->ev_fetch_ready, c->ev_layer_done};
+  for (auto &pool : c->timing_pool)
+    for (hipEvent_t e : pool) (void)hipEventDestroy(e);
+  hipEvent_t evs[] = {c->ev_origin, c->ev_fetch_start, c->ev_fetch_ready, c->ev_layer_done,
+                      c->ev_layer_ingest};
   for (hipEvent_t e : evs)
     if (e) (void)hipEventDestroy(e);
   for (int i = 0; i < 8; ++i) {
