@@ -102,8 +102,9 @@ struct Scratch {
   int32_t *cnt;        // [E]
   int32_t *off;        // [E+1]
   int32_t *off_pad;    // [E+1]
-  Tile *tiles;         // [2][max_tiles]: resident list, fetched list
-  int32_t *n_tiles;    // [2]
+  Tile *tiles;         // [4][max_tiles]: list 2*f + r for resident (f = 0) or
+                       // fetched (f = 1) experts; r = 1: 64-row remainder tiles
+  int32_t *n_tiles;    // [4]
   int32_t *pos_of;     // [max_rows * k] grouped row of each flat pair or -1
   int32_t *perm;       // [max_mpad] flat pair of each grouped row or -1
   float *wrow;         // [max_mpad] routing coefficient of each grouped row
@@ -132,21 +133,26 @@ hipError_t launch_ingest(const Arena &a, int row0, int n_rows, int k, int E, int
                          int t_max, const int32_t *token_idx, const void *x, size_t x_row_bytes,
                          const int32_t *topk_id, const float *topk_w, uint32_t *err,
                          hipStream_t s);
+// split_cu > 0 (bf16 batches with 256-row tiles): the scan may move each
+// expert's last partial tile of at most 128 rows to 64-row remainder tiles
+// when its makespan estimate for split_cu compute units and GEMM1's
+// n_tiles_n 256-wide column tiles improves.
 hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int E,
                         int align, int expected_pairs, int max_mpad, int max_tiles,
-                        uint64_t fetched_mask, int x_dtype, bool fp8, int d, uint32_t *err,
-                        hipStream_t s);
+                        uint64_t fetched_mask, int x_dtype, bool fp8, int d, int split_cu,
+                        int n_tiles_n, uint32_t *err, hipStream_t s);
 hipError_t launch_combine(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int d,
                           float *out, hipStream_t s);
 
-// grouped GEMMs over tile list `which` (0 resident, 1 fetched) of a scratch
-// whose lists hold list_cap tiles each; the grid covers grid_tiles M tiles
-// with M tile `align` (the batch's row alignment)
-hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles, int align,
-                        const BlobTable &bt, const BlobLayout &L, bool fp8, int d, int I,
-                        hipStream_t s);
-hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles, int align,
-                        const BlobTable &bt, const BlobLayout &L, bool fp8, int d, int I,
-                        hipStream_t s);
+// grouped GEMMs over the tile lists of `which` (0 resident, 1 fetched) of a
+// scratch whose lists hold list_cap tiles each; the grid covers grid_tiles
+// M tiles with M tile `align` (the batch's row alignment), then, if
+// split_tiles > 0, up to split_tiles 64-row remainder tiles
+hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles,
+                        int split_tiles, int align, const BlobTable &bt, const BlobLayout &L,
+                        bool fp8, int d, int I, hipStream_t s);
+hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles,
+                        int split_tiles, int align, const BlobTable &bt, const BlobLayout &L,
+                        bool fp8, int d, int I, hipStream_t s);
 
 }  // namespace cep

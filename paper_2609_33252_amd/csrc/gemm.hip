@@ -8,11 +8,11 @@
 namespace cep {
 namespace {
 
-GemmArgs base_args(const Scratch &sc, int which, int list_cap, int grid_tiles,
+GemmArgs base_args(const Scratch &sc, int list, int list_cap, int grid_tiles,
                    const BlobTable &bt) {
   GemmArgs g{};
-  g.tiles = sc.tiles + (size_t)which * list_cap;
-  g.n_tiles = sc.n_tiles + which;
+  g.tiles = sc.tiles + (size_t)list * list_cap;
+  g.n_tiles = sc.n_tiles + list;
   g.max_tiles = grid_tiles;
   g.bt = bt;
   g.s_ld = sc.s_ld;
@@ -20,21 +20,29 @@ GemmArgs base_args(const Scratch &sc, int which, int list_cap, int grid_tiles,
 }
 
 template <bool SWIGLU>
-hipError_t launch_any(const GemmArgs &g, int grid_tiles, int align, bool fp8, hipStream_t s) {
+hipError_t launch_any(const GemmArgs &g, int grid_tiles, int split_tiles, int align, bool fp8,
+                      const Scratch &sc, int which, int list_cap, hipStream_t s) {
   if (fp8) {
     if (align != kFp8TileM) return hipErrorInvalidValue;
     return launch_fp8<SWIGLU>(g, grid_tiles, s);
   }
-  return launch_bf16<SWIGLU>(g, grid_tiles, align, s);
+  hipError_t e = launch_bf16<SWIGLU>(g, grid_tiles, align, s);
+  if (e != hipSuccess || split_tiles <= 0) return e;
+  // remainder tiles: same operands and output, the 64-row list
+  GemmArgs r = g;
+  r.tiles = sc.tiles + (size_t)(2 * which + 1) * list_cap;
+  r.n_tiles = sc.n_tiles + 2 * which + 1;
+  r.max_tiles = split_tiles;
+  return launch_bf16<SWIGLU>(r, split_tiles, kBf16SmallTileM, s);
 }
 
 }  // namespace
 
-hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles, int align,
-                        const BlobTable &bt, const BlobLayout &L, bool fp8, int d, int I,
-                        hipStream_t s) {
+hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles,
+                        int split_tiles, int align, const BlobTable &bt, const BlobLayout &L,
+                        bool fp8, int d, int I, hipStream_t s) {
   if (grid_tiles <= 0) return hipSuccess;
-  GemmArgs g = base_args(sc, which, list_cap, grid_tiles, bt);
+  GemmArgs g = base_args(sc, 2 * which, list_cap, grid_tiles, bt);
   g.A = (const uint8_t *)sc.xg;
   g.As = sc.xs;
   g.K = d;
@@ -43,14 +51,14 @@ hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_til
   g.bs_off = L.s1_off;
   g.out = sc.h;
   g.out_s = sc.hs;
-  return launch_any<true>(g, grid_tiles, align, fp8, s);
+  return launch_any<true>(g, grid_tiles, split_tiles, align, fp8, sc, which, list_cap, s);
 }
 
-hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles, int align,
-                        const BlobTable &bt, const BlobLayout &L, bool fp8, int d, int I,
-                        hipStream_t s) {
+hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles,
+                        int split_tiles, int align, const BlobTable &bt, const BlobLayout &L,
+                        bool fp8, int d, int I, hipStream_t s) {
   if (grid_tiles <= 0) return hipSuccess;
-  GemmArgs g = base_args(sc, which, list_cap, grid_tiles, bt);
+  GemmArgs g = base_args(sc, 2 * which, list_cap, grid_tiles, bt);
   g.A = (const uint8_t *)sc.h;
   g.As = sc.hs;
   g.K = I;
@@ -59,7 +67,7 @@ hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_til
   g.bs_off = L.s2_off;
   g.out = sc.y;
   g.wrow = sc.wrow;
-  return launch_any<false>(g, grid_tiles, align, fp8, s);
+  return launch_any<false>(g, grid_tiles, split_tiles, align, fp8, sc, which, list_cap, s);
 }
 
 }  // namespace cep

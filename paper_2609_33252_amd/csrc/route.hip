@@ -97,10 +97,11 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_count(const int32_t *__
 __global__ __launch_bounds__(256) void k_route_scan(Scratch sc, int n_blocks, int E, int align,
                                                     int expected_pairs, int max_mpad,
                                                     int max_tiles, uint64_t fetched_mask,
-                                                    uint32_t *err) {
+                                                    int split_cu, int n_tiles_n, uint32_t *err) {
   __shared__ int s_part[256];  // [group][expert]: range sum, then exclusive prefix
   __shared__ int s_cnt[kMaxExperts], s_off[kMaxExperts + 1], s_pad[kMaxExperts + 1];
-  __shared__ int s_tile0[kMaxExperts];
+  __shared__ int s_tile0[kMaxExperts], s_rtile0[kMaxExperts];
+  __shared__ int s_split;
   const int tid = threadIdx.x;
   const int G = 256 / E, e = tid % E, grp = tid / E;
   const bool mine = grp < G;
@@ -123,23 +124,51 @@ __global__ __launch_bounds__(256) void k_route_scan(Scratch sc, int n_blocks, in
   }
   __syncthreads();
   if (tid == 0) {
+    // Remainder split: an expert's last partial tile of at most align/2 rows
+    // can run as 64-row tiles (64 x 128 outputs, two workgroups per CU, about
+    // a quarter of a full tile's time each) instead of a full tile.  Split
+    // when that shortens the estimated makespan in full-tile rounds of
+    // split_cu CUs; results are the same either way.
+    int split = 0;
+    if (split_cu > 0) {
+      long long full = 0, kept = 0, rem = 0;
+      for (int x = 0; x < E; ++x) {
+        const int c = s_cnt[x], r = c % align;
+        full += (c + align - 1) / align;
+        kept += c / align + (r > align / 2 ? 1 : 0);
+        rem += (r > 0 && r <= align / 2) ? (r + kBf16SmallTileM - 1) / kBf16SmallTileM : 0;
+      }
+      const long long wn = n_tiles_n, cu = split_cu;
+      const long long rounds_full = (full * wn + cu - 1) / cu;
+      const long long rounds_kept = (kept * wn + cu - 1) / cu;
+      const long long rounds_rem = (rem * 2 * wn + 2 * cu - 1) / (2 * cu);  // quarter rounds
+      split = rem > 0 && 4 * rounds_kept + rounds_rem < 4 * rounds_full;
+    }
+    s_split = split;
     int o = 0, op = 0;
-    int t0[2] = {0, 0};
+    int t0[4] = {0, 0, 0, 0};
     for (int x = 0; x < E; ++x) {
       s_off[x] = o;
       s_pad[x] = op;
       const int which = (int)((fetched_mask >> x) & 1);
-      s_tile0[x] = t0[which];
-      t0[which] += (s_cnt[x] + align - 1) / align;
-      o += s_cnt[x];
-      op += (s_cnt[x] + align - 1) / align * align;
+      const int c = s_cnt[x], r = c % align;
+      const bool rem = split && r > 0 && r <= align / 2;
+      s_tile0[x] = t0[2 * which];
+      s_rtile0[x] = t0[2 * which + 1];
+      t0[2 * which] += rem ? c / align : (c + align - 1) / align;
+      t0[2 * which + 1] += rem ? (r + kBf16SmallTileM - 1) / kBf16SmallTileM : 0;
+      o += c;
+      op += (c + align - 1) / align * align;
     }
     s_off[E] = o;
     s_pad[E] = op;
     if (o != expected_pairs) atomicOr(err, kErrPairCount);
-    if (op > max_mpad || t0[0] > max_tiles || t0[1] > max_tiles) atomicOr(err, kErrOverflow);
-    sc.n_tiles[0] = min(t0[0], max_tiles);
-    sc.n_tiles[1] = min(t0[1], max_tiles);
+    bool over = op > max_mpad;
+    for (int l = 0; l < 4; ++l) {
+      over = over || t0[l] > max_tiles;
+      sc.n_tiles[l] = min(t0[l], max_tiles);
+    }
+    if (over) atomicOr(err, kErrOverflow);
   }
   __syncthreads();
   if (tid <= E) {
@@ -161,13 +190,25 @@ __global__ __launch_bounds__(256) void k_route_scan(Scratch sc, int n_blocks, in
   }
   if (tid < E) {
     const int which = (int)((fetched_mask >> tid) & 1);
-    Tile *list = sc.tiles + (size_t)which * max_tiles;
-    const int nt = (s_cnt[tid] + align - 1) / align;
+    const int c = s_cnt[tid], r = c % align;
+    const bool rem = s_split && r > 0 && r <= align / 2;
+    Tile *list = sc.tiles + (size_t)(2 * which) * max_tiles;
+    const int nt = rem ? c / align : (c + align - 1) / align;
     for (int q = 0; q < nt; ++q) {
       const int ti = s_tile0[tid] + q;
       const int row0 = s_pad[tid] + q * align;
       if (ti >= max_tiles || row0 + align > max_mpad) break;
-      list[ti] = Tile{tid, row0, min(align, s_cnt[tid] - q * align), 0};
+      list[ti] = Tile{tid, row0, min(align, c - q * align), 0};
+    }
+    if (rem) {
+      Tile *rlist = sc.tiles + (size_t)(2 * which + 1) * max_tiles;
+      const int base = s_pad[tid] + nt * align;
+      for (int q = 0; q * kBf16SmallTileM < r; ++q) {
+        const int ti = s_rtile0[tid] + q;
+        const int row0 = base + q * kBf16SmallTileM;
+        if (ti >= max_tiles || row0 + kBf16SmallTileM > max_mpad) break;
+        rlist[ti] = Tile{tid, row0, min(kBf16SmallTileM, r - q * kBf16SmallTileM), 0};
+      }
     }
   }
 }
@@ -436,15 +477,15 @@ hipError_t launch_ingest(const Arena &a, int row0, int n_rows, int k, int E, int
 
 hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int E,
                         int align, int expected_pairs, int max_mpad, int max_tiles,
-                        uint64_t fetched_mask, int x_dtype, bool fp8, int d, uint32_t *err,
-                        hipStream_t s) {
+                        uint64_t fetched_mask, int x_dtype, bool fp8, int d, int split_cu,
+                        int n_tiles_n, uint32_t *err, hipStream_t s) {
   const int n_flat = n_rows * k;
   const int nb = (n_flat + kRoutePairs - 1) / kRoutePairs;
   if (nb == 0) return hipSuccess;
   hipLaunchKernelGGL(k_route_count, dim3(nb), dim3(kRouteThreads), 0, s,
                      a.ids + (size_t)row0 * k, n_flat, E, sc.blk_cnt);
   hipLaunchKernelGGL(k_route_scan, dim3(1), dim3(256), 0, s, sc, nb, E, align, expected_pairs,
-                     max_mpad, max_tiles, fetched_mask, err);
+                     max_mpad, max_tiles, fetched_mask, split_cu, n_tiles_n, err);
   hipLaunchKernelGGL(k_route_scatter, dim3(nb), dim3(kRouteThreads), 0, s, a, sc, row0, n_flat,
                      k, E, max_mpad);
   // grouped rows: at most every pair plus one partial tile per expert

@@ -60,6 +60,7 @@ struct cep_ctx {
   int arena_cap = 0;
   uint32_t *d_err = nullptr;
   int max_pairs = 0, max_mpad = 0, max_tiles = 0, max_blocks = 0, max_rows = 0;
+  int n_cu = 0;  // compute units of the device (tile-plan makespan estimate)
   hipStream_t ingest = nullptr;
   hipStream_t st[8] = {}, helper[8] = {};
   // slot streams and helper streams that ran batches since the last layer
@@ -219,8 +220,13 @@ int launch_pending(cep_ctx *c) {
     HIPCHK(c, hipStreamWaitEvent(s, c->ev_ingest[slot], 0));
   }
   HIPCHK(c, hipEventRecord(b.ev_start, s));
+  // 256-row bf16 tiles: the scan may move small remainders to 64-row tiles
+  // (at most two per expert), run by a second launch of the 64-row kernel
+  const bool split = !c->fp8 && A == kBf16TileM;
+  const int split_tiles = split ? 2 * E : 0;
   HIPCHK(c, launch_route(c->arena, sc, b.row0, b.n_rows, k, E, A, P, c->max_mpad, c->max_tiles,
-                         c->fetched_mask, cfg.x_dtype, c->fp8, d, c->d_err, s));
+                         c->fetched_mask, cfg.x_dtype, c->fp8, d, split ? c->n_cu : 0,
+                         2 * I / kBf16TileN, c->d_err, s));
   HIPCHK(c, hipEventRecord(b.ev_phase[0], s));
 
   BlobTable bt{c->w_res, c->fetch_buf, c->L.bytes, c->fetched_mask};
@@ -232,13 +238,13 @@ int launch_pending(cep_ctx *c) {
     HIPCHK(c, hipEventRecord(c->ev_routed[slot], s));
     HIPCHK(c, hipStreamWaitEvent(h, c->ev_routed[slot], 0));
     HIPCHK(c, hipStreamWaitEvent(h, c->ev_fetch_ready, 0));
-    HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, A, bt, c->L, c->fp8, d, I, h));
-    HIPCHK(c, launch_gemm2(sc, 1, c->max_tiles, tiles, A, bt, c->L, c->fp8, d, I, h));
+    HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->fp8, d, I, h));
+    HIPCHK(c, launch_gemm2(sc, 1, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->fp8, d, I, h));
     HIPCHK(c, hipEventRecord(c->ev_helper[slot], h));
   }
-  HIPCHK(c, launch_gemm1(sc, 0, c->max_tiles, tiles, A, bt, c->L, c->fp8, d, I, s));
+  HIPCHK(c, launch_gemm1(sc, 0, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->fp8, d, I, s));
   HIPCHK(c, hipEventRecord(b.ev_phase[1], s));
-  HIPCHK(c, launch_gemm2(sc, 0, c->max_tiles, tiles, A, bt, c->L, c->fp8, d, I, s));
+  HIPCHK(c, launch_gemm2(sc, 0, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->fp8, d, I, s));
   HIPCHK(c, hipEventRecord(b.ev_phase[2], s));
   if (b.helper) HIPCHK(c, hipStreamWaitEvent(s, c->ev_helper[slot], 0));
   HIPCHK(c, launch_combine(c->arena, sc, b.row0, b.n_rows, k, d, c->out, s));
@@ -322,9 +328,11 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
     return fail(nullptr, CEP_EINVAL, "cep_init_experts: NULL weight or scale pointer");
   cep_ctx *c = new cep_ctx();
   c->cfg = *cfg;
-  if (hipGetDevice(&c->device) != hipSuccess) {
+  if (hipGetDevice(&c->device) != hipSuccess ||
+      hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, c->device) !=
+          hipSuccess) {
     delete c;
-    return fail(nullptr, CEP_EHIP, "cep_init_experts: hipGetDevice failed");
+    return fail(nullptr, CEP_EHIP, "cep_init_experts: device query failed");
   }
   const int E = cfg->n_local_experts, k = cfg->top_k, d = cfg->d_model, I = cfg->d_ff;
   c->fp8 = cfg->w_dtype == CEP_FP8_E4M3_B128;
@@ -362,8 +370,8 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
     sc.cnt = (int32_t *)A(sizeof(int32_t) * E);
     sc.off = (int32_t *)A(sizeof(int32_t) * (E + 1));
     sc.off_pad = (int32_t *)A(sizeof(int32_t) * (E + 1));
-    sc.tiles = (Tile *)A(sizeof(Tile) * 2 * c->max_tiles);
-    sc.n_tiles = (int32_t *)A(sizeof(int32_t) * 2);
+    sc.tiles = (Tile *)A(sizeof(Tile) * 4 * c->max_tiles);
+    sc.n_tiles = (int32_t *)A(sizeof(int32_t) * 4);
     sc.pos_of = (int32_t *)A(sizeof(int32_t) * (size_t)c->max_rows * k);
     sc.perm = (int32_t *)A(sizeof(int32_t) * c->max_mpad);
     sc.wrow = (float *)A(sizeof(float) * c->max_mpad);

@@ -210,6 +210,24 @@ def test_large_and_small_m_tiles_agree_bitwise():
     U.compare(wl, a, U.reference(wl))
 
 
+def test_remainder_tiles_agree_bitwise():
+    # Full-size wait-all batch: two experts overflow 4 full 256-row tiles by a
+    # few rows, which the tile plan runs as 64-row remainder tiles next to the
+    # 256-row tiles (fewer full-tile rounds on a 256-CU device).  Per-chunk
+    # batches use 64-row tiles only.  Same K order, same bits.
+    wl = W.generate("sync_d4096", 0)
+    cnt = np.bincount(wl.topk_local[wl.topk_local >= 0], minlength=wl.cfg["E"])
+    assert any(0 < c % 256 <= 128 for c in cnt)
+    run = harness.Runner(wl, n_streams=1)
+    run.run(policy=cep.CEP_WAIT_ALL)
+    a = _out(run)
+    run.out.zero_()
+    run.run(policy=cep.CEP_PER_CHUNK)
+    b = _out(run)
+    run.close()
+    assert np.array_equal(a, b)
+
+
 def test_fetched_experts_equal_resident_bitwise():
     wl = W.generate("fp8_fetch_d6144", 0, T=256, cpr=2)
     a = harness.Runner(wl, n_streams=2, use_fetch=True)
