@@ -39,7 +39,7 @@ namespace {
 template <int BM, int BN, int BK, int STAGES, int OCC, bool PIPE, bool SWIGLU>
 __global__ __launch_bounds__(256, OCC) void k_gemm_bf16(GemmArgs g) {
   static_assert(BK == 32 || BK == 64, "LDS swizzle covers 4 or 8 chunks per row");
-  static_assert(STAGES >= 3 && STAGES <= 5, "wait counts below");
+  static_assert(STAGES >= 3 && STAGES <= 8, "wait counts below");
   constexpr int CH = BK / 8;                  // 16-byte chunks per LDS row
   constexpr int RPS = 1024 / (BK * 2);        // rows per 1 KB load segment
   constexpr int SH = CH == 4 ? 2 : 1;         // swz(r) = (r >> SH) & (CH - 1)

@@ -35,31 +35,40 @@ struct GemmArgs {
 
 __device__ inline float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
 
-// Grouped tile order: GM consecutive M tiles x all N tiles form a group, M
-// fastest inside it, so the workgroups an XCD runs together share GM row
-// panels of A and the weight panels of their N tiles in that XCD's L2.
+// Grouped tile order over the n_live M tiles: GM consecutive M tiles x all
+// N tiles form a group, M fastest inside it, so the workgroups an XCD runs
+// together share GM row panels of A and the weight panels of their N tiles
+// in that XCD's L2.  The last group holds the n_live % GM remaining M tiles,
+// so the order covers live tiles only.
 template <int GM>
-__device__ inline void tile_of(int L, int n_tiles_n, int *mt, int *nt) {
-  const int grp = L / (GM * n_tiles_n), idx = L % (GM * n_tiles_n);
-  *mt = grp * GM + idx % GM;
-  *nt = idx / GM;
+__device__ inline void tile_of(int L, int n_live, int n_tiles_n, int *mt, int *nt) {
+  const int full = n_live / GM, full_work = full * GM * n_tiles_n;
+  if (L < full_work) {
+    const int grp = L / (GM * n_tiles_n), idx = L % (GM * n_tiles_n);
+    *mt = grp * GM + idx % GM;
+    *nt = idx / GM;
+  } else {
+    const int gl = n_live - full * GM, idx = L - full_work;
+    *mt = full * GM + idx % gl;
+    *nt = idx / gl;
+  }
 }
 
 // Work item of this workgroup, balanced over the XCDs.  The grid covers the
 // host's upper bound on M tiles; the live count is on the device.  The live
-// work W (whole groups) is cut into 8 contiguous shares, one per XCD
+// work W = n_live x N tiles is cut into 8 contiguous shares, one per XCD
 // (workgroup ids are dispatched round-robin over the XCDs), so the surplus
 // workgroups of the bound never leave an XCD idle while another holds the
 // tail.  Returns false for a surplus workgroup.
 template <int GM>
 __device__ inline bool balanced_tile(int n_live, int n_tiles_n, int *mt, int *nt) {
-  const int W = (n_live + GM - 1) / GM * GM * n_tiles_n;
+  const int W = n_live * n_tiles_n;
   const int C = (W + 7) / 8;
   const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
   const int L = x * C + j;
   if (j >= C || L >= W) return false;
-  tile_of<GM>(L, n_tiles_n, mt, nt);
-  return *mt < n_live;
+  tile_of<GM>(L, n_live, n_tiles_n, mt, nt);
+  return true;
 }
 
 // Grid for balanced_tile: at least the bound's work, a multiple of 8.
@@ -104,6 +113,16 @@ __device__ inline void wait_vmcnt() {
 // of this wave are outstanding.
 template <int PER, int R>
 __device__ inline void wait_stages(int r) {
+  static_assert(R <= 6, "deeper rings need more cases");
+  if constexpr (R >= 6) {
+    if (r >= 6) return wait_vmcnt<6 * PER>();
+  }
+  if constexpr (R >= 5) {
+    if (r >= 5) return wait_vmcnt<5 * PER>();
+  }
+  if constexpr (R >= 4) {
+    if (r >= 4) return wait_vmcnt<4 * PER>();
+  }
   if constexpr (R >= 3) {
     if (r >= 3) return wait_vmcnt<3 * PER>();
   }
