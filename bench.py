@@ -138,6 +138,79 @@ def sweep(args):
     run.close()
 
 
+def calibrate_theta(args):
+    """Launch-threshold calibration: FFN throughput of one grouped invocation
+    against its expert-token count N (prefixes of the streaming workload's
+    chunks in arrival order, wait-all over each prefix), the library's
+    profile of it, theta(rho) and F(N).  One JSON line per profiled count,
+    one per held-out count (F(N) prediction vs measured), and a summary."""
+    import statistics
+
+    import torch
+    from paper_2609_33252_amd import cep, harness, workload as W
+
+    wl = W.generate(args.workload, 0, cpr=args.cal_cpr)
+    c = wl.cfg
+    run = harness.Runner(wl, n_streams=1)
+    order = sorted(range(len(run.chunks)), key=lambda i: run.chunks[i].arrival_ms)
+    cum, tot = [], 0
+    for i in order:
+        tot += run.chunks[i].n_pairs
+        cum.append(tot)
+
+    def measure(m):
+        # batch span (routing .. combine) of a layer over the first m+1 chunks
+        sub = order[:m + 1]
+        span = []
+        for it in range(args.warmup + args.steps):
+            run.run_subset(sub)
+            torch.cuda.synchronize()
+            if it >= args.warmup:
+                b = run.stats()["batches"][0]
+                span.append(b["end_ms"] - b["start_ms"])
+        return statistics.median(span)
+
+    def prefix_for(target):
+        return next(m for m, v in enumerate(cum) if v >= target)
+
+    counts, tput = [], []
+    target = 16
+    while True:
+        m = prefix_for(min(target, tot))
+        if not counts or cum[m] > counts[-1]:
+            ms = measure(m)
+            counts.append(cum[m])
+            tput.append(cum[m] / ms)
+            print(json.dumps({"profile_n": cum[m], "ms": round(ms, 5),
+                              "pairs_per_ms": round(cum[m] / ms, 2),
+                              "tflops": round(6.0 * c["d"] * c["I"] * cum[m] / ms / 1e9, 2)}),
+                  flush=True)
+        if target >= tot:
+            break
+        target *= 2
+    prof = cep.FfnProfile(counts, tput)
+    # held-out counts (geometric midpoints): model F(N) against measurement
+    errs = []
+    for a, b in zip(counts, counts[1:]):
+        m = prefix_for(int((a * b) ** 0.5))
+        if cum[m] in (a, b):
+            continue
+        ms = measure(m)
+        pred = prof.latency(cum[m])
+        errs.append(abs(pred - ms) / ms)
+        print(json.dumps({"heldout_n": cum[m], "measured_ms": round(ms, 5),
+                          "model_ms": round(pred, 5), "rel_err": round(errs[-1], 4)}),
+              flush=True)
+    line = {"workload": args.workload, "chunks_per_replica": args.cal_cpr, "rho": args.rho,
+            "theta": prof.theta(args.rho), "peak_pairs_per_ms": round(prof.peak, 2),
+            "eta": {str(n): round(prof.eta(n), 4) for n in counts},
+            "heldout_mean_rel_err": round(sum(errs) / len(errs), 4) if errs else None}
+    print(json.dumps(line), flush=True)
+    prof.close()
+    cep.cep_get_status(run.ctx)
+    run.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -155,7 +228,20 @@ def main():
     ap.add_argument("--thetas", default="32,64,128,256,512,1024,2048,4096")
     ap.add_argument("--time-scale", type=float, default=1.0,
                     help="scale of the arrival schedule in --sweep (1 = as generated)")
+    ap.add_argument("--calibrate-theta", action="store_true",
+                    help="profile FFN throughput vs expert-token count; theta(rho) and F(N)")
+    ap.add_argument("--rho", type=float, default=0.9)
+    ap.add_argument("--cal-cpr", type=int, default=64,
+                    help="chunks per replica of the calibration workload (finer prefixes)")
     args = ap.parse_args()
+    if args.calibrate_theta:
+        if args.gpus != 1:
+            print("bench.py runs on one GPU only", file=sys.stderr)
+            sys.exit(2)
+        if args.workload == "sync_d4096":
+            args.workload = "zipf_imbalanced_d7168"
+        calibrate_theta(args)
+        return
     if args.sweep:
         if args.gpus != 1:
             print("bench.py runs on one GPU only", file=sys.stderr)

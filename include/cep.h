@@ -217,6 +217,42 @@ const char *cep_last_error(const cep_ctx *ctx);
 /* Wait for all work, release every resource.  NULL is a no-op. */
 int cep_destroy(cep_ctx *ctx);
 
+/* ------------------------------------------------------------------------
+ * FFN throughput profile (host only; no GPU work).
+ *
+ * streamFFN's launch threshold theta is the smallest profiled expert-token
+ * count whose FFN throughput reaches a fraction rho of the observed peak
+ * (Section 3.2, "Launch threshold"); the FFN latency model is
+ * F(N) = N / (eta(N) * P_peak), eta(N) in (0, 1] the throughput normalised
+ * to the observed peak P_peak (Section 3.3, Eq. ffn-throughput-latency).
+ * Between profiled counts eta is linear in N; below the smallest profiled
+ * count n_0, F(N) = F(n_0); above the largest, eta keeps its last value.
+ * Failures return CEP_EINVAL / CEP_ENOMEM with a message in
+ * cep_last_error(NULL).
+ */
+typedef struct cep_ffn_profile cep_ffn_profile;
+
+/* n[count]: profiled expert-token counts, positive and strictly increasing;
+ * tput[count]: FFN throughput measured at each, positive and finite, in
+ * expert tokens per time unit (F is then in that unit).  Both host arrays,
+ * copied.  *out receives a profile owned by the caller. */
+int cep_profile_create(const int64_t *n, const double *tput, int count, cep_ffn_profile **out);
+
+/* Observed peak throughput P_peak (0 for NULL). */
+double cep_profile_peak(const cep_ffn_profile *p);
+
+/* *theta = smallest profiled count with tput / P_peak >= rho, rho in (0, 1]. */
+int cep_profile_theta(const cep_ffn_profile *p, double rho, int64_t *theta);
+
+/* *eta = eta(N) for N >= 1. */
+int cep_profile_eta(const cep_ffn_profile *p, int64_t N, double *eta);
+
+/* *latency = F(N) for N >= 0 (F(0) = 0). */
+int cep_profile_latency(const cep_ffn_profile *p, int64_t N, double *latency);
+
+/* Release a profile; NULL is a no-op. */
+void cep_profile_destroy(cep_ffn_profile *p);
+
 #ifdef __cplusplus
 }
 #endif

@@ -18,7 +18,7 @@ OUT = os.path.join(HERE, "libcep.so")
 OBJ = os.path.join(HERE, "_build")
 ARCH = "gfx950"
 
-SOURCES = ["route.hip", "gemm.hip", "gemm_bf16.hip", "gemm_fp8.hip", "runtime.hip"]
+SOURCES = ["route.hip", "gemm.hip", "gemm_bf16.hip", "gemm_fp8.hip", "runtime.hip", "profile.cpp"]
 # Per-source extra flags.  The e4m3 GEMM promotes every MFMA result with
 # VALU arithmetic; taking MFMA results in VGPRs saves one accvgpr read per
 # promoted element.
@@ -53,7 +53,7 @@ def build(verbose: bool = False) -> str:
     objs = []
     cmds = []
     for src in SOURCES:
-        o = os.path.join(OBJ, src.replace(".hip", ".o"))
+        o = os.path.join(OBJ, os.path.splitext(src)[0] + ".o")
         objs.append(o)
         cmds.append([cc, *CFLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", o])
     with ThreadPoolExecutor(min(len(cmds), os.cpu_count() or 1)) as ex:

@@ -22,7 +22,9 @@ STATUS_NAMES = {0: "CEP_OK", -1: "CEP_EINVAL", -2: "CEP_ENOMEM", -3: "CEP_EHIP",
 EXPORTED = ["cep_packed_expert_bytes", "cep_pack_experts", "cep_init_experts", "cep_set_policy",
             "cep_begin_layer", "cep_submit_chunk", "cep_flush", "cep_weight_fetch",
             "cep_combine", "cep_get_batch_routing", "cep_get_batch_count", "cep_get_stats",
-            "cep_get_status", "cep_last_error", "cep_destroy"]
+            "cep_get_status", "cep_last_error", "cep_destroy", "cep_profile_create",
+            "cep_profile_peak", "cep_profile_theta", "cep_profile_eta", "cep_profile_latency",
+            "cep_profile_destroy"]
 
 
 class cep_config(ctypes.Structure):
@@ -78,8 +80,18 @@ def lib():
         L.cep_last_error.argtypes = [vp]
         L.cep_last_error.restype = ctypes.c_char_p
         L.cep_destroy.argtypes = [vp]
+        i64, f64 = ctypes.c_int64, ctypes.c_double
+        L.cep_profile_create.argtypes = [P(i64), P(f64), i32, P(vp)]
+        L.cep_profile_peak.argtypes = [vp]
+        L.cep_profile_peak.restype = f64
+        L.cep_profile_theta.argtypes = [vp, f64, P(i64)]
+        L.cep_profile_eta.argtypes = [vp, i64, P(f64)]
+        L.cep_profile_latency.argtypes = [vp, i64, P(f64)]
+        L.cep_profile_destroy.argtypes = [vp]
+        L.cep_profile_destroy.restype = None
         for name in EXPORTED:
-            if name not in ("cep_packed_expert_bytes", "cep_last_error"):
+            if name not in ("cep_packed_expert_bytes", "cep_last_error", "cep_profile_peak",
+                            "cep_profile_destroy"):
                 getattr(L, name).restype = i32
         _lib = L
     return _lib
@@ -239,3 +251,48 @@ def cep_last_error(ctx) -> str:
 
 def cep_destroy(ctx):
     _check(None, lib().cep_destroy(ctx))
+
+
+# ------------------------------------------------------------ FFN profile
+class FfnProfile:
+    """Owns a cep_ffn_profile: launch threshold theta(rho) and F(N)."""
+
+    def __init__(self, counts, tput):
+        n = list(counts)
+        if len(n) != len(tput):
+            raise ValueError("counts and throughputs differ in length")
+        a = (ctypes.c_int64 * max(len(n), 1))(*n)
+        b = (ctypes.c_double * max(len(n), 1))(*[float(x) for x in tput])
+        h = ctypes.c_void_p()
+        _check(None, lib().cep_profile_create(a, b, len(n), ctypes.byref(h)))
+        self.handle = h.value
+
+    @property
+    def peak(self) -> float:
+        return lib().cep_profile_peak(self.handle)
+
+    def theta(self, rho: float) -> int:
+        out = ctypes.c_int64()
+        _check(None, lib().cep_profile_theta(self.handle, rho, ctypes.byref(out)))
+        return out.value
+
+    def eta(self, n: int) -> float:
+        out = ctypes.c_double()
+        _check(None, lib().cep_profile_eta(self.handle, n, ctypes.byref(out)))
+        return out.value
+
+    def latency(self, n: int) -> float:
+        out = ctypes.c_double()
+        _check(None, lib().cep_profile_latency(self.handle, n, ctypes.byref(out)))
+        return out.value
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().cep_profile_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

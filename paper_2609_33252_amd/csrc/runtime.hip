@@ -108,6 +108,18 @@ int fail(cep_ctx *c, int code, const char *fmt, ...) {
   return code;
 }
 
+}  // namespace
+
+namespace cep {
+// records the message of a failure that has no context (cep_last_error(NULL))
+int set_global_error(int code, const char *msg) {
+  g_err = msg;
+  return code;
+}
+}  // namespace cep
+
+namespace {
+
 #define HIPCHK(ctx, call)                                                              \
   do {                                                                                 \
     hipError_t e_ = (call);                                                            \

@@ -139,6 +139,23 @@ class Runner:
                                  ch.x, ch.ids, ch.w, ev)
         return cep.cep_combine(ctx, stream)
 
+    def run_subset(self, indices, stream=None):
+        """One wait-all layer over the chunks `indices` (in that order) only,
+        with resident inputs: a single grouped invocation of their pairs."""
+        ctx = self.ctx
+        stream = torch.cuda.current_stream(self.device) if stream is None else stream
+        cpr = [0] * len(self.chunks_per_replica)
+        for i in indices:
+            cpr[self.chunks[i].replica] += 1
+        cep.cep_set_policy(ctx, cep.CEP_WAIT_ALL, 1, 1)
+        self.gen += 1
+        cep.cep_begin_layer(ctx, self.gen, cpr, self.out)
+        for i in indices:
+            ch = self.chunks[i]
+            cep.cep_submit_chunk(ctx, self.gen, ch.replica, ch.n_rows, ch.n_pairs, ch.token_idx,
+                                 ch.x, ch.ids, ch.w, None)
+        return cep.cep_combine(ctx, stream)
+
     def stats(self):
         return cep.cep_get_stats(self.ctx)
 
