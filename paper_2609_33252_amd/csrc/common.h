@@ -15,7 +15,8 @@ constexpr int kMaxTopK = 16;
 constexpr int kMaxDim = 32768;  // largest d_model and d_ff (fp8 GEMM keeps K/128 weight scales per row in LDS)
 constexpr int kBf16TileM = 256;      // bf16 grouped GEMM tile
 constexpr int kBf16TileN = 256;
-constexpr int kFp8TileM = 128;       // e4m3 grouped GEMM tile
+constexpr int kFp8TileM = 128;       // e4m3 grouped GEMM tile (4 waves)
+constexpr int kFp8LargeTileM = 256;  // e4m3 tile for large batches (8 waves)
 constexpr int kRouteThreads = 256;   // threads per routing block
 constexpr int kRoutePairs = 2048;    // flat pairs per routing block (8 rounds of 256)
 constexpr int kInterleave = 32;      // gate/up column interleave of the packed W1
@@ -66,7 +67,7 @@ constexpr int kBf16SmallTileM = 64;  // bf16 tile for batches with few rows per 
 // weights with four times as many workgroups.  Both bf16 tiles accumulate K
 // in the same order with the same MFMA, so results do not depend on it.
 inline int batch_align(bool fp8, int pairs, int n_experts) {
-  if (fp8) return kFp8TileM;
+  if (fp8) return pairs >= kFp8LargeTileM * n_experts ? kFp8LargeTileM : kFp8TileM;
   return pairs >= kBf16TileM * n_experts ? kBf16TileM : kBf16SmallTileM;
 }
 constexpr int kMinAlign = 64;

@@ -22,10 +22,7 @@ GemmArgs base_args(const Scratch &sc, int list, int list_cap, int grid_tiles,
 template <bool SWIGLU>
 hipError_t launch_any(const GemmArgs &g, int grid_tiles, int split_tiles, int align, bool fp8,
                       const Scratch &sc, int which, int list_cap, hipStream_t s) {
-  if (fp8) {
-    if (align != kFp8TileM) return hipErrorInvalidValue;
-    return launch_fp8<SWIGLU>(g, grid_tiles, s);
-  }
+  if (fp8) return launch_fp8<SWIGLU>(g, grid_tiles, align, s);
   hipError_t e = launch_bf16<SWIGLU>(g, grid_tiles, align, s);
   if (e != hipSuccess || split_tiles <= 0) return e;
   // remainder tiles: same operands and output, the 64-row list

@@ -21,8 +21,9 @@
 namespace cep {
 namespace {
 
-// BM x BN output tile, 4 waves as 2x2, each wave (BM/2) x (BN/2) built from
-// 32x32 MFMA fragments.  K advances in steps of BK through a ring of STAGES
+// BM x BN output tile, 4 waves as WGM x (4/WGM), each wave owning a
+// (BM/WGM) x (BN/(4/WGM)) block of 32x32 MFMA fragments (for SwiGLU a
+// wave's columns hold whole gate/up pairs of 32).  K advances in steps of BK through a ring of STAGES
 // LDS buffers filled by direct global->LDS loads (no staging registers), one
 // barrier per step.  An LDS row holds BK bf16 = CH 16-byte chunks; chunk c of
 // row r lives at slot c ^ swz(r), with swz chosen so that sixteen consecutive
@@ -36,14 +37,15 @@ namespace {
 // the MFMAs; loads run STAGES-2 steps ahead.  Otherwise (weight-streaming
 // tile): fragments are read right before their MFMAs and loads run STAGES-1
 // steps ahead, which keeps more weight bytes in flight per LDS byte.
-template <int BM, int BN, int BK, int STAGES, int OCC, bool PIPE, bool SWIGLU>
+template <int BM, int BN, int BK, int STAGES, int OCC, bool PIPE, bool SWIGLU, int WGM = 2>
 __global__ __launch_bounds__(256, OCC) void k_gemm_bf16(GemmArgs g) {
   static_assert(BK == 32 || BK == 64, "LDS swizzle covers 4 or 8 chunks per row");
   static_assert(STAGES >= 3 && STAGES <= 8, "wait counts below");
   constexpr int CH = BK / 8;                  // 16-byte chunks per LDS row
   constexpr int RPS = 1024 / (BK * 2);        // rows per 1 KB load segment
   constexpr int SH = CH == 4 ? 2 : 1;         // swz(r) = (r >> SH) & (CH - 1)
-  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int WGN = 4 / WGM;  // waves along M x along N
+  constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int FM = WM / 32, FN = WN / 32;
   constexpr int A_LD = BM * BK * 2 / 1024 / 4, B_LD = BN * BK * 2 / 1024 / 4;  // per wave
   constexpr int PER = A_LD + B_LD;            // loads per thread per step
@@ -52,7 +54,7 @@ __global__ __launch_bounds__(256, OCC) void k_gemm_bf16(GemmArgs g) {
   const Tile t = g.tiles[mt];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wid >> 1, wn = wid & 1;
+  const int wm = wid / WGN, wn = wid % WGN;
   const int K = g.K, nk = K / BK;
   const char *Ag = (const char *)(g.A + (size_t)t.row0 * K * 2);
   const char *Bg = (const char *)(blob_of(g.bt, t.expert) + g.b_off + (size_t)nt * BN * K * 2);

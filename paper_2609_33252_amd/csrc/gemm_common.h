@@ -139,6 +139,6 @@ __device__ inline void wait_stages(int r) {
 template <bool SWIGLU>
 hipError_t launch_bf16(const GemmArgs &g, int grid_tiles, int align, hipStream_t s);
 template <bool SWIGLU>
-hipError_t launch_fp8(const GemmArgs &g, int grid_tiles, hipStream_t s);
+hipError_t launch_fp8(const GemmArgs &g, int grid_tiles, int align, hipStream_t s);
 
 }  // namespace cep

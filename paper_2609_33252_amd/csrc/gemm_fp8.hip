@@ -13,34 +13,38 @@
 namespace cep {
 namespace {
 
-// 128x256 output tile, K step 128 (one scale block), 4 waves side by side,
-// each owning all 128 rows x 64 columns, built from 8x4
-// v_mfma_scale_f32_16x16x128_f8f6f4 with unit hardware scales.  Every
-// instruction covers one whole K block, so its result is promoted into the
-// float32 accumulator with the product of the row's activation scale and the
-// weight block's scale: two VALU operations per output element and K block,
-// which is why each wave holds few column scale blocks (GEMM1: the gate and
-// the up block of its 32 h columns; GEMM2: one) and few rows per lane.
+// BM x 256 output tile, K step 128 (one scale block).  NW waves: four
+// column groups of 64 x (NW/4) row groups of 128, each wave owning 128 rows x
+// 64 columns built from 8x4 v_mfma_scale_f32_16x16x128_f8f6f4 with unit
+// hardware scales.  Every instruction covers one whole K block, so its
+// result is promoted into the float32 accumulator with the product of the
+// row's activation scale and the weight block's scale: two VALU operations
+// per output element and K block, which is why each wave holds few column
+// scale blocks (GEMM1: the gate and the up block of its 32 h columns; GEMM2:
+// one) and few rows per lane.  With 8 waves (two per SIMD) one wave's
+// promotion overlaps the other's MFMAs.
 //
-// Operands stream through a ring of 3 LDS stages filled by direct
-// global->LDS loads issued two steps ahead (48 KB of codes + 512 B of row
-// scales per stage).  An LDS row is 128 codes = eight 16-byte chunks; chunk c
-// of row r lives at slot c ^ ((r >> 1) & 7), so the operand reads (sixteen
-// rows at one chunk per LDS cycle) are conflict-free.
+// Operands stream through a ring of STAGES LDS stages filled by direct
+// global->LDS loads issued STAGES-1 steps ahead ((BM + 256) x 128 codes + BM
+// row scales per stage).  An LDS row is 128 codes = eight 16-byte chunks;
+// chunk c of row r lives at slot c ^ ((r >> 1) & 7), so the operand reads
+// (sixteen rows at one chunk per LDS cycle) are conflict-free.
 //
 // GEMM1 epilogue: h = silu(gate) * up over the tile's 128 h columns, one
-// amax per row (lanes, then the four waves via LDS), scale = amax / 448,
-// e4m3 codes of h / scale.
-template <bool SWIGLU>
-__global__ __launch_bounds__(256, 1) void k_gemm_fp8(GemmArgs g) {
-  constexpr int BM = 128, BN = 256, BK = 128, STAGES = 3, WN = BN / 4;
-  constexpr int A_LD = BM * BK / 1024 / 4, B_LD = BN * BK / 1024 / 4;  // loads per wave
+// amax per row (lanes, then the four column waves via LDS), scale =
+// amax / 448, e4m3 codes of h / scale.
+template <int NW, int STAGES, bool SWIGLU>
+__global__ __launch_bounds__(64 * NW, 1) void k_gemm_fp8(GemmArgs g) {
+  constexpr int BM = 128 * NW / 4, BN = 256, BK = 128, WN = BN / 4;
+  constexpr int A_LD = BM * BK / 1024 / NW, B_LD = BN * BK / 1024 / NW;  // loads per wave
   constexpr int PER = A_LD + B_LD;  // per thread per step; wave 0 adds one (row scales)
+  static_assert(BM / 4 <= 64, "one load of BM row scales");
   int mt, nt;
   if (!balanced_tile<kGroupM>(*g.n_tiles, g.N / BN, &mt, &nt)) return;
   const Tile t = g.tiles[mt];
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wn = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wid >> 2, wn = wid & 3;
   const int K = g.K, nkb = K / BK;
   const uint8_t *blob = blob_of(g.bt, t.expert);
   const char *Ag = (const char *)(g.A + (size_t)t.row0 * K);
@@ -63,16 +67,16 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp8(GemmArgs g) {
   {                                                                                \
     const int buf_ = (kb) % STAGES;                                                \
     _Pragma("unroll") for (int i = 0; i < A_LD; ++i) {                             \
-      const int seg = wn * A_LD + i;                                               \
+      const int seg = wid * A_LD + i;                                              \
       dma16(Ag + (size_t)(kb) * BK + CEP_F8_OFF(seg),                              \
             __builtin_amdgcn_readfirstlane(lds_offset(&sA[buf_][seg * 64])));      \
     }                                                                              \
     _Pragma("unroll") for (int i = 0; i < B_LD; ++i) {                             \
-      const int seg = wn * B_LD + i;                                               \
+      const int seg = wid * B_LD + i;                                              \
       dma16(Bg + (size_t)(kb) * BK + CEP_F8_OFF(seg),                              \
             __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf_][seg * 64])));      \
     }                                                                              \
-    if (wn == 0 && lane < 32)                                                      \
+    if (wid == 0 && lane < BM / 4)                                                 \
       dma16(Asg + (size_t)(kb) * g.s_ld * 4 + lane * 16,                           \
             __builtin_amdgcn_readfirstlane(lds_offset(&sAs[buf_][0])));            \
   }
@@ -93,7 +97,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp8(GemmArgs g) {
   {
     const int nbs = (SWIGLU ? BN / kInterleave : BN / 128) * nkb;
     const float *src = Bs + (size_t)nt * nbs;
-    for (int i = tid; i < nbs; i += 256) sBs[i] = src[i];
+    for (int i = tid; i < nbs; i += 64 * NW) sBs[i] = src[i];
   }
   __syncthreads();
 
@@ -104,14 +108,14 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp8(GemmArgs g) {
   const float *sb_row0 = &sBs[(SWIGLU ? 2 * wn : wn / 2) * nkb];
   const float *sb_row1 = &sBs[(SWIGLU ? 2 * wn + 1 : wn / 2) * nkb];
   for (int kb = 0; kb < nkb; ++kb) {
-    if (kb + 1 < nkb) {
-      if (wn == 0)
-        wait_vmcnt<PER + 1>();
-      else
-        wait_vmcnt<PER>();
-    } else {
-      wait_vmcnt<0>();
-    }
+    // this wave's loads of step kb are done when at most the loads of the
+    // steps issued after it are outstanding
+    const int later = min(nkb - 1, kb + STAGES - 2) - kb;
+    if (wid == 0)
+      wait_stages<PER + 1, STAGES - 2>(later);
+    else
+      wait_stages<PER, STAGES - 2>(later);
+    // every wave's loads of step kb landed; step kb-1 fully consumed
     __builtin_amdgcn_s_barrier();
     if (kb + STAGES - 1 < nkb) CEP_F8_STAGE(kb + STAGES - 1);
     const int cur = kb % STAGES;
@@ -127,7 +131,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp8(GemmArgs g) {
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int row = i * 16 + (lane & 15);
+      const int row = wm * 128 + i * 16 + (lane & 15);
       const u32x4 lo = sA[cur][row * 8 + (c0 ^ rsw)];
       const u32x4 hi = sA[cur][row * 8 + ((c0 + 1) ^ rsw)];
       const i32x8 a =
@@ -137,7 +141,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp8(GemmArgs g) {
       for (int j = 0; j < 4; ++j)
         p[j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b[j], f32x4{}, 0, 0, 0, 127,
                                                                0, 127);
-      const f32x4 sa = *(const f32x4 *)&sAs[cur][i * 16 + 4 * (lane >> 4)];
+      const f32x4 sa = *(const f32x4 *)&sAs[cur][wm * 128 + i * 16 + 4 * (lane >> 4)];
       const f32x4 s0 = sa * sb0, s1 = sa * sb1;
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] += p[j] * (j < 2 ? s0 : s1);
@@ -164,7 +168,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp8(GemmArgs g) {
         float m = fmaxf(fabsf(h[i][0][r]), fabsf(h[i][1][r]));
 #pragma unroll
         for (int sh = 1; sh < 16; sh <<= 1) m = fmaxf(m, __shfl_xor(m, sh, 16));
-        if ((lane & 15) == 0) red[wn][i * 16 + 4 * (lane >> 4) + r] = m;
+        if ((lane & 15) == 0) red[wn][wm * 128 + i * 16 + 4 * (lane >> 4) + r] = m;
       }
     __syncthreads();
     uint8_t *H = (uint8_t *)g.out;
@@ -173,7 +177,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp8(GemmArgs g) {
     for (int i = 0; i < 8; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int rt = i * 16 + 4 * (lane >> 4) + r;
+        const int rt = wm * 128 + i * 16 + 4 * (lane >> 4) + r;
         if (rt >= t.rows) continue;
         const float amax = fmaxf(fmaxf(red[0][rt], red[1][rt]), fmaxf(red[2][rt], red[3][rt]));
         const float scale = amax > 0.f ? amax / 448.0f : 1.0f;
@@ -192,7 +196,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp8(GemmArgs g) {
     for (int i = 0; i < 8; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int rt = i * 16 + 4 * (lane >> 4) + r;
+        const int rt = wm * 128 + i * 16 + 4 * (lane >> 4) + r;
         if (rt >= t.rows) continue;
         const size_t row = (size_t)t.row0 + rt;
         const float w = g.wrow[row];
@@ -206,14 +210,19 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp8(GemmArgs g) {
 }  // namespace
 
 template <bool SWIGLU>
-hipError_t launch_fp8(const GemmArgs &g, int grid_tiles, hipStream_t s) {
+hipError_t launch_fp8(const GemmArgs &g, int grid_tiles, int align, hipStream_t s) {
   if (g.N % 256 || g.K % 128 || g.K > kMaxDim || g.s_ld % 4) return hipErrorInvalidValue;
   const int grid = balanced_grid(grid_tiles, kGroupM, g.N / 256);
-  hipLaunchKernelGGL(k_gemm_fp8<SWIGLU>, dim3(grid), dim3(256), 0, s, g);
+  if (align == kFp8TileM)
+    hipLaunchKernelGGL((k_gemm_fp8<4, 3, SWIGLU>), dim3(grid), dim3(256), 0, s, g);
+  else if (align == kFp8LargeTileM)
+    hipLaunchKernelGGL((k_gemm_fp8<8, 2, SWIGLU>), dim3(grid), dim3(512), 0, s, g);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
-template hipError_t launch_fp8<true>(const GemmArgs &, int, hipStream_t);
-template hipError_t launch_fp8<false>(const GemmArgs &, int, hipStream_t);
+template hipError_t launch_fp8<true>(const GemmArgs &, int, int, hipStream_t);
+template hipError_t launch_fp8<false>(const GemmArgs &, int, int, hipStream_t);
 
 }  // namespace cep
