@@ -34,7 +34,7 @@ HBM_PEAK_GBS = 8000.0
 # by workload, valid only for the GEMM sources with this sha1 prefix (the
 # report is null once the kernel changes).
 GEMM_SOURCES = ["paper_2609_33252_amd/csrc/gemm_bf16.hip", "paper_2609_33252_amd/csrc/gemm_common.h"]
-TRAFFIC_BYTES = {"sync_d4096": ("0056644c2648", 802311884)}
+TRAFFIC_BYTES = {"sync_d4096": ("dc863139dc6c", 646127094)}
 
 
 def measured_traffic(workload):
@@ -313,7 +313,9 @@ def main():
     g1_ms = avg["gemm1_ms"] / n_launch
     achieved = g1_flops / (g1_ms * 1e-3) / 1e12
     traffic = measured_traffic(args.workload)
-    roofline = {"bound": "mfma", "kernel": "k_gemm_%s<SwiGLU> (grouped gate/up GEMM)" % dtype,
+    roofline = {"bound": "mfma",
+                "kernel": "k_gemm_%s<SwiGLU> (grouped gate/up GEMM; bf16 256-row tiles plus "
+                          "64-row remainder tiles when planned)" % dtype,
                 "achieved": round(achieved, 2), "peak": PEAK[dtype], "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK[dtype], 4), "traffic": traffic,
                 "launch_ms": round(g1_ms, 4), "flop_per_launch": g1_flops}
