@@ -189,6 +189,7 @@ def calibrate_theta(args):
             break
         target *= 2
     prof = cep.FfnProfile(counts, tput)
+    blob_bytes = run.blob_bytes
     # held-out counts (geometric midpoints): model F(N) against measurement
     errs = []
     for a, b in zip(counts, counts[1:]):
@@ -209,6 +210,63 @@ def calibrate_theta(args):
     prof.close()
     cep.cep_get_status(run.ctx)
     run.close()
+    return counts, tput, blob_bytes
+
+
+def oewf_sim(args):
+    """OEWF coordinator on simulated imbalanced layers, with the FFN latency
+    model measured on this GPU (the --calibrate-theta profile) and this
+    workload's expert size: layer completion with and without weight
+    fetching, commits, and the coordinator's call latency."""
+    import numpy as np
+
+    from paper_2609_33252_amd import cep, layer_sim
+
+    counts, tput, blob = calibrate_theta(args)
+    prof = cep.FfnProfile(counts, tput)
+    rng = np.random.default_rng(0)
+    R, E = 8, 8
+    bw = args.fetch_gbps * 1e6          # bytes per ms
+    budget = args.fetch_experts * blob
+    ratios, commits, improved = [], 0, 0
+    t_calls, n_calls = 0.0, 0
+
+    class Timed:
+        def __init__(self, co):
+            self.co = co
+
+        def __getattr__(self, name):
+            f = getattr(self.co, name)
+
+            def g(*a, **k):
+                nonlocal t_calls, n_calls
+                t0 = time.perf_counter()
+                out = f(*a, **k)
+                t_calls += time.perf_counter() - t0
+                n_calls += 1
+                return out
+            return g
+
+    for _ in range(args.oewf_layers):
+        attn, disp, tok, _ = layer_sim.random_layer(rng, R, E)
+        b = np.full(E, blob, dtype=np.int64)
+        co = cep.Coordinator(R, prof)
+        base, final, c, _ = layer_sim.simulate(Timed(co), prof.latency, attn, disp, tok, b,
+                                               budget=budget, bw=bw, rng=rng)
+        co.close()
+        ratios.append(final / base)
+        commits += c
+        improved += final < base * (1 - 1e-9)
+    line = {"oewf_layers": args.oewf_layers, "ranks": R, "experts_per_rank": E,
+            "expert_bytes": blob, "fetch_budget_experts": args.fetch_experts,
+            "fetch_gbps": args.fetch_gbps,
+            "layer_time_ratio_mean": round(float(np.mean(ratios)), 4),
+            "layer_time_ratio_min": round(float(np.min(ratios)), 4),
+            "layer_time_ratio_max": round(float(np.max(ratios)), 4),
+            "layers_improved": improved, "commits": commits,
+            "coordinator_call_us": round(t_calls / max(n_calls, 1) * 1e6, 2)}
+    print(json.dumps(line), flush=True)
+    prof.close()
 
 
 def main():
@@ -233,7 +291,19 @@ def main():
     ap.add_argument("--rho", type=float, default=0.9)
     ap.add_argument("--cal-cpr", type=int, default=64,
                     help="chunks per replica of the calibration workload (finer prefixes)")
+    ap.add_argument("--oewf-sim", action="store_true",
+                    help="calibrate, then run the OEWF coordinator on simulated layers")
+    ap.add_argument("--oewf-layers", type=int, default=200)
+    ap.add_argument("--fetch-gbps", type=float, default=153.0,
+                    help="donor-to-helper copy bandwidth (one xGMI link)")
+    ap.add_argument("--fetch-experts", type=int, default=4,
+                    help="fetch buffer capacity in experts (byte budget B_h)")
     args = ap.parse_args()
+    if args.oewf_sim:
+        if args.workload == "sync_d4096":
+            args.workload = "zipf_imbalanced_d7168"
+        oewf_sim(args)
+        return
     if args.calibrate_theta:
         if args.gpus != 1:
             print("bench.py runs on one GPU only", file=sys.stderr)

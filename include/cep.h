@@ -253,6 +253,97 @@ int cep_profile_latency(const cep_ffn_profile *p, int64_t N, double *latency);
 /* Release a profile; NULL is a no-op. */
 void cep_profile_destroy(cep_ffn_profile *p);
 
+/* ------------------------------------------------------------------------
+ * Opportunistic expert weight fetching: the coordinator (host only).
+ *
+ * The joint plan S of one MoE layer over R ranks (each an attention replica
+ * and an expert-parallel rank; Section 3.3).  Per rank: whether it still
+ * computes attention (a candidate donor), its remaining attention time A
+ * (Eq. attention-remaining) and dispatch latency D, the expert tokens N it
+ * receives, and, once out of attention, the completion time T of its own FFN
+ * work.  A donor's predicted completion is T_d(S) = A_d + D_d + F(N_d)
+ * (Eq. donor-completion), F from an FFN profile.  All times share one clock
+ * measured from the decision instant, in the profile's time unit.
+ *
+ * cep_oewf_select is Algorithm 1 (SelectWeights): the donor with the latest
+ * T_d(S) among the other ranks still in attention (lowest rank on ties); its
+ * experts that hold tokens of the helper, by descending tokens / bytes
+ * (ascending id on ties), taken greedily while they fit the byte budget B_h.
+ * One decision per rank per layer (Appendix C, "One-shot weight fetching");
+ * the helper then copies the selected experts with cep_weight_fetch.
+ * cep_oewf_evaluate is the cost-based reassignment test (Eqs.
+ * swf-completion-times, swf-admission) on the latest plan, with the helper's
+ * completion max{T_h(S), s_h + F(N_trans)} for a reassigned invocation
+ * planned to launch s_h after the decision, s_h in [0, T_h(S)] (Appendix E;
+ * alpha_h = max{0, s_h + F(N_trans) - T_h(S)} / F(N_trans)).
+ * cep_oewf_commit applies an admitted decision only if the donor's and the
+ * helper's plan entries are unchanged since the evaluation, the plan's
+ * tokens are unclaimed and the donor has not submitted them (Appendix C,
+ * "FFN reassignment commit and fallback"); then the donor's N and the
+ * helper's T change together.  Otherwise execution stays with the donor.
+ * Calls on one coordinator are serialised internally.  Failures return
+ * CEP_EINVAL / CEP_ENOMEM / CEP_EBUSY with a message in cep_last_error(NULL).
+ */
+#define CEP_OEWF_MAX_EXPERTS 64
+
+typedef struct cep_oewf cep_oewf;
+
+typedef struct {
+  int helper, donor;     /* donor -1: no candidate donor                      */
+  int n_experts;         /* selected experts; 0 = empty selection (no fetch)  */
+  int experts[CEP_OEWF_MAX_EXPERTS];     /* donor expert ids, selection order */
+  int64_t tokens[CEP_OEWF_MAX_EXPERTS];  /* helper's tokens per selected expert */
+  int64_t bytes;         /* bytes to fetch (sum of the selected b_e)          */
+  int64_t plan_id;       /* the coordinator's record of this plan (-1: none)  */
+} cep_oewf_fetch;
+
+typedef struct {
+  int admit;             /* Eq. swf-admission holds                           */
+  double Td, Th;         /* T_d(S), T_h(S)                                    */
+  double Td2, Th2;       /* T_d(S'), T_h(S')                                  */
+  double alpha;          /* alpha_h                                           */
+  int64_t plan_id, n_trans;
+  uint64_t donor_version, helper_version; /* plan entries the test read       */
+} cep_oewf_decision;
+
+/* A coordinator for n_ranks ranks (1..4096) with FFN model F (copied). */
+int cep_oewf_create(int n_ranks, const cep_ffn_profile *F, cep_oewf **out);
+
+/* New layer: every rank may decide once more; earlier plans and decisions
+ * become stale (they no longer commit).  Rank entries are kept. */
+int cep_oewf_begin_layer(cep_oewf *o);
+
+/* Set rank r's entry (times and counts >= 0); bumps its version. */
+int cep_oewf_set_rank(cep_oewf *o, int r, int in_attention, double A, double D, int64_t N,
+                      double T);
+
+/* *t = T_r(S): the donor model while r is in attention, else its T. */
+int cep_oewf_completion(cep_oewf *o, int r, double *t);
+
+/* *t = max_r T_r(S). */
+int cep_oewf_makespan(cep_oewf *o, double *t);
+
+/* Algorithm 1 for helper h.  tokens: host [n_ranks][n_experts], tokens h
+ * dispatched to expert e of rank d; expert_bytes: host [n_experts] (> 0),
+ * bytes of one expert's weights and scales; budget: B_h bytes.  n_experts
+ * <= CEP_OEWF_MAX_EXPERTS.  CEP_EBUSY if h already decided this layer. */
+int cep_oewf_select(cep_oewf *o, int helper, int n_experts, const int64_t *tokens,
+                    const int64_t *expert_bytes, int64_t budget, cep_oewf_fetch *plan);
+
+/* Reassignment test for moving n_trans (0 <= n_trans <= min(plan tokens,
+ * N_d)) of a plan's unstarted tokens to its helper, launched s_h after the
+ * decision.  Changes nothing. */
+int cep_oewf_evaluate(cep_oewf *o, const cep_oewf_fetch *plan, int64_t n_trans, double s_h,
+                      cep_oewf_decision *dec);
+
+/* Version-checked commit; *committed = 1 if applied, 0 on fallback (also
+ * for a decision taken before the last cep_oewf_begin_layer). */
+int cep_oewf_commit(cep_oewf *o, const cep_oewf_decision *dec, int donor_submitted,
+                    int *committed);
+
+/* Release a coordinator; NULL is a no-op. */
+void cep_oewf_destroy(cep_oewf *o);
+
 #ifdef __cplusplus
 }
 #endif

@@ -24,7 +24,11 @@ EXPORTED = ["cep_packed_expert_bytes", "cep_pack_experts", "cep_init_experts", "
             "cep_combine", "cep_get_batch_routing", "cep_get_batch_count", "cep_get_stats",
             "cep_get_status", "cep_last_error", "cep_destroy", "cep_profile_create",
             "cep_profile_peak", "cep_profile_theta", "cep_profile_eta", "cep_profile_latency",
-            "cep_profile_destroy"]
+            "cep_profile_destroy", "cep_oewf_create", "cep_oewf_begin_layer", "cep_oewf_set_rank",
+            "cep_oewf_completion", "cep_oewf_makespan", "cep_oewf_select", "cep_oewf_evaluate",
+            "cep_oewf_commit", "cep_oewf_destroy"]
+
+OEWF_MAX_EXPERTS = 64
 
 
 class cep_config(ctypes.Structure):
@@ -40,6 +44,20 @@ class cep_weights(ctypes.Structure):
     _fields_ = [("w_gate", ctypes.c_void_p), ("w_up", ctypes.c_void_p),
                 ("w_down", ctypes.c_void_p), ("s_gate", ctypes.c_void_p),
                 ("s_up", ctypes.c_void_p), ("s_down", ctypes.c_void_p)]
+
+
+class cep_oewf_fetch(ctypes.Structure):
+    _fields_ = [("helper", ctypes.c_int), ("donor", ctypes.c_int), ("n_experts", ctypes.c_int),
+                ("experts", ctypes.c_int * OEWF_MAX_EXPERTS),
+                ("tokens", ctypes.c_int64 * OEWF_MAX_EXPERTS), ("bytes", ctypes.c_int64),
+                ("plan_id", ctypes.c_int64)]
+
+
+class cep_oewf_decision(ctypes.Structure):
+    _fields_ = [("admit", ctypes.c_int), ("Td", ctypes.c_double), ("Th", ctypes.c_double),
+                ("Td2", ctypes.c_double), ("Th2", ctypes.c_double), ("alpha", ctypes.c_double),
+                ("plan_id", ctypes.c_int64), ("n_trans", ctypes.c_int64),
+                ("donor_version", ctypes.c_uint64), ("helper_version", ctypes.c_uint64)]
 
 
 class CepError(RuntimeError):
@@ -89,9 +107,19 @@ def lib():
         L.cep_profile_latency.argtypes = [vp, i64, P(f64)]
         L.cep_profile_destroy.argtypes = [vp]
         L.cep_profile_destroy.restype = None
+        L.cep_oewf_create.argtypes = [i32, vp, P(vp)]
+        L.cep_oewf_begin_layer.argtypes = [vp]
+        L.cep_oewf_set_rank.argtypes = [vp, i32, i32, f64, f64, i64, f64]
+        L.cep_oewf_completion.argtypes = [vp, i32, P(f64)]
+        L.cep_oewf_makespan.argtypes = [vp, P(f64)]
+        L.cep_oewf_select.argtypes = [vp, i32, i32, P(i64), P(i64), i64, P(cep_oewf_fetch)]
+        L.cep_oewf_evaluate.argtypes = [vp, P(cep_oewf_fetch), i64, f64, P(cep_oewf_decision)]
+        L.cep_oewf_commit.argtypes = [vp, P(cep_oewf_decision), i32, P(i32)]
+        L.cep_oewf_destroy.argtypes = [vp]
+        L.cep_oewf_destroy.restype = None
         for name in EXPORTED:
             if name not in ("cep_packed_expert_bytes", "cep_last_error", "cep_profile_peak",
-                            "cep_profile_destroy"):
+                            "cep_profile_destroy", "cep_oewf_destroy"):
                 getattr(L, name).restype = i32
         _lib = L
     return _lib
@@ -289,6 +317,70 @@ class FfnProfile:
     def close(self):
         if getattr(self, "handle", None):
             lib().cep_profile_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# ------------------------------------------------------ OEWF coordinator
+class Coordinator:
+    """Owns a cep_oewf: the joint plan of one MoE layer over n_ranks ranks."""
+
+    def __init__(self, n_ranks: int, profile: FfnProfile):
+        h = ctypes.c_void_p()
+        _check(None, lib().cep_oewf_create(n_ranks, profile.handle, ctypes.byref(h)))
+        self.handle = h.value
+        self.n_ranks = n_ranks
+
+    def begin_layer(self):
+        _check(None, lib().cep_oewf_begin_layer(self.handle))
+
+    def set_rank(self, r, in_attention, A, D, N, T):
+        _check(None, lib().cep_oewf_set_rank(self.handle, r, 1 if in_attention else 0, float(A),
+                                             float(D), int(N), float(T)))
+
+    def completion(self, r) -> float:
+        out = ctypes.c_double()
+        _check(None, lib().cep_oewf_completion(self.handle, r, ctypes.byref(out)))
+        return out.value
+
+    def makespan(self) -> float:
+        out = ctypes.c_double()
+        _check(None, lib().cep_oewf_makespan(self.handle, ctypes.byref(out)))
+        return out.value
+
+    def select(self, helper, tokens, expert_bytes, budget) -> cep_oewf_fetch:
+        """tokens: [n_ranks][n_experts] ints; expert_bytes: [n_experts]."""
+        n_e = len(expert_bytes)
+        flat = [int(v) for row in tokens for v in row]
+        if len(flat) != self.n_ranks * n_e:
+            raise ValueError("tokens must be n_ranks x n_experts")
+        a = (ctypes.c_int64 * len(flat))(*flat)
+        b = (ctypes.c_int64 * n_e)(*[int(v) for v in expert_bytes])
+        plan = cep_oewf_fetch()
+        _check(None, lib().cep_oewf_select(self.handle, helper, n_e, a, b, int(budget),
+                                           ctypes.byref(plan)))
+        return plan
+
+    def evaluate(self, plan, n_trans, s_h) -> cep_oewf_decision:
+        dec = cep_oewf_decision()
+        _check(None, lib().cep_oewf_evaluate(self.handle, ctypes.byref(plan), int(n_trans),
+                                             float(s_h), ctypes.byref(dec)))
+        return dec
+
+    def commit(self, dec, donor_submitted=False) -> bool:
+        out = ctypes.c_int()
+        _check(None, lib().cep_oewf_commit(self.handle, ctypes.byref(dec),
+                                           1 if donor_submitted else 0, ctypes.byref(out)))
+        return bool(out.value)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().cep_oewf_destroy(self.handle)
             self.handle = None
 
     def __del__(self):

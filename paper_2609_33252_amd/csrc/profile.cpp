@@ -7,21 +7,29 @@
 // largest, eta keeps its last value.
 #include "cep.h"
 #include "common.h"
+#include "profile.h"
 
 #include <cmath>
-#include <cstdint>
 #include <new>
-#include <vector>
-
-struct cep_ffn_profile {
-  std::vector<int64_t> n;   // profiled expert-token counts, ascending
-  std::vector<double> eta;  // throughput / peak at those counts
-  double peak = 0;          // observed peak throughput
-};
 
 namespace cep {
-int set_global_error(int code, const char *msg);
+
+double profile_eta(const cep_ffn_profile &p, int64_t N) {
+  const std::vector<int64_t> &n = p.n;
+  const size_t last = n.size() - 1;
+  if (N <= n[0]) return p.eta[0] * (double)N / (double)n[0];
+  if (N >= n[last]) return p.eta[last];
+  size_t i = 0;
+  while (n[i + 1] < N) ++i;  // n[i] < N <= n[i+1]
+  const double f = (double)(N - n[i]) / (double)(n[i + 1] - n[i]);
+  return p.eta[i] + f * (p.eta[i + 1] - p.eta[i]);
 }
+
+double profile_latency(const cep_ffn_profile &p, int64_t N) {
+  return N == 0 ? 0.0 : (double)N / (profile_eta(p, N) * p.peak);
+}
+
+}  // namespace cep
 
 CEP_API int cep_profile_create(const int64_t *n, const double *tput, int count,
                                cep_ffn_profile **out) {
@@ -66,18 +74,7 @@ CEP_API int cep_profile_theta(const cep_ffn_profile *p, double rho, int64_t *the
 CEP_API int cep_profile_eta(const cep_ffn_profile *p, int64_t N, double *eta) {
   if (!p || !eta) return cep::set_global_error(CEP_EINVAL, "cep_profile_eta: NULL argument");
   if (N < 1) return cep::set_global_error(CEP_EINVAL, "cep_profile_eta: N must be >= 1");
-  const std::vector<int64_t> &n = p->n;
-  const size_t last = n.size() - 1;
-  if (N <= n[0]) {
-    *eta = p->eta[0] * (double)N / (double)n[0];
-  } else if (N >= n[last]) {
-    *eta = p->eta[last];
-  } else {
-    size_t i = 0;
-    while (n[i + 1] < N) ++i;  // n[i] < N <= n[i+1]
-    const double f = (double)(N - n[i]) / (double)(n[i + 1] - n[i]);
-    *eta = p->eta[i] + f * (p->eta[i + 1] - p->eta[i]);
-  }
+  *eta = cep::profile_eta(*p, N);
   return CEP_OK;
 }
 
@@ -85,14 +82,7 @@ CEP_API int cep_profile_latency(const cep_ffn_profile *p, int64_t N, double *lat
   if (!p || !latency)
     return cep::set_global_error(CEP_EINVAL, "cep_profile_latency: NULL argument");
   if (N < 0) return cep::set_global_error(CEP_EINVAL, "cep_profile_latency: N must be >= 0");
-  if (N == 0) {
-    *latency = 0.0;
-    return CEP_OK;
-  }
-  double eta = 0;
-  const int rc = cep_profile_eta(p, N, &eta);
-  if (rc != CEP_OK) return rc;
-  *latency = (double)N / (eta * p->peak);
+  *latency = cep::profile_latency(*p, N);
   return CEP_OK;
 }
 
