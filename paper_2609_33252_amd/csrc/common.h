@@ -19,7 +19,9 @@ constexpr int kFp8TileM = 128;       // e4m3 grouped GEMM tile (4 waves)
 constexpr int kFp8LargeTileM = 256;  // e4m3 tile for large batches (8 waves)
 constexpr int kRouteThreads = 256;   // threads per routing block
 constexpr int kRoutePairs = 2048;    // flat pairs per routing block (8 rounds of 256)
-constexpr int kInterleave = 32;      // gate/up column interleave of the packed W1
+constexpr int kInterleave = 32;
+constexpr int kFusedRoutePairs = 1 << 15;  // batches up to this many flat (row, slot)
+                                           // entries route in one block (ids in LDS)      // gate/up column interleave of the packed W1
 
 // One M tile of a grouped GEMM: expert, first grouped row, valid rows in it.
 struct Tile {

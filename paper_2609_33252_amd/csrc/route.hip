@@ -88,21 +88,121 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_count(const int32_t *__
   if (tid < E) blk_cnt[blockIdx.x * E + tid] = hist[tid];
 }
 
+// ------------------------------------------------------------ tile plan
+// Batch-wide quantities shared by both routing variants.
+struct PlanArgs {
+  int E, align, expected_pairs, max_mpad, max_tiles;
+  uint64_t fetched_mask;
+  int split_cu, n_tiles_n;
+  uint32_t *err;
+};
+
+struct PlanLds {
+  int cnt[kMaxExperts], off[kMaxExperts + 1], pad[kMaxExperts + 1];
+  int tile0[kMaxExperts], rtile0[kMaxExperts];
+  int split;
+};
+
+// Given the per-expert totals in L.cnt (visible to the block), computes the
+// unpadded and tile-aligned exclusive scans, the tile plan and the M-tile
+// lists of the resident and the fetched experts, marks the padding rows of
+// each expert's last tile (no pair), and publishes cnt / off / off_pad /
+// n_tiles.  Called by all nthr threads of the block; ends with L.pad visible.
+__device__ void plan_batch(const Scratch &sc, PlanLds &L, const PlanArgs &a, int tid, int nthr) {
+  const int E = a.E, align = a.align;
+  if (tid == 0) {
+    // Remainder split: an expert's last partial tile of at most align/2 rows
+    // can run as 64-row tiles (64 x 128 outputs, two workgroups per CU, about
+    // a quarter of a full tile's time each) instead of a full tile.  Split
+    // when that shortens the estimated makespan in full-tile rounds of
+    // split_cu CUs; results are the same either way.
+    int split = 0;
+    if (a.split_cu > 0) {
+      long long full = 0, kept = 0, rem = 0;
+      for (int x = 0; x < E; ++x) {
+        const int c = L.cnt[x], r = c % align;
+        full += (c + align - 1) / align;
+        kept += c / align + (r > align / 2 ? 1 : 0);
+        rem += (r > 0 && r <= align / 2) ? (r + kBf16SmallTileM - 1) / kBf16SmallTileM : 0;
+      }
+      const long long wn = a.n_tiles_n, cu = a.split_cu;
+      const long long rounds_full = (full * wn + cu - 1) / cu;
+      const long long rounds_kept = (kept * wn + cu - 1) / cu;
+      const long long rounds_rem = (rem * 2 * wn + 2 * cu - 1) / (2 * cu);  // quarter rounds
+      split = rem > 0 && 4 * rounds_kept + rounds_rem < 4 * rounds_full;
+    }
+    L.split = split;
+    int o = 0, op = 0;
+    int t0[4] = {0, 0, 0, 0};
+    for (int x = 0; x < E; ++x) {
+      L.off[x] = o;
+      L.pad[x] = op;
+      const int which = (int)((a.fetched_mask >> x) & 1);
+      const int c = L.cnt[x], r = c % align;
+      const bool rem = split && r > 0 && r <= align / 2;
+      L.tile0[x] = t0[2 * which];
+      L.rtile0[x] = t0[2 * which + 1];
+      t0[2 * which] += rem ? c / align : (c + align - 1) / align;
+      t0[2 * which + 1] += rem ? (r + kBf16SmallTileM - 1) / kBf16SmallTileM : 0;
+      o += c;
+      op += (c + align - 1) / align * align;
+    }
+    L.off[E] = o;
+    L.pad[E] = op;
+    if (o != a.expected_pairs) atomicOr(a.err, kErrPairCount);
+    bool over = op > a.max_mpad;
+    for (int l = 0; l < 4; ++l) {
+      over = over || t0[l] > a.max_tiles;
+      sc.n_tiles[l] = min(t0[l], a.max_tiles);
+    }
+    if (over) atomicOr(a.err, kErrOverflow);
+  }
+  __syncthreads();
+  if (tid <= E) {
+    sc.off[tid] = L.off[tid];
+    sc.off_pad[tid] = L.pad[tid];
+  }
+  if (tid < E) sc.cnt[tid] = L.cnt[tid];
+  // padding rows of each expert's last tile carry no pair
+  for (int i = tid; i < E * align; i += nthr) {
+    const int x = i / align, r = L.pad[x] + L.cnt[x] + i % align;
+    if (r < L.pad[x + 1] && r < a.max_mpad) sc.perm[r] = -1;
+  }
+  if (tid < E) {
+    const int which = (int)((a.fetched_mask >> tid) & 1);
+    const int c = L.cnt[tid], r = c % align;
+    const bool rem = L.split && r > 0 && r <= align / 2;
+    Tile *list = sc.tiles + (size_t)(2 * which) * a.max_tiles;
+    const int nt = rem ? c / align : (c + align - 1) / align;
+    for (int q = 0; q < nt; ++q) {
+      const int ti = L.tile0[tid] + q;
+      const int row0 = L.pad[tid] + q * align;
+      if (ti >= a.max_tiles || row0 + align > a.max_mpad) break;
+      list[ti] = Tile{tid, row0, min(align, c - q * align), 0};
+    }
+    if (rem) {
+      Tile *rlist = sc.tiles + (size_t)(2 * which + 1) * a.max_tiles;
+      const int base = L.pad[tid] + nt * align;
+      for (int q = 0; q * kBf16SmallTileM < r; ++q) {
+        const int ti = L.rtile0[tid] + q;
+        const int row0 = base + q * kBf16SmallTileM;
+        if (ti >= a.max_tiles || row0 + kBf16SmallTileM > a.max_mpad) break;
+        rlist[ti] = Tile{tid, row0, min(kBf16SmallTileM, r - q * kBf16SmallTileM), 0};
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------------ scan
-// One block: per-expert totals, unpadded and tile-aligned exclusive scans,
-// the first grouped row of every routing block's pairs of every expert, and
-// the M-tile lists of the resident and the fetched experts.  Thread t serves
-// expert t % E over a contiguous range of routing blocks (group t / E), so
-// the block counts are read in parallel and scanned in LDS.
-__global__ __launch_bounds__(256) void k_route_scan(Scratch sc, int n_blocks, int E, int align,
-                                                    int expected_pairs, int max_mpad,
-                                                    int max_tiles, uint64_t fetched_mask,
-                                                    int split_cu, int n_tiles_n, uint32_t *err) {
+// One block: per-expert totals over the routing blocks' counts, the tile
+// plan, and the first grouped row of every routing block's pairs of every
+// expert.  Thread t serves expert t % E over a contiguous range of routing
+// blocks (group t / E), so the block counts are read in parallel and
+// scanned in LDS.
+__global__ __launch_bounds__(256) void k_route_scan(Scratch sc, int n_blocks, PlanArgs pa) {
   __shared__ int s_part[256];  // [group][expert]: range sum, then exclusive prefix
-  __shared__ int s_cnt[kMaxExperts], s_off[kMaxExperts + 1], s_pad[kMaxExperts + 1];
-  __shared__ int s_tile0[kMaxExperts], s_rtile0[kMaxExperts];
-  __shared__ int s_split;
-  const int tid = threadIdx.x;
+  __shared__ PlanLds L;
+  const int tid = threadIdx.x, E = pa.E;
   const int G = 256 / E, e = tid % E, grp = tid / E;
   const bool mine = grp < G;
   const int span = (n_blocks + G - 1) / G;
@@ -120,95 +220,78 @@ __global__ __launch_bounds__(256) void k_route_scan(Scratch sc, int n_blocks, in
       s_part[q * E + tid] = run;
       run += v;
     }
-    s_cnt[tid] = run;
+    L.cnt[tid] = run;
   }
   __syncthreads();
-  if (tid == 0) {
-    // Remainder split: an expert's last partial tile of at most align/2 rows
-    // can run as 64-row tiles (64 x 128 outputs, two workgroups per CU, about
-    // a quarter of a full tile's time each) instead of a full tile.  Split
-    // when that shortens the estimated makespan in full-tile rounds of
-    // split_cu CUs; results are the same either way.
-    int split = 0;
-    if (split_cu > 0) {
-      long long full = 0, kept = 0, rem = 0;
-      for (int x = 0; x < E; ++x) {
-        const int c = s_cnt[x], r = c % align;
-        full += (c + align - 1) / align;
-        kept += c / align + (r > align / 2 ? 1 : 0);
-        rem += (r > 0 && r <= align / 2) ? (r + kBf16SmallTileM - 1) / kBf16SmallTileM : 0;
-      }
-      const long long wn = n_tiles_n, cu = split_cu;
-      const long long rounds_full = (full * wn + cu - 1) / cu;
-      const long long rounds_kept = (kept * wn + cu - 1) / cu;
-      const long long rounds_rem = (rem * 2 * wn + 2 * cu - 1) / (2 * cu);  // quarter rounds
-      split = rem > 0 && 4 * rounds_kept + rounds_rem < 4 * rounds_full;
-    }
-    s_split = split;
-    int o = 0, op = 0;
-    int t0[4] = {0, 0, 0, 0};
-    for (int x = 0; x < E; ++x) {
-      s_off[x] = o;
-      s_pad[x] = op;
-      const int which = (int)((fetched_mask >> x) & 1);
-      const int c = s_cnt[x], r = c % align;
-      const bool rem = split && r > 0 && r <= align / 2;
-      s_tile0[x] = t0[2 * which];
-      s_rtile0[x] = t0[2 * which + 1];
-      t0[2 * which] += rem ? c / align : (c + align - 1) / align;
-      t0[2 * which + 1] += rem ? (r + kBf16SmallTileM - 1) / kBf16SmallTileM : 0;
-      o += c;
-      op += (c + align - 1) / align * align;
-    }
-    s_off[E] = o;
-    s_pad[E] = op;
-    if (o != expected_pairs) atomicOr(err, kErrPairCount);
-    bool over = op > max_mpad;
-    for (int l = 0; l < 4; ++l) {
-      over = over || t0[l] > max_tiles;
-      sc.n_tiles[l] = min(t0[l], max_tiles);
-    }
-    if (over) atomicOr(err, kErrOverflow);
-  }
-  __syncthreads();
-  if (tid <= E) {
-    sc.off[tid] = s_off[tid];
-    sc.off_pad[tid] = s_pad[tid];
-  }
-  if (tid < E) sc.cnt[tid] = s_cnt[tid];
+  plan_batch(sc, L, pa, tid, 256);
   if (mine) {
-    int run = s_pad[e] + s_part[grp * E + e];
+    int run = L.pad[e] + s_part[grp * E + e];
     for (int b = b0; b < b1; ++b) {
       sc.blk_base[b * E + e] = run;
       run += sc.blk_cnt[b * E + e];
     }
   }
-  // padding rows of each expert's last tile carry no pair
-  for (int i = tid; i < E * align; i += 256) {
-    const int x = i / align, r = s_pad[x] + s_cnt[x] + i % align;
-    if (r < s_pad[x + 1] && r < max_mpad) sc.perm[r] = -1;
+}
+
+// ---------------------------------------------------- fused (one block)
+// Histogram, scan, tile plan and stable scatter of a batch in one block of
+// 16 waves, for batches whose ids fit in LDS: one coalesced pass stages the
+// ids, then everything runs from LDS.  Wave w owns the contiguous flat pairs
+// [w*span, (w+1)*span) and walks them in order, so a pair's grouped row is
+// its expert's first row + the pairs of that expert in lower waves + those
+// earlier in its own wave: the same stable order as the multi-block path.
+constexpr int kFusedWaves = 16;
+
+__global__ __launch_bounds__(64 * kFusedWaves) void k_route_fused(Arena a, Scratch sc, int row0,
+                                                                  int n_flat, int k,
+                                                                  PlanArgs pa) {
+  __shared__ int s_ids[kFusedRoutePairs];
+  __shared__ int wcnt[kFusedWaves][kMaxExperts];  // counts, then running rows
+  __shared__ PlanLds L;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, E = pa.E;
+  constexpr int NT = 64 * kFusedWaves;
+  const int32_t *ids = a.ids + (size_t)row0 * k;
+  for (int i = tid; i < kFusedWaves * kMaxExperts; i += NT) (&wcnt[0][0])[i] = 0;
+#pragma unroll 8
+  for (int i = tid; i < n_flat; i += NT) s_ids[i] = ids[i];
+  __syncthreads();
+  const int span = (n_flat + 64 * kFusedWaves - 1) / (64 * kFusedWaves) * 64;
+  const int p0 = min(wid * span, n_flat), p1 = min(p0 + span, n_flat);
+  for (int p = p0 + lane; p < p1; p += 64) {
+    const int id = s_ids[p];
+    if (id >= 0) atomicAdd(&wcnt[wid][id], 1);
   }
+  __syncthreads();
   if (tid < E) {
-    const int which = (int)((fetched_mask >> tid) & 1);
-    const int c = s_cnt[tid], r = c % align;
-    const bool rem = s_split && r > 0 && r <= align / 2;
-    Tile *list = sc.tiles + (size_t)(2 * which) * max_tiles;
-    const int nt = rem ? c / align : (c + align - 1) / align;
-    for (int q = 0; q < nt; ++q) {
-      const int ti = s_tile0[tid] + q;
-      const int row0 = s_pad[tid] + q * align;
-      if (ti >= max_tiles || row0 + align > max_mpad) break;
-      list[ti] = Tile{tid, row0, min(align, c - q * align), 0};
+    int run = 0;
+    for (int w = 0; w < kFusedWaves; ++w) {
+      const int v = wcnt[w][tid];
+      wcnt[w][tid] = run;
+      run += v;
     }
-    if (rem) {
-      Tile *rlist = sc.tiles + (size_t)(2 * which + 1) * max_tiles;
-      const int base = s_pad[tid] + nt * align;
-      for (int q = 0; q * kBf16SmallTileM < r; ++q) {
-        const int ti = s_rtile0[tid] + q;
-        const int row0 = base + q * kBf16SmallTileM;
-        if (ti >= max_tiles || row0 + kBf16SmallTileM > max_mpad) break;
-        rlist[ti] = Tile{tid, row0, min(kBf16SmallTileM, r - q * kBf16SmallTileM), 0};
-      }
+    L.cnt[tid] = run;
+  }
+  __syncthreads();
+  plan_batch(sc, L, pa, tid, NT);
+  for (int base = p0; base < p1; base += 64) {
+    const int p = base + lane;
+    const int id = p < p1 ? s_ids[p] : -1;
+    int pos = -1;
+    uint64_t active = __ballot(id >= 0);
+    while (active) {
+      const int leader = __builtin_ctzll(active);
+      const int e = __shfl(id, leader);
+      const uint64_t m = __ballot(id == e);
+      // lanes of expert e read the wave's running row before the leader
+      // advances it (LDS operations of one wave complete in order)
+      if (id == e) pos = L.pad[e] + wcnt[wid][e] + (int)lanemask_lt_popc(m);
+      if (lane == leader) wcnt[wid][e] += (int)__popcll(m);
+      active &= ~m;
+    }
+    if (pos >= pa.max_mpad) pos = -1;
+    if (p < p1) {
+      sc.pos_of[p] = pos;
+      if (pos >= 0) sc.perm[pos] = p;
     }
   }
 }
@@ -218,8 +301,7 @@ __global__ __launch_bounds__(256) void k_route_scan(Scratch sc, int n_blocks, in
 // block's first row for its expert, plus pairs of that expert in earlier
 // rounds of this block, in earlier waves of this round, and in lower lanes
 // of this wave (stable in canonical order).  Writes the inverse map (grouped
-// row of each pair), the permutation (pair of each grouped row) and the
-// routing coefficient of each grouped row.
+// row of each pair) and the permutation (pair of each grouped row).
 __global__ __launch_bounds__(kRouteThreads) void k_route_scatter(Arena a, Scratch sc, int row0,
                                                                  int n_flat, int k, int E,
                                                                  int max_mpad) {
@@ -232,16 +314,13 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_scatter(Arena a, Scratc
     (&wave_cnt[0][0])[i] = 0;
   __syncthreads();
   const int32_t *ids = a.ids + (size_t)row0 * k;
-  const float *wts = a.w + (size_t)row0 * k;
   const int base = b * kRoutePairs;
   constexpr int R = kRoutePairs / kRouteThreads;
   int idv[R];  // all loads first: one memory latency per block, not one per round
-  float wv[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int p = base + r * kRouteThreads + tid;
     idv[r] = p < n_flat ? ids[p] : -1;
-    wv[r] = p < n_flat ? wts[p] : 0.f;
   }
 #pragma unroll
   for (int r = 0; r < R; ++r) {
@@ -275,17 +354,15 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_scatter(Arena a, Scratc
     }
     __syncthreads();  // wave_cnt cleared before the next round writes it
     if (p < n_flat) sc.pos_of[p] = pos;
-    if (pos >= 0) {
-      sc.perm[pos] = p;
-      sc.wrow[pos] = wv[r];
-    }
+    if (pos >= 0) sc.perm[pos] = p;
   }
 }
 
 // ----------------------------------------------------------------- pack
 // One wave per grouped row (kPackRows rows per block): the pair's input row
 // is copied (bf16), converted (f32 -> bf16) or quantised (e4m3, one scale per
-// 128 channels) into its grouped row.  Padding rows (no pair) are skipped.
+// 128 channels) into its grouped row, and its routing coefficient goes to the
+// row's slot of wrow.  Padding rows (no pair) are skipped.
 constexpr int kPackRows = 8;
 
 template <int XMODE>  // 0: bf16 -> bf16, 1: f32 -> bf16, 2: bf16 -> e4m3 + scales
@@ -298,6 +375,7 @@ __global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0
     if (pos >= end) return;
     const int p = sc.perm[pos];
     if (p < 0) continue;
+    if (lane == 0) sc.wrow[pos] = a.w[(size_t)row0 * k + p];  // the row's routing coefficient
     const char *src = (const char *)a.xrow[row0 + p / k];
     if (XMODE == 0) {
       const uint4 *s4 = (const uint4 *)src;
@@ -482,12 +560,18 @@ hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows,
   const int n_flat = n_rows * k;
   const int nb = (n_flat + kRoutePairs - 1) / kRoutePairs;
   if (nb == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_route_count, dim3(nb), dim3(kRouteThreads), 0, s,
-                     a.ids + (size_t)row0 * k, n_flat, E, sc.blk_cnt);
-  hipLaunchKernelGGL(k_route_scan, dim3(1), dim3(256), 0, s, sc, nb, E, align, expected_pairs,
-                     max_mpad, max_tiles, fetched_mask, split_cu, n_tiles_n, err);
-  hipLaunchKernelGGL(k_route_scatter, dim3(nb), dim3(kRouteThreads), 0, s, a, sc, row0, n_flat,
-                     k, E, max_mpad);
+  const PlanArgs pa{E, align, expected_pairs, max_mpad, max_tiles, fetched_mask, split_cu,
+                    n_tiles_n, err};
+  if (n_flat <= kFusedRoutePairs) {
+    hipLaunchKernelGGL(k_route_fused, dim3(1), dim3(64 * kFusedWaves), 0, s, a, sc, row0,
+                       n_flat, k, pa);
+  } else {
+    hipLaunchKernelGGL(k_route_count, dim3(nb), dim3(kRouteThreads), 0, s,
+                       a.ids + (size_t)row0 * k, n_flat, E, sc.blk_cnt);
+    hipLaunchKernelGGL(k_route_scan, dim3(1), dim3(256), 0, s, sc, nb, pa);
+    hipLaunchKernelGGL(k_route_scatter, dim3(nb), dim3(kRouteThreads), 0, s, a, sc, row0,
+                       n_flat, k, E, max_mpad);
+  }
   // grouped rows: at most every pair plus one partial tile per expert
   const long long bound = ((long long)(expected_pairs + align - 1) / align + E) * align;
   const int n_pad = (int)std::min<long long>(bound, max_mpad);
