@@ -142,8 +142,10 @@ int cep_begin_layer(cep_ctx *ctx, uint32_t generation, int n_replicas,
  *   topk_id   [n_rows][k] int32 local expert id in [0, E) or -1 (remote slot)
  *   topk_w    [n_rows][k] float32 routing coefficients
  * n_pairs: host-known count of valid (id >= 0) entries.  arrival: event after
- * which the data is valid (NULL: valid now).  May launch batches per policy;
- * never blocks.  chunk_id (optional) receives the chunk's sequence number.
+ * which the data is valid (NULL: valid now); the wait is enqueued here, so
+ * the event may be recorded again afterwards.  The chunk's metadata is read
+ * when its batch launches (all chunks of a batch in one staging launch).
+ * May launch batches per policy; never blocks.  chunk_id (optional) receives the chunk's sequence number.
  * Errors: CEP_ESTATE for a wrong generation or a closed layer, CEP_EINVAL
  * for bad sizes, CEP_ENOMEM if the layer's rows exceed the arena
  * (R_max * T_max rows) or n_pairs exceeds max_pairs_per_batch.  Ids outside

@@ -132,10 +132,21 @@ hipError_t launch_pack_scales(const float *sg, const float *su, const float *sd,
                               float *dst_s1, float *dst_s2, hipStream_t s);
 
 // routing
-hipError_t launch_ingest(const Arena &a, int row0, int n_rows, int k, int E, int replica,
-                         int t_max, const int32_t *token_idx, const void *x, size_t x_row_bytes,
-                         const int32_t *topk_id, const float *topk_w, uint32_t *err,
-                         hipStream_t s);
+// One staging launch covers up to kIngestGroup chunks (passed by value).
+struct IngestChunk {
+  const int32_t *token_idx;
+  const void *x;
+  const int32_t *topk_id;
+  const float *topk_w;
+  int row0, n_rows, replica;
+};
+constexpr int kIngestGroup = 32;
+struct IngestGroup {
+  IngestChunk c[kIngestGroup];
+  int n;
+};
+hipError_t launch_ingest(const Arena &a, const IngestGroup &grp, int k, int E, int t_max,
+                         size_t x_row_bytes, uint32_t *err, hipStream_t s);
 // split_cu > 0 (bf16 batches with 256-row tiles): the scan may move each
 // expert's last partial tile of at most 128 rows to 64-row remainder tiles
 // when its makespan estimate for split_cu compute units and GEMM1's

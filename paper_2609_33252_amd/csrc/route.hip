@@ -22,34 +22,32 @@ __device__ inline uint64_t lanemask_lt_popc(uint64_t m) {
 }
 
 // ---------------------------------------------------------------- ingest
-// Copies one chunk's routing metadata into the layer's arena (one entry per
-// row, in submission order), so that a batch of whole chunks is a contiguous
-// arena range.  Ids outside [-1, E) are flagged and treated as remote; token
-// slots outside [0, T_max) are flagged and their row dropped.
-__global__ __launch_bounds__(256) void k_ingest(Arena a, int row0, int n_rows, int k, int E,
-                                                int replica, int t_max,
-                                                const int32_t *__restrict__ token_idx,
-                                                const char *__restrict__ x, size_t x_row_bytes,
-                                                const int32_t *__restrict__ topk_id,
-                                                const float *__restrict__ topk_w,
-                                                uint32_t *err) {
+// Stages the routing metadata of a group of ready chunks into the layer's
+// arena (one entry per row, in submission order), so that a batch of whole
+// chunks is a contiguous arena range; blockIdx.y names the chunk.  Ids
+// outside [-1, E) are flagged and treated as remote; token slots outside
+// [0, T_max) are flagged and their row dropped.
+__global__ __launch_bounds__(256) void k_ingest(Arena a, IngestGroup grp, int k, int E, int t_max,
+                                                size_t x_row_bytes, uint32_t *err) {
+  const IngestChunk &c = grp.c[blockIdx.y];
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n_rows) return;
-  const int t = token_idx[i];
+  if (i >= c.n_rows) return;
+  const int row = c.row0 + i;
+  const int t = c.token_idx[i];
   int dst = -1;
-  if (t >= 0 && t < t_max) dst = replica * t_max + t;
+  if (t >= 0 && t < t_max) dst = c.replica * t_max + t;
   else atomicOr(err, kErrBadToken);
-  a.dst[row0 + i] = dst;
-  a.xrow[row0 + i] = x + (size_t)i * x_row_bytes;
+  a.dst[row] = dst;
+  a.xrow[row] = (const char *)c.x + (size_t)i * x_row_bytes;
   for (int s = 0; s < k; ++s) {
-    int id = topk_id[(size_t)i * k + s];
+    int id = c.topk_id[(size_t)i * k + s];
     if (id < -1 || id >= E) {
       atomicOr(err, kErrBadId);
       id = -1;
     }
     if (dst < 0) id = -1;
-    a.ids[(size_t)(row0 + i) * k + s] = id;
-    a.w[(size_t)(row0 + i) * k + s] = topk_w[(size_t)i * k + s];
+    a.ids[(size_t)row * k + s] = id;
+    a.w[(size_t)row * k + s] = c.topk_w[(size_t)i * k + s];
   }
 }
 
@@ -542,14 +540,13 @@ hipError_t launch_pack_scales(const float *sg, const float *su, const float *sd,
   return hipGetLastError();
 }
 
-hipError_t launch_ingest(const Arena &a, int row0, int n_rows, int k, int E, int replica,
-                         int t_max, const int32_t *token_idx, const void *x, size_t x_row_bytes,
-                         const int32_t *topk_id, const float *topk_w, uint32_t *err,
-                         hipStream_t s) {
-  if (n_rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_ingest, dim3((n_rows + 255) / 256), dim3(256), 0, s, a, row0, n_rows, k,
-                     E, replica, t_max, token_idx, (const char *)x, x_row_bytes, topk_id,
-                     topk_w, err);
+hipError_t launch_ingest(const Arena &a, const IngestGroup &grp, int k, int E, int t_max,
+                         size_t x_row_bytes, uint32_t *err, hipStream_t s) {
+  int rows = 0;
+  for (int i = 0; i < grp.n; ++i) rows = std::max(rows, grp.c[i].n_rows);
+  if (grp.n <= 0 || rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_ingest, dim3((rows + 255) / 256, grp.n), dim3(256), 0, s, a, grp, k, E,
+                     t_max, x_row_bytes, err);
   return hipGetLastError();
 }
 

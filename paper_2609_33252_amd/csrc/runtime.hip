@@ -25,6 +25,10 @@ struct ChunkRec {
   int replica;
   int row0, n_rows, n_pairs;
   hipEvent_t arrival;  // caller-owned, may be null
+  const int32_t *token_idx;
+  const void *x;
+  const int32_t *topk_id;
+  const float *topk_w;
 };
 
 struct BatchRec {
@@ -76,6 +80,7 @@ struct cep_ctx {
   int n_rep = 0, expected_chunks = 0;
   float *out = nullptr;
   int rows_used = 0;
+  int64_t staged = 0;  // chunks [0, staged) have their metadata in the arena
   std::vector<ChunkRec> chunks;
   int64_t pending_first = 0;
   int pending_pairs = 0, pending_rows = 0;
@@ -186,6 +191,24 @@ void free_batch_records(cep_ctx *c) {
   c->batches.clear();
 }
 
+// Stages the metadata of chunks [c->staged, upto) into the arena on stream s
+// (one launch per group of chunks), after their arrival waits.
+int stage_chunks(cep_ctx *c, int64_t upto, hipStream_t s) {
+  const size_t xrb = (size_t)c->cfg.d_model * (c->cfg.x_dtype == CEP_F32 ? 4 : 2);
+  while (c->staged < upto) {
+    IngestGroup g{};
+    while (g.n < kIngestGroup && c->staged < upto) {
+      const ChunkRec &ch = c->chunks[c->staged++];
+      if (ch.n_rows > 0)
+        g.c[g.n++] = IngestChunk{ch.token_idx, ch.x, ch.topk_id, ch.topk_w, ch.row0, ch.n_rows,
+                                 ch.replica};
+    }
+    HIPCHK(c, launch_ingest(c->arena, g, c->cfg.top_k, c->cfg.n_local_experts,
+                            c->cfg.max_tokens_per_replica, xrb, c->d_err, s));
+  }
+  return CEP_OK;
+}
+
 // Launch all pending chunks as one grouped invocation on the next stream slot.
 int launch_pending(cep_ctx *c) {
   const int64_t nch = (int64_t)c->chunks.size() - c->pending_first;
@@ -226,12 +249,18 @@ int launch_pending(cep_ctx *c) {
       !b.ev_phase[3])
     return fail(c, CEP_EHIP, "hipEventCreate failed");
 
-  // the batch sees its chunks only after the ingest stream has staged them
+  // the chunks' arrival waits sit on the ingest stream: the batch stream
+  // follows it, then stages every chunk submitted so far (the batch's, and
+  // chunks without local pairs before it) in one launch per group
   if (s != c->ingest) {
     HIPCHK(c, hipEventRecord(c->ev_ingest[slot], c->ingest));
     HIPCHK(c, hipStreamWaitEvent(s, c->ev_ingest[slot], 0));
   }
   HIPCHK(c, hipEventRecord(b.ev_start, s));
+  {
+    const int rc = stage_chunks(c, (int64_t)c->chunks.size(), s);
+    if (rc != CEP_OK) return rc;
+  }
   // 256-row bf16 tiles: the scan may move small remainders to 64-row tiles
   // (at most two per expert), run by a second launch of the 64-row kernel
   const bool split = !c->fp8 && A == kBf16TileM;
@@ -477,6 +506,7 @@ CEP_API int cep_begin_layer(cep_ctx *c, uint32_t generation, int n_replicas,
   c->expected_chunks = (int)tot;
   c->out = out;
   c->rows_used = 0;
+  c->staged = 0;
   c->chunks.clear();
   c->pending_first = 0;
   c->pending_pairs = c->pending_rows = 0;
@@ -505,12 +535,10 @@ CEP_API int cep_submit_chunk(cep_ctx *c, uint32_t generation, int replica, int n
     return fail(c, CEP_ENOMEM, "layer rows exceed max_replicas * max_tokens_per_replica");
   if (n_pairs > c->max_pairs)
     return fail(c, CEP_ENOMEM, "chunk pairs %d exceed max_pairs_per_batch %d", n_pairs, c->max_pairs);
+  // readiness: later work on the ingest stream (and every batch, which
+  // follows it) runs after the chunk's arrival
   if (arrival) HIPCHK(c, hipStreamWaitEvent(c->ingest, arrival, 0));
-  const size_t xrb = (size_t)c->cfg.d_model * (c->cfg.x_dtype == CEP_F32 ? 4 : 2);
-  HIPCHK(c, launch_ingest(c->arena, c->rows_used, n_rows, c->cfg.top_k, c->cfg.n_local_experts,
-                          replica, c->cfg.max_tokens_per_replica, token_idx, x, xrb, topk_id,
-                          topk_w, c->d_err, c->ingest));
-  ChunkRec ch{replica, c->rows_used, n_rows, n_pairs, arrival};
+  ChunkRec ch{replica, c->rows_used, n_rows, n_pairs, arrival, token_idx, x, topk_id, topk_w};
   c->rows_used += n_rows;
   const int64_t id = (int64_t)c->chunks.size();
   if (chunk_id) *chunk_id = id;
@@ -591,8 +619,12 @@ CEP_API int cep_combine(cep_ctx *c, hipStream_t s, hipEvent_t *done) {
                 (int)c->chunks.size(), c->expected_chunks);
   int rc = launch_pending(c);
   if (rc != CEP_OK) return rc;
+  // chunks after the last batch (no local pairs) are still staged, so their
+  // ids are validated and the caller may release them after `done`
+  rc = stage_chunks(c, (int64_t)c->chunks.size(), c->ingest);
+  if (rc != CEP_OK) return rc;
   // every batch of the layer ran on a used slot stream or on the ingest
-  // stream (which also staged every chunk)
+  // stream
   for (int i = 0; i < c->cfg.n_streams; ++i) {
     if ((c->used_st >> i) & 1) {
       HIPCHK(c, hipEventRecord(c->ev_ingest[i], c->st[i]));
