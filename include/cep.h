@@ -194,6 +194,13 @@ int cep_get_batch_routing(cep_ctx *ctx, int batch, int *align, int *n_pairs, int
                           int32_t *cnt, int32_t *off, int32_t *off_pad, int32_t *perm_src,
                           int32_t *pos_of, int64_t *chunks, int *n_chunks);
 
+/* Per-phase timing of the following layers' batches: on (default) records
+ * a HIP event after each phase (routing, GEMM1, GEMM2, combine) on the batch
+ * stream, each costing a few microseconds of launch gap; off reports the
+ * batch start and the phase durations as -1 in cep_get_stats (the batch end
+ * stays).  Only between layers (CEP_ESTATE otherwise). */
+int cep_set_phase_timing(cep_ctx *ctx, int on);
+
 /* Number of batches launched in the current (or last) layer. */
 int cep_get_batch_count(const cep_ctx *ctx);
 

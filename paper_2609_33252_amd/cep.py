@@ -22,7 +22,8 @@ STATUS_NAMES = {0: "CEP_OK", -1: "CEP_EINVAL", -2: "CEP_ENOMEM", -3: "CEP_EHIP",
 EXPORTED = ["cep_packed_expert_bytes", "cep_pack_experts", "cep_init_experts", "cep_set_policy",
             "cep_begin_layer", "cep_submit_chunk", "cep_flush", "cep_weight_fetch",
             "cep_combine", "cep_get_batch_routing", "cep_get_batch_count", "cep_get_stats",
-            "cep_get_status", "cep_last_error", "cep_destroy", "cep_profile_create",
+            "cep_get_status", "cep_last_error", "cep_destroy", "cep_set_phase_timing",
+            "cep_profile_create",
             "cep_profile_peak", "cep_profile_theta", "cep_profile_eta", "cep_profile_latency",
             "cep_profile_destroy", "cep_oewf_create", "cep_oewf_begin_layer", "cep_oewf_set_rank",
             "cep_oewf_completion", "cep_oewf_makespan", "cep_oewf_select", "cep_oewf_evaluate",
@@ -98,6 +99,7 @@ def lib():
         L.cep_last_error.argtypes = [vp]
         L.cep_last_error.restype = ctypes.c_char_p
         L.cep_destroy.argtypes = [vp]
+        L.cep_set_phase_timing.argtypes = [vp, i32]
         i64, f64 = ctypes.c_int64, ctypes.c_double
         L.cep_profile_create.argtypes = [P(i64), P(f64), i32, P(vp)]
         L.cep_profile_peak.argtypes = [vp]
@@ -267,6 +269,10 @@ def cep_get_stats(ctx) -> dict:
             continue
         _check(ctx, rc)
         return json.loads(buf.value.decode())
+
+
+def cep_set_phase_timing(ctx, on=True):
+    _check(ctx, lib().cep_set_phase_timing(ctx, 1 if on else 0))
 
 
 def cep_get_status(ctx):

@@ -41,6 +41,7 @@ struct BatchRec {
   hipEvent_t ev_start, ev_end;
   // on the batch stream after: routing, GEMM1, GEMM2, combine
   hipEvent_t ev_phase[4];
+  bool phases;  // ev_phase recorded (phase timing on at launch)
   // recorded routing (record_routing only), pinned host memory
   int32_t *h_cnt = nullptr, *h_off = nullptr, *h_off_pad = nullptr, *h_perm = nullptr,
           *h_pos = nullptr;
@@ -81,6 +82,7 @@ struct cep_ctx {
   float *out = nullptr;
   int rows_used = 0;
   int64_t staged = 0;  // chunks [0, staged) have their metadata in the arena
+  bool phase_timing = true;  // record per-phase events in each batch
   std::vector<ChunkRec> chunks;
   int64_t pending_first = 0;
   int pending_pairs = 0, pending_rows = 0;
@@ -242,11 +244,13 @@ int launch_pending(cep_ctx *c) {
   b.align = A;
   const int tiles = std::min(c->max_tiles, (P + A - 1) / A + E);
   b.mpad_bound = std::min(c->max_mpad, tiles * A);
-  b.ev_start = timing_event(c, false);
-  b.ev_end = timing_event(c, true);
-  for (hipEvent_t &e : b.ev_phase) e = timing_event(c, false);
-  if (!b.ev_start || !b.ev_end || !b.ev_phase[0] || !b.ev_phase[1] || !b.ev_phase[2] ||
-      !b.ev_phase[3])
+  // the end event is fenced only when the host reads routing copies after it
+  b.phases = c->phase_timing;
+  b.ev_start = b.phases ? timing_event(c, false) : nullptr;
+  b.ev_end = timing_event(c, cfg.record_routing != 0);
+  for (hipEvent_t &e : b.ev_phase) e = b.phases ? timing_event(c, false) : nullptr;
+  if ((b.phases && !b.ev_start) || !b.ev_end ||
+      (b.phases && (!b.ev_phase[0] || !b.ev_phase[1] || !b.ev_phase[2] || !b.ev_phase[3])))
     return fail(c, CEP_EHIP, "hipEventCreate failed");
 
   // the chunks' arrival waits sit on the ingest stream: the batch stream
@@ -256,7 +260,7 @@ int launch_pending(cep_ctx *c) {
     HIPCHK(c, hipEventRecord(c->ev_ingest[slot], c->ingest));
     HIPCHK(c, hipStreamWaitEvent(s, c->ev_ingest[slot], 0));
   }
-  HIPCHK(c, hipEventRecord(b.ev_start, s));
+  if (b.phases) HIPCHK(c, hipEventRecord(b.ev_start, s));
   {
     const int rc = stage_chunks(c, (int64_t)c->chunks.size(), s);
     if (rc != CEP_OK) return rc;
@@ -268,7 +272,7 @@ int launch_pending(cep_ctx *c) {
   HIPCHK(c, launch_route(c->arena, sc, b.row0, b.n_rows, k, E, A, P, c->max_mpad, c->max_tiles,
                          c->fetched_mask, cfg.x_dtype, c->fp8, d, split ? c->n_cu : 0,
                          2 * I / kBf16TileN, c->d_err, s));
-  HIPCHK(c, hipEventRecord(b.ev_phase[0], s));
+  if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[0], s));
 
   BlobTable bt{c->w_res, c->fetch_buf, c->L.bytes, c->fetched_mask};
 
@@ -284,12 +288,12 @@ int launch_pending(cep_ctx *c) {
     HIPCHK(c, hipEventRecord(c->ev_helper[slot], h));
   }
   HIPCHK(c, launch_gemm1(sc, 0, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->fp8, d, I, s));
-  HIPCHK(c, hipEventRecord(b.ev_phase[1], s));
+  if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[1], s));
   HIPCHK(c, launch_gemm2(sc, 0, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->fp8, d, I, s));
-  HIPCHK(c, hipEventRecord(b.ev_phase[2], s));
+  if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[2], s));
   if (b.helper) HIPCHK(c, hipStreamWaitEvent(s, c->ev_helper[slot], 0));
   HIPCHK(c, launch_combine(c->arena, sc, b.row0, b.n_rows, k, d, c->out, s));
-  HIPCHK(c, hipEventRecord(b.ev_phase[3], s));
+  if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[3], s));
 
   if (cfg.record_routing) {
     HIPCHK(c, hipHostMalloc((void **)&b.h_cnt, sizeof(int32_t) * E, 0));
@@ -458,6 +462,13 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
     return rc;
   }
   *out = c;
+  return CEP_OK;
+}
+
+CEP_API int cep_set_phase_timing(cep_ctx *c, int on) {
+  if (!c) return CEP_EINVAL;
+  if (c->state != kIdle) return fail(c, CEP_ESTATE, "cep_set_phase_timing inside an open layer");
+  c->phase_timing = on != 0;
   return CEP_OK;
 }
 
@@ -680,11 +691,11 @@ CEP_API int cep_get_stats(cep_ctx *c, char *buf, size_t cap) {
   for (size_t i = 0; i < c->batches.size(); ++i) {
     const BatchRec &b = c->batches[i];
     HIPCHK(c, hipEventSynchronize(b.ev_end));
-    float t0 = 0, t1 = 0, ph[4] = {0, 0, 0, 0};
-    HIPCHK(c, hipEventElapsedTime(&t0, c->ev_origin, b.ev_start));
+    float t0 = -1, t1 = 0, ph[4] = {-1, -1, -1, -1};
+    if (b.phases) HIPCHK(c, hipEventElapsedTime(&t0, c->ev_origin, b.ev_start));
     HIPCHK(c, hipEventElapsedTime(&t1, c->ev_origin, b.ev_end));
     hipEvent_t prev = b.ev_start;
-    for (int p = 0; p < 4; ++p) {
+    for (int p = 0; b.phases && p < 4; ++p) {
       HIPCHK(c, hipEventElapsedTime(&ph[p], prev, b.ev_phase[p]));
       prev = b.ev_phase[p];
     }

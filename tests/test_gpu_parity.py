@@ -300,6 +300,24 @@ def test_error_paths():
     run.close()
 
 
+def test_phase_timing_switch_keeps_results():
+    wl = W.generate("tiny", 0)
+    run = harness.Runner(wl, n_streams=2)
+    run.run(policy=cep.CEP_THRESHOLD, theta=300, n_streams=2)
+    a = _out(run)
+    st = run.stats()
+    assert all(b["gemm1_ms"] >= 0 for b in st["batches"])
+    cep.cep_set_phase_timing(run.ctx, False)
+    run.out.zero_()
+    run.run(policy=cep.CEP_THRESHOLD, theta=300, n_streams=2)
+    b = _out(run)
+    st = run.stats()
+    assert all(x["route_ms"] == -1 and x["gemm1_ms"] == -1 for x in st["batches"])
+    assert all(x["start_ms"] == -1 and x["end_ms"] >= 0 for x in st["batches"])
+    run.close()
+    assert np.array_equal(a, b)
+
+
 def test_all_remote_chunk_launches_nothing():
     wl = W.generate("tiny", 0)
     run = harness.Runner(wl)
