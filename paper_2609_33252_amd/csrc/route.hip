@@ -428,23 +428,52 @@ __global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0
 // --------------------------------------------------------------- combine
 // One block per batch row: out[dst] = sum over its valid slots, in slot
 // order, of the grouped output rows (already scaled by their coefficient).
+// The row's valid slot positions are gathered once into LDS; each thread
+// then issues the loads of all its columns before summing, slot by slot.
+constexpr int kCombineCols = 4;  // float4 columns per thread per pass
+
 __global__ __launch_bounds__(256) void k_combine(Arena a, Scratch sc, int row0, int k, int d,
                                                  float *__restrict__ out) {
+  __shared__ int s_pos[kMaxTopK];
+  __shared__ int s_n;
   const int i = blockIdx.x;
   const int dst = a.dst[row0 + i];
   if (dst < 0) return;
-  const int32_t *pos = sc.pos_of + (size_t)i * k;
-  float4 *o = (float4 *)(out + (size_t)dst * d);
-  const float4 *y = (const float4 *)sc.y;
-  for (int c = threadIdx.x; c < d / 4; c += blockDim.x) {
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (threadIdx.x == 0) {
+    const int32_t *pos = sc.pos_of + (size_t)i * k;
+    int n = 0;
     for (int s = 0; s < k; ++s) {
       const int ps = pos[s];
-      if (ps < 0) continue;
-      const float4 v = y[(size_t)ps * (d / 4) + c];
-      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+      if (ps >= 0) s_pos[n++] = ps;
     }
-    o[c] = acc;
+    s_n = n;
+  }
+  __syncthreads();
+  const int n = s_n, d4 = d / 4;
+  float4 *o = (float4 *)(out + (size_t)dst * d);
+  const float4 *y = (const float4 *)sc.y;
+  for (int c0 = threadIdx.x; c0 < d4; c0 += blockDim.x * kCombineCols) {
+    float4 acc[kCombineCols];
+#pragma unroll
+    for (int u = 0; u < kCombineCols; ++u) acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int j = 0; j < n; ++j) {
+      const float4 *yr = y + (size_t)s_pos[j] * d4;
+      float4 v[kCombineCols];
+#pragma unroll
+      for (int u = 0; u < kCombineCols; ++u) {
+        const int c = c0 + u * blockDim.x;
+        v[u] = c < d4 ? yr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < kCombineCols; ++u) {
+        acc[u].x += v[u].x; acc[u].y += v[u].y; acc[u].z += v[u].z; acc[u].w += v[u].w;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kCombineCols; ++u) {
+      const int c = c0 + u * blockDim.x;
+      if (c < d4) o[c] = acc[u];
+    }
   }
 }
 
