@@ -11,6 +11,9 @@ Modules (each function cites the passage of the paper it follows):
 
 * ``fp8``     -- OCP e4m3fn decode/encode written from the format definition,
                  plus 1x128 activation block quantisation.
+* ``mx``      -- OCP MX formats: E2M1 and E8M0 decode, packed MXFP4 weight
+                 matrices, MXFP8 (E4M3) block quantisation (the paper's
+                 MXFP4 expert precision, Section 4.1).
 * ``routing`` -- per-batch expert histogram, exclusive scan, tile-aligned
                  offsets, stable permutation and inverse map (Appendix C,
                  "Grouped FFN invocations").
@@ -22,6 +25,11 @@ Modules (each function cites the passage of the paper it follows):
                  GEMM (Appendix C), each routed contribution weighted by its
                  routing coefficient exactly once and summed at the source
                  token (Appendix C, "Output return and combine").  float64.
+* ``calibration`` -- launch threshold theta(rho) and the FFN latency model
+                 F(N) from a throughput profile (Section 3.2).
+* ``oewf``    -- the OEWF coordinator: Algorithm 1, the reassignment
+                 admission test and the versioned commit (Section 3.3,
+                 Appendix C, Appendix E).
 
 Precision readings (the paper fixes none of them) are stated per function.
 """

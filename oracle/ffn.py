@@ -20,10 +20,12 @@ Readings where the paper is silent:
 * ``h_mode`` mirrors the dtype the second GEMM consumes: None keeps h in
   float64, "bf16" rounds h to bfloat16 (nearest, ties to even), "fp8"
   rounds h to float32 then quantises it per (row, 128 columns) exactly like
-  the activations (see ``oracle.fp8``);
+  the activations (see ``oracle.fp8``), "mxfp8" rounds h to float32 then
+  quantises it to MXFP8 per (row, 32 columns) (see ``oracle.mx``);
 * ``x_mode`` "fp8" quantises each input row per 128 channels before the
   first GEMM (the "activations with their quantization metadata" the layout
-  transform packs), else inputs are used exactly;
+  transform packs), "mxfp8" to MXFP8 per 32 channels, else inputs are used
+  exactly;
 * the result is rounded once to float32 at the end.
 """
 from __future__ import annotations
@@ -31,6 +33,7 @@ from __future__ import annotations
 import numpy as np
 
 from . import fp8 as _fp8
+from . import mx as _mx
 
 
 def bf16_bits_to_f64(bits) -> np.ndarray:
@@ -66,6 +69,9 @@ def expert_ffn(x: np.ndarray, wg: np.ndarray, wu: np.ndarray, wd: np.ndarray,
     elif h_mode == "fp8":
         codes, scale = _fp8.quantize_blocks(h.astype(np.float32))
         h = _fp8.dequantize_blocks(codes, scale)
+    elif h_mode == "mxfp8":
+        codes, scode = _mx.quantize_mxfp8(h.astype(np.float32))
+        h = _mx.dequantize_mxfp8(codes, scode)
     elif h_mode is not None:
         raise ValueError(h_mode)
     return h @ wd
@@ -78,6 +84,10 @@ class ExpertBank:
     e4m3 codes with one float32 scale per 128x128 block.
     gate/up are [E][d][I], down is [E][I][d]; fp8 scales are
     [E][d/128][I/128] and [E][I/128][d/128].
+    kind "mxfp4": stored output-major with K packed, as MX checkpoints keep
+    linear layers: gate/up codes [E][I][d/2] with E8M0 scales [E][I][d/32],
+    down codes [E][d][I/2] with scales [E][d][I/32]; decoded and transposed
+    to math orientation here.
     """
 
     def __init__(self, kind, w_gate, w_up, w_down, s_gate=None, s_up=None, s_down=None):
@@ -93,6 +103,8 @@ class ExpertBank:
             return bf16_bits_to_f64(a)
         if self.kind == "fp8":
             return _fp8.dequantize_weight(np.asarray(a, np.uint8), np.asarray(s, np.float32))
+        if self.kind == "mxfp4":
+            return _mx.dequantize_mxfp4(np.asarray(a, np.uint8), np.asarray(s, np.uint8)).T
         raise ValueError(self.kind)
 
     def __call__(self, e: int):
@@ -125,6 +137,9 @@ def routed_output(x64: np.ndarray, ids: np.ndarray, w: np.ndarray, bank, n_exper
         if x_mode == "fp8":
             codes, scale = _fp8.quantize_blocks(xg.astype(np.float32))
             xg = _fp8.dequantize_blocks(codes, scale)
+        elif x_mode == "mxfp8":
+            codes, scode = _mx.quantize_mxfp8(xg.astype(np.float32))
+            xg = _mx.dequantize_mxfp8(codes, scode)
         elif x_mode is not None:
             raise ValueError(x_mode)
         idg, wgt = ids[lo:hi], w[lo:hi]
