@@ -62,8 +62,11 @@ enum cep_status {
 enum cep_dtype {
   CEP_F32 = 0,          /* float32 (converted to bf16 inside the library)     */
   CEP_BF16 = 1,         /* bfloat16                                            */
-  CEP_FP8_E4M3_B128 = 2 /* weights only: OCP e4m3fn codes, one float32 scale
+  CEP_FP8_E4M3_B128 = 2, /* weights only: OCP e4m3fn codes, one float32 scale
                            per 128x128 block                                   */
+  CEP_MXFP4 = 3          /* weights only: OCP MXFP4 (e2m1 codes, one E8M0 scale
+                           per 32 along K; Section 4.1's DeepSeek-V4 experts);
+                           activations and h run as MXFP8 inside the library */
 };
 
 enum cep_policy {
@@ -89,13 +92,20 @@ typedef struct {
                                  for cep_get_batch_routing (test/debug aid)   */
 } cep_config;
 
-/* Expert weights in math orientation (y = x W), device memory:
+/* Expert weights, device memory.
+ * F32 / BF16 / FP8, math orientation (y = x W):
  *   w_gate, w_up : [E][d][I]     w_down : [E][I][d]   (element type w_dtype)
  *   FP8 only, float32 block scales (value = code * scale of its block):
- *   s_gate, s_up : [E][d/128][I/128]   s_down : [E][I/128][d/128]            */
+ *   s_gate, s_up : [E][d/128][I/128]   s_down : [E][I/128][d/128]
+ * MXFP4, output-major with K packed (the layout MX checkpoints use for a
+ * linear layer's weight), two e2m1 codes per byte, the even K in the low
+ * nibble, and uint8 E8M0 scales (2^(s-127)) per 32 consecutive K:
+ *   w_gate, w_up : [E][I][d/2]   s_gate, s_up : [E][I][d/32]
+ *   w_down       : [E][d][I/2]   s_down       : [E][d][I/32]
+ * Scale pointers are unused (may be NULL) for F32 and BF16.                  */
 typedef struct {
   const void *w_gate, *w_up, *w_down;
-  const float *s_gate, *s_up, *s_down;
+  const void *s_gate, *s_up, *s_down; /* float32 (FP8) or uint8 E8M0 (MXFP4) */
 } cep_weights;
 
 /* Bytes of one expert's packed weight blob (the library's device layout of

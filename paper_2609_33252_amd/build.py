@@ -18,7 +18,7 @@ OUT = os.path.join(HERE, "libcep.so")
 OBJ = os.path.join(HERE, "_build")
 ARCH = "gfx950"
 
-SOURCES = ["route.hip", "gemm.hip", "gemm_bf16.hip", "gemm_fp8.hip", "runtime.hip", "profile.cpp", "oewf.cpp"]
+SOURCES = ["route.hip", "gemm.hip", "gemm_bf16.hip", "gemm_fp8.hip", "gemm_mx.hip", "runtime.hip", "profile.cpp", "oewf.cpp"]
 # Per-source extra flags.  The e4m3 GEMM promotes every MFMA result with
 # VALU arithmetic; taking MFMA results in VGPRs saves one accvgpr read per
 # promoted element.

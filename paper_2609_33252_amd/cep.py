@@ -14,7 +14,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libcep.so")
 
 CEP_OK, CEP_EINVAL, CEP_ENOMEM, CEP_EHIP, CEP_ESTATE, CEP_EBUSY = 0, -1, -2, -3, -4, -5
-CEP_F32, CEP_BF16, CEP_FP8_E4M3_B128 = 0, 1, 2
+CEP_F32, CEP_BF16, CEP_FP8_E4M3_B128, CEP_MXFP4 = 0, 1, 2, 3
 CEP_WAIT_ALL, CEP_PER_CHUNK, CEP_THRESHOLD = 0, 1, 2
 STATUS_NAMES = {0: "CEP_OK", -1: "CEP_EINVAL", -2: "CEP_ENOMEM", -3: "CEP_EHIP",
                 -4: "CEP_ESTATE", -5: "CEP_EBUSY"}

@@ -19,9 +19,13 @@ constexpr int kFp8TileM = 128;       // e4m3 grouped GEMM tile (4 waves)
 constexpr int kFp8LargeTileM = 256;  // e4m3 tile for large batches (8 waves)
 constexpr int kRouteThreads = 256;   // threads per routing block
 constexpr int kRoutePairs = 2048;    // flat pairs per routing block (8 rounds of 256)
-constexpr int kInterleave = 32;
+constexpr int kInterleave = 32;           // gate/up column interleave of the packed W1
 constexpr int kFusedRoutePairs = 1 << 15;  // batches up to this many flat (row, slot)
-                                           // entries route in one block (ids in LDS)      // gate/up column interleave of the packed W1
+                                           // entries route in one block (ids in LDS)
+constexpr int kMxBlock = 32;               // MX scale block along K
+
+// Expert weight format of a context (from cep_config.w_dtype).
+enum WKind : int { kWBf16 = 0, kWFp8 = 1, kWMx = 2 };
 
 // One M tile of a grouped GEMM: expert, first grouped row, valid rows in it.
 struct Tile {
@@ -52,6 +56,8 @@ __host__ __device__ inline const uint8_t *blob_of(const BlobTable &t, int e) {
 // Packed blob layout of one expert (byte offsets from the blob start).
 //   bf16: W1p [2I][d] bf16 (K contiguous), W2p [d][I] bf16
 //   fp8 : W1p [2I][d] u8, W2p [d][I] u8, S1 [2I/32][d/128] f32, S2 [d/128][I/128] f32
+//   mx  : W1p [2I][d/2], W2p [d][I/2] packed e2m1 (even K in the low nibble),
+//         S1, S2: E8M0 bytes in mx_weight_scale_offset order (N = 2I or d)
 // Row n' of W1p holds column j = (n'/64)*32 + n'%32 of the gate weights when
 // (n'/32) is even and of the up weights when it is odd, so that one 64-row
 // group carries matching gate and up columns for the fused SwiGLU.
@@ -68,15 +74,24 @@ constexpr int kBf16SmallTileM = 64;  // bf16 tile for batches with few rows per 
 // per local expert on average use the small tile: the GEMMs then stream the
 // weights with four times as many workgroups.  Both bf16 tiles accumulate K
 // in the same order with the same MFMA, so results do not depend on it.
-inline int batch_align(bool fp8, int pairs, int n_experts) {
-  if (fp8) return pairs >= kFp8LargeTileM * n_experts ? kFp8LargeTileM : kFp8TileM;
+inline int batch_align(int wk, int pairs, int n_experts) {
+  if (wk != kWBf16) return pairs >= kFp8LargeTileM * n_experts ? kFp8LargeTileM : kFp8TileM;
   return pairs >= kBf16TileM * n_experts ? kBf16TileM : kBf16SmallTileM;
 }
 constexpr int kMinAlign = 64;
 constexpr int kMaxAlign = 256;
 
-inline BlobLayout blob_layout(int d, int I, bool fp8) {
+inline BlobLayout blob_layout(int d, int I, int wk) {
   BlobLayout L{};
+  if (wk == kWMx) {
+    L.w1_off = 0;
+    L.w2_off = align_up((size_t)I * d, 256);
+    L.s1_off = align_up(L.w2_off + (size_t)d * I / 2, 256);
+    L.s2_off = align_up(L.s1_off + (size_t)2 * I * d / kMxBlock, 256);
+    L.bytes = align_up(L.s2_off + (size_t)d * I / kMxBlock, 256);
+    return L;
+  }
+  const bool fp8 = wk == kWFp8;
   size_t es = fp8 ? 1 : 2;
   L.w1_off = 0;
   L.w2_off = align_up(L.w1_off + (size_t)2 * I * d * es, 256);
@@ -88,6 +103,26 @@ inline BlobLayout blob_layout(int d, int I, bool fp8) {
   }
   L.bytes = align_up(end, 256);
   return L;
+}
+
+// MXFP8 scales of grouped rows (activations and h; s_ld a multiple of 256,
+// row groups of 128).  The E8M0 scale of row R, K block b (32 channels) sits
+// where one K step of 128 (4 blocks) of a 128-row group is 512 contiguous
+// bytes and the scales of rows R%16 + 16i, i = 0..7, of one block are one
+// 8-byte word: the four-byte halves feed the MFMA's byte-selected scale
+// operand of row fragments i = 0..3 and 4..7.
+__host__ __device__ inline size_t mx_row_scale_offset(int R, int b, int s_ld) {
+  return ((size_t)(b >> 2) * (s_ld >> 7) + (R >> 7)) * 512 + (b & 3) * 128 + (R & 15) * 8 +
+         ((R & 127) >> 4);
+}
+
+// E8M0 weight scales in a blob (B = [N][K] packed weights, N a multiple of
+// 256): for each 256-column tile and K step of 128 one 1 KB record holding,
+// for the wave of column group wn (64 columns), the lane of K block g and
+// column n16, the scales of its four 16-column fragments j as one word.
+__host__ __device__ inline size_t mx_weight_scale_offset(int n, int b, int K) {
+  const int nt = n >> 8, wn = (n >> 6) & 3, j = (n >> 4) & 3, n16 = n & 15;
+  return ((size_t)nt * (K >> 7) + (b >> 2)) * 1024 + ((wn * 4 + (b & 3)) * 16 + n16) * 4 + j;
 }
 
 // Chunk arena of one layer: one entry per submitted row, in submission order.
@@ -112,9 +147,10 @@ struct Scratch {
   int32_t *perm;       // [max_mpad] flat pair of each grouped row or -1
   float *wrow;         // [max_mpad] routing coefficient of each grouped row
   void *xg;            // [max_mpad][d] bf16 or e4m3
-  float *xs;           // [d/128][s_ld] e4m3 activation scales, k-block major
+  float *xs;           // e4m3: [d/128][s_ld] activation scales, k-block major;
+                       // mx: E8M0 bytes at mx_row_scale_offset (same size)
   void *h;             // [max_mpad][I] bf16 or e4m3
-  float *hs;           // [I/128][s_ld] e4m3 scales of h, k-block major
+  float *hs;           // scales of h, laid out like xs (K = I)
   int s_ld;            // row stride of xs / hs (= max_mpad, a multiple of 256)
   float *y;            // [max_mpad][d] f32, already scaled by the coefficient
 };
@@ -130,6 +166,11 @@ hipError_t launch_pack_w2(const void *wd, int w_dtype, int d, int I, uint8_t *ds
                           hipStream_t s);
 hipError_t launch_pack_scales(const float *sg, const float *su, const float *sd, int d, int I,
                               float *dst_s1, float *dst_s2, hipStream_t s);
+// MXFP4 experts: caller layout gate/up [I][d/2] + [I][d/32], down [d][I/2] +
+// [d][I/32] (output-major, K packed) into the blob of layout L
+hipError_t launch_pack_mx(const uint8_t *wg, const uint8_t *wu, const uint8_t *wd,
+                          const uint8_t *sg, const uint8_t *su, const uint8_t *sd, int d, int I,
+                          uint8_t *blob, const BlobLayout &L, hipStream_t s);
 
 // routing
 // One staging launch covers up to kIngestGroup chunks (passed by value).
@@ -153,7 +194,7 @@ hipError_t launch_ingest(const Arena &a, const IngestGroup &grp, int k, int E, i
 // n_tiles_n 256-wide column tiles improves.
 hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int E,
                         int align, int expected_pairs, int max_mpad, int max_tiles,
-                        uint64_t fetched_mask, int x_dtype, bool fp8, int d, int split_cu,
+                        uint64_t fetched_mask, int x_dtype, int wk, int d, int split_cu,
                         int n_tiles_n, uint32_t *err, hipStream_t s);
 hipError_t launch_combine(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int d,
                           float *out, hipStream_t s);
@@ -164,9 +205,9 @@ hipError_t launch_combine(const Arena &a, const Scratch &sc, int row0, int n_row
 // split_tiles > 0, up to split_tiles 64-row remainder tiles
 hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles,
                         int split_tiles, int align, const BlobTable &bt, const BlobLayout &L,
-                        bool fp8, int d, int I, hipStream_t s);
+                        int wk, int d, int I, hipStream_t s);
 hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles,
                         int split_tiles, int align, const BlobTable &bt, const BlobLayout &L,
-                        bool fp8, int d, int I, hipStream_t s);
+                        int wk, int d, int I, hipStream_t s);
 
 }  // namespace cep

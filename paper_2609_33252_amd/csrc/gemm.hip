@@ -1,8 +1,8 @@
 // Launchers of the grouped expert GEMMs (Appendix C, "Grouped FFN
 // invocations"): GEMM1 = gate/up projection with SwiGLU (and, for e4m3
-// weights, the h re-quantisation) in the epilogue; GEMM2 = down projection
-// scaled by each row's routing coefficient.  Kernels: gemm_bf16.hip,
-// gemm_fp8.hip.
+// and MXFP4 weights, the h re-quantisation) in the epilogue; GEMM2 = down
+// projection scaled by each row's routing coefficient.  Kernels:
+// gemm_bf16.hip, gemm_fp8.hip, gemm_mx.hip.
 #include "gemm_common.h"
 
 namespace cep {
@@ -20,9 +20,10 @@ GemmArgs base_args(const Scratch &sc, int list, int list_cap, int grid_tiles,
 }
 
 template <bool SWIGLU>
-hipError_t launch_any(const GemmArgs &g, int grid_tiles, int split_tiles, int align, bool fp8,
+hipError_t launch_any(const GemmArgs &g, int grid_tiles, int split_tiles, int align, int wk,
                       const Scratch &sc, int which, int list_cap, hipStream_t s) {
-  if (fp8) return launch_fp8<SWIGLU>(g, grid_tiles, align, s);
+  if (wk == kWFp8) return launch_fp8<SWIGLU>(g, grid_tiles, align, s);
+  if (wk == kWMx) return launch_mx<SWIGLU>(g, grid_tiles, align, s);
   hipError_t e = launch_bf16<SWIGLU>(g, grid_tiles, align, s);
   if (e != hipSuccess || split_tiles <= 0) return e;
   // remainder tiles: same operands and output, the 64-row list
@@ -37,7 +38,7 @@ hipError_t launch_any(const GemmArgs &g, int grid_tiles, int split_tiles, int al
 
 hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles,
                         int split_tiles, int align, const BlobTable &bt, const BlobLayout &L,
-                        bool fp8, int d, int I, hipStream_t s) {
+                        int wk, int d, int I, hipStream_t s) {
   if (grid_tiles <= 0) return hipSuccess;
   GemmArgs g = base_args(sc, 2 * which, list_cap, grid_tiles, bt);
   g.A = (const uint8_t *)sc.xg;
@@ -48,12 +49,12 @@ hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_til
   g.bs_off = L.s1_off;
   g.out = sc.h;
   g.out_s = sc.hs;
-  return launch_any<true>(g, grid_tiles, split_tiles, align, fp8, sc, which, list_cap, s);
+  return launch_any<true>(g, grid_tiles, split_tiles, align, wk, sc, which, list_cap, s);
 }
 
 hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles,
                         int split_tiles, int align, const BlobTable &bt, const BlobLayout &L,
-                        bool fp8, int d, int I, hipStream_t s) {
+                        int wk, int d, int I, hipStream_t s) {
   if (grid_tiles <= 0) return hipSuccess;
   GemmArgs g = base_args(sc, 2 * which, list_cap, grid_tiles, bt);
   g.A = (const uint8_t *)sc.h;
@@ -64,7 +65,7 @@ hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_til
   g.bs_off = L.s2_off;
   g.out = sc.y;
   g.wrow = sc.wrow;
-  return launch_any<false>(g, grid_tiles, split_tiles, align, fp8, sc, which, list_cap, s);
+  return launch_any<false>(g, grid_tiles, split_tiles, align, wk, sc, which, list_cap, s);
 }
 
 }  // namespace cep

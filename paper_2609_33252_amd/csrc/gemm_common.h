@@ -1,4 +1,4 @@
-// Device helpers shared by the grouped GEMM kernels (bf16 and e4m3).
+// Device helpers shared by the grouped GEMM kernels (bf16, e4m3, MXFP4).
 // Internal to libcep.
 #pragma once
 
@@ -20,8 +20,9 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // list (expert, first row, valid rows) built by the routing scan.
 struct GemmArgs {
   const uint8_t *A;       // grouped rows [mpad][K] (bf16 or e4m3)
-  const float *As;        // e4m3: [K/128][s_ld] row scales, k-block major
-  int s_ld;               // e4m3: row stride of the scale matrices
+  const float *As;        // e4m3: [K/128][s_ld] row scales, k-block major;
+                          // mx: E8M0 bytes at mx_row_scale_offset
+  int s_ld;               // quantised A: row stride of the scale matrices
   const Tile *tiles;      // tile list
   const int32_t *n_tiles; // live tiles in the list
   int max_tiles;          // grid extent in M tiles (host upper bound)
@@ -29,7 +30,7 @@ struct GemmArgs {
   size_t b_off, bs_off;   // offsets of B and its scales in each blob
   BlobTable bt;
   void *out;              // H [mpad][N/2] (GEMM1) or Y [mpad][N] f32 (GEMM2)
-  float *out_s;           // e4m3 GEMM1: h scales [N/256][s_ld]
+  float *out_s;           // quantised GEMM1: h scales (layout of As, K = N/2)
   const float *wrow;      // GEMM2: routing coefficient per grouped row
 };
 
@@ -140,5 +141,7 @@ template <bool SWIGLU>
 hipError_t launch_bf16(const GemmArgs &g, int grid_tiles, int align, hipStream_t s);
 template <bool SWIGLU>
 hipError_t launch_fp8(const GemmArgs &g, int grid_tiles, int align, hipStream_t s);
+template <bool SWIGLU>
+hipError_t launch_mx(const GemmArgs &g, int grid_tiles, int align, hipStream_t s);
 
 }  // namespace cep

@@ -359,11 +359,13 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_scatter(Arena a, Scratc
 // ----------------------------------------------------------------- pack
 // One wave per grouped row (kPackRows rows per block): the pair's input row
 // is copied (bf16), converted (f32 -> bf16) or quantised (e4m3, one scale per
-// 128 channels) into its grouped row, and its routing coefficient goes to the
-// row's slot of wrow.  Padding rows (no pair) are skipped.
+// 128 channels; or MXFP8, one E8M0 scale per 32 channels) into its grouped
+// row, and its routing coefficient goes to the row's slot of wrow.  Padding
+// rows (no pair) are skipped.
 constexpr int kPackRows = 8;
 
-template <int XMODE>  // 0: bf16 -> bf16, 1: f32 -> bf16, 2: bf16 -> e4m3 + scales
+// 0: bf16 -> bf16, 1: f32 -> bf16, 2: bf16 -> e4m3 + scales, 3: bf16 -> MXFP8
+template <int XMODE>
 __global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0, int k, int E,
                                                    int d, int n_rows_pad) {
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
@@ -388,6 +390,43 @@ __global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0
         o.h[0] = (__bf16)lo.x; o.h[1] = (__bf16)lo.y; o.h[2] = (__bf16)lo.z; o.h[3] = (__bf16)lo.w;
         o.h[4] = (__bf16)hi.x; o.h[5] = (__bf16)hi.y; o.h[6] = (__bf16)hi.z; o.h[7] = (__bf16)hi.w;
         d4[c] = o.u;
+      }
+    } else if (XMODE == 3) {
+      // 4 lanes x 8 channels = one 32-channel MX block: E8M0 scale
+      // 2^(floor(log2 amax) - 8), codes e4m3(x / scale) saturated at 448
+      const uint4 *s4 = (const uint4 *)src;
+      uint8_t *dq = (uint8_t *)sc.xg + (size_t)pos * d;
+      uint8_t *ds = (uint8_t *)sc.xs;
+      for (int c0 = 0; c0 < d; c0 += 512) {
+        const int c = c0 + lane * 8;
+        const bool ok = c < d;
+        float v[8];
+        float amax = 0.f;
+        if (ok) {
+          union { uint4 u; __bf16 h[8]; } in;
+          in.u = s4[c / 8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            v[j] = (float)in.h[j];
+            amax = fmaxf(amax, fabsf(v[j]));
+          }
+        }
+        amax = fmaxf(amax, __shfl_xor(amax, 1, 4));
+        amax = fmaxf(amax, __shfl_xor(amax, 2, 4));
+        if (ok) {
+          const int code = max((int)((__float_as_uint(amax) >> 23) & 0xff) - 8, 0);
+          const int e = 127 - code;
+          float q[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) q[j] = fminf(fmaxf(ldexpf(v[j], e), -448.0f), 448.0f);
+          int lo = 0, hi = 0;
+          lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[0], q[1], lo, false);
+          lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], lo, true);
+          hi = __builtin_amdgcn_cvt_pk_fp8_f32(q[4], q[5], hi, false);
+          hi = __builtin_amdgcn_cvt_pk_fp8_f32(q[6], q[7], hi, true);
+          *(uint2 *)(dq + c) = make_uint2((uint32_t)lo, (uint32_t)hi);
+          if ((lane & 3) == 0) ds[mx_row_scale_offset(pos, c / kMxBlock, sc.s_ld)] = (uint8_t)code;
+        }
       }
     } else {
       // 16 lanes x 8 channels = one 128-channel scale block
@@ -523,9 +562,56 @@ __global__ void k_pack_scales(const float *sg, const float *su, const float *sd,
   }
 }
 
+// MXFP4 experts.  W1p row n' is row (n'/64)*32 + n'%32 of the gate
+// (n'/32 even) or up (odd) codes [I][d/2]: the caller's layout is already K
+// packed, so packing is a row gather, one block per row.
+__global__ __launch_bounds__(256) void k_pack_mx_w1(const uint8_t *wg, const uint8_t *wu,
+                                                    int row_bytes, uint8_t *dst) {
+  const int n = blockIdx.x;
+  const uint8_t *src = (((n / kInterleave) & 1) ? wu : wg) +
+                       (size_t)((n / (2 * kInterleave)) * kInterleave + n % kInterleave) * row_bytes;
+  const uint4 *s4 = (const uint4 *)src;
+  uint4 *d4 = (uint4 *)(dst + (size_t)n * row_bytes);
+  for (int c = threadIdx.x; c < row_bytes / 16; c += blockDim.x) d4[c] = s4[c];
+}
+
+// E8M0 scales [N][K/32] (row n of B) into mx_weight_scale_offset order;
+// interleave: N = 2I rows gathered from gate (sa) and up (sb) like W1p.
+__global__ void k_pack_mx_scales(const uint8_t *sa, const uint8_t *sb, int N, int K,
+                                 int interleave, uint8_t *dst) {
+  const int nblk = K / kMxBlock;
+  const size_t total = (size_t)N * nblk;
+  for (size_t t = (size_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
+       t += (size_t)gridDim.x * blockDim.x) {
+    const int n = (int)(t / nblk), b = (int)(t % nblk);
+    const uint8_t *src = sa;
+    int row = n;
+    if (interleave) {
+      src = ((n / kInterleave) & 1) ? sb : sa;
+      row = (n / (2 * kInterleave)) * kInterleave + n % kInterleave;
+    }
+    dst[mx_weight_scale_offset(n, b, K)] = src[(size_t)row * nblk + b];
+  }
+}
+
 }  // namespace
 
 // ================================================================ launchers
+hipError_t launch_pack_mx(const uint8_t *wg, const uint8_t *wu, const uint8_t *wd,
+                          const uint8_t *sg, const uint8_t *su, const uint8_t *sd, int d, int I,
+                          uint8_t *blob, const BlobLayout &L, hipStream_t s) {
+  hipLaunchKernelGGL(k_pack_mx_w1, dim3(2 * I), dim3(256), 0, s, wg, wu, d / 2, blob + L.w1_off);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  e = hipMemcpyAsync(blob + L.w2_off, wd, (size_t)d * I / 2, hipMemcpyDeviceToDevice, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_pack_mx_scales, dim3(256), dim3(256), 0, s, sg, su, 2 * I, d, 1,
+                     blob + L.s1_off);
+  hipLaunchKernelGGL(k_pack_mx_scales, dim3(256), dim3(256), 0, s, sd, (const uint8_t *)nullptr,
+                     d, I, 0, blob + L.s2_off);
+  return hipGetLastError();
+}
+
 hipError_t launch_pack_w1(const void *wg, const void *wu, int w_dtype, int d, int I,
                           uint8_t *dst, hipStream_t s) {
   dim3 grid((I + 63) / 64, (d + 63) / 64);
@@ -581,7 +667,7 @@ hipError_t launch_ingest(const Arena &a, const IngestGroup &grp, int k, int E, i
 
 hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int E,
                         int align, int expected_pairs, int max_mpad, int max_tiles,
-                        uint64_t fetched_mask, int x_dtype, bool fp8, int d, int split_cu,
+                        uint64_t fetched_mask, int x_dtype, int wk, int d, int split_cu,
                         int n_tiles_n, uint32_t *err, hipStream_t s) {
   const int n_flat = n_rows * k;
   const int nb = (n_flat + kRoutePairs - 1) / kRoutePairs;
@@ -602,7 +688,9 @@ hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows,
   const long long bound = ((long long)(expected_pairs + align - 1) / align + E) * align;
   const int n_pad = (int)std::min<long long>(bound, max_mpad);
   const dim3 pgrid((n_pad + kPackRows - 1) / kPackRows);
-  if (fp8)
+  if (wk == kWMx)
+    hipLaunchKernelGGL(k_pack_rows<3>, pgrid, dim3(256), 0, s, a, sc, row0, k, E, d, n_pad);
+  else if (wk == kWFp8)
     hipLaunchKernelGGL(k_pack_rows<2>, pgrid, dim3(256), 0, s, a, sc, row0, k, E, d, n_pad);
   else if (x_dtype == 0)
     hipLaunchKernelGGL(k_pack_rows<1>, pgrid, dim3(256), 0, s, a, sc, row0, k, E, d, n_pad);

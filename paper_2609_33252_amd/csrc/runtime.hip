@@ -56,7 +56,7 @@ struct cep_ctx {
   cep_config cfg{};
   int device = 0;
   std::string err;
-  bool fp8 = false;
+  int wk = kWBf16;  // expert weight format
   BlobLayout L{};
   uint8_t *w_res = nullptr;  // E blobs
   std::vector<uint8_t> resident;
@@ -146,13 +146,17 @@ bool valid_config(const cep_config *c, std::string *why) {
   if (c->top_k < 1 || c->top_k > kMaxTopK) return bad("top_k must be in 1..16");
   if (c->max_replicas < 1 || c->max_tokens_per_replica < 1) return bad("max_replicas and max_tokens_per_replica must be >= 1");
   if ((long long)c->max_replicas * c->max_tokens_per_replica > (1LL << 24)) return bad("max_replicas * max_tokens_per_replica too large");
-  if (c->w_dtype < CEP_F32 || c->w_dtype > CEP_FP8_E4M3_B128) return bad("bad w_dtype");
+  if (c->w_dtype < CEP_F32 || c->w_dtype > CEP_MXFP4) return bad("bad w_dtype");
   if (c->x_dtype != CEP_F32 && c->x_dtype != CEP_BF16) return bad("x_dtype must be CEP_F32 or CEP_BF16");
   if (c->w_dtype == CEP_FP8_E4M3_B128 && c->x_dtype != CEP_BF16) return bad("fp8 weights need bf16 token rows");
-  if (c->w_dtype == CEP_FP8_E4M3_B128 && c->d_model % 256) return bad("fp8 weights need d_model multiple of 256");
+  if (c->w_dtype == CEP_MXFP4 && c->x_dtype != CEP_BF16) return bad("MXFP4 weights need bf16 token rows");
   if (c->n_streams < 1 || c->n_streams > 8) return bad("n_streams must be in 1..8");
   if (c->max_pairs_per_batch < 0) return bad("max_pairs_per_batch must be >= 0");
   return true;
+}
+
+int weight_kind(int w_dtype) {
+  return w_dtype == CEP_FP8_E4M3_B128 ? kWFp8 : (w_dtype == CEP_MXFP4 ? kWMx : kWBf16);
 }
 
 void *dalloc(cep_ctx *c, size_t bytes, hipError_t *e) {
@@ -240,7 +244,7 @@ int launch_pending(cep_ctx *c) {
   if (s != c->ingest) c->used_st |= 1u << slot;
   const Scratch &sc = c->sc[slot];
   const int P = b.n_pairs;
-  const int A = batch_align(c->fp8, b.n_pairs, E);
+  const int A = batch_align(c->wk, b.n_pairs, E);
   b.align = A;
   const int tiles = std::min(c->max_tiles, (P + A - 1) / A + E);
   b.mpad_bound = std::min(c->max_mpad, tiles * A);
@@ -267,10 +271,10 @@ int launch_pending(cep_ctx *c) {
   }
   // 256-row bf16 tiles: the scan may move small remainders to 64-row tiles
   // (at most two per expert), run by a second launch of the 64-row kernel
-  const bool split = !c->fp8 && A == kBf16TileM;
+  const bool split = c->wk == kWBf16 && A == kBf16TileM;
   const int split_tiles = split ? 2 * E : 0;
   HIPCHK(c, launch_route(c->arena, sc, b.row0, b.n_rows, k, E, A, P, c->max_mpad, c->max_tiles,
-                         c->fetched_mask, cfg.x_dtype, c->fp8, d, split ? c->n_cu : 0,
+                         c->fetched_mask, cfg.x_dtype, c->wk, d, split ? c->n_cu : 0,
                          2 * I / kBf16TileN, c->d_err, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[0], s));
 
@@ -283,13 +287,13 @@ int launch_pending(cep_ctx *c) {
     HIPCHK(c, hipEventRecord(c->ev_routed[slot], s));
     HIPCHK(c, hipStreamWaitEvent(h, c->ev_routed[slot], 0));
     HIPCHK(c, hipStreamWaitEvent(h, c->ev_fetch_ready, 0));
-    HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->fp8, d, I, h));
-    HIPCHK(c, launch_gemm2(sc, 1, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->fp8, d, I, h));
+    HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->wk, d, I, h));
+    HIPCHK(c, launch_gemm2(sc, 1, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->wk, d, I, h));
     HIPCHK(c, hipEventRecord(c->ev_helper[slot], h));
   }
-  HIPCHK(c, launch_gemm1(sc, 0, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->fp8, d, I, s));
+  HIPCHK(c, launch_gemm1(sc, 0, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->wk, d, I, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[1], s));
-  HIPCHK(c, launch_gemm2(sc, 0, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->fp8, d, I, s));
+  HIPCHK(c, launch_gemm2(sc, 0, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->wk, d, I, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[2], s));
   if (b.helper) HIPCHK(c, hipStreamWaitEvent(s, c->ev_helper[slot], 0));
   HIPCHK(c, launch_combine(c->arena, sc, b.row0, b.n_rows, k, d, c->out, s));
@@ -324,14 +328,15 @@ int launch_pending(cep_ctx *c) {
 CEP_API size_t cep_packed_expert_bytes(const cep_config *cfg) {
   std::string why;
   if (!valid_config(cfg, &why)) return 0;
-  return blob_layout(cfg->d_model, cfg->d_ff, cfg->w_dtype == CEP_FP8_E4M3_B128).bytes;
+  return blob_layout(cfg->d_model, cfg->d_ff, weight_kind(cfg->w_dtype)).bytes;
 }
 
 static int pack_range(const cep_config *cfg, const cep_weights *w, int first, int n, uint8_t *dst,
                       hipStream_t s, cep_ctx *c, const uint8_t *mask) {
   const int d = cfg->d_model, I = cfg->d_ff;
-  const bool fp8 = cfg->w_dtype == CEP_FP8_E4M3_B128;
-  const BlobLayout L = blob_layout(d, I, fp8);
+  const int wk = weight_kind(cfg->w_dtype);
+  const bool fp8 = wk == kWFp8;
+  const BlobLayout L = blob_layout(d, I, wk);
   const size_t es = cfg->w_dtype == CEP_F32 ? 4 : (fp8 ? 1 : 2);
   const size_t mat = (size_t)d * I * es;
   const size_t smat = (size_t)(d / 128) * (I / 128);
@@ -339,12 +344,24 @@ static int pack_range(const cep_config *cfg, const cep_weights *w, int first, in
     const int e = first + q;
     if (mask && !mask[e]) continue;
     uint8_t *blob = dst + (size_t)q * L.bytes;
+    if (wk == kWMx) {
+      // codes: gate/up [I][d/2], down [d][I/2]; E8M0 scales [I][d/32], [d][I/32]
+      const size_t cm = (size_t)d * I / 2, sm = (size_t)d * I / kMxBlock;
+      const uint8_t *sg = (const uint8_t *)w->s_gate, *su = (const uint8_t *)w->s_up,
+                    *sd = (const uint8_t *)w->s_down;
+      HIPCHK(c, launch_pack_mx((const uint8_t *)w->w_gate + e * cm, (const uint8_t *)w->w_up + e * cm,
+                               (const uint8_t *)w->w_down + e * cm, sg + e * sm, su + e * sm,
+                               sd + e * sm, d, I, blob, L, s));
+      continue;
+    }
     HIPCHK(c, launch_pack_w1((const uint8_t *)w->w_gate + e * mat, (const uint8_t *)w->w_up + e * mat,
                              cfg->w_dtype, d, I, blob + L.w1_off, s));
     HIPCHK(c, launch_pack_w2((const uint8_t *)w->w_down + e * mat, cfg->w_dtype, d, I,
                              blob + L.w2_off, s));
     if (fp8)
-      HIPCHK(c, launch_pack_scales(w->s_gate + e * smat, w->s_up + e * smat, w->s_down + e * smat,
+      HIPCHK(c, launch_pack_scales((const float *)w->s_gate + e * smat,
+                                   (const float *)w->s_up + e * smat,
+                                   (const float *)w->s_down + e * smat,
                                    d, I, (float *)(blob + L.s1_off), (float *)(blob + L.s2_off), s));
   }
   return CEP_OK;
@@ -357,7 +374,7 @@ CEP_API int cep_pack_experts(const cep_config *cfg, const cep_weights *w, int fi
   if (!w || !dst || first < 0 || n < 0 || first + n > cfg->n_local_experts)
     return fail(nullptr, CEP_EINVAL, "cep_pack_experts: bad weights, dst or expert range");
   if (!w->w_gate || !w->w_up || !w->w_down ||
-      (cfg->w_dtype == CEP_FP8_E4M3_B128 && (!w->s_gate || !w->s_up || !w->s_down)))
+      (weight_kind(cfg->w_dtype) != kWBf16 && (!w->s_gate || !w->s_up || !w->s_down)))
     return fail(nullptr, CEP_EINVAL, "cep_pack_experts: NULL weight or scale pointer");
   return pack_range(cfg, w, first, n, (uint8_t *)dst, s, nullptr, nullptr);
 }
@@ -369,7 +386,7 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
   std::string why;
   if (!valid_config(cfg, &why)) return fail(nullptr, CEP_EINVAL, "cep_init_experts: %s", why.c_str());
   if (!w || !w->w_gate || !w->w_up || !w->w_down ||
-      (cfg->w_dtype == CEP_FP8_E4M3_B128 && (!w->s_gate || !w->s_up || !w->s_down)))
+      (weight_kind(cfg->w_dtype) != kWBf16 && (!w->s_gate || !w->s_up || !w->s_down)))
     return fail(nullptr, CEP_EINVAL, "cep_init_experts: NULL weight or scale pointer");
   cep_ctx *c = new cep_ctx();
   c->cfg = *cfg;
@@ -380,8 +397,8 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
     return fail(nullptr, CEP_EHIP, "cep_init_experts: device query failed");
   }
   const int E = cfg->n_local_experts, k = cfg->top_k, d = cfg->d_model, I = cfg->d_ff;
-  c->fp8 = cfg->w_dtype == CEP_FP8_E4M3_B128;
-  c->L = blob_layout(d, I, c->fp8);
+  c->wk = weight_kind(cfg->w_dtype);
+  c->L = blob_layout(d, I, c->wk);
   c->resident.assign(E, 1);
   if (resident)
     for (int e = 0; e < E; ++e) c->resident[e] = resident[e] ? 1 : 0;
@@ -407,7 +424,7 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
   c->arena.dst = (int32_t *)A(sizeof(int32_t) * c->arena_cap);
   c->arena.xrow = (const void **)A(sizeof(void *) * c->arena_cap);
   c->d_err = (uint32_t *)A(sizeof(uint32_t));
-  const size_t xes = c->fp8 ? 1 : 2;
+  const size_t xes = c->wk != kWBf16 ? 1 : 2;
   for (int i = 0; i < cfg->n_streams; ++i) {
     Scratch &sc = c->sc[i];
     sc.blk_cnt = (int32_t *)A(sizeof(int32_t) * c->max_blocks * E);
@@ -423,7 +440,7 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
     sc.xg = A(xes * c->max_mpad * d);
     sc.h = A(xes * c->max_mpad * I);
     sc.y = (float *)A(sizeof(float) * c->max_mpad * d);
-    if (c->fp8) {
+    if (c->wk != kWBf16) {  // e4m3 float scales per 128, or E8M0 bytes per 32: same size
       sc.xs = (float *)A(sizeof(float) * c->max_mpad * (d / 128));
       sc.hs = (float *)A(sizeof(float) * c->max_mpad * (I / 128));
       sc.s_ld = c->max_mpad;

@@ -18,7 +18,8 @@ import torch
 from . import cep
 from . import workload as W
 
-_DT = {W.F32: cep.CEP_F32, W.BF16: cep.CEP_BF16, W.FP8: cep.CEP_FP8_E4M3_B128}
+_DT = {W.F32: cep.CEP_F32, W.BF16: cep.CEP_BF16, W.FP8: cep.CEP_FP8_E4M3_B128,
+       W.MXFP4: cep.CEP_MXFP4}
 
 
 class DeviceChunk:
@@ -34,7 +35,7 @@ class Runner:
         c = wl.cfg
         self.device = torch.device(device)
         self.use_fetch = use_fetch and bool(wl.fetched)
-        fp8 = c["w"] == W.FP8
+        scaled = c["w"] in (W.FP8, W.MXFP4)
         self.cfg = cep.make_config(
             d_model=c["d"], d_ff=c["I"], n_local_experts=c["E"], top_k=c["k"],
             max_replicas=c["R"], max_tokens_per_replica=c["T"], w_dtype=_DT[c["w"]],
@@ -49,7 +50,7 @@ class Runner:
         dev = self.device
         wg, wu, wd = (t.to(dev) for t in (wl.w_gate, wl.w_up, wl.w_down))
         sg = su = sd = None
-        if fp8:
+        if scaled:
             sg, su, sd = (t.to(dev) for t in (wl.s_gate, wl.s_up, wl.s_down))
         weights = cep.make_weights(wg, wu, wd, sg, su, sd)
         stream = torch.cuda.current_stream(dev)

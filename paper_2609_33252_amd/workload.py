@@ -25,7 +25,7 @@ from typing import Optional
 import numpy as np
 import torch
 
-F32, BF16, FP8 = "f32", "bf16", "fp8_e4m3_b128"
+F32, BF16, FP8, MXFP4 = "f32", "bf16", "fp8_e4m3_b128", "mxfp4"
 FP8_BLOCK = 128
 FP8_MAX = 448.0
 
@@ -47,6 +47,12 @@ PRESETS = {
                                   fetch_frac=0.0),
     "fp8_fetch_d6144": dict(d=6144, I=2560, E=16, Eg=160, k=8, R=8, T=8192, cpr=1, zipf=1.5,
                             w=FP8, x=BF16, arrival="simultaneous", skew=None, fetch_frac=0.25),
+    # DeepSeek-V4-Flash's routed experts at one EP8 rank's share (Table 1:
+    # 256 routed experts, 6 per token, intermediate 2048; MXFP4 weights,
+    # Section 4.1), balanced routing, eight chunks per replica
+    "mxfp4_dsv4flash_d4096": dict(d=4096, I=2048, E=32, Eg=256, k=6, R=8, T=8192, cpr=8,
+                                  zipf=None, w=MXFP4, x=BF16, arrival="lognormal", skew=None,
+                                  fetch_frac=0.0),
 }
 # The five numbered configurations in order.
 CONFIG_ORDER = ["tiny", "sync_d4096", "zipf_stream_d7168", "zipf_imbalanced_d7168",
@@ -74,13 +80,14 @@ class Workload:
     cfg: dict
     seed: int
     # expert weights in math orientation; bf16/f32 as torch CPU tensors,
-    # fp8 as uint8 codes (OCP e4m3fn) plus float32 128x128 block scales
-    w_gate: torch.Tensor      # [E][d][I]
-    w_up: torch.Tensor        # [E][d][I]
-    w_down: torch.Tensor      # [E][I][d]
-    s_gate: Optional[torch.Tensor]  # fp8: [E][d/128][I/128]
+    # fp8 as uint8 codes (OCP e4m3fn) plus float32 128x128 block scales;
+    # mxfp4 output-major with K packed: uint8 code pairs plus E8M0 scales
+    w_gate: torch.Tensor      # [E][d][I]; mxfp4 [E][I][d/2]
+    w_up: torch.Tensor        # [E][d][I]; mxfp4 [E][I][d/2]
+    w_down: torch.Tensor      # [E][I][d]; mxfp4 [E][d][I/2]
+    s_gate: Optional[torch.Tensor]  # fp8: [E][d/128][I/128]; mxfp4 [E][I][d/32]
     s_up: Optional[torch.Tensor]
-    s_down: Optional[torch.Tensor]  # fp8: [E][I/128][d/128]
+    s_down: Optional[torch.Tensor]  # fp8: [E][I/128][d/128]; mxfp4 [E][d][I/32]
     x: torch.Tensor           # [R][T][d] hidden rows (bf16 or f32)
     topk_global: np.ndarray   # int32 [R][T][k] global expert ids, slot order
     topk_local: np.ndarray    # int32 [R][T][k] local id or -1 (remote)
@@ -142,6 +149,34 @@ def _normal(ss: np.random.SeedSequence, n: int, scale: float) -> np.ndarray:
         with ThreadPoolExecutor(_threads()) as ex:
             list(ex.map(fill, range(nblk)))
     return out
+
+
+def _bytes(ss: np.random.SeedSequence, n: int, lo: int, hi: int) -> np.ndarray:
+    """n uint8 draws uniform in [lo, hi), block-seeded like _normal."""
+    out = np.empty(n, np.uint8)
+    nblk = (n + _ROW_BLOCK - 1) // _ROW_BLOCK
+    kids = ss.spawn(nblk)
+
+    def fill(b):
+        sl = out[b * _ROW_BLOCK:min(n, (b + 1) * _ROW_BLOCK)]
+        sl[:] = np.random.default_rng(kids[b]).integers(lo, hi, size=sl.shape[0], dtype=np.uint8)
+
+    if nblk == 1:
+        fill(0)
+    else:
+        with ThreadPoolExecutor(_threads()) as ex:
+            list(ex.map(fill, range(nblk)))
+    return out
+
+
+def _mxfp4_matrix(ss: np.random.SeedSequence, E: int, rows: int, K: int):
+    """MXFP4 weights drawn directly in the checkpoint format: uniform code
+    bytes (every e2m1 value equally likely) and E8M0 scales 2^-8 or 2^-7,
+    an element RMS of about 0.018.  rows x K, blocks of 32 along K."""
+    c_ss, s_ss = ss.spawn(2)
+    codes = _bytes(c_ss, E * rows * K // 2, 0, 256).reshape(E, rows, K // 2)
+    scales = _bytes(s_ss, E * rows * K // 32, 119, 121).reshape(E, rows, K // 32)
+    return torch.from_numpy(codes), torch.from_numpy(scales)
 
 
 def _to_dtype(a: np.ndarray, dt: str) -> torch.Tensor:
@@ -237,18 +272,24 @@ def generate(name: str = "tiny", seed: int = 0, **overrides) -> Workload:
     ss_w, ss_x, ss_r, ss_l, ss_a, ss_f = np.random.SeedSequence(seed).spawn(6)
 
     # weights: N(0, 0.02) float32 draws, then stored in the config dtype
+    # (MXFP4: drawn directly as codes and scales)
     wg_ss, wu_ss, wd_ss = ss_w.spawn(3)
-    wg = _normal(wg_ss, E * d * I, 0.02).reshape(E, d, I)
-    wu = _normal(wu_ss, E * d * I, 0.02).reshape(E, d, I)
-    wd = _normal(wd_ss, E * I * d, 0.02).reshape(E, I, d)
     s_gate = s_up = s_down = None
-    if cfg["w"] == FP8:
-        w_gate, s_gate = _fp8_blocks(wg)
-        w_up, s_up = _fp8_blocks(wu)
-        w_down, s_down = _fp8_blocks(wd)
+    if cfg["w"] == MXFP4:
+        w_gate, s_gate = _mxfp4_matrix(wg_ss, E, I, d)
+        w_up, s_up = _mxfp4_matrix(wu_ss, E, I, d)
+        w_down, s_down = _mxfp4_matrix(wd_ss, E, d, I)
     else:
-        w_gate, w_up, w_down = (_to_dtype(a, cfg["w"]) for a in (wg, wu, wd))
-    del wg, wu, wd
+        wg = _normal(wg_ss, E * d * I, 0.02).reshape(E, d, I)
+        wu = _normal(wu_ss, E * d * I, 0.02).reshape(E, d, I)
+        wd = _normal(wd_ss, E * I * d, 0.02).reshape(E, I, d)
+        if cfg["w"] == FP8:
+            w_gate, s_gate = _fp8_blocks(wg)
+            w_up, s_up = _fp8_blocks(wu)
+            w_down, s_down = _fp8_blocks(wd)
+        else:
+            w_gate, w_up, w_down = (_to_dtype(a, cfg["w"]) for a in (wg, wu, wd))
+        del wg, wu, wd
 
     x = _to_dtype(_normal(ss_x, R * T * d, 1.0), cfg["x"]).view(R, T, d)
 

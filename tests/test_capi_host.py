@@ -56,6 +56,12 @@ def test_packed_bytes_and_validation(L):
     fp8 = _cfg(w_dtype=cep.CEP_FP8_E4M3_B128)
     b = cep.cep_packed_expert_bytes(fp8)
     assert b >= 3 * 256 * 128 and b % 256 == 0
+    # MXFP4: half-byte codes plus one E8M0 byte per 32 along K, no padding
+    # at these sizes
+    mx = _cfg(w_dtype=cep.CEP_MXFP4)
+    assert cep.cep_packed_expert_bytes(mx) == 3 * 256 * 128 // 2 + 3 * 256 * 128 // 32
+    assert cep.cep_packed_expert_bytes(_cfg(w_dtype=cep.CEP_MXFP4, x_dtype=cep.CEP_F32)) == 0
+    assert cep.cep_packed_expert_bytes(_cfg(w_dtype=4)) == 0
     for bad in (dict(d_model=100), dict(d_ff=96), dict(n_local_experts=0),
                 dict(n_local_experts=65), dict(top_k=0), dict(top_k=17), dict(n_streams=9),
                 dict(x_dtype=cep.CEP_FP8_E4M3_B128), dict(max_replicas=0),

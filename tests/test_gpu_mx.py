@@ -1,0 +1,120 @@
+"""GPU parity of the MXFP4 expert path (through the C ABI) against the oracle.
+
+Weights are MXFP4, activations and h MXFP8 (the oracle mirrors both
+quantisations); outputs are held to the e4m3 relative-RMS bound.
+
+* reduced DeepSeek-V4-Flash-shaped workload over every row, both M tiles
+* full-size workload on sampled tokens, hottest and coldest experts included
+* 128-row and 256-row M tiles give the same bits; a fetched expert equals a
+  resident one; a zero-gate expert gives exact zeros
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_33252_amd import cep, harness, workload as W
+
+from . import _util as U
+
+pytestmark = pytest.mark.gpu
+
+NAME = "mxfp4_dsv4flash_d4096"
+# the oracle finishes this in seconds: 8 experts of 2048 x 1024, ~1.5k pairs
+SMALL = dict(d=2048, I=1024, E=8, Eg=64, R=4, T=512, cpr=4)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    cep.lib()
+    torch.cuda.set_device(0)
+
+
+def _out(run):
+    torch.cuda.synchronize()
+    cep.cep_get_status(run.ctx)
+    return run.out.cpu().numpy()
+
+
+def test_mxfp4_reduced_all_rows():
+    wl = W.generate(NAME, 0, **SMALL)
+    run = harness.Runner(wl, n_streams=2, record_routing=True)
+    run.run(policy=cep.CEP_THRESHOLD, theta=max(1, wl.n_pairs // 3), n_streams=2)
+    got = _out(run)
+    aligns = {cep.cep_get_batch_routing(run.ctx, b, wl.cfg["E"], wl.cfg["k"])["align"]
+              for b in range(cep.cep_get_batch_count(run.ctx))}
+    run.close()
+    ref = U.reference(wl)
+    mx, rel = U.compare(wl, got, ref)
+    assert not got[~wl.delivered].any()
+    print(f"mxfp4 reduced: pairs={wl.n_pairs} aligns={sorted(aligns)} max_abs={mx:.3e} "
+          f"rel_rms={rel:.3e}")
+
+
+def test_mxfp4_large_and_small_m_tiles_agree_bitwise():
+    # wait-all: >= 256 rows per expert (256-row tile); per chunk: 128-row tile
+    wl = W.generate(NAME, 1, d=1024, I=512, E=4, Eg=32, R=4, T=2048, cpr=8)
+    assert wl.n_pairs >= 256 * wl.cfg["E"]
+    run = harness.Runner(wl, n_streams=2, record_routing=True)
+    run.run(policy=cep.CEP_WAIT_ALL)
+    a = _out(run)
+    assert cep.cep_get_batch_routing(run.ctx, 0, wl.cfg["E"], wl.cfg["k"])["align"] == 256
+    run.out.zero_()
+    run.run(policy=cep.CEP_PER_CHUNK, n_streams=2)
+    b = _out(run)
+    assert cep.cep_get_batch_routing(run.ctx, 0, wl.cfg["E"], wl.cfg["k"])["align"] == 128
+    run.close()
+    assert np.array_equal(a, b)
+    U.compare(wl, a, U.reference(wl))
+
+
+def test_mxfp4_full_size_sampled_tokens():
+    wl = W.generate(NAME, 0)
+    run = harness.Runner(wl, n_streams=1)
+    run.run(policy=cep.CEP_WAIT_ALL)
+    got = _out(run)
+    run.close()
+    rng = np.random.default_rng(2)
+    deliv = np.argwhere(wl.delivered)
+    pick = deliv[rng.choice(len(deliv), size=16, replace=False)]
+    cnt = np.bincount(wl.topk_local[wl.topk_local >= 0], minlength=wl.cfg["E"])
+    for e in (int(cnt.argmax()), int(np.argmin(np.where(cnt > 0, cnt, 1 << 30)))):
+        rt = np.argwhere((wl.topk_local == e).any(axis=2))
+        pick = np.vstack([pick, rt[-2:]])
+    ref = U.reference(wl, tokens=pick)
+    mx, rel = U.compare(wl, got[pick[:, 0], pick[:, 1]], ref)
+    assert not got[~wl.delivered].any()
+    print(f"mxfp4 full: pairs={wl.n_pairs} sampled={len(pick)} max_abs={mx:.3e} rel={rel:.3e}")
+
+
+def test_mxfp4_fetched_experts_equal_resident_bitwise():
+    wl = W.generate(NAME, 3, **dict(SMALL, fetch_frac=0.25))
+    assert wl.fetched
+    a = harness.Runner(wl, n_streams=2, use_fetch=True)
+    a.run(policy=cep.CEP_THRESHOLD, theta=500, n_streams=2)
+    ga = _out(a)
+    assert all(b["helper"] for b in a.stats()["batches"])
+    a.close()
+    b = harness.Runner(wl, n_streams=1, use_fetch=False)
+    b.run(policy=cep.CEP_WAIT_ALL)
+    gb = _out(b)
+    b.close()
+    assert np.array_equal(ga, gb)
+
+
+def test_mxfp4_zero_gate_codes_give_exact_zero():
+    # all gate codes of expert 0 are +0: gate = 0, silu(0) * up = 0, h = 0,
+    # so every row routed only to expert 0 comes out exactly 0
+    wl = W.generate(NAME, 4, d=1024, I=512, E=4, Eg=8, R=2, T=256, cpr=2)
+    wg = wl.w_gate.clone()
+    wg[0] = 0
+    wl.w_gate = wg
+    only0 = np.where(wl.topk_local == 0, 0, -1).astype(np.int32)
+    wl.topk_local = only0
+    run = harness.Runner(wl, n_streams=1)
+    run.run(policy=cep.CEP_WAIT_ALL)
+    got = _out(run)
+    run.close()
+    assert wl.n_pairs > 0
+    assert not got.any()
