@@ -27,8 +27,11 @@ namespace {
 // Operands stream through a ring of STAGES LDS stages filled by direct
 // global->LDS loads issued STAGES-1 steps ahead ((BM + 256) x 128 codes + BM
 // row scales per stage).  An LDS row is 128 codes = eight 16-byte chunks;
-// chunk c of row r lives at slot c ^ ((r >> 1) & 7), so the operand reads
-// (sixteen rows at one chunk per LDS cycle) are conflict-free.
+// chunk c of row r lives at slot c ^ ((r >> 1) & 7).  A lane reads chunks
+// g and g + 4 of its row (g = lane / 16): a 16-byte LDS read serves per
+// cycle the sixteen lanes of one half-wave whose quad index (lane bits 2-4)
+// has one parity, and those lanes then touch sixteen distinct slots of 256
+// bytes (reading chunks 2g, 2g + 1 instead measured two-way bank conflicts).
 //
 // GEMM1 epilogue: h = silu(gate) * up over the tile's 128 h columns, one
 // amax per row (lanes, then the four column waves via LDS), scale =
@@ -102,7 +105,10 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_fp8(GemmArgs g) {
   __syncthreads();
 
   const int rsw = ((lane & 15) >> 1) & 7;  // swizzle of every operand row this lane reads
-  const int c0 = (lane >> 4) * 2;          // this lane's two chunks: K bytes [c0*16, c0*16+32)
+  // this lane's two chunks: K bytes [16g, 16g+16) and [64+16g, 64+16g+16),
+  // g = lane / 16, the instruction's own K order (A and B alike); reading the
+  // chunk pair (g, g + 4) keeps every 16-lane LDS cycle on distinct banks
+  const int c0 = lane >> 4, c1 = c0 + 4;
   // scale rows of this wave's column blocks: GEMM1 blocks j = 0,1 (gate) use
   // row 2*wn, j = 2,3 (up) row 2*wn + 1; GEMM2's 64 columns lie in row wn/2
   const float *sb_row0 = &sBs[(SWIGLU ? 2 * wn : wn / 2) * nkb];
@@ -126,14 +132,14 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_fp8(GemmArgs g) {
     for (int j = 0; j < 4; ++j) {
       const int row = wn * WN + j * 16 + (lane & 15);
       const u32x4 lo = sB[cur][row * 8 + (c0 ^ rsw)];
-      const u32x4 hi = sB[cur][row * 8 + ((c0 + 1) ^ rsw)];
+      const u32x4 hi = sB[cur][row * 8 + (c1 ^ rsw)];
       b[j] = __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int row = wm * 128 + i * 16 + (lane & 15);
       const u32x4 lo = sA[cur][row * 8 + (c0 ^ rsw)];
-      const u32x4 hi = sA[cur][row * 8 + ((c0 + 1) ^ rsw)];
+      const u32x4 hi = sA[cur][row * 8 + (c1 ^ rsw)];
       const i32x8 a =
           __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
       f32x4 p[4];

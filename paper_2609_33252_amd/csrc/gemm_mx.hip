@@ -46,13 +46,18 @@ __device__ inline f32x4 mx_mfma(const i32x8 &a, const i32x8 &b, const f32x4 &c, 
 //
 // LDS rows: A rows are 128 bytes (8 chunks), chunk c of row r at slot
 // c ^ ((r >> 1) & 7); B rows are 64 bytes (4 chunks), chunk c at slot
-// c ^ ((r >> 2) & 3).  Sixteen consecutive lanes then read sixteen distinct
-// 16-byte slots of every 256 bytes.
+// c ^ bsw(r), bsw(r) = (r & 1) | ((r >> 1) & 2).  A 16-byte LDS read serves
+// per cycle the sixteen lanes of one half-wave whose quad index (lane bits
+// 2-4) has one parity, on 64 four-byte banks (mapped lane pair by lane pair
+// with SQ_LDS_BANK_CONFLICT); with these swizzles each such group reads
+// sixteen distinct 16-byte slots of 256 bytes in both operand reads.
 //
 // GEMM1 epilogue: h = silu(gate) * up; each wave's 32 h columns of a row
 // are one MX block, so the block amax needs only a 16-lane reduction; the
 // E8M0 scale is 2^(floor(log2 amax) - 8), the codes e4m3(h / scale)
 // saturated at 448.
+__device__ inline int bsw_of(int r) { return (r & 1) | ((r >> 1) & 2); }
+
 template <int NW, int STAGES, bool SWIGLU>
 __global__ __launch_bounds__(64 * NW, 1) void k_gemm_mx(GemmArgs g) {
   constexpr int BM = 128 * NW / 4, BN = 256, BK = 128;
@@ -92,7 +97,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_mx(GemmArgs g) {
     }                                                                               \
     _Pragma("unroll") for (int i = 0; i < B_LD; ++i) {                              \
       const int seg = wid * B_LD + i, r = seg * 16 + b_row;                         \
-      dma16(Bg + (size_t)(kb) * (BK / 2) + (size_t)r * KB + (((lane & 3) ^ ((r >> 2) & 3)) * 16), \
+      dma16(Bg + (size_t)(kb) * (BK / 2) + (size_t)r * KB + (((lane & 3) ^ bsw_of(r)) * 16), \
             __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf_][seg * 64])));       \
     }                                                                               \
     if (wid == 0 && lane < BM / 4)                                                  \
@@ -115,7 +120,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_mx(GemmArgs g) {
 
   const int r16 = lane & 15, grp = lane >> 4;
   const int asw = (r16 >> 1) & 7;  // A swizzle of every row this lane reads
-  const int bsw = (r16 >> 2) & 3;  // B swizzle of every row this lane reads
+  const int bsw = bsw_of(r16);     // B swizzle of every row this lane reads
   for (int kb = 0; kb < nkb; ++kb) {
     const int later = min(nkb - 1, kb + STAGES - 2) - kb;
     if (wid < 2)
