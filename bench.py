@@ -27,7 +27,9 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "routed-expert FFN TFLOP/s (% MFMA peak) + time-to-last-chunk-done, 1 GPU"
-PEAK = {"bf16": 2500.0, "fp8": 5000.0}   # dense MFMA TFLOP/s, MI355X
+# dense MFMA TFLOP/s, MI355X.  MXFP4 weights meet MXFP8 activations in one
+# block-scaled MFMA, which issues at the fp8 rate when either operand is e4m3.
+PEAK = {"bf16": 2500.0, "fp8": 5000.0, "mxfp4": 5000.0}
 HBM_PEAK_GBS = 8000.0
 # Measured HBM traffic of the dominant kernel (GEMM1) per launch: rocprofv3
 # FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0 KiB (factors from a 1 GiB copy), keyed
@@ -71,11 +73,11 @@ def cpu_baseline(wl, budget_s=12.0):
     def bits(t):
         return None if t is None else (t.view(torch.int16).numpy().view(np.uint16)
                                        if t.dtype == torch.bfloat16 else t.numpy())
-    kind = {"f32": "f32", "bf16": "bf16", "fp8_e4m3_b128": "fp8"}[c["w"]]
+    kind = {"f32": "f32", "bf16": "bf16", "fp8_e4m3_b128": "fp8", "mxfp4": "mxfp4"}[c["w"]]
     bank = ffn.ExpertBank(kind, bits(wl.w_gate), bits(wl.w_up), bits(wl.w_down),
                           bits(wl.s_gate), bits(wl.s_up), bits(wl.s_down))
-    h_mode = {"f32": None, "bf16": "bf16", "fp8": "fp8"}[kind]
-    x_mode = "fp8" if kind == "fp8" else None
+    h_mode = {"f32": None, "bf16": "bf16", "fp8": "fp8", "mxfp4": "mxfp8"}[kind]
+    x_mode = {"fp8": "fp8", "mxfp4": "mxfp8"}.get(kind)
     deliv = np.argwhere(wl.delivered)
     rng = np.random.default_rng(0)
     deliv = deliv[rng.permutation(len(deliv))]
@@ -89,7 +91,7 @@ def cpu_baseline(wl, budget_s=12.0):
         w = wl.topk_w[sel[:, 0], sel[:, 1]]
         t0 = time.perf_counter()
         x = ffn.decode_rows(xb, "bf16" if c["x"] == "bf16" else "f32")
-        ffn.routed_output(x, ids, w, bank, c["E"], h_mode=h_mode, x_mode=x_mode)
+        ffn.routed_output(x, ids, w, bank, c["E"], h_mode=h_mode, x_mode=x_mode, y_mode="bf16")
         t_total += time.perf_counter() - t0
         done_pairs += int((ids >= 0).sum())
         n_tok += len(sel)
@@ -349,7 +351,7 @@ def main():
     run = harness.Runner(wl, n_streams=max(1, args.streams))
     pol = POLICIES[args.policy]
     flops_step = 6.0 * c["d"] * c["I"] * run.n_pairs
-    dtype = "fp8" if c["w"] == W.FP8 else "bf16"
+    dtype = {W.FP8: "fp8", W.MXFP4: "mxfp4"}.get(c["w"], "bf16")
 
     # the chunk inputs are generated once and resident in HBM: steady-state
     # layers carry no arrival events (the library orders each layer after the
@@ -389,7 +391,7 @@ def main():
     traffic = measured_traffic(args.workload)
     roofline = {"bound": "mfma",
                 "kernel": "k_gemm_%s<SwiGLU> (grouped gate/up GEMM; bf16 256-row tiles plus "
-                          "64-row remainder tiles when planned)" % dtype,
+                          "64-row remainder tiles when planned)" % {"mxfp4": "mx"}.get(dtype, dtype),
                 "achieved": round(achieved, 2), "peak": PEAK[dtype], "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK[dtype], 4), "traffic": traffic,
                 "launch_ms": round(g1_ms, 4), "flop_per_launch": g1_flops}

@@ -26,6 +26,9 @@ Readings where the paper is silent:
   first GEMM (the "activations with their quantization metadata" the layout
   transform packs), "mxfp8" to MXFP8 per 32 channels, else inputs are used
   exactly;
+* ``y_mode`` "bf16" rounds each weighted expert output w * y to bfloat16
+  before the slot-order sum (the dtype in which an expert-parallel combine
+  returns outputs to their source); None keeps it in float64;
 * the result is rounded once to float32 at the end.
 """
 from __future__ import annotations
@@ -122,7 +125,7 @@ def decode_rows(x, kind) -> np.ndarray:
 
 
 def routed_output(x64: np.ndarray, ids: np.ndarray, w: np.ndarray, bank, n_experts: int,
-                  h_mode=None, x_mode=None, group: int = 1024) -> np.ndarray:
+                  h_mode=None, x_mode=None, y_mode=None, group: int = 1024) -> np.ndarray:
     """y for token rows x64 [n][d] (float64) with local ids [n][k] (-1 =
     remote) and coefficients w [n][k]; returns float32 [n][d]."""
     x64 = np.asarray(x64, np.float64)
@@ -149,8 +152,12 @@ def routed_output(x64: np.ndarray, ids: np.ndarray, w: np.ndarray, bank, n_exper
             if rows.size == 0:
                 continue
             wg_, wu_, wd_ = bank(e)
-            y = expert_ffn(xg[rows], wg_, wu_, wd_, h_mode)
-            contrib[rows, slots] = wgt[rows, slots][:, None] * y
+            y = wgt[rows, slots][:, None] * expert_ffn(xg[rows], wg_, wu_, wd_, h_mode)
+            if y_mode == "bf16":
+                y = round_bf16(y)
+            elif y_mode is not None:
+                raise ValueError(y_mode)
+            contrib[rows, slots] = y
         acc = np.zeros((hi - lo, d), np.float64)
         for s in range(k):                         # ascending slot order
             m = idg[:, s] >= 0

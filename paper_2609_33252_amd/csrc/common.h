@@ -152,7 +152,7 @@ struct Scratch {
   void *h;             // [max_mpad][I] bf16 or e4m3
   float *hs;           // scales of h, laid out like xs (K = I)
   int s_ld;            // row stride of xs / hs (= max_mpad, a multiple of 256)
-  float *y;            // [max_mpad][d] f32, already scaled by the coefficient
+  __bf16 *y;           // [max_mpad][d] bf16, already scaled by the coefficient
 };
 
 // Device error word bits.

@@ -21,8 +21,8 @@
 namespace cep {
 namespace {
 
-// BM x BN output tile, 4 waves as WGM x (4/WGM), each wave owning a
-// (BM/WGM) x (BN/(4/WGM)) block of 32x32 MFMA fragments (for SwiGLU a
+// BM x BN output tile, NW waves as WGM x (NW/WGM), each wave owning a
+// (BM/WGM) x (BN/(NW/WGM)) block of 32x32 MFMA fragments (for SwiGLU a
 // wave's columns hold whole gate/up pairs of 32).  K advances in steps of BK through a ring of STAGES
 // LDS buffers filled by direct global->LDS loads (no staging registers), one
 // barrier per step.  An LDS row holds BK bf16 = CH 16-byte chunks; chunk c of
@@ -37,17 +37,21 @@ namespace {
 // the MFMAs; loads run STAGES-2 steps ahead.  Otherwise (weight-streaming
 // tile): fragments are read right before their MFMAs and loads run STAGES-1
 // steps ahead, which keeps more weight bytes in flight per LDS byte.
-template <int BM, int BN, int BK, int STAGES, int OCC, bool PIPE, bool SWIGLU, int WGM = 2>
-__global__ __launch_bounds__(256, OCC) void k_gemm_bf16(GemmArgs g) {
+template <int BM, int BN, int BK, int STAGES, int OCC, bool PIPE, bool SWIGLU, int WGM = 2,
+          int NW = 4>
+__global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
   static_assert(BK == 32 || BK == 64, "LDS swizzle covers 4 or 8 chunks per row");
   static_assert(STAGES >= 3 && STAGES <= 8, "wait counts below");
   constexpr int CH = BK / 8;                  // 16-byte chunks per LDS row
   constexpr int RPS = 1024 / (BK * 2);        // rows per 1 KB load segment
   constexpr int SH = CH == 4 ? 2 : 1;         // swz(r) = (r >> SH) & (CH - 1)
-  constexpr int WGN = 4 / WGM;  // waves along M x along N
+  constexpr int WGN = NW / WGM;  // waves along M x along N
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int FM = WM / 32, FN = WN / 32;
-  constexpr int A_LD = BM * BK * 2 / 1024 / 4, B_LD = BN * BK * 2 / 1024 / 4;  // per wave
+  constexpr int A_LD = BM * BK * 2 / 1024 / NW, B_LD = BN * BK * 2 / 1024 / NW;  // per wave
+  static_assert(A_LD * NW * 1024 == BM * BK * 2 && B_LD * NW * 1024 == BN * BK * 2,
+                "loads split evenly over the waves");
+  static_assert(!SWIGLU || (BN / WGN) % 64 == 0, "a wave's columns hold whole gate/up pairs");
   constexpr int PER = A_LD + B_LD;            // loads per thread per step
   int mt, nt;
   if (!balanced_tile<kGroupM>(*g.n_tiles, g.N / BN, &mt, &nt)) return;
@@ -198,10 +202,10 @@ __global__ __launch_bounds__(256, OCC) void k_gemm_bf16(GemmArgs g) {
           H[hbase + j2 * 32] = (__bf16)silu_mul(acc[i][2 * j2][r], acc[i][2 * j2 + 1][r]);
       } else {
         const float w = g.wrow[row];
-        float *Y = (float *)g.out;
+        __bf16 *Y = (__bf16 *)g.out;
         const size_t ybase = row * g.N + nt * BN + wn * WN + (lane & 31);
 #pragma unroll
-        for (int j = 0; j < FN; ++j) Y[ybase + j * 32] = acc[i][j][r] * w;
+        for (int j = 0; j < FN; ++j) Y[ybase + j * 32] = (__bf16)(acc[i][j][r] * w);
       }
     }
   }

@@ -29,7 +29,7 @@ struct GemmArgs {
   int K, N;               // contraction length, packed output columns
   size_t b_off, bs_off;   // offsets of B and its scales in each blob
   BlobTable bt;
-  void *out;              // H [mpad][N/2] (GEMM1) or Y [mpad][N] f32 (GEMM2)
+  void *out;              // H [mpad][N/2] (GEMM1) or Y [mpad][N] bf16 (GEMM2)
   float *out_s;           // quantised GEMM1: h scales (layout of As, K = N/2)
   const float *wrow;      // GEMM2: routing coefficient per grouped row
 };

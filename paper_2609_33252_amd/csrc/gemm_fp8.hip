@@ -197,7 +197,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_fp8(GemmArgs g) {
         if (wn == 0 && (lane & 15) == 0) g.out_s[(size_t)nt * g.s_ld + row] = scale;
       }
   } else {
-    float *Y = (float *)g.out;
+    __bf16 *Y = (__bf16 *)g.out;
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
@@ -208,7 +208,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_fp8(GemmArgs g) {
         const float w = g.wrow[row];
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          Y[row * g.N + nt * BN + wn * WN + j * 16 + (lane & 15)] = acc[i][j][r] * w;
+          Y[row * g.N + nt * BN + wn * WN + j * 16 + (lane & 15)] = (__bf16)(acc[i][j][r] * w);
       }
   }
 }

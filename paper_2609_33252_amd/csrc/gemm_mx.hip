@@ -187,7 +187,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_mx(GemmArgs g) {
         if (r16 == 0) Hs[mx_row_scale_offset((int)row, hblk, g.s_ld)] = (uint8_t)code;
       }
   } else {
-    float *Y = (float *)g.out;
+    __bf16 *Y = (__bf16 *)g.out;
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
@@ -197,7 +197,8 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_mx(GemmArgs g) {
         const size_t row = (size_t)t.row0 + rt;
         const float w = g.wrow[row];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) Y[row * g.N + nt * BN + wn * 64 + j * 16 + r16] = acc[i][j][r] * w;
+        for (int j = 0; j < 4; ++j)
+          Y[row * g.N + nt * BN + wn * 64 + j * 16 + r16] = (__bf16)(acc[i][j][r] * w);
       }
   }
 }

@@ -364,6 +364,68 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_scatter(Arena a, Scratc
 // rows (no pair) are skipped.
 constexpr int kPackRows = 8;
 
+constexpr int kQuantPass = 8;  // 512-channel groups loaded per pass of a quantised row
+
+__device__ inline void bf16x8_to_f32(const uint4 &u, float v[8]) {
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    v[2 * j] = __uint_as_float(w[j] << 16);
+    v[2 * j + 1] = __uint_as_float(w[j] & 0xffff0000u);
+  }
+}
+
+__device__ inline uint2 e4m3x8(const float q[8]) {
+  int lo = 0, hi = 0;
+  lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[0], q[1], lo, false);
+  lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], lo, true);
+  hi = __builtin_amdgcn_cvt_pk_fp8_f32(q[4], q[5], hi, false);
+  hi = __builtin_amdgcn_cvt_pk_fp8_f32(q[6], q[7], hi, true);
+  return make_uint2((uint32_t)lo, (uint32_t)hi);
+}
+
+// 16 lanes x 8 channels = one 128-channel block: scale = amax / 448 (1 for
+// an all-zero block), codes e4m3(x / scale); scales k-block major at
+// ds[b * s_ld].  Every lane takes part in the shuffles.
+__device__ inline void quant_e4m3_b128(const uint4 &in, bool ok, int lane, int c, uint8_t *dq,
+                                       float *ds, int s_ld) {
+  float v[8];
+  bf16x8_to_f32(in, v);
+  float amax = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(v[j]));
+#pragma unroll
+  for (int sh = 1; sh < 16; sh <<= 1) amax = fmaxf(amax, __shfl_xor(amax, sh, 16));
+  const float scale = amax > 0.f ? amax / 448.0f : 1.0f;
+  if (!ok) return;
+  float q[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) q[j] = v[j] / scale;
+  *(uint2 *)(dq + c) = e4m3x8(q);
+  if ((lane & 15) == 0) ds[(size_t)(c / 128) * s_ld] = scale;
+}
+
+// 4 lanes x 8 channels = one 32-channel MX block: E8M0 scale
+// 2^(floor(log2 amax) - 8), codes e4m3(x / scale) saturated at 448.
+__device__ inline void quant_mx8(const uint4 &in, bool ok, int lane, int c, uint8_t *dq,
+                                 uint8_t *ds, int pos, int s_ld) {
+  float v[8];
+  bf16x8_to_f32(in, v);
+  float amax = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(v[j]));
+  amax = fmaxf(amax, __shfl_xor(amax, 1, 4));
+  amax = fmaxf(amax, __shfl_xor(amax, 2, 4));
+  if (!ok) return;
+  const int code = max((int)((__float_as_uint(amax) >> 23) & 0xff) - 8, 0);
+  const int e = 127 - code;
+  float q[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) q[j] = fminf(fmaxf(ldexpf(v[j], e), -448.0f), 448.0f);
+  *(uint2 *)(dq + c) = e4m3x8(q);
+  if ((lane & 3) == 0) ds[mx_row_scale_offset(pos, c / kMxBlock, s_ld)] = (uint8_t)code;
+}
+
 // 0: bf16 -> bf16, 1: f32 -> bf16, 2: bf16 -> e4m3 + scales, 3: bf16 -> MXFP8
 template <int XMODE>
 __global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0, int k, int E,
@@ -391,73 +453,27 @@ __global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0
         o.h[4] = (__bf16)hi.x; o.h[5] = (__bf16)hi.y; o.h[6] = (__bf16)hi.z; o.h[7] = (__bf16)hi.w;
         d4[c] = o.u;
       }
-    } else if (XMODE == 3) {
-      // 4 lanes x 8 channels = one 32-channel MX block: E8M0 scale
-      // 2^(floor(log2 amax) - 8), codes e4m3(x / scale) saturated at 448
-      const uint4 *s4 = (const uint4 *)src;
-      uint8_t *dq = (uint8_t *)sc.xg + (size_t)pos * d;
-      uint8_t *ds = (uint8_t *)sc.xs;
-      for (int c0 = 0; c0 < d; c0 += 512) {
-        const int c = c0 + lane * 8;
-        const bool ok = c < d;
-        float v[8];
-        float amax = 0.f;
-        if (ok) {
-          union { uint4 u; __bf16 h[8]; } in;
-          in.u = s4[c / 8];
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            v[j] = (float)in.h[j];
-            amax = fmaxf(amax, fabsf(v[j]));
-          }
-        }
-        amax = fmaxf(amax, __shfl_xor(amax, 1, 4));
-        amax = fmaxf(amax, __shfl_xor(amax, 2, 4));
-        if (ok) {
-          const int code = max((int)((__float_as_uint(amax) >> 23) & 0xff) - 8, 0);
-          const int e = 127 - code;
-          float q[8];
-#pragma unroll
-          for (int j = 0; j < 8; ++j) q[j] = fminf(fmaxf(ldexpf(v[j], e), -448.0f), 448.0f);
-          int lo = 0, hi = 0;
-          lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[0], q[1], lo, false);
-          lo = __builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], lo, true);
-          hi = __builtin_amdgcn_cvt_pk_fp8_f32(q[4], q[5], hi, false);
-          hi = __builtin_amdgcn_cvt_pk_fp8_f32(q[6], q[7], hi, true);
-          *(uint2 *)(dq + c) = make_uint2((uint32_t)lo, (uint32_t)hi);
-          if ((lane & 3) == 0) ds[mx_row_scale_offset(pos, c / kMxBlock, sc.s_ld)] = (uint8_t)code;
-        }
-      }
     } else {
-      // 16 lanes x 8 channels = one 128-channel scale block
+      // quantised rows: a pass first loads up to kQuantPass 512-channel
+      // groups (eight channels per lane), then quantises them, so that many
+      // loads are in flight per wave
       const uint4 *s4 = (const uint4 *)src;
       uint8_t *dq = (uint8_t *)sc.xg + (size_t)pos * d;
-      float *ds = sc.xs + pos;  // k-block major: block b at ds[b * s_ld]
-      for (int c0 = 0; c0 < d; c0 += 512) {
-        const int c = c0 + lane * 8;
-        const bool ok = c < d;
-        float v[8];
-        float amax = 0.f;
-        if (ok) {
-          union { uint4 u; __bf16 h[8]; } in;
-          in.u = s4[c / 8];
+      for (int p0 = 0; p0 < d; p0 += 512 * kQuantPass) {
+        uint4 in[kQuantPass];
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            v[j] = (float)in.h[j];
-            amax = fmaxf(amax, fabsf(v[j]));
-          }
+        for (int u = 0; u < kQuantPass; ++u) {
+          const int c = p0 + u * 512 + lane * 8;
+          in[u] = c < d ? s4[c / 8] : make_uint4(0u, 0u, 0u, 0u);
         }
 #pragma unroll
-        for (int sh = 1; sh < 16; sh <<= 1) amax = fmaxf(amax, __shfl_xor(amax, sh, 16));
-        const float scale = amax > 0.f ? amax / 448.0f : 1.0f;
-        if (ok) {
-          int lo = 0, hi = 0;
-          lo = __builtin_amdgcn_cvt_pk_fp8_f32(v[0] / scale, v[1] / scale, lo, false);
-          lo = __builtin_amdgcn_cvt_pk_fp8_f32(v[2] / scale, v[3] / scale, lo, true);
-          hi = __builtin_amdgcn_cvt_pk_fp8_f32(v[4] / scale, v[5] / scale, hi, false);
-          hi = __builtin_amdgcn_cvt_pk_fp8_f32(v[6] / scale, v[7] / scale, hi, true);
-          *(uint2 *)(dq + c) = make_uint2((uint32_t)lo, (uint32_t)hi);
-          if ((lane & 15) == 0) ds[(size_t)(c / 128) * sc.s_ld] = scale;
+        for (int u = 0; u < kQuantPass; ++u) {
+          if (p0 + u * 512 >= d) break;  // uniform over the wave
+          const int c = p0 + u * 512 + lane * 8;
+          if (XMODE == 3)
+            quant_mx8(in[u], c < d, lane, c, dq, (uint8_t *)sc.xs, pos, sc.s_ld);
+          else
+            quant_e4m3_b128(in[u], c < d, lane, c, dq, sc.xs + pos, sc.s_ld);
         }
       }
     }
@@ -466,7 +482,8 @@ __global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0
 
 // --------------------------------------------------------------- combine
 // One block per batch row: out[dst] = sum over its valid slots, in slot
-// order, of the grouped output rows (already scaled by their coefficient).
+// order, of the grouped output rows (bf16, already scaled by their
+// coefficient), accumulated in float32.
 // The row's valid slot positions are gathered once into LDS; each thread
 // then issues the loads of all its columns before summing, slot by slot.
 constexpr int kCombineCols = 4;  // float4 columns per thread per pass
@@ -490,22 +507,25 @@ __global__ __launch_bounds__(256) void k_combine(Arena a, Scratch sc, int row0, 
   __syncthreads();
   const int n = s_n, d4 = d / 4;
   float4 *o = (float4 *)(out + (size_t)dst * d);
-  const float4 *y = (const float4 *)sc.y;
+  const uint2 *y = (const uint2 *)sc.y;  // four bf16 per column group
   for (int c0 = threadIdx.x; c0 < d4; c0 += blockDim.x * kCombineCols) {
     float4 acc[kCombineCols];
 #pragma unroll
     for (int u = 0; u < kCombineCols; ++u) acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int j = 0; j < n; ++j) {
-      const float4 *yr = y + (size_t)s_pos[j] * d4;
-      float4 v[kCombineCols];
+      const uint2 *yr = y + (size_t)s_pos[j] * d4;
+      uint2 v[kCombineCols];
 #pragma unroll
       for (int u = 0; u < kCombineCols; ++u) {
         const int c = c0 + u * blockDim.x;
-        v[u] = c < d4 ? yr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+        v[u] = c < d4 ? yr[c] : make_uint2(0u, 0u);
       }
 #pragma unroll
-      for (int u = 0; u < kCombineCols; ++u) {
-        acc[u].x += v[u].x; acc[u].y += v[u].y; acc[u].z += v[u].z; acc[u].w += v[u].w;
+      for (int u = 0; u < kCombineCols; ++u) {  // bf16 -> f32: the upper half of the word
+        acc[u].x += __uint_as_float(v[u].x << 16);
+        acc[u].y += __uint_as_float(v[u].x & 0xffff0000u);
+        acc[u].z += __uint_as_float(v[u].y << 16);
+        acc[u].w += __uint_as_float(v[u].y & 0xffff0000u);
       }
     }
 #pragma unroll

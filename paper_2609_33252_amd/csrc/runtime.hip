@@ -439,7 +439,7 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
     sc.wrow = (float *)A(sizeof(float) * c->max_mpad);
     sc.xg = A(xes * c->max_mpad * d);
     sc.h = A(xes * c->max_mpad * I);
-    sc.y = (float *)A(sizeof(float) * c->max_mpad * d);
+    sc.y = (__bf16 *)A(sizeof(__bf16) * c->max_mpad * d);
     if (c->wk != kWBf16) {  // e4m3 float scales per 128, or E8M0 bytes per 32: same size
       sc.xs = (float *)A(sizeof(float) * c->max_mpad * (d / 128));
       sc.hs = (float *)A(sizeof(float) * c->max_mpad * (I / 128));

@@ -51,14 +51,15 @@ def reference(wl, tokens=None, bank_=None):
         x = ffn.decode_rows(np_bits(wl.x).reshape(c["R"] * c["T"], c["d"]), xk)
         ids = wl.topk_local.reshape(-1, c["k"])
         w = wl.topk_w.reshape(-1, c["k"])
-        out = ffn.routed_output(x, ids, w, bank_, c["E"], h_mode=h_mode, x_mode=x_mode)
+        out = ffn.routed_output(x, ids, w, bank_, c["E"], h_mode=h_mode, x_mode=x_mode,
+                                y_mode="bf16")
         return out.reshape(c["R"], c["T"], c["d"])
     tokens = np.asarray(tokens)
     r, t = tokens[:, 0], tokens[:, 1]
     xb = np_bits(wl.x)[r, t]
     x = ffn.decode_rows(xb, xk)
     return ffn.routed_output(x, wl.topk_local[r, t], wl.topk_w[r, t], bank_, c["E"],
-                             h_mode=h_mode, x_mode=x_mode)
+                             h_mode=h_mode, x_mode=x_mode, y_mode="bf16")
 
 
 def compare(wl, got, ref):

@@ -180,3 +180,33 @@ def test_workload_banks_decode_stored_dtypes():
     np.testing.assert_array_equal(bank2(1)[0], ref)
     bits = wl2.x.view(torch.int16).numpy().view(np.uint16)
     np.testing.assert_array_equal(ffn.bf16_bits_to_f64(bits), wl2.x.double().numpy())
+
+
+def test_bf16_y_mode_rounds_each_weighted_contribution():
+    # each w * y rounded to bf16 (torch's cast, per scalar) and summed in slot
+    # order: the oracle's y_mode against the brute-force token loop
+    x, wg, wu, wd, ids, w = _tiny(21)
+    got = ffn.routed_output(x, ids, w, _bank64(wg, wu, wd), 3, y_mode="bf16")
+
+    def rb(v):
+        return float(torch.tensor(v, dtype=torch.float64).to(torch.bfloat16).double())
+
+    for t in range(x.shape[0]):
+        ref = np.zeros(x.shape[1])
+        for s, e in enumerate(ids[t]):
+            if e < 0:
+                continue
+            y = ffn.brute_force_token(x[t], [e], [1.0], wg, wu, wd)
+            ref += np.array([rb(float(w[t, s]) * v) for v in y])
+        np.testing.assert_allclose(got[t], np.float32(ref), rtol=1e-6, atol=1e-9)
+    # and it differs from the unrounded result by at most 2^-8 (the unit
+    # roundoff of 8 significant bits) per contribution
+    exact = ffn.routed_output(x, ids, w, _bank64(wg, wu, wd), 3)
+    bound = np.zeros_like(exact, dtype=np.float64)
+    for t in range(x.shape[0]):
+        for s, e in enumerate(ids[t]):
+            if e >= 0:
+                y = np.array(ffn.brute_force_token(x[t], [e], [w[t, s]], wg, wu, wd))
+                bound[t] += 2.0 ** -8 * np.abs(y)
+    assert (np.abs(got.astype(np.float64) - exact) <= bound + 1e-6).all()
+    assert not np.array_equal(got, exact)
