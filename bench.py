@@ -31,24 +31,32 @@ METRIC = "routed-expert FFN TFLOP/s (% MFMA peak) + time-to-last-chunk-done, 1 G
 # block-scaled MFMA, which issues at the fp8 rate when either operand is e4m3.
 PEAK = {"bf16": 2500.0, "fp8": 5000.0, "mxfp4": 5000.0}
 HBM_PEAK_GBS = 8000.0
-# Measured HBM traffic of the dominant kernel (GEMM1) per launch: rocprofv3
+# Measured HBM traffic of the dominant kernel (GEMM1) per layer: rocprofv3
 # FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0 KiB (factors from a 1 GiB copy), keyed
-# by workload, valid only for the GEMM sources with this sha1 prefix (the
-# report is null once the kernel changes).
-GEMM_SOURCES = ["paper_2609_33252_amd/csrc/gemm_bf16.hip", "paper_2609_33252_amd/csrc/gemm_common.h"]
-TRAFFIC_BYTES = {"sync_d4096": ("dc863139dc6c", 646127094)}
+# by workload, valid only while the GEMM sources hash to the recorded sha1
+# prefix (the report is null once the kernel changes).
+GEMM_SOURCES = {
+    "bf16": ["paper_2609_33252_amd/csrc/gemm_bf16.hip", "paper_2609_33252_amd/csrc/gemm_common.h"],
+    "mxfp4": ["paper_2609_33252_amd/csrc/gemm_mx.hip", "paper_2609_33252_amd/csrc/gemm_common.h"],
+}
+TRAFFIC_BYTES = {}  # workload -> (dtype, sha1 prefix, bytes)
+
+
+def gemm_source_hash(dtype):
+    import hashlib
+    m = hashlib.sha1()
+    for p in GEMM_SOURCES[dtype]:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            m.update(f.read())
+    return m.hexdigest()[:12]
 
 
 def measured_traffic(workload):
-    import hashlib
     entry = TRAFFIC_BYTES.get(workload)
     if entry is None:
         return None
-    m = hashlib.sha1()
-    for p in GEMM_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            m.update(f.read())
-    return entry[1] if m.hexdigest()[:12] == entry[0] else None
+    dtype, sha, nbytes = entry
+    return nbytes if gemm_source_hash(dtype) == sha else None
 
 POLICIES = {"wait_all": 0, "per_chunk": 1, "threshold": 2}
 

@@ -38,7 +38,7 @@ namespace {
 // tile): fragments are read right before their MFMAs and loads run STAGES-1
 // steps ahead, which keeps more weight bytes in flight per LDS byte.
 template <int BM, int BN, int BK, int STAGES, int OCC, bool PIPE, bool SWIGLU, int WGM = 2,
-          int NW = 4>
+          int NW = 4, int GM = kGroupM>
 __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
   static_assert(BK == 32 || BK == 64, "LDS swizzle covers 4 or 8 chunks per row");
   static_assert(STAGES >= 3 && STAGES <= 8, "wait counts below");
@@ -54,7 +54,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
   static_assert(!SWIGLU || (BN / WGN) % 64 == 0, "a wave's columns hold whole gate/up pairs");
   constexpr int PER = A_LD + B_LD;            // loads per thread per step
   int mt, nt;
-  if (!balanced_tile<kGroupM>(*g.n_tiles, g.N / BN, &mt, &nt)) return;
+  if (!balanced_tile<GM>(*g.n_tiles, g.N / BN, &mt, &nt)) return;
   const Tile t = g.tiles[mt];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);

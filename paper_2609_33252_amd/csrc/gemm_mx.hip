@@ -58,6 +58,7 @@ __device__ inline f32x4 mx_mfma(const i32x8 &a, const i32x8 &b, const f32x4 &c, 
 // saturated at 448.
 __device__ inline int bsw_of(int r) { return (r & 1) | ((r >> 1) & 2); }
 
+
 template <int NW, int STAGES, bool SWIGLU>
 __global__ __launch_bounds__(64 * NW, 1) void k_gemm_mx(GemmArgs g) {
   constexpr int BM = 128 * NW / 4, BN = 256, BK = 128;
@@ -212,7 +213,7 @@ hipError_t launch_mx(const GemmArgs &g, int grid_tiles, int align, hipStream_t s
   if (align == kFp8TileM)
     hipLaunchKernelGGL((k_gemm_mx<4, 4, SWIGLU>), dim3(grid), dim3(256), 0, s, g);
   else if (align == kFp8LargeTileM)
-    hipLaunchKernelGGL((k_gemm_mx<8, 3, SWIGLU>), dim3(grid), dim3(512), 0, s, g);
+    hipLaunchKernelGGL((k_gemm_mx<8, 2, SWIGLU>), dim3(grid), dim3(512), 0, s, g);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
