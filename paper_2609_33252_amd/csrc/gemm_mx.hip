@@ -142,18 +142,26 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_mx(GemmArgs g) {
       const u32x4 v = sB[cur][row * 4 + (grp ^ bsw)];
       b[j] = __builtin_bit_cast(i32x8, __builtin_shufflevector(v, v, 0, 1, 2, 3, -1, -1, -1, -1));
     }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    // A fragments one row group ahead: the reads of group i+1 are issued
+    // before the MFMAs of group i, so LDS latency hides behind them
+    auto read_a = [&](int i) {
       const int row = wm * 128 + i * 16 + r16;
       const u32x4 lo = sA[cur][row * 8 + (grp ^ asw)];
       const u32x4 hi = sA[cur][row * 8 + ((grp + 4) ^ asw)];
-      const i32x8 a =
-          __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      return __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    };
+    i32x8 a_next = read_a(0);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const i32x8 a = a_next;
+      if (i + 1 < 8) a_next = read_a(i + 1);
+      __builtin_amdgcn_sched_barrier(0);
       const int sai = (int)(i < 4 ? sa.x : sa.y);
       acc[i][0] = mx_mfma<0>(a, b[0], acc[i][0], i & 3, sai, (int)sb);
       acc[i][1] = mx_mfma<1>(a, b[1], acc[i][1], i & 3, sai, (int)sb);
       acc[i][2] = mx_mfma<2>(a, b[2], acc[i][2], i & 3, sai, (int)sb);
       acc[i][3] = mx_mfma<3>(a, b[3], acc[i][3], i & 3, sai, (int)sb);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 #undef CEP_MX_STAGE
