@@ -203,9 +203,13 @@ hipError_t launch_combine(const Arena &a, const Scratch &sc, int row0, int n_row
 // scratch whose lists hold list_cap tiles each; the grid covers grid_tiles
 // M tiles with M tile `align` (the batch's row alignment), then, if
 // split_tiles > 0, up to split_tiles 64-row remainder tiles
+// gather (bf16 weights and rows only): GEMM1 reads the batch's input rows
+// (arena rows from row0) in place through the permutation instead of a
+// packed copy
 hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles,
                         int split_tiles, int align, const BlobTable &bt, const BlobLayout &L,
-                        int wk, int d, int I, hipStream_t s);
+                        int wk, int d, int I, const Arena *gather, int row0, int k,
+                        hipStream_t s);
 hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles,
                         int split_tiles, int align, const BlobTable &bt, const BlobLayout &L,
                         int wk, int d, int I, hipStream_t s);

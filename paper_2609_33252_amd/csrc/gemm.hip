@@ -38,10 +38,18 @@ hipError_t launch_any(const GemmArgs &g, int grid_tiles, int split_tiles, int al
 
 hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles,
                         int split_tiles, int align, const BlobTable &bt, const BlobLayout &L,
-                        int wk, int d, int I, hipStream_t s) {
+                        int wk, int d, int I, const Arena *gather, int row0, int k,
+                        hipStream_t s) {
   if (grid_tiles <= 0) return hipSuccess;
   GemmArgs g = base_args(sc, 2 * which, list_cap, grid_tiles, bt);
   g.A = (const uint8_t *)sc.xg;
+  if (gather) {  // bf16 rows read in place through the permutation
+    g.A = nullptr;
+    g.xrow = gather->xrow;
+    g.perm = sc.perm;
+    g.arow0 = row0;
+    g.k = k;
+  }
   g.As = sc.xs;
   g.K = d;
   g.N = 2 * I;

@@ -38,7 +38,7 @@ namespace {
 // tile): fragments are read right before their MFMAs and loads run STAGES-1
 // steps ahead, which keeps more weight bytes in flight per LDS byte.
 template <int BM, int BN, int BK, int STAGES, int OCC, bool PIPE, bool SWIGLU, int WGM = 2,
-          int NW = 4, int GM = kGroupM>
+          int NW = 4, int GM = kGroupM, bool GATHER = false>
 __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
   static_assert(BK == 32 || BK == 64, "LDS swizzle covers 4 or 8 chunks per row");
   static_assert(STAGES >= 3 && STAGES <= 8, "wait counts below");
@@ -60,7 +60,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wid / WGN, wn = wid % WGN;
   const int K = g.K, nk = K / BK;
-  const char *Ag = (const char *)(g.A + (size_t)t.row0 * K * 2);
+  const char *Ag = GATHER ? nullptr : (const char *)(g.A + (size_t)t.row0 * K * 2);
   const char *Bg = (const char *)(blob_of(g.bt, t.expert) + g.b_off + (size_t)nt * BN * K * 2);
 
   __shared__ u32x4 sA[STAGES][BM * CH];
@@ -74,12 +74,25 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
 #define CEP_LANE_OFF(seg)                                                           \
   ((uint32_t)((seg) * RPS + seg_row) * K * 2 +                                      \
    (uint32_t)(((lane % CH) ^ ((((seg) * RPS + seg_row) >> SH) & (CH - 1))) * 16))
+  // GATHER: each lane's A rows are fixed for the whole K loop, so their
+  // input-row addresses (plus the lane's chunk) are looked up once
+  const char *arow[A_LD];
+  if constexpr (GATHER) {
+#pragma unroll
+    for (int i = 0; i < A_LD; ++i) {
+      const int r = (wid * A_LD + i) * RPS + seg_row;
+      const int p = g.perm[t.row0 + r];
+      arow[i] = (const char *)g.xrow[g.arow0 + (p >= 0 ? p / g.k : 0)] +
+                ((lane % CH) ^ ((r >> SH) & (CH - 1))) * 16;
+    }
+  }
 #define CEP_DMA_STAGE(kt)                                                           \
   {                                                                                 \
     const int buf_ = (kt) % STAGES;                                                 \
     _Pragma("unroll") for (int i = 0; i < A_LD; ++i) {                              \
       const int seg = wid * A_LD + i;                                               \
-      dma16(Ag + (size_t)(kt) * BK * 2 + CEP_LANE_OFF(seg),                         \
+      dma16(GATHER ? arow[i] + (size_t)(kt) * BK * 2                                \
+                   : Ag + (size_t)(kt) * BK * 2 + CEP_LANE_OFF(seg),                \
             __builtin_amdgcn_readfirstlane(lds_offset(&sA[buf_][seg * 64])));       \
     }                                                                               \
     _Pragma("unroll") for (int i = 0; i < B_LD; ++i) {                              \
@@ -213,24 +226,36 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
 
 }  // namespace
 
-template <bool SWIGLU>
-hipError_t launch_bf16(const GemmArgs &g, int grid_tiles, int align, hipStream_t s) {
+template <bool SWIGLU, bool GATHER>
+hipError_t launch_bf16_as(const GemmArgs &g, int grid_tiles, int align, hipStream_t s) {
   if (align == kBf16TileM) {
     constexpr int BN = 256;
     if (g.N % BN) return hipErrorInvalidValue;
     const int grid = balanced_grid(grid_tiles, kGroupM, g.N / BN);
-    hipLaunchKernelGGL((k_gemm_bf16<kBf16TileM, BN, 32, 4, 1, true, SWIGLU>), dim3(grid), dim3(256), 0,
-                       s, g);
+    hipLaunchKernelGGL((k_gemm_bf16<kBf16TileM, BN, 32, 4, 1, true, SWIGLU, 2, 4, kGroupM, GATHER>),
+                       dim3(grid), dim3(256), 0, s, g);
   } else if (align == kBf16SmallTileM) {
     constexpr int BN = 128;
     if (g.N % BN || g.K % 64) return hipErrorInvalidValue;
     const int grid = balanced_grid(grid_tiles, kGroupM, g.N / BN);
-    hipLaunchKernelGGL((k_gemm_bf16<kBf16SmallTileM, BN, 64, 3, 2, false, SWIGLU>), dim3(grid),
-                       dim3(256), 0, s, g);
+    hipLaunchKernelGGL(
+        (k_gemm_bf16<kBf16SmallTileM, BN, 64, 3, 2, false, SWIGLU, 2, 4, kGroupM, GATHER>),
+        dim3(grid), dim3(256), 0, s, g);
   } else {
     return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+template <bool SWIGLU>
+hipError_t launch_bf16(const GemmArgs &g, int grid_tiles, int align, hipStream_t s) {
+  if constexpr (SWIGLU) {
+    if (g.A == nullptr) {
+      if (!g.xrow || !g.perm || g.k < 1) return hipErrorInvalidValue;
+      return launch_bf16_as<true, true>(g, grid_tiles, align, s);
+    }
+  }
+  return launch_bf16_as<SWIGLU, false>(g, grid_tiles, align, s);
 }
 
 template hipError_t launch_bf16<true>(const GemmArgs &, int, int, hipStream_t);

@@ -32,6 +32,11 @@ struct GemmArgs {
   void *out;              // H [mpad][N/2] (GEMM1) or Y [mpad][N] bf16 (GEMM2)
   float *out_s;           // quantised GEMM1: h scales (layout of As, K = N/2)
   const float *wrow;      // GEMM2: routing coefficient per grouped row
+  // bf16 GEMM1 with A == nullptr: grouped row r is the batch's input row
+  // xrow[arow0 + perm[r] / k] (padding rows, perm -1, read row arow0)
+  const void *const *xrow;
+  const int32_t *perm;
+  int arow0, k;
 };
 
 __device__ inline float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }

@@ -289,7 +289,10 @@ __global__ __launch_bounds__(64 * kFusedWaves) void k_route_fused(Arena a, Scrat
     if (pos >= pa.max_mpad) pos = -1;
     if (p < p1) {
       sc.pos_of[p] = pos;
-      if (pos >= 0) sc.perm[pos] = p;
+      if (pos >= 0) {
+        sc.perm[pos] = p;
+        sc.wrow[pos] = a.w[(size_t)row0 * k + p];  // the row's routing coefficient
+      }
     }
   }
 }
@@ -299,7 +302,8 @@ __global__ __launch_bounds__(64 * kFusedWaves) void k_route_fused(Arena a, Scrat
 // block's first row for its expert, plus pairs of that expert in earlier
 // rounds of this block, in earlier waves of this round, and in lower lanes
 // of this wave (stable in canonical order).  Writes the inverse map (grouped
-// row of each pair) and the permutation (pair of each grouped row).
+// row of each pair), the permutation (pair of each grouped row) and each
+// grouped row's routing coefficient.
 __global__ __launch_bounds__(kRouteThreads) void k_route_scatter(Arena a, Scratch sc, int row0,
                                                                  int n_flat, int k, int E,
                                                                  int max_mpad) {
@@ -352,16 +356,19 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_scatter(Arena a, Scratc
     }
     __syncthreads();  // wave_cnt cleared before the next round writes it
     if (p < n_flat) sc.pos_of[p] = pos;
-    if (pos >= 0) sc.perm[pos] = p;
+    if (pos >= 0) {
+      sc.perm[pos] = p;
+      sc.wrow[pos] = a.w[(size_t)row0 * k + p];  // the row's routing coefficient
+    }
   }
 }
 
 // ----------------------------------------------------------------- pack
 // One wave per grouped row (kPackRows rows per block): the pair's input row
-// is copied (bf16), converted (f32 -> bf16) or quantised (e4m3, one scale per
-// 128 channels; or MXFP8, one E8M0 scale per 32 channels) into its grouped
-// row, and its routing coefficient goes to the row's slot of wrow.  Padding
-// rows (no pair) are skipped.
+// is converted (f32 -> bf16) or quantised (e4m3, one scale per 128 channels;
+// or MXFP8, one E8M0 scale per 32 channels) into its grouped row.  Padding
+// rows (no pair) are skipped.  bf16 rows are not packed: the bf16 GEMM1
+// gathers them through the permutation.
 constexpr int kPackRows = 8;
 
 constexpr int kQuantPass = 8;  // 512-channel groups loaded per pass of a quantised row
@@ -426,7 +433,7 @@ __device__ inline void quant_mx8(const uint4 &in, bool ok, int lane, int c, uint
   if ((lane & 3) == 0) ds[mx_row_scale_offset(pos, c / kMxBlock, s_ld)] = (uint8_t)code;
 }
 
-// 0: bf16 -> bf16, 1: f32 -> bf16, 2: bf16 -> e4m3 + scales, 3: bf16 -> MXFP8
+// 1: f32 -> bf16, 2: bf16 -> e4m3 + scales, 3: bf16 -> MXFP8
 template <int XMODE>
 __global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0, int k, int E,
                                                    int d, int n_rows_pad) {
@@ -437,13 +444,8 @@ __global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0
     if (pos >= end) return;
     const int p = sc.perm[pos];
     if (p < 0) continue;
-    if (lane == 0) sc.wrow[pos] = a.w[(size_t)row0 * k + p];  // the row's routing coefficient
     const char *src = (const char *)a.xrow[row0 + p / k];
-    if (XMODE == 0) {
-      const uint4 *s4 = (const uint4 *)src;
-      uint4 *d4 = (uint4 *)((char *)sc.xg + (size_t)pos * d * 2);
-      for (int c = lane; c < d / 8; c += 64) d4[c] = s4[c];
-    } else if (XMODE == 1) {
+    if (XMODE == 1) {
       const float4 *s4 = (const float4 *)src;
       uint4 *d4 = (uint4 *)((char *)sc.xg + (size_t)pos * d * 2);
       for (int c = lane; c < d / 8; c += 64) {
@@ -714,8 +716,7 @@ hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows,
     hipLaunchKernelGGL(k_pack_rows<2>, pgrid, dim3(256), 0, s, a, sc, row0, k, E, d, n_pad);
   else if (x_dtype == 0)
     hipLaunchKernelGGL(k_pack_rows<1>, pgrid, dim3(256), 0, s, a, sc, row0, k, E, d, n_pad);
-  else
-    hipLaunchKernelGGL(k_pack_rows<0>, pgrid, dim3(256), 0, s, a, sc, row0, k, E, d, n_pad);
+  // bf16 rows with bf16 weights: GEMM1 reads them in place
   return hipGetLastError();
 }
 

@@ -279,6 +279,8 @@ int launch_pending(cep_ctx *c) {
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[0], s));
 
   BlobTable bt{c->w_res, c->fetch_buf, c->L.bytes, c->fetched_mask};
+  // bf16 rows with bf16 weights are not packed: GEMM1 reads them in place
+  const Arena *gather = c->wk == kWBf16 && cfg.x_dtype == CEP_BF16 ? &c->arena : nullptr;
 
   b.helper = c->fetched_mask != 0;
   if (b.helper) {
@@ -287,11 +289,13 @@ int launch_pending(cep_ctx *c) {
     HIPCHK(c, hipEventRecord(c->ev_routed[slot], s));
     HIPCHK(c, hipStreamWaitEvent(h, c->ev_routed[slot], 0));
     HIPCHK(c, hipStreamWaitEvent(h, c->ev_fetch_ready, 0));
-    HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->wk, d, I, h));
+    HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->wk, d, I,
+                           gather, b.row0, k, h));
     HIPCHK(c, launch_gemm2(sc, 1, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->wk, d, I, h));
     HIPCHK(c, hipEventRecord(c->ev_helper[slot], h));
   }
-  HIPCHK(c, launch_gemm1(sc, 0, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->wk, d, I, s));
+  HIPCHK(c, launch_gemm1(sc, 0, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->wk, d, I,
+                         gather, b.row0, k, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[1], s));
   HIPCHK(c, launch_gemm2(sc, 0, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->wk, d, I, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[2], s));
@@ -437,7 +441,8 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
     sc.pos_of = (int32_t *)A(sizeof(int32_t) * (size_t)c->max_rows * k);
     sc.perm = (int32_t *)A(sizeof(int32_t) * c->max_mpad);
     sc.wrow = (float *)A(sizeof(float) * c->max_mpad);
-    sc.xg = A(xes * c->max_mpad * d);
+    // bf16 rows with bf16 weights are read in place by GEMM1 (no packed copy)
+    if (!(c->wk == kWBf16 && cfg->x_dtype == CEP_BF16)) sc.xg = A(xes * c->max_mpad * d);
     sc.h = A(xes * c->max_mpad * I);
     sc.y = (__bf16 *)A(sizeof(__bf16) * c->max_mpad * d);
     if (c->wk != kWBf16) {  // e4m3 float scales per 128, or E8M0 bytes per 32: same size
@@ -559,6 +564,7 @@ CEP_API int cep_submit_chunk(cep_ctx *c, uint32_t generation, int replica, int n
     return fail(c, CEP_EINVAL, "bad n_rows %d / n_pairs %d", n_rows, n_pairs);
   if (n_rows > 0 && (!token_idx || !x || !topk_id || !topk_w))
     return fail(c, CEP_EINVAL, "NULL chunk array");
+  if (((uintptr_t)x & 15) != 0) return fail(c, CEP_EINVAL, "x must be 16-byte aligned");
   if (c->rows_used + n_rows > c->arena_cap)
     return fail(c, CEP_ENOMEM, "layer rows exceed max_replicas * max_tokens_per_replica");
   if (n_pairs > c->max_pairs)
