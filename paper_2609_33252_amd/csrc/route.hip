@@ -21,6 +21,20 @@ __device__ inline uint64_t lanemask_lt_popc(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
 }
 
+// The lanes of this wave whose id equals this lane's (ids in [-1, 64); -1
+// is key 127): one ballot per key bit, intersected.  Called with every lane
+// of the wave active.
+__device__ inline uint64_t same_id_lanes(int id) {
+  const int key = id & 127;
+  uint64_t m = __ballot(1);
+#pragma unroll
+  for (int b = 0; b < 7; ++b) {
+    const uint64_t v = __ballot((key >> b) & 1);
+    m &= ((key >> b) & 1) ? v : ~v;
+  }
+  return m;
+}
+
 // ---------------------------------------------------------------- ingest
 // Stages the routing metadata of a group of ready chunks into the layer's
 // arena (one entry per row, in submission order), so that a batch of whole
@@ -53,8 +67,8 @@ __global__ __launch_bounds__(256) void k_ingest(Arena a, IngestGroup grp, int k,
 
 // ------------------------------------------------------------ histogram
 // Block b counts the valid pairs of flat pairs [b*2048, (b+1)*2048) per
-// expert.  Each wave resolves its 64 ids with ballots: the lowest pending
-// lane names an expert, one ballot finds all lanes holding it.
+// expert.  Each wave resolves its 64 ids with seven ballots (the lanes
+// sharing each lane's id); the lowest lane of each id adds the group's size.
 __global__ __launch_bounds__(kRouteThreads) void k_route_count(const int32_t *__restrict__ ids,
                                                                int n_flat, int E,
                                                                int32_t *__restrict__ blk_cnt) {
@@ -73,14 +87,8 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_count(const int32_t *__
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int id = idv[r];
-    uint64_t active = __ballot(id >= 0);
-    while (active) {
-      const int leader = __builtin_ctzll(active);
-      const int e = __shfl(id, leader);
-      const uint64_t m = __ballot(id == e);
-      if (lane == leader) atomicAdd(&hist[e], (int)__popcll(m));
-      active &= ~m;
-    }
+    const uint64_t m = same_id_lanes(id);
+    if (id >= 0 && lane == __builtin_ctzll(m)) atomicAdd(&hist[id], (int)__popcll(m));
   }
   __syncthreads();
   if (tid < E) blk_cnt[blockIdx.x * E + tid] = hist[tid];
@@ -255,9 +263,11 @@ __global__ __launch_bounds__(64 * kFusedWaves) void k_route_fused(Arena a, Scrat
   __syncthreads();
   const int span = (n_flat + 64 * kFusedWaves - 1) / (64 * kFusedWaves) * 64;
   const int p0 = min(wid * span, n_flat), p1 = min(p0 + span, n_flat);
-  for (int p = p0 + lane; p < p1; p += 64) {
-    const int id = s_ids[p];
-    if (id >= 0) atomicAdd(&wcnt[wid][id], 1);
+  for (int base = p0; base < p1; base += 64) {
+    const int p = base + lane;
+    const int id = p < p1 ? s_ids[p] : -1;
+    const uint64_t m = same_id_lanes(id);
+    if (id >= 0 && lane == __builtin_ctzll(m)) wcnt[wid][id] += (int)__popcll(m);
   }
   __syncthreads();
   if (tid < E) {
@@ -275,17 +285,17 @@ __global__ __launch_bounds__(64 * kFusedWaves) void k_route_fused(Arena a, Scrat
     const int p = base + lane;
     const int id = p < p1 ? s_ids[p] : -1;
     int pos = -1;
-    uint64_t active = __ballot(id >= 0);
-    while (active) {
-      const int leader = __builtin_ctzll(active);
-      const int e = __shfl(id, leader);
-      const uint64_t m = __ballot(id == e);
-      // lanes of expert e read the wave's running row before the leader
-      // advances it (LDS operations of one wave complete in order)
-      if (id == e) pos = L.pad[e] + wcnt[wid][e] + (int)lanemask_lt_popc(m);
-      if (lane == leader) wcnt[wid][e] += (int)__popcll(m);
-      active &= ~m;
+    // each id's lowest lane reads and advances the wave's running row; the
+    // other lanes of that id take the old value from it
+    const uint64_t m = same_id_lanes(id);
+    const int leader = __builtin_ctzll(m);
+    int run = 0;
+    if (id >= 0 && lane == leader) {
+      run = wcnt[wid][id];
+      wcnt[wid][id] = run + (int)__popcll(m);
     }
+    run = __shfl(run, leader);
+    if (id >= 0) pos = L.pad[id] + run + (int)lanemask_lt_popc(m);
     if (pos >= pa.max_mpad) pos = -1;
     if (p < p1) {
       sc.pos_of[p] = pos;
@@ -328,16 +338,9 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_scatter(Arena a, Scratc
   for (int r = 0; r < R; ++r) {
     const int p = base + r * kRouteThreads + tid;
     const int id = idv[r];
-    int rank = 0;
-    uint64_t active = __ballot(id >= 0);
-    while (active) {
-      const int leader = __builtin_ctzll(active);
-      const int e = __shfl(id, leader);
-      const uint64_t m = __ballot(id == e);
-      if (id == e) rank = (int)lanemask_lt_popc(m);
-      if (lane == leader) wave_cnt[wid][e] = (int)__popcll(m);
-      active &= ~m;
-    }
+    const uint64_t m = same_id_lanes(id);
+    const int rank = (int)lanemask_lt_popc(m);
+    if (id >= 0 && lane == __builtin_ctzll(m)) wave_cnt[wid][id] = (int)__popcll(m);
     __syncthreads();
     int pos = -1;
     if (id >= 0) {

@@ -78,6 +78,11 @@ def test_null_and_invalid_arguments_fail_cleanly(L):
                               None, None) == cep.CEP_EINVAL
     assert L.cep_init_experts(ctypes.byref(h), ctypes.byref(_cfg()), ctypes.byref(w), None,
                               None) == cep.CEP_EINVAL  # NULL weight pointers
+    # MXFP4 weights without their E8M0 scales
+    wx = cep.cep_weights(1 << 20, 1 << 20, 1 << 20, None, None, None)
+    assert L.cep_init_experts(ctypes.byref(h), ctypes.byref(_cfg(w_dtype=cep.CEP_MXFP4)),
+                              ctypes.byref(wx), None, None) == cep.CEP_EINVAL
+    assert b"scale" in L.cep_last_error(None)
     assert L.cep_pack_experts(ctypes.byref(_cfg()), ctypes.byref(w), 0, 1, None, None) == cep.CEP_EINVAL
     for fn, args in (("cep_set_policy", (0, 1, 1)), ("cep_flush", ()), ("cep_get_status", ()),
                      ("cep_combine", (None, None))):

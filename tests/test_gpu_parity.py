@@ -264,6 +264,9 @@ def test_error_paths():
     with E(cep.CepError) as e:  # more pairs than rows * k
         cep.cep_submit_chunk(ctx, 7, 0, 1, 5, ch.token_idx, ch.x, ch.ids, ch.w)
     assert e.value.status == cep.CEP_EINVAL
+    with E(cep.CepError) as e:  # rows not 16-byte aligned (checked before any read)
+        cep.cep_submit_chunk(ctx, 7, 0, 1, 1, ch.token_idx, ch.x.view(-1)[1:], ch.ids, ch.w)
+    assert e.value.status == cep.CEP_EINVAL and "aligned" in str(e.value)
     with E(cep.CepError) as e:  # policy change inside a layer
         cep.cep_set_policy(ctx, cep.CEP_PER_CHUNK)
     assert e.value.status == cep.CEP_ESTATE
