@@ -148,7 +148,10 @@ int cep_begin_layer(cep_ctx *ctx, uint32_t generation, int n_replicas,
  * contains the chunk has finished (cep_combine's event covers all):
  *   token_idx [n_rows] int32 token slot in [0, T_max), each (replica, token)
  *             at most once per layer
- *   x         [n_rows][d] rows (x_dtype), 16-byte aligned
+ *   x         [n_rows][d] rows (x_dtype), 16-byte aligned.  With bf16 rows
+ *             and bf16 weights the first grouped GEMM reads them in place
+ *             (no packed copy): keeping a layer's chunks in one receive
+ *             region keeps that gather within few pages
  *   topk_id   [n_rows][k] int32 local expert id in [0, E) or -1 (remote slot)
  *   topk_w    [n_rows][k] float32 routing coefficients
  * n_pairs: host-known count of valid (id >= 0) entries.  arrival: event after

@@ -181,7 +181,7 @@ struct IngestChunk {
   const float *topk_w;
   int row0, n_rows, replica;
 };
-constexpr int kIngestGroup = 32;
+constexpr int kIngestGroup = 64;  // 3 KB of kernel arguments per staging launch
 struct IngestGroup {
   IngestChunk c[kIngestGroup];
   int n;

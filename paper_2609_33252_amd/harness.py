@@ -67,7 +67,13 @@ class Runner:
         torch.cuda.synchronize(dev)
         del wg, wu, wd, sg, su, sd, weights
 
+        # token rows land in one receive buffer, chunk after chunk in arrival
+        # order (as a dispatch writes them into its registered receive
+        # region); each chunk's x is a view of it
+        n_recv = sum(ch.n_rows for ch in wl.chunks)
+        self.recv = torch.empty(max(1, n_recv), c["d"], dtype=wl.x.dtype, device=dev)
         self.chunks = []
+        r0 = 0
         for ch in wl.chunks:
             x, ids, w = wl.chunk_rows(ch)
             dc = DeviceChunk()
@@ -75,7 +81,9 @@ class Runner:
             dc.n_rows = ch.n_rows
             dc.n_pairs = int((ids >= 0).sum())
             dc.token_idx = torch.from_numpy(ch.token_idx.astype(np.int32)).to(dev)
-            dc.x = x.contiguous().to(dev)
+            dc.x = self.recv[r0:r0 + ch.n_rows]
+            dc.x.copy_(x)
+            r0 += ch.n_rows
             dc.ids = torch.from_numpy(np.ascontiguousarray(ids, np.int32)).to(dev)
             dc.w = torch.from_numpy(np.ascontiguousarray(w, np.float32)).to(dev)
             dc.arrival_ms = ch.arrival_ms
