@@ -39,7 +39,10 @@ GEMM_SOURCES = {
     "bf16": ["paper_2609_33252_amd/csrc/gemm_bf16.hip", "paper_2609_33252_amd/csrc/gemm_common.h"],
     "mxfp4": ["paper_2609_33252_amd/csrc/gemm_mx.hip", "paper_2609_33252_amd/csrc/gemm_common.h"],
 }
-TRAFFIC_BYTES = {}  # workload -> (dtype, sha1 prefix, bytes)
+TRAFFIC_BYTES = {  # workload -> (GEMM family, sha1 prefix of its sources, bytes per layer)
+    "sync_d4096": ("bf16", "884ffe18f563", 504332947),
+    "mxfp4_dsv4flash_d4096": ("mxfp4", "f45c983fceec", 1374121505),
+}
 
 
 def gemm_source_hash(dtype):
