@@ -15,7 +15,9 @@
 //     for many weight bytes in flight per CU.
 // Both accumulate each output over K in the same order (ascending 16-wide
 // steps of v_mfma_f32_32x32x16_bf16), so a row's result does not depend on
-// which tile its batch used.
+// which tile its batch used.  With bf16 token rows GEMM1 runs as GATHER: its
+// A rows are the batch's input rows themselves, found through the
+// permutation (the layout transform's row pack reduced to an address lookup).
 #include "gemm_common.h"
 
 namespace cep {
