@@ -40,8 +40,8 @@ GEMM_SOURCES = {
     "mxfp4": ["paper_2609_33252_amd/csrc/gemm_mx.hip", "paper_2609_33252_amd/csrc/gemm_common.h"],
 }
 TRAFFIC_BYTES = {  # workload -> (GEMM family, sha1 prefix of its sources, bytes per layer)
-    "sync_d4096": ("bf16", "884ffe18f563", 504332947),
-    "mxfp4_dsv4flash_d4096": ("mxfp4", "f45c983fceec", 1374121505),
+    "sync_d4096": ("bf16", "c7f4698b9115", 504377329),
+    "mxfp4_dsv4flash_d4096": ("mxfp4", "f45c983fceec", 1372612937),
 }
 
 
