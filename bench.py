@@ -118,6 +118,7 @@ def cpu_baseline(wl, budget_s=12.0):
 def sweep(args):
     """Timed replay of a streaming workload under each launch policy: one
     JSON line per policy (mean over --steps layers after --warmup)."""
+    import numpy as np
     import torch
     from paper_2609_33252_amd import cep, harness, streaming, workload as W
 
@@ -128,17 +129,31 @@ def sweep(args):
     plan = [("wait_all", 1, 1), ("per_chunk", 1, 1), ("per_chunk", 1, 4)]
     thetas = [int(t) for t in args.thetas.split(",")]
     plan += [("threshold", t, s) for t in thetas for s in (1, 4)]
+    # GEMM1 weight bytes of each expert (gate and up), and the local experts
+    # each chunk touches: a batch streams the weights of every expert it
+    # touches once, so GEMM1's weight rate is the streaming roofline figure
+    w1_bytes = 2 * c["I"] * c["d"] * {W.BF16: 2, W.F32: 2, W.FP8: 1}.get(c["w"], 0.5)
+    touched = [set(int(e) for e in np.unique(wl.topk_local[ch.replica][ch.token_idx]) if e >= 0)
+               for ch in wl.chunks]
     base = None
     for name, theta, streams in plan:
         pol = POLICIES[name]
-        res = []
+        res, wbytes, g1ms = [], 0.0, 0.0
         for i in range(args.warmup + args.steps):
             run.run(policy=pol, theta=theta, n_streams=streams, timed=True,
                     time_scale=args.time_scale)
             torch.cuda.synchronize()
             if i >= args.warmup:
-                res.append(streaming.layer_metrics(run.stats(), flops))
+                st = run.stats()
+                res.append(streaming.layer_metrics(st, flops))
+                for b in st["batches"]:
+                    ex = set().union(*touched[b["first_chunk"]:b["first_chunk"] + b["n_chunks"]])
+                    wbytes += len(ex) * w1_bytes
+                    g1ms += b["gemm1_ms"]
         m = streaming.mean_metrics(res)
+        if g1ms > 0:
+            m["gemm1_weight_tbps"] = round(wbytes / (g1ms * 1e-3) / 1e12, 3)
+            m["gemm1_weight_frac_hbm"] = round(wbytes / (g1ms * 1e-3) / 1e12 / (HBM_PEAK_GBS / 1e3), 4)
         if name == "wait_all":
             base = m
         line = {"workload": args.workload, "policy": name, "theta": theta, "streams": streams,
