@@ -244,6 +244,24 @@ def test_fetched_experts_equal_resident_bitwise():
     assert np.array_equal(ga, gb)
 
 
+def test_fetched_bf16_experts_equal_resident_bitwise():
+    # bf16 rows are read in place by GEMM1 on the helper stream too
+    wl = W.generate("zipf_stream_d7168", 0, d=1024, I=512, E=8, Eg=32, T=512, cpr=4,
+                    fetch_frac=0.25)
+    assert wl.fetched
+    a = harness.Runner(wl, n_streams=3, use_fetch=True)
+    a.run(policy=cep.CEP_THRESHOLD, theta=300, n_streams=3)
+    ga = _out(a)
+    assert all(b["helper"] for b in a.stats()["batches"])
+    a.close()
+    b = harness.Runner(wl, n_streams=1, use_fetch=False)
+    b.run(policy=cep.CEP_WAIT_ALL)
+    gb = _out(b)
+    b.close()
+    assert np.array_equal(ga, gb)
+    U.compare(wl, gb, U.reference(wl))
+
+
 # ----------------------------------------------------------- error paths
 def test_error_paths():
     wl = W.generate("tiny", 0)
