@@ -41,6 +41,7 @@ GEMM_SOURCES = {
 }
 TRAFFIC_BYTES = {  # workload -> (GEMM family, sha1 prefix of its sources, bytes per layer)
     "sync_d4096": ("bf16", "c7f4698b9115", 504377329),
+    "zipf_imbalanced_d7168/per_chunk": ("bf16", "c7f4698b9115", 473926251),
     "mxfp4_dsv4flash_d4096": ("mxfp4", "f45c983fceec", 1372612937),
 }
 
@@ -413,14 +414,36 @@ def main():
     n_launch = len(st["batches"])
     g1_flops = 4.0 * c["d"] * c["I"] * run.n_pairs / n_launch
     g1_ms = avg["gemm1_ms"] / n_launch
-    achieved = g1_flops / (g1_ms * 1e-3) / 1e12
-    traffic = measured_traffic(args.workload)
-    roofline = {"bound": "mfma",
-                "kernel": "k_gemm_%s<SwiGLU> (grouped gate/up GEMM; bf16 256-row tiles plus "
-                          "64-row remainder tiles when planned)" % {"mxfp4": "mx"}.get(dtype, dtype),
-                "achieved": round(achieved, 2), "peak": PEAK[dtype], "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK[dtype], 4), "traffic": traffic,
-                "launch_ms": round(g1_ms, 4), "flop_per_launch": g1_flops}
+    # algorithmic bytes of GEMM1 per launch: the gate/up weights of every
+    # local expert a batch touches (each streamed once), the batch's rows in
+    # and h out
+    import numpy as np
+    elem = {W.BF16: 2, W.F32: 2, W.FP8: 1}.get(c["w"], 0.5)
+    xel = 2 if dtype == "bf16" else 1
+    touched = [set(int(e) for e in np.unique(wl.topk_local[ch.replica][ch.token_idx]) if e >= 0)
+               for ch in wl.chunks]
+    g1_bytes = sum(len(set().union(*touched[b["first_chunk"]:b["first_chunk"] + b["n_chunks"]]))
+                   for b in st["batches"]) * 2.0 * c["I"] * c["d"] * elem / n_launch
+    g1_bytes += run.n_pairs * (c["d"] + c["I"]) * xel / n_launch
+    # the roofline that bounds a launch: MFMA time vs HBM time at peak
+    hbm_bound = g1_bytes / (HBM_PEAK_GBS * 1e9) > g1_flops / (PEAK[dtype] * 1e12)
+    traffic = measured_traffic(args.workload if args.policy == "wait_all"
+                               else f"{args.workload}/{args.policy}")
+    kernel = ("k_gemm_%s<SwiGLU> (grouped gate/up GEMM; %s)" %
+              ({"mxfp4": "mx"}.get(dtype, dtype),
+               "64-row weight-streaming tiles" if hbm_bound else
+               "256-row tiles, bf16 plus 64-row remainder tiles when planned"))
+    if hbm_bound:
+        achieved = g1_bytes / (g1_ms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 1),
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": traffic, "launch_ms": round(g1_ms, 4),
+                    "bytes_per_launch": round(g1_bytes)}
+    else:
+        achieved = g1_flops / (g1_ms * 1e-3) / 1e12
+        roofline = {"bound": "mfma", "kernel": kernel, "achieved": round(achieved, 2),
+                    "peak": PEAK[dtype], "unit": "TFLOP/s", "frac": round(achieved / PEAK[dtype], 4),
+                    "traffic": traffic, "launch_ms": round(g1_ms, 4), "flop_per_launch": g1_flops}
     line = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
