@@ -15,6 +15,7 @@ the CPU oracle's throughput on a bounded sample.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
        [--workload NAME] [--policy wait_all|per_chunk|threshold --theta N --streams S]
+       python bench.py --sweep | --matched-work | --calibrate-theta | --oewf-sim
 """
 import argparse
 import json
@@ -162,6 +163,61 @@ def sweep(args):
         if base and m.get("busy_tflops") and base.get("busy_tflops"):
             line["ffn_efficiency_vs_wait_all"] = m["busy_tflops"] / base["busy_tflops"]
             line["exposed_tail_vs_wait_all"] = m["exposed_tail_ms"] / base["exposed_tail_ms"]
+        print(json.dumps(line), flush=True)
+    cep.cep_get_status(run.ctx)
+    run.close()
+
+
+def matched_work(args):
+    """Matched-work FFN throughput: the same layer (same weights, same
+    per-expert token counts) run as one wait-all invocation and as streamed
+    invocations (per chunk, or threshold theta) on 1..4 streams, inputs
+    resident and no arrival timing, so only the batching and the stream
+    overlap differ.  One JSON line per (policy, theta, streams) with the
+    layer's throughput and its ratio to wait-all on one stream."""
+    import torch
+    from paper_2609_33252_amd import cep, harness, workload as W
+
+    wl = W.generate(args.workload, 0)
+    c = wl.cfg
+    run = harness.Runner(wl, n_streams=4)
+    flops = 6.0 * c["d"] * c["I"] * run.n_pairs
+    thetas = [int(t) for t in args.thetas.split(",")]
+    plan = [("wait_all", 1, 1)] + [("per_chunk", 1, s) for s in (1, 2, 4)]
+    plan += [("threshold", t, s) for t in thetas for s in (1, 2, 4)]
+    cep.cep_set_phase_timing(run.ctx, False)
+
+    def layer_ms(pol, theta, streams):
+        for _ in range(args.warmup):
+            run.run(policy=pol, theta=theta, n_streams=streams, inputs_ready=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            run.run(policy=pol, theta=theta, n_streams=streams, inputs_ready=True)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / args.steps * 1e3
+
+    # the GPU reaches its steady clocks only after some layers: a warm-up
+    # well beyond --warmup comes first; then wait-all is timed before and
+    # after the others and the base is the mean of the two, so drift over
+    # the run does not favour either side
+    for _ in range(max(20, 4 * args.warmup)):
+        run.run(policy=cep.CEP_WAIT_ALL, theta=1, n_streams=1, inputs_ready=True)
+    first = layer_ms(cep.CEP_WAIT_ALL, 1, 1)
+    runs = []
+    for name, theta, streams in plan[1:]:
+        ms = layer_ms(POLICIES[name], theta, streams)
+        runs.append((name, theta, streams, cep.cep_get_batch_count(run.ctx), ms))
+    last = layer_ms(cep.CEP_WAIT_ALL, 1, 1)
+    base = flops / ((first + last) / 2) / 1e9
+    runs = [("wait_all", 1, 1, 1, (first + last) / 2)] + runs
+    for name, theta, streams, n_batches, ms in runs:
+        tflops = flops / ms / 1e9
+        line = {"workload": args.workload, "policy": name, "theta": theta,
+                "streams": streams, "batches": n_batches, "ms_per_layer": round(ms, 4),
+                "tflops": round(tflops, 2), "throughput_vs_wait_all": round(tflops / base, 4)}
+        if name == "wait_all":
+            line["wait_all_first_last_ms"] = [round(first, 4), round(last, 4)]
         print(json.dumps(line), flush=True)
     cep.cep_get_status(run.ctx)
     run.close()
@@ -315,6 +371,8 @@ def main():
     ap.add_argument("--thetas", default="32,64,128,256,512,1024,2048,4096")
     ap.add_argument("--time-scale", type=float, default=1.0,
                     help="scale of the arrival schedule in --sweep (1 = as generated)")
+    ap.add_argument("--matched-work", action="store_true",
+                    help="wait-all vs streamed invocations on identical resident inputs")
     ap.add_argument("--calibrate-theta", action="store_true",
                     help="profile FFN throughput vs expert-token count; theta(rho) and F(N)")
     ap.add_argument("--rho", type=float, default=0.9)
@@ -340,6 +398,14 @@ def main():
         if args.workload == "sync_d4096":
             args.workload = "zipf_imbalanced_d7168"
         calibrate_theta(args)
+        return
+    if args.matched_work:
+        if args.gpus != 1:
+            print("bench.py runs on one GPU only", file=sys.stderr)
+            sys.exit(2)
+        if args.workload == "sync_d4096":
+            args.workload = "zipf_imbalanced_d7168"
+        matched_work(args)
         return
     if args.sweep:
         if args.gpus != 1:

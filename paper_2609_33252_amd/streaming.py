@@ -10,8 +10,9 @@ every chunk's arrival.  From them:
   asynchronous execution shortens, Section 3.2);
 * per-chunk latency: end of the batch holding the chunk minus its arrival;
 * busy time: length of the union of the batches' [start, end] intervals, and
-  the aggregate TFLOP/s of the layer's routed-expert work over it (the
-  matched-work FFN efficiency comparison of Section 4.3).
+  the aggregate TFLOP/s of the layer's routed-expert work over it (a
+  timed-arrival counterpart of the matched-work FFN efficiency comparison of
+  Section 4.3, which bench.py --matched-work runs on resident inputs).
 """
 from __future__ import annotations
 
