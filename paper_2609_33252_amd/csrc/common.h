@@ -68,6 +68,16 @@ struct BlobLayout {
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 constexpr int kBf16SmallTileM = 64;  // bf16 tile for batches with few rows per expert
+// Such batches with at least kBf16VarMinRows pairs per local expert on
+// average run both GEMMs in 128-row tiles over the same 64-aligned layout:
+// an expert's rows in tiles of 128, the last of them a 64-row half tile when
+// at most 64 rows remain (a hot expert then reads its weights once per 128
+// rows instead of once per 64)
+constexpr int kBf16VarTileM = 128;
+constexpr int kBf16VarMinRows = 64;
+inline bool batch_var_tiles(int wk, int align, int pairs, int n_experts) {
+  return wk == kWBf16 && align == kBf16SmallTileM && pairs >= kBf16VarMinRows * n_experts;
+}
 
 // Per-expert row alignment A of one batch's grouped layout = M tile of the
 // GEMMs that run it.  bf16 batches with fewer than one large tile of rows
@@ -191,11 +201,12 @@ hipError_t launch_ingest(const Arena &a, const IngestGroup &grp, int k, int E, i
 // split_cu > 0 (bf16 batches with 256-row tiles): the scan may move each
 // expert's last partial tile of at most 128 rows to 64-row remainder tiles
 // when its makespan estimate for split_cu compute units and GEMM1's
-// n_tiles_n 256-wide column tiles improves.
+// n_tiles_n 256-wide column tiles improves.  var (batch_var_tiles): the
+// scan also lists the 128-row tiles, in the second list of each kind.
 hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int E,
                         int align, int expected_pairs, int max_mpad, int max_tiles,
                         uint64_t fetched_mask, int x_dtype, int wk, int d, int split_cu,
-                        int n_tiles_n, uint32_t *err, hipStream_t s);
+                        int n_tiles_n, bool var, uint32_t *err, hipStream_t s);
 hipError_t launch_combine(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int d,
                           float *out, hipStream_t s);
 
@@ -205,13 +216,13 @@ hipError_t launch_combine(const Arena &a, const Scratch &sc, int row0, int n_row
 // split_tiles > 0, up to split_tiles 64-row remainder tiles
 // gather (bf16 weights and rows only): GEMM1 reads the batch's input rows
 // (arena rows from row0) in place through the permutation instead of a
-// packed copy
+// packed copy.  var: both GEMMs run the 128-row tile list instead.
 hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles,
-                        int split_tiles, int align, const BlobTable &bt, const BlobLayout &L,
-                        int wk, int d, int I, const Arena *gather, int row0, int k,
-                        hipStream_t s);
+                        int split_tiles, int align, bool var, const BlobTable &bt,
+                        const BlobLayout &L, int wk, int d, int I, const Arena *gather, int row0,
+                        int k, hipStream_t s);
 hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles,
-                        int split_tiles, int align, const BlobTable &bt, const BlobLayout &L,
-                        int wk, int d, int I, hipStream_t s);
+                        int split_tiles, int align, bool var, const BlobTable &bt,
+                        const BlobLayout &L, int wk, int d, int I, hipStream_t s);
 
 }  // namespace cep

@@ -34,12 +34,19 @@ hipError_t launch_any(const GemmArgs &g, int grid_tiles, int split_tiles, int al
   return launch_bf16<SWIGLU>(r, split_tiles, kBf16SmallTileM, s);
 }
 
+// the scan's second list of `which`: the batch's 128-row tiles
+GemmArgs var_list(GemmArgs g, const Scratch &sc, int which, int list_cap) {
+  g.tiles = sc.tiles + (size_t)(2 * which + 1) * list_cap;
+  g.n_tiles = sc.n_tiles + 2 * which + 1;
+  return g;
+}
+
 }  // namespace
 
 hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles,
-                        int split_tiles, int align, const BlobTable &bt, const BlobLayout &L,
-                        int wk, int d, int I, const Arena *gather, int row0, int k,
-                        hipStream_t s) {
+                        int split_tiles, int align, bool var, const BlobTable &bt,
+                        const BlobLayout &L, int wk, int d, int I, const Arena *gather, int row0,
+                        int k, hipStream_t s) {
   if (grid_tiles <= 0) return hipSuccess;
   GemmArgs g = base_args(sc, 2 * which, list_cap, grid_tiles, bt);
   g.A = (const uint8_t *)sc.xg;
@@ -57,12 +64,13 @@ hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_til
   g.bs_off = L.s1_off;
   g.out = sc.h;
   g.out_s = sc.hs;
+  if (var) return launch_bf16_var<true>(var_list(g, sc, which, list_cap), grid_tiles, s);
   return launch_any<true>(g, grid_tiles, split_tiles, align, wk, sc, which, list_cap, s);
 }
 
 hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles,
-                        int split_tiles, int align, const BlobTable &bt, const BlobLayout &L,
-                        int wk, int d, int I, hipStream_t s) {
+                        int split_tiles, int align, bool var, const BlobTable &bt,
+                        const BlobLayout &L, int wk, int d, int I, hipStream_t s) {
   if (grid_tiles <= 0) return hipSuccess;
   GemmArgs g = base_args(sc, 2 * which, list_cap, grid_tiles, bt);
   g.A = (const uint8_t *)sc.h;
@@ -73,6 +81,7 @@ hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_til
   g.bs_off = L.s2_off;
   g.out = sc.y;
   g.wrow = sc.wrow;
+  if (var) return launch_bf16_var<false>(var_list(g, sc, which, list_cap), grid_tiles, s);
   return launch_any<false>(g, grid_tiles, split_tiles, align, wk, sc, which, list_cap, s);
 }
 

@@ -7,18 +7,24 @@
 // projection and scales each row by its routing coefficient (the one place
 // the coefficient is applied).
 //
-// One kernel template, two instantiations:
+// One kernel template, three uses:
 //   large batches: 256 x 256 tile, K steps of 32 through 4 LDS stages, one
 //     workgroup per CU -- MFMA-bound, each 16-byte LDS read feeds 4 MFMAs;
 //   small batches (few rows per expert): 64 x 128 tile, K steps of 64 through
 //     3 stages, two workgroups per CU -- weight-streaming (HBM) bound, sized
-//     for many weight bytes in flight per CU.
-// Both accumulate each output over K in the same order (ascending 16-wide
+//     for many weight bytes in flight per CU;
+//   mid-size batches (VAR): 128 x 128 tiles whose last tile per expert may be
+//     a 64-row half (it loads and multiplies its first 64 rows only), the
+//     weights three stages deep and the rows two, so that two workgroups
+//     still fit a CU: a hot expert streams its weights once per 128 rows.
+// All accumulate each output over K in the same order (ascending 16-wide
 // steps of v_mfma_f32_32x32x16_bf16), so a row's result does not depend on
 // which tile its batch used.  With bf16 token rows GEMM1 runs as GATHER: its
 // A rows are the batch's input rows themselves, found through the
 // permutation (the layout transform's row pack reduced to an address lookup).
 #include "gemm_common.h"
+
+#include <type_traits>
 
 namespace cep {
 namespace {
@@ -40,9 +46,12 @@ namespace {
 // tile): fragments are read right before their MFMAs and loads run STAGES-1
 // steps ahead, which keeps more weight bytes in flight per LDS byte.
 template <int BM, int BN, int BK, int STAGES, int OCC, bool PIPE, bool SWIGLU, int WGM = 2,
-          int NW = 4, int GM = kGroupM, bool GATHER = false>
+          int NW = 4, int GM = kGroupM, bool GATHER = false, bool VAR = false, int ASTG = 0>
 __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
   static_assert(BK == 32 || BK == 64, "LDS swizzle covers 4 or 8 chunks per row");
+  static_assert(!VAR || (!PIPE && WGM == 2 && BM == 128), "VAR: 128-row tile, two wave rows");
+  static_assert(ASTG == 0 || (ASTG == 2 && !PIPE && STAGES >= 3), "A ring: all stages or two");
+  constexpr int AS = ASTG ? ASTG : STAGES;  // depth of the A ring (B: STAGES)
   static_assert(STAGES >= 3 && STAGES <= 8, "wait counts below");
   constexpr int CH = BK / 8;                  // 16-byte chunks per LDS row
   constexpr int RPS = 1024 / (BK * 2);        // rows per 1 KB load segment
@@ -65,7 +74,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
   const char *Ag = GATHER ? nullptr : (const char *)(g.A + (size_t)t.row0 * K * 2);
   const char *Bg = (const char *)(blob_of(g.bt, t.expert) + g.b_off + (size_t)nt * BN * K * 2);
 
-  __shared__ u32x4 sA[STAGES][BM * CH];
+  __shared__ u32x4 sA[AS][BM * CH];
   __shared__ u32x4 sB[STAGES][BN * CH];
 
   // Lane l of a load fills slot l of a 1 KB segment (RPS rows x CH chunks):
@@ -77,32 +86,38 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
   ((uint32_t)((seg) * RPS + seg_row) * K * 2 +                                      \
    (uint32_t)(((lane % CH) ^ ((((seg) * RPS + seg_row) >> SH) & (CH - 1))) * 16))
   // GATHER: each lane's A rows are fixed for the whole K loop, so their
-  // input-row addresses (plus the lane's chunk) are looked up once
-  const char *arow[A_LD];
-  if constexpr (GATHER) {
-#pragma unroll
-    for (int i = 0; i < A_LD; ++i) {
-      const int r = (wid * A_LD + i) * RPS + seg_row;
-      const int p = g.perm[t.row0 + r];
-      arow[i] = (const char *)g.xrow[g.arow0 + (p >= 0 ? p / g.k : 0)] +
-                ((lane % CH) ^ ((r >> SH) & (CH - 1))) * 16;
-    }
+  // input-row addresses (plus the lane's chunk) are looked up once.  NAL_
+  // (the A loads per wave in the current schedule) is defined in each scope
+  // that expands these macros.
+#define CEP_AROWS(arow_)                                                            \
+  if constexpr (GATHER) {                                                           \
+    _Pragma("unroll") for (int i = 0; i < NAL_; ++i) {                              \
+      const int r = (wid * NAL_ + i) * RPS + seg_row;                               \
+      const int p = g.perm[t.row0 + r];                                             \
+      arow_[i] = (const char *)g.xrow[g.arow0 + (p >= 0 ? p / g.k : 0)] +           \
+                 ((lane % CH) ^ ((r >> SH) & (CH - 1))) * 16;                       \
+    }                                                                               \
   }
-#define CEP_DMA_STAGE(kt)                                                           \
+#define CEP_DMA_A(kt)                                                               \
   {                                                                                 \
-    const int buf_ = (kt) % STAGES;                                                 \
-    _Pragma("unroll") for (int i = 0; i < A_LD; ++i) {                              \
-      const int seg = wid * A_LD + i;                                               \
+    const int buf_ = (kt) % AS;                                                     \
+    _Pragma("unroll") for (int i = 0; i < NAL_; ++i) {                              \
+      const int seg = wid * NAL_ + i;                                               \
       dma16(GATHER ? arow[i] + (size_t)(kt) * BK * 2                                \
                    : Ag + (size_t)(kt) * BK * 2 + CEP_LANE_OFF(seg),                \
             __builtin_amdgcn_readfirstlane(lds_offset(&sA[buf_][seg * 64])));       \
     }                                                                               \
+  }
+#define CEP_DMA_B(kt)                                                               \
+  {                                                                                 \
+    const int buf_ = (kt) % STAGES;                                                 \
     _Pragma("unroll") for (int i = 0; i < B_LD; ++i) {                              \
       const int seg = wid * B_LD + i;                                               \
       dma16(Bg + (size_t)(kt) * BK * 2 + CEP_LANE_OFF(seg),                         \
             __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf_][seg * 64])));       \
     }                                                                               \
   }
+#define CEP_DMA_STAGE(kt) { CEP_DMA_A(kt) CEP_DMA_B(kt) }
 
   f32x16 acc[FM][FN];
 #pragma unroll
@@ -110,21 +125,29 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x16{};
 
-  // every fragment row r = (wave base) + i*32 + lane%32 has
-  // swz(r) == swz(lane % 32) because the bases are multiples of 32
+  // First row of A fragment i of this wave.  VAR interleaves the waves'
+  // fragments (i*64 + wm*32) so that a half tile's 64 rows are fragment 0
+  // of every wave.  Every fragment row r = base + lane%32 has
+  // swz(r) == swz(lane % 32) because the bases are multiples of 32.
+  auto frow = [&](int i) { return VAR ? i * (BM / FM) + wm * 32 : wm * WM + i * 32; };
   const int rsw = ((lane & 31) >> SH) & (CH - 1);
-#define CEP_LOAD_FRAG(fa_, fb_, buf_, kk_)                                          \
+#define CEP_LOAD_FRAG(fa_, fb_, abuf_, bbuf_, kk_, nfa_)                            \
   {                                                                                 \
     const int slot_ = ((kk_) * 2 + (lane >> 5)) ^ rsw;                              \
-    _Pragma("unroll") for (int i = 0; i < FM; ++i) fa_[i] = __builtin_bit_cast(     \
-        bf16x8, sA[buf_][(wm * WM + i * 32 + (lane & 31)) * CH + slot_]);           \
+    _Pragma("unroll") for (int i = 0; i < (nfa_); ++i) fa_[i] = __builtin_bit_cast( \
+        bf16x8, sA[abuf_][(frow(i) + (lane & 31)) * CH + slot_]);                   \
     _Pragma("unroll") for (int j = 0; j < FN; ++j) fb_[j] = __builtin_bit_cast(     \
-        bf16x8, sB[buf_][(wn * WN + j * 32 + (lane & 31)) * CH + slot_]);           \
+        bf16x8, sB[bbuf_][(wn * WN + j * 32 + (lane & 31)) * CH + slot_]);          \
   }
 
   constexpr int KK = BK / 16;
   static_assert(!PIPE || KK % 2 == 0, "fragment double buffer alternates per sub-step");
+  // a VAR tile of at most BM/2 rows loads and multiplies its first half only
+  const bool half = VAR && t.rows <= BM / 2;
   if constexpr (PIPE) {
+    constexpr int NAL_ = A_LD;
+    const char *arow[NAL_];
+    CEP_AROWS(arow)
     // Stage s is issued at the barrier of step s - STAGES + 1 (the prologue
     // issues stages 0 .. STAGES-2), into the buffer of stage s - STAGES,
     // whose last fragment reads completed before the MFMAs of step
@@ -139,14 +162,14 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
     // The last sub-step of step kt first waits for stage kt+1, issues the
     // loads of stage kt+STAGES-1 and reads the first fragments of kt+1.
     bf16x8 fa[2][FM], fb[2][FN];
-    CEP_LOAD_FRAG(fa[0], fb[0], 0, 0);
+    CEP_LOAD_FRAG(fa[0], fb[0], 0, 0, 0, FM);
     for (int kt = 0; kt < nk; ++kt) {
       const int cur = kt % STAGES;
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
         const int p = kk & 1, q = p ^ 1;
         if (kk + 1 < KK) {
-          CEP_LOAD_FRAG(fa[q], fb[q], cur, kk + 1);
+          CEP_LOAD_FRAG(fa[q], fb[q], cur, cur, kk + 1, FM);
         } else if (kt + 1 < nk) {
           // this thread's loads of stage kt+1 are done when at most the
           // loads of the stages issued after it (up to kt+STAGES-2) are
@@ -154,7 +177,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
           wait_stages<PER, STAGES - 3>(min(nk - 1, kt + STAGES - 2) - (kt + 1));
           __builtin_amdgcn_s_barrier();
           if (kt + STAGES - 1 < nk) CEP_DMA_STAGE(kt + STAGES - 1);
-          CEP_LOAD_FRAG(fa[q], fb[q], (kt + 1) % STAGES, 0);
+          CEP_LOAD_FRAG(fa[q], fb[q], (kt + 1) % STAGES, (kt + 1) % STAGES, 0, FM);
         }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -167,44 +190,93 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
       }
     }
   } else {
-    // Stage s is issued at the top of step s - STAGES + 1, into the buffer
-    // of stage s - STAGES, which every wave finished reading in step
-    // s - STAGES (before this step's barrier).
+    // NFA A fragments per wave and NAL_ A loads per wave and step (all of
+    // them, or for a VAR half tile those of its first BM/2 rows); every wave
+    // issues the same number of loads per step, so the vmcnt waits count
+    // whole steps.
+    auto run = [&](auto nfa_c, auto nal_c) {
+      constexpr int NFA = decltype(nfa_c)::value, NAL_ = decltype(nal_c)::value;
+      constexpr int PERX = NAL_ + B_LD;
+      const char *arow[NAL_];
+      CEP_AROWS(arow)
+      if constexpr (ASTG == 2) {
+        // B (weights, from HBM) runs STAGES-1 steps ahead, A (rows, mostly
+        // L2 hits) one step ahead in a ring of two: the top of step j issues
+        // A(j+1), then B(j+STAGES-1), into buffers last read in step j-1.
+        // The prologue is "step -1" after B(0 .. STAGES-3).
 #pragma unroll
-    for (int s = 0; s < STAGES - 1; ++s)
-      if (s < nk) CEP_DMA_STAGE(s);
-    for (int kt = 0; kt < nk; ++kt) {
-      // this thread's loads of step kt are done when at most the loads of
-      // the steps issued after it are outstanding
-      wait_stages<PER, STAGES - 2>(min(nk - 1, kt + STAGES - 2) - kt);
-      // every wave's loads of step kt landed; step kt-1 fully consumed.  A
-      // bare barrier: __syncthreads() would also drain the later loads.
-      __builtin_amdgcn_s_barrier();
-      if (kt + STAGES - 1 < nk) CEP_DMA_STAGE(kt + STAGES - 1);
-      const int cur = kt % STAGES;
+        for (int s = 0; s < STAGES - 2; ++s)
+          if (s < nk) CEP_DMA_B(s);
+        CEP_DMA_A(0);
+        if (STAGES - 2 < nk) CEP_DMA_B(STAGES - 2);
+      } else {
+        // Stage s is issued at the top of step s - STAGES + 1, into the
+        // buffer of stage s - STAGES, which every wave finished reading in
+        // step s - STAGES (before this step's barrier).
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        bf16x8 fa[FM], fb[FN];
-        CEP_LOAD_FRAG(fa, fb, cur, kk);
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-          for (int j = 0; j < FN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+        for (int s = 0; s < STAGES - 1; ++s)
+          if (s < nk) CEP_DMA_STAGE(s);
       }
+      for (int kt = 0; kt < nk; ++kt) {
+        if constexpr (ASTG == 2) {
+          // A(kt) and B(kt) are done when only B(kt+STAGES-2), issued after
+          // A(kt) at the top of step kt-1, may be outstanding
+          if (kt + STAGES - 2 < nk)
+            wait_vmcnt<B_LD>();
+          else
+            wait_vmcnt<0>();
+        } else {
+          // this thread's loads of step kt are done when at most the loads
+          // of the steps issued after it are outstanding
+          wait_stages<PERX, STAGES - 2>(min(nk - 1, kt + STAGES - 2) - kt);
+        }
+        // every wave's loads of step kt landed; step kt-1 fully consumed.  A
+        // bare barrier: __syncthreads() would also drain the later loads.
+        __builtin_amdgcn_s_barrier();
+        if constexpr (ASTG == 2) {
+          if (kt + 1 < nk) CEP_DMA_A(kt + 1);
+          if (kt + STAGES - 1 < nk) CEP_DMA_B(kt + STAGES - 1);
+        } else {
+          if (kt + STAGES - 1 < nk) CEP_DMA_STAGE(kt + STAGES - 1);
+        }
+        const int acur = kt % AS, cur = kt % STAGES;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+          bf16x8 fa[FM], fb[FN];
+          CEP_LOAD_FRAG(fa, fb, acur, cur, kk, NFA);
+#pragma unroll
+          for (int i = 0; i < NFA; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+              acc[i][j] =
+                  __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+        }
+      }
+    };
+    if constexpr (VAR) {
+      if (half)
+        run(std::integral_constant<int, 1>{}, std::integral_constant<int, A_LD / 2>{});
+      else
+        run(std::integral_constant<int, FM>{}, std::integral_constant<int, A_LD>{});
+    } else {
+      run(std::integral_constant<int, FM>{}, std::integral_constant<int, A_LD>{});
     }
   }
 #undef CEP_LOAD_FRAG
 #undef CEP_DMA_STAGE
+#undef CEP_DMA_A
+#undef CEP_DMA_B
+#undef CEP_AROWS
 #undef CEP_LANE_OFF
 
   // 32x32 accumulator layout: lane l, element r -> column l%32,
   // row 8*(r/4) + 4*(l/32) + r%4.
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
+    if (half && i > 0) break;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int rt = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      const int rt = frow(i) + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
       if (rt >= t.rows) continue;
       const size_t row = (size_t)t.row0 + rt;
       if (SWIGLU) {
@@ -260,6 +332,30 @@ hipError_t launch_bf16(const GemmArgs &g, int grid_tiles, int align, hipStream_t
   return launch_bf16_as<SWIGLU, false>(g, grid_tiles, align, s);
 }
 
+template <bool SWIGLU, bool GATHER>
+hipError_t launch_bf16_var_as(const GemmArgs &g, int grid_tiles, hipStream_t s) {
+  constexpr int BN = 128;
+  if (g.N % BN || g.K % 64) return hipErrorInvalidValue;
+  const int grid = balanced_grid(grid_tiles, kGroupM, g.N / BN);
+  hipLaunchKernelGGL(
+      (k_gemm_bf16<kBf16VarTileM, BN, 64, 3, 2, false, SWIGLU, 2, 4, kGroupM, GATHER, true, 2>),
+      dim3(grid), dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+
+template <bool SWIGLU>
+hipError_t launch_bf16_var(const GemmArgs &g, int grid_tiles, hipStream_t s) {
+  if constexpr (SWIGLU) {
+    if (g.A == nullptr) {
+      if (!g.xrow || !g.perm || g.k < 1) return hipErrorInvalidValue;
+      return launch_bf16_var_as<true, true>(g, grid_tiles, s);
+    }
+  }
+  return launch_bf16_var_as<SWIGLU, false>(g, grid_tiles, s);
+}
+
+template hipError_t launch_bf16_var<true>(const GemmArgs &, int, hipStream_t);
+template hipError_t launch_bf16_var<false>(const GemmArgs &, int, hipStream_t);
 template hipError_t launch_bf16<true>(const GemmArgs &, int, int, hipStream_t);
 template hipError_t launch_bf16<false>(const GemmArgs &, int, int, hipStream_t);
 

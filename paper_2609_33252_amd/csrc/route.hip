@@ -100,6 +100,7 @@ struct PlanArgs {
   int E, align, expected_pairs, max_mpad, max_tiles;
   uint64_t fetched_mask;
   int split_cu, n_tiles_n;
+  int var;  // also list each expert's 128-row tiles (second list of each kind)
   uint32_t *err;
 };
 
@@ -149,7 +150,9 @@ __device__ void plan_batch(const Scratch &sc, PlanLds &L, const PlanArgs &a, int
       L.tile0[x] = t0[2 * which];
       L.rtile0[x] = t0[2 * which + 1];
       t0[2 * which] += rem ? c / align : (c + align - 1) / align;
-      t0[2 * which + 1] += rem ? (r + kBf16SmallTileM - 1) / kBf16SmallTileM : 0;
+      t0[2 * which + 1] += rem    ? (r + kBf16SmallTileM - 1) / kBf16SmallTileM
+                           : a.var ? (c + kBf16VarTileM - 1) / kBf16VarTileM
+                                   : 0;
       o += c;
       op += (c + align - 1) / align * align;
     }
@@ -185,6 +188,19 @@ __device__ void plan_batch(const Scratch &sc, PlanLds &L, const PlanArgs &a, int
       const int row0 = L.pad[tid] + q * align;
       if (ti >= a.max_tiles || row0 + align > a.max_mpad) break;
       list[ti] = Tile{tid, row0, min(align, c - q * align), 0};
+    }
+    if (a.var) {
+      // the second list holds the 128-row tiles; a tile of more than 64
+      // rows spans 128 rows of the expert's 64-aligned region
+      Tile *vlist = sc.tiles + (size_t)(2 * which + 1) * a.max_tiles;
+      for (int q = 0; q * kBf16VarTileM < c; ++q) {
+        const int ti = L.rtile0[tid] + q;
+        const int rows = min(kBf16VarTileM, c - q * kBf16VarTileM);
+        const int row0 = L.pad[tid] + q * kBf16VarTileM;
+        const int span = rows > kBf16VarTileM / 2 ? kBf16VarTileM : kBf16VarTileM / 2;
+        if (ti >= a.max_tiles || row0 + span > a.max_mpad) break;
+        vlist[ti] = Tile{tid, row0, rows, 0};
+      }
     }
     if (rem) {
       Tile *rlist = sc.tiles + (size_t)(2 * which + 1) * a.max_tiles;
@@ -693,12 +709,12 @@ hipError_t launch_ingest(const Arena &a, const IngestGroup &grp, int k, int E, i
 hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int E,
                         int align, int expected_pairs, int max_mpad, int max_tiles,
                         uint64_t fetched_mask, int x_dtype, int wk, int d, int split_cu,
-                        int n_tiles_n, uint32_t *err, hipStream_t s) {
+                        int n_tiles_n, bool var, uint32_t *err, hipStream_t s) {
   const int n_flat = n_rows * k;
   const int nb = (n_flat + kRoutePairs - 1) / kRoutePairs;
   if (nb == 0) return hipSuccess;
   const PlanArgs pa{E, align, expected_pairs, max_mpad, max_tiles, fetched_mask, split_cu,
-                    n_tiles_n, err};
+                    n_tiles_n, var ? 1 : 0, err};
   if (n_flat <= kFusedRoutePairs) {
     hipLaunchKernelGGL(k_route_fused, dim3(1), dim3(64 * kFusedWaves), 0, s, a, sc, row0,
                        n_flat, k, pa);

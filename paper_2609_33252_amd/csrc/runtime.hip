@@ -273,9 +273,11 @@ int launch_pending(cep_ctx *c) {
   // (at most two per expert), run by a second launch of the 64-row kernel
   const bool split = c->wk == kWBf16 && A == kBf16TileM;
   const int split_tiles = split ? 2 * E : 0;
+  // 64-row bf16 batches with enough rows per expert: 128-row tiles
+  const bool var = batch_var_tiles(c->wk, A, P, E);
   HIPCHK(c, launch_route(c->arena, sc, b.row0, b.n_rows, k, E, A, P, c->max_mpad, c->max_tiles,
                          c->fetched_mask, cfg.x_dtype, c->wk, d, split ? c->n_cu : 0,
-                         2 * I / kBf16TileN, c->d_err, s));
+                         2 * I / kBf16TileN, var, c->d_err, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[0], s));
 
   BlobTable bt{c->w_res, c->fetch_buf, c->L.bytes, c->fetched_mask};
@@ -289,15 +291,15 @@ int launch_pending(cep_ctx *c) {
     HIPCHK(c, hipEventRecord(c->ev_routed[slot], s));
     HIPCHK(c, hipStreamWaitEvent(h, c->ev_routed[slot], 0));
     HIPCHK(c, hipStreamWaitEvent(h, c->ev_fetch_ready, 0));
-    HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->wk, d, I,
+    HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
                            gather, b.row0, k, h));
-    HIPCHK(c, launch_gemm2(sc, 1, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->wk, d, I, h));
+    HIPCHK(c, launch_gemm2(sc, 1, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I, h));
     HIPCHK(c, hipEventRecord(c->ev_helper[slot], h));
   }
-  HIPCHK(c, launch_gemm1(sc, 0, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->wk, d, I,
+  HIPCHK(c, launch_gemm1(sc, 0, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
                          gather, b.row0, k, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[1], s));
-  HIPCHK(c, launch_gemm2(sc, 0, c->max_tiles, tiles, split_tiles, A, bt, c->L, c->wk, d, I, s));
+  HIPCHK(c, launch_gemm2(sc, 0, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[2], s));
   if (b.helper) HIPCHK(c, hipStreamWaitEvent(s, c->ev_helper[slot], 0));
   HIPCHK(c, launch_combine(c->arena, sc, b.row0, b.n_rows, k, d, c->out, s));

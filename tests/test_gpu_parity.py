@@ -210,6 +210,39 @@ def test_large_and_small_m_tiles_agree_bitwise():
     U.compare(wl, a, U.reference(wl))
 
 
+def test_var_tiles_agree_bitwise():
+    # 64-row bf16 batches with at least 64 pairs per local expert run both
+    # GEMMs in 128-row tiles, an expert's last tile a 64-row half when at
+    # most 64 rows remain: a hot expert spans several tiles and ends in a
+    # half tile.  Same K order as the wait-all batch's 256-row tiles and the
+    # per-chunk batches' 64-row tiles, so the same bits.
+    wl = W.generate("zipf_imbalanced_d7168", 6, d=1024, I=512, R=8, T=4096, cpr=4)
+    E, k = wl.cfg["E"], wl.cfg["k"]
+    run = harness.Runner(wl, n_streams=2, record_routing=True)
+    run.run(policy=cep.CEP_WAIT_ALL)
+    a = _out(run)
+    assert cep.cep_get_batch_routing(run.ctx, 0, E, k)["align"] == 256
+    small = var_multi_half = 0
+    for pol, theta in ((cep.CEP_PER_CHUNK, 1), (cep.CEP_THRESHOLD, 300),
+                       (cep.CEP_THRESHOLD, 600), (cep.CEP_THRESHOLD, 1200)):
+        run.out.zero_()
+        run.run(policy=pol, theta=theta, n_streams=2)
+        b = _out(run)
+        assert np.array_equal(a, b), theta
+        for i in range(cep.cep_get_batch_count(run.ctx)):
+            m = cep.cep_get_batch_routing(run.ctx, i, E, k)
+            if m["align"] != 64:
+                continue
+            c = m["cnt"]
+            if c.sum() < 64 * E:
+                small += 1
+            else:
+                var_multi_half += int(((c > 128) & (c % 128 > 0) & (c % 128 <= 64)).any())
+    run.close()
+    assert small > 0 and var_multi_half > 0, (small, var_multi_half)
+    U.compare(wl, a, U.reference(wl))
+
+
 def test_remainder_tiles_agree_bitwise():
     # Full-size wait-all batch: two experts overflow 4 full 256-row tiles by a
     # few rows, which the tile plan runs as 64-row remainder tiles next to the
