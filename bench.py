@@ -32,7 +32,7 @@ METRIC = "routed-expert FFN TFLOP/s (% MFMA peak) + time-to-last-chunk-done, 1 G
 # block-scaled MFMA, which issues at the fp8 rate when either operand is e4m3.
 PEAK = {"bf16": 2500.0, "fp8": 5000.0, "mxfp4": 5000.0}
 HBM_PEAK_GBS = 8000.0
-# Measured HBM traffic of the dominant kernel (GEMM1) per layer: rocprofv3
+# Measured HBM traffic of the dominant kernel (GEMM1) per batch: rocprofv3
 # FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0 KiB (factors from a 1 GiB copy), keyed
 # by workload, valid only while the GEMM sources hash to the recorded sha1
 # prefix (the report is null once the kernel changes).
@@ -40,10 +40,10 @@ GEMM_SOURCES = {
     "bf16": ["paper_2609_33252_amd/csrc/gemm_bf16.hip", "paper_2609_33252_amd/csrc/gemm_common.h"],
     "mxfp4": ["paper_2609_33252_amd/csrc/gemm_mx.hip", "paper_2609_33252_amd/csrc/gemm_common.h"],
 }
-TRAFFIC_BYTES = {  # workload -> (GEMM family, sha1 prefix of its sources, bytes per layer)
-    "sync_d4096": ("bf16", "c7f4698b9115", 504377329),
-    "zipf_imbalanced_d7168/per_chunk": ("bf16", "c7f4698b9115", 473926251),
-    "mxfp4_dsv4flash_d4096": ("mxfp4", "f45c983fceec", 1372612937),
+TRAFFIC_BYTES = {  # workload -> (GEMM family, sha1 prefix of its sources, bytes per batch)
+    "sync_d4096": ("bf16", "d9670eec4ffb", 504327155),
+    "zipf_imbalanced_d7168/per_chunk": ("bf16", "d9670eec4ffb", 473940796),
+    "mxfp4_dsv4flash_d4096": ("mxfp4", "19441607a333", 1374603549),
 }
 
 
