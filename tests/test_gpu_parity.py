@@ -243,6 +243,28 @@ def test_var_tiles_agree_bitwise():
     U.compare(wl, a, U.reference(wl))
 
 
+def test_var_tiles_packed_rows_agree_bitwise():
+    # f32 rows are packed to bf16, so GEMM1 reads the packed copy: the
+    # wait-all batch (1536 pairs, 180-212 rows per expert: a 128-row tile,
+    # then a half or a second full tile) runs the 128-row tiles, single
+    # chunks (384 pairs) the 64-row tiles
+    wl = W.generate("tiny", 1, R=2, T=384)
+    E, k = wl.cfg["E"], wl.cfg["k"]
+    assert 64 * E <= wl.n_pairs < 256 * E
+    assert max(wl.chunk_pairs(c) for c in wl.chunks) < 64 * E
+    run = harness.Runner(wl, n_streams=2, record_routing=True)
+    run.run(policy=cep.CEP_WAIT_ALL)
+    a = _out(run)
+    c = cep.cep_get_batch_routing(run.ctx, 0, E, k)["cnt"]
+    assert (c > 128).all() and (c % 128 <= 64).any() and (c % 128 > 64).any(), c
+    run.out.zero_()
+    run.run(policy=cep.CEP_PER_CHUNK, n_streams=2)
+    b = _out(run)
+    run.close()
+    assert np.array_equal(a, b)
+    U.compare(wl, a, U.reference(wl))
+
+
 def test_remainder_tiles_agree_bitwise():
     # Full-size wait-all batch: two experts overflow 4 full 256-row tiles by a
     # few rows, which the tile plan runs as 64-row remainder tiles next to the
