@@ -20,8 +20,11 @@ constexpr int kFp8LargeTileM = 256;  // e4m3 tile for large batches (8 waves)
 constexpr int kRouteThreads = 256;   // threads per routing block
 constexpr int kRoutePairs = 2048;    // flat pairs per routing block (8 rounds of 256)
 constexpr int kInterleave = 32;           // gate/up column interleave of the packed W1
-constexpr int kFusedRoutePairs = 1 << 15;  // batches up to this many flat (row, slot)
-                                           // entries route in one block (ids in LDS)
+// batches up to this many flat (row, slot) entries route in one block (ids
+// in LDS); beyond it the three-kernel path is faster (one block's scatter
+// grows with the entries, the other path's cost is mostly its launches:
+// equal at ~24 K entries with 8 experts, 11 us faster at ~30 K with 32)
+constexpr int kFusedRoutePairs = 1 << 14;
 constexpr int kMxBlock = 32;               // MX scale block along K
 
 // Expert weight format of a context (from cep_config.w_dtype).
