@@ -258,21 +258,35 @@ def calibrate_theta(args):
     def prefix_for(target):
         return next(m for m, v in enumerate(cum) if v >= target)
 
-    counts, tput = [], []
-    target = 16
+    # profiled prefixes: N ~ 16 x 2^(j/2) up to all pairs, plus the last
+    # prefix below and the first at or above each count where the library
+    # changes its row tile (64 and 256 rows per local expert on average), so
+    # that the piecewise-linear profile does not cut across those steps
+    picks = set()
+    target = 16.0
     while True:
-        m = prefix_for(min(target, tot))
-        if not counts or cum[m] > counts[-1]:
-            ms = measure(m)
-            counts.append(cum[m])
-            tput.append(cum[m] / ms)
-            print(json.dumps({"profile_n": cum[m], "ms": round(ms, 5),
-                              "pairs_per_ms": round(cum[m] / ms, 2),
-                              "tflops": round(6.0 * c["d"] * c["I"] * cum[m] / ms / 1e9, 2)}),
-                  flush=True)
+        picks.add(prefix_for(min(int(target), tot)))
         if target >= tot:
             break
-        target *= 2
+        target *= 2 ** 0.5
+    for per_expert in (64, 256):
+        step = per_expert * c["E"]
+        if step <= tot:
+            m_at = prefix_for(step)
+            picks.add(m_at)
+            if m_at > 0:
+                picks.add(m_at - 1)
+    counts, tput = [], []
+    for m in sorted(picks):
+        if counts and cum[m] <= counts[-1]:
+            continue
+        ms = measure(m)
+        counts.append(cum[m])
+        tput.append(cum[m] / ms)
+        print(json.dumps({"profile_n": cum[m], "ms": round(ms, 5),
+                          "pairs_per_ms": round(cum[m] / ms, 2),
+                          "tflops": round(6.0 * c["d"] * c["I"] * cum[m] / ms / 1e9, 2)}),
+              flush=True)
     prof = cep.FfnProfile(counts, tput)
     blob_bytes = run.blob_bytes
     # held-out counts (geometric midpoints): model F(N) against measurement
