@@ -15,8 +15,8 @@ constexpr int kMaxTopK = 16;
 constexpr int kMaxDim = 32768;  // largest d_model and d_ff (fp8 GEMM keeps K/128 weight scales per row in LDS)
 constexpr int kBf16TileM = 256;      // bf16 grouped GEMM tile
 constexpr int kBf16TileN = 256;
-constexpr int kFp8TileM = 128;       // e4m3 grouped GEMM tile (4 waves)
-constexpr int kFp8LargeTileM = 256;  // e4m3 tile for large batches (8 waves)
+constexpr int kFp8TileM = 128;       // e4m3 / MXFP4 grouped GEMM tile (4 waves)
+constexpr int kFp8LargeTileM = 256;  // e4m3 / MXFP4 tile for large batches (8 waves)
 constexpr int kRouteThreads = 256;   // threads per routing block
 constexpr int kRoutePairs = 2048;    // flat pairs per routing block (8 rounds of 256)
 constexpr int kInterleave = 32;           // gate/up column interleave of the packed W1
@@ -155,6 +155,7 @@ struct Scratch {
   int32_t *off_pad;    // [E+1]
   Tile *tiles;         // [4][max_tiles]: list 2*f + r for resident (f = 0) or
                        // fetched (f = 1) experts; r = 1: 64-row remainder tiles
+                       // (256-row batches) or 128-row tiles (batch_var_tiles)
   int32_t *n_tiles;    // [4]
   int32_t *pos_of;     // [max_rows * k] grouped row of each flat pair or -1
   int32_t *perm;       // [max_mpad] flat pair of each grouped row or -1
