@@ -3,10 +3,14 @@
 * routing metadata and batch composition: bit-exact, every config
 * outputs: elementwise tolerance (bf16, f32 inputs) or relative RMS (fp8),
   at reduced token counts over all rows and at full size on sampled tokens
-* closed forms on the GPU: identity-permutation expert, zero expert
+* closed forms on the GPU: identity-permutation expert, zero expert;
+  exact linearity in the coefficients and the down weights; one-hot
+  coefficients equal routing to that slot alone
 * invariance: chunking, submission order, policy and stream count do not
   change the output (bitwise); a fetched expert equals a resident one
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -172,6 +176,46 @@ def test_zero_down_weights_give_exact_zero():
 
 
 # ------------------------------------------------------------ invariance
+def _run_threshold(wl):
+    run = harness.Runner(wl, n_streams=2)
+    run.run(policy=cep.CEP_THRESHOLD, theta=max(1, wl.n_pairs // 3), n_streams=2)
+    got = _out(run)
+    run.close()
+    return got
+
+
+def test_linearity_in_coefficients_and_down_weights_bitwise():
+    # doubling every routing coefficient, or the down weights, doubles the
+    # output exactly: a factor of two commutes with every rounding on the
+    # path (bf16 products, f32 sums, the bf16 output rows, the f32 combine)
+    wl = W.generate("zipf_stream_d7168", 2, d=1024, I=512, T=512, cpr=4)
+    a = _run_threshold(wl)
+    assert np.abs(a).max() > 0
+    b = _run_threshold(dataclasses.replace(wl, topk_w=wl.topk_w * 2))
+    assert np.array_equal(b, 2 * a)
+    c = _run_threshold(dataclasses.replace(wl, w_down=wl.w_down * 2))
+    assert np.array_equal(c, 2 * a)
+
+
+def test_one_hot_coefficients_equal_dropped_slots_bitwise():
+    # coefficients one-hot on each token's first local slot give the bits of
+    # routing the token to that slot alone: the other slots add exact zeros
+    wl = W.generate("zipf_stream_d7168", 3, d=1024, I=512, T=512, cpr=4)
+    ids = wl.topk_local
+    local = ids >= 0
+    first = np.argmax(local, axis=2)
+    one = np.zeros_like(wl.topk_w)
+    np.put_along_axis(one, first[..., None], 1.0, axis=2)
+    one[~local] = 0.0
+    only = np.where(one > 0, ids, -1).astype(ids.dtype)
+    a = _run_threshold(dataclasses.replace(wl, topk_w=one))
+    wl_b = dataclasses.replace(wl, topk_local=only, topk_w=one)
+    b = _run_threshold(wl_b)
+    assert wl_b.n_pairs < wl.n_pairs
+    assert np.array_equal(a, b)
+    U.compare(wl_b, b, U.reference(wl_b))
+
+
 def test_chunking_order_policy_streams_invariance_bitwise():
     wl = W.generate("zipf_imbalanced_d7168", 0, T=512, cpr=8)
     run = harness.Runner(wl, n_streams=4)
