@@ -20,6 +20,14 @@ constexpr int kFp8LargeTileM = 256;  // e4m3 / MXFP4 tile for large batches (8 w
 constexpr int kRouteThreads = 256;   // threads per routing block
 constexpr int kRoutePairs = 2048;    // flat pairs per routing block (8 rounds of 256)
 constexpr int kInterleave = 32;           // gate/up column interleave of the packed W1
+// Packed bf16 weights ([N][K], K contiguous per output column n) are stored
+// in 1 KB blocks of 16 columns x 32 K: block (n/16, k/32) at element
+// ((n/16)*(K/32) + k/32)*512, column n%16 at 32 elements, k%32 within it.  A
+// GEMM's 1 KB direct-to-LDS load then reads one contiguous block (or two
+// 512-byte halves) instead of sixteen 64-byte pieces K*2 bytes apart.
+__host__ __device__ inline size_t bf16_block_index(int n, int k, int K) {
+  return ((size_t)(n >> 4) * (K >> 5) + (k >> 5)) * 512 + (n & 15) * 32 + (k & 31);
+}
 // batches up to this many flat (row, slot) entries route in one block (ids
 // in LDS); beyond it the three-kernel path is faster (one block's scatter
 // grows with the entries, the other path's cost is mostly its launches:

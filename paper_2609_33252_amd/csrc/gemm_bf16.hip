@@ -38,7 +38,8 @@ namespace {
 // rows read at one chunk (what one LDS cycle serves of an MFMA operand read)
 // cover all sixteen 16-byte slots of a 256-byte bank window.  A load
 // instruction fills 64 consecutive slots, so each lane fetches the global
-// chunk that belongs in its slot.
+// chunk that belongs in its slot; weight chunks come from the 1 KB blocks of
+// the packed layout, so one load reads one block (BK 32) or two halves.
 //
 // Two schedules.  PIPE (MFMA-bound tile): each 16-wide sub-step multiplies
 // fragments read during the previous sub-step, so LDS latency hides behind
@@ -72,7 +73,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
   const int wm = wid / WGN, wn = wid % WGN;
   const int K = g.K, nk = K / BK;
   const char *Ag = GATHER ? nullptr : (const char *)(g.A + (size_t)t.row0 * K * 2);
-  const char *Bg = (const char *)(blob_of(g.bt, t.expert) + g.b_off + (size_t)nt * BN * K * 2);
+  const char *Bg = (const char *)(blob_of(g.bt, t.expert) + g.b_off);
 
   __shared__ u32x4 sA[AS][BM * CH];
   __shared__ u32x4 sB[STAGES][BN * CH];
@@ -85,6 +86,13 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
 #define CEP_LANE_OFF(seg)                                                           \
   ((uint32_t)((seg) * RPS + seg_row) * K * 2 +                                      \
    (uint32_t)(((lane % CH) ^ ((((seg) * RPS + seg_row) >> SH) & (CH - 1))) * 16))
+  // B (packed weights, bf16_block_index layout): the byte offset of the
+  // lane's chunk of segment seg in K step 0; step kt adds kt * BK/32 blocks.
+  auto b_lane_off = [&](int seg) -> size_t {
+    const int tr = seg * RPS + seg_row, n = nt * BN + tr;
+    const int kc = ((lane % CH) ^ ((tr >> SH) & (CH - 1))) * 8;  // K element of the chunk
+    return bf16_block_index(n, kc, K) * 2;
+  };
   // GATHER: each lane's A rows are fixed for the whole K loop, so their
   // input-row addresses (plus the lane's chunk) are looked up once.  NAL_
   // (the A loads per wave in the current schedule) is defined in each scope
@@ -113,7 +121,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
     const int buf_ = (kt) % STAGES;                                                 \
     _Pragma("unroll") for (int i = 0; i < B_LD; ++i) {                              \
       const int seg = wid * B_LD + i;                                               \
-      dma16(Bg + (size_t)(kt) * BK * 2 + CEP_LANE_OFF(seg),                         \
+      dma16(Bg + b_lane_off(seg) + (size_t)(kt) * (BK / 32) * 1024,                 \
             __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf_][seg * 64])));       \
     }                                                                               \
   }
