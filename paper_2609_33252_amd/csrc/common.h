@@ -65,9 +65,10 @@ __host__ __device__ inline const uint8_t *blob_of(const BlobTable &t, int e) {
 }
 
 // Packed blob layout of one expert (byte offsets from the blob start).
-//   bf16: W1p [2I][d] bf16 (K contiguous), W2p [d][I] bf16
+//   bf16: W1p [2I][d] bf16, W2p [d][I] bf16, in bf16_block_index order
 //   fp8 : W1p [2I][d] u8, W2p [d][I] u8, S1 [2I/32][d/128] f32, S2 [d/128][I/128] f32
-//   mx  : W1p [2I][d/2], W2p [d][I/2] packed e2m1 (even K in the low nibble),
+//   mx  : W1p [2I][d/2], W2p [d][I/2] packed e2m1 (even K in the low nibble)
+//         in mx_block_index order,
 //         S1, S2: E8M0 bytes in mx_weight_scale_offset order (N = 2I or d)
 // Row n' of W1p holds column j = (n'/64)*32 + n'%32 of the gate weights when
 // (n'/32) is even and of the up weights when it is odd, so that one 64-row
@@ -141,6 +142,14 @@ __host__ __device__ inline size_t mx_row_scale_offset(int R, int b, int s_ld) {
 // 256): for each 256-column tile and K step of 128 one 1 KB record holding,
 // for the wave of column group wn (64 columns), the lane of K block g and
 // column n16, the scales of its four 16-column fragments j as one word.
+// Packed e2m1 weights ([N][K/2] bytes, row_bytes = K/2 per output column n)
+// are stored in 1 KB blocks of 16 columns x 64 bytes (128 K), so that one
+// 1 KB direct-to-LDS load of a 128-wide K step reads one contiguous block:
+// byte k of column n at ((n/16)*(row_bytes/64) + k/64)*1024 + (n%16)*64 + k%64.
+__host__ __device__ inline size_t mx_block_index(int n, int k, int row_bytes) {
+  return ((size_t)(n >> 4) * (row_bytes >> 6) + (k >> 6)) * 1024 + (n & 15) * 64 + (k & 63);
+}
+
 __host__ __device__ inline size_t mx_weight_scale_offset(int n, int b, int K) {
   const int nt = n >> 8, wn = (n >> 6) & 3, j = (n >> 4) & 3, n16 = n & 15;
   return ((size_t)nt * (K >> 7) + (b >> 2)) * 1024 + ((wn * 4 + (b & 3)) * 16 + n16) * 4 + j;

@@ -76,7 +76,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_mx(GemmArgs g) {
   const int K = g.K, nkb = K / BK, KB = K / 2;  // KB: bytes of one packed weight row
   const uint8_t *blob = blob_of(g.bt, t.expert);
   const char *Ag = (const char *)(g.A + (size_t)t.row0 * K);
-  const char *Bg = (const char *)(blob + g.b_off + (size_t)nt * BN * KB);
+  const char *Bg = (const char *)(blob + g.b_off);  // mx_block_index layout
   // row scales of K step kb: 512 bytes per 128-row group, groups contiguous
   const char *Asg = (const char *)g.As + (size_t)(t.row0 >> 7) * 512;
   const size_t as_step = (size_t)(g.s_ld >> 7) * 512;
@@ -98,7 +98,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_mx(GemmArgs g) {
     }                                                                               \
     _Pragma("unroll") for (int i = 0; i < B_LD; ++i) {                              \
       const int seg = wid * B_LD + i, r = seg * 16 + b_row;                         \
-      dma16(Bg + (size_t)(kb) * (BK / 2) + (size_t)r * KB + (((lane & 3) ^ bsw_of(r)) * 16), \
+      dma16(Bg + mx_block_index(nt * BN + r, (kb) * (BK / 2) + ((lane & 3) ^ bsw_of(r)) * 16, KB), \
             __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf_][seg * 64])));       \
     }                                                                               \
     if (wid == 0 && lane < BM / 4)                                                  \

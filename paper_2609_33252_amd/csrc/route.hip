@@ -613,14 +613,20 @@ __global__ void k_pack_scales(const float *sg, const float *su, const float *sd,
 // MXFP4 experts.  W1p row n' is row (n'/64)*32 + n'%32 of the gate
 // (n'/32 even) or up (odd) codes [I][d/2]: the caller's layout is already K
 // packed, so packing is a row gather, one block per row.
-__global__ __launch_bounds__(256) void k_pack_mx_w1(const uint8_t *wg, const uint8_t *wu,
-                                                    int row_bytes, uint8_t *dst) {
+// Row n of packed e2m1 weights into mx_block_index order; interleave (W1p):
+// row n is gathered from gate (wg) or up (wu) like the bf16 W1p, otherwise
+// (W2p) it is row n of wg.
+__global__ __launch_bounds__(256) void k_pack_mx_rows(const uint8_t *wg, const uint8_t *wu,
+                                                      int row_bytes, int interleave,
+                                                      uint8_t *dst) {
   const int n = blockIdx.x;
-  const uint8_t *src = (((n / kInterleave) & 1) ? wu : wg) +
-                       (size_t)((n / (2 * kInterleave)) * kInterleave + n % kInterleave) * row_bytes;
+  const uint8_t *src =
+      interleave ? (((n / kInterleave) & 1) ? wu : wg) +
+                       (size_t)((n / (2 * kInterleave)) * kInterleave + n % kInterleave) * row_bytes
+                 : wg + (size_t)n * row_bytes;
   const uint4 *s4 = (const uint4 *)src;
-  uint4 *d4 = (uint4 *)(dst + (size_t)n * row_bytes);
-  for (int c = threadIdx.x; c < row_bytes / 16; c += blockDim.x) d4[c] = s4[c];
+  for (int c = threadIdx.x; c < row_bytes / 16; c += blockDim.x)
+    *(uint4 *)(dst + mx_block_index(n, c * 16, row_bytes)) = s4[c];
 }
 
 // E8M0 scales [N][K/32] (row n of B) into mx_weight_scale_offset order;
@@ -648,10 +654,11 @@ __global__ void k_pack_mx_scales(const uint8_t *sa, const uint8_t *sb, int N, in
 hipError_t launch_pack_mx(const uint8_t *wg, const uint8_t *wu, const uint8_t *wd,
                           const uint8_t *sg, const uint8_t *su, const uint8_t *sd, int d, int I,
                           uint8_t *blob, const BlobLayout &L, hipStream_t s) {
-  hipLaunchKernelGGL(k_pack_mx_w1, dim3(2 * I), dim3(256), 0, s, wg, wu, d / 2, blob + L.w1_off);
+  hipLaunchKernelGGL(k_pack_mx_rows, dim3(2 * I), dim3(256), 0, s, wg, wu, d / 2, 1,
+                     blob + L.w1_off);
+  hipLaunchKernelGGL(k_pack_mx_rows, dim3(d), dim3(256), 0, s, wd, (const uint8_t *)nullptr, I / 2,
+                     0, blob + L.w2_off);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  e = hipMemcpyAsync(blob + L.w2_off, wd, (size_t)d * I / 2, hipMemcpyDeviceToDevice, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_pack_mx_scales, dim3(256), dim3(256), 0, s, sg, su, 2 * I, d, 1,
                      blob + L.s1_off);
