@@ -66,8 +66,7 @@ __host__ __device__ inline const uint8_t *blob_of(const BlobTable &t, int e) {
 
 // Packed blob layout of one expert (byte offsets from the blob start).
 //   bf16: W1p [2I][d] bf16, W2p [d][I] bf16, in bf16_block_index order
-//   fp8 : W1p [2I][d] u8, W2p [d][I] u8 in fp8_block_index order,
-//         S1 [2I/32][d/128] f32, S2 [d/128][I/128] f32
+//   fp8 : W1p [2I][d] u8, W2p [d][I] u8, S1 [2I/32][d/128] f32, S2 [d/128][I/128] f32
 //   mx  : W1p [2I][d/2], W2p [d][I/2] packed e2m1 (even K in the low nibble)
 //         in mx_block_index order,
 //         S1, S2: E8M0 bytes in mx_weight_scale_offset order (N = 2I or d)
@@ -143,12 +142,6 @@ __host__ __device__ inline size_t mx_row_scale_offset(int R, int b, int s_ld) {
 // 256): for each 256-column tile and K step of 128 one 1 KB record holding,
 // for the wave of column group wn (64 columns), the lane of K block g and
 // column n16, the scales of its four 16-column fragments j as one word.
-// Packed e4m3 weights ([N][K] bytes) are stored in 1 KB blocks of 8 columns
-// x 128 K, one block per 1 KB load of the e4m3 GEMM's 128-wide K step.
-__host__ __device__ inline size_t fp8_block_index(int n, int k, int K) {
-  return ((size_t)(n >> 3) * (K >> 7) + (k >> 7)) * 1024 + (n & 7) * 128 + (k & 127);
-}
-
 // Packed e2m1 weights ([N][K/2] bytes, row_bytes = K/2 per output column n)
 // are stored in 1 KB blocks of 16 columns x 64 bytes (128 K), so that one
 // 1 KB direct-to-LDS load of a 128-wide K step reads one contiguous block:

@@ -51,7 +51,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_fp8(GemmArgs g) {
   const int K = g.K, nkb = K / BK;
   const uint8_t *blob = blob_of(g.bt, t.expert);
   const char *Ag = (const char *)(g.A + (size_t)t.row0 * K);
-  const char *Bg = (const char *)(blob + g.b_off);  // fp8_block_index layout
+  const char *Bg = (const char *)(blob + g.b_off + (size_t)nt * BN * K);
   const char *Asg = (const char *)(g.As + t.row0);  // k-block kb at + kb * s_ld floats
   const float *Bs = (const float *)(blob + g.bs_off);
 
@@ -76,8 +76,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_fp8(GemmArgs g) {
     }                                                                              \
     _Pragma("unroll") for (int i = 0; i < B_LD; ++i) {                             \
       const int seg = wid * B_LD + i;                                              \
-      dma16(Bg + ((size_t)(nt * (BN / 8) + seg) * (K / BK) + (kb)) * 1024 +           \
-                (uint32_t)(seg_row * 128 + ((lane & 7) ^ ((((seg) * 8 + seg_row) >> 1) & 7)) * 16), \
+      dma16(Bg + (size_t)(kb) * BK + CEP_F8_OFF(seg),                              \
             __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf_][seg * 64])));      \
     }                                                                              \
     if (wid == 0 && lane < BM / 4)                                                 \

@@ -562,8 +562,8 @@ __global__ __launch_bounds__(256) void k_combine(Arena a, Scratch sc, int row0, 
 // ------------------------------------------------------- weight packing
 // out[map(c)][r] = in[r][c] for a [rows][cols] matrix, 64x64 tiles via LDS.
 // MAP 0: identity; MAP 1: gate half of the W1 interleave; MAP 2: up half.
-// The output is stored blocked: bf16 in bf16_block_index order (1 KB blocks
-// of 16 columns x 32 K), e4m3 in fp8_block_index order (8 columns x 128 K).
+// e4m3 outputs are row-major [cols][rows]; bf16 outputs are stored in the
+// blocked layout of bf16_block_index (1 KB blocks of 16 rows x 32 K).
 template <typename TI, typename TO, int MAP>
 __global__ __launch_bounds__(256) void k_transpose(const TI *__restrict__ in, TO *__restrict__ out,
                                                    int rows, int cols) {
@@ -584,7 +584,7 @@ __global__ __launch_bounds__(256) void k_transpose(const TI *__restrict__ in, TO
       if constexpr (std::is_same<TO, __bf16>::value)
         out[bf16_block_index(oc, r, rows)] = tile[tx][j];
       else
-        out[fp8_block_index(oc, r, rows)] = tile[tx][j];
+        out[(size_t)oc * rows + r] = tile[tx][j];
     }
   }
 }
