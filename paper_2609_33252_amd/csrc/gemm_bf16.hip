@@ -25,9 +25,22 @@
 #include "gemm_common.h"
 
 #include <type_traits>
+#include <utility>
 
 namespace cep {
 namespace {
+
+template <int V>
+using ic = std::integral_constant<int, V>;
+template <class F, int... I>
+__device__ inline void static_for_impl(F &&f, std::integer_sequence<int, I...>) {
+  (f(ic<I>{}), ...);
+}
+// f(ic<0>{}), ..., f(ic<N-1>{}): indices that stay compile-time constants
+template <int N, class F>
+__device__ inline void static_for(F &&f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 // BM x BN output tile, NW waves as WGM x (NW/WGM), each wave owning a
 // (BM/WGM) x (BN/(NW/WGM)) block of 32x32 MFMA fragments (for SwiGLU a
@@ -167,36 +180,111 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
     wait_stages<PER, STAGES - 2>(min(nk - 1, STAGES - 2));
     __builtin_amdgcn_s_barrier();
 
-    // The last sub-step of step kt first waits for stage kt+1, issues the
-    // loads of stage kt+STAGES-1 and reads the first fragments of kt+1.
+    // Every step issues one stage of loads, so the vmcnt waits are constants
+    // and the loop body is one basic block: steps past the end reload the
+    // last K step into a buffer nobody reads again.  Sub-steps 0 .. KK-2 of
+    // step kt read the fragments of the next sub-step, then multiply the
+    // current ones.  The last sub-step multiplies while it waits for stage
+    // kt+1, passes the barrier, reads the first fragments of kt+1 and issues
+    // the loads of stage kt+STAGES-1: those instructions sit between its
+    // MFMAs, so the matrix pipe always has the next MFMA queued, and the
+    // LDS-read wait before an MFMA never counts the reads issued after it.
     bf16x8 fa[2][FM], fb[2][FN];
-    CEP_LOAD_FRAG(fa[0], fb[0], 0, 0, 0, FM);
-    for (int kt = 0; kt < nk; ++kt) {
-      const int cur = kt % STAGES;
+    constexpr int NM = FM * FN;   // MFMAs per sub-step
+    constexpr int NR = FM + FN;   // fragment reads per sub-step
+    constexpr int PL = (KK - 1) & 1, QL = PL ^ 1;
+    static_assert(NM >= 2 + PER + NR / 2 && NR % 2 == 0,
+                  "enough MFMAs to spread the last sub-step over");
+    auto mfma_one = [&](auto p_c, auto idx_c) {
+      constexpr int p = decltype(p_c)::value, idx = decltype(idx_c)::value;
+      constexpr int i = idx / FN, j = idx % FN;
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[p][i], fb[p][j], acc[i][j], 0, 0, 0);
+    };
+    auto read_one = [&](auto q_c, int buf, auto idx_c) {
+      constexpr int q = decltype(q_c)::value, idx = decltype(idx_c)::value;
+      const int slot = (lane >> 5) ^ rsw;  // K sub-step 0
+      if constexpr (idx < FM)
+        fa[q][idx] = __builtin_bit_cast(bf16x8, sA[buf][(frow(idx) + (lane & 31)) * CH + slot]);
+      else
+        fb[q][idx - FM] = __builtin_bit_cast(
+            bf16x8, sB[buf][(wn * WN + (idx - FM) * 32 + (lane & 31)) * CH + slot]);
+    };
+    // load piece idx of K step ks into LDS buffer buf: idx < A_LD is an A
+    // segment, the rest B segments
+    auto dma_one = [&](int ks, int buf, auto idx_c) {
+      constexpr int idx = decltype(idx_c)::value;
+      if constexpr (idx < A_LD) {
+        const int seg = wid * A_LD + idx;
+        dma16(GATHER ? arow[idx] + (size_t)ks * BK * 2
+                     : Ag + (size_t)ks * BK * 2 + CEP_LANE_OFF(seg),
+              __builtin_amdgcn_readfirstlane(lds_offset(&sA[buf][seg * 64])));
+      } else {
+        const int seg = wid * B_LD + (idx - A_LD);
+        dma16(Bg + b_lane_off(seg) + (size_t)ks * (BK / 32) * 1024,
+              __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf][seg * 64])));
+      }
+    };
+    // sub-steps 0 .. KK-2 of the step in buffer cur
+    auto early_subs = [&](int cur) {
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
+      for (int kk = 0; kk + 1 < KK; ++kk) {
         const int p = kk & 1, q = p ^ 1;
-        if (kk + 1 < KK) {
-          CEP_LOAD_FRAG(fa[q], fb[q], cur, cur, kk + 1, FM);
-        } else if (kt + 1 < nk) {
-          // this thread's loads of stage kt+1 are done when at most the
-          // loads of the stages issued after it (up to kt+STAGES-2) are
-          // outstanding
-          wait_stages<PER, STAGES - 3>(min(nk - 1, kt + STAGES - 2) - (kt + 1));
-          __builtin_amdgcn_s_barrier();
-          if (kt + STAGES - 1 < nk) CEP_DMA_STAGE(kt + STAGES - 1);
-          CEP_LOAD_FRAG(fa[q], fb[q], (kt + 1) % STAGES, (kt + 1) % STAGES, 0, FM);
-        }
+        CEP_LOAD_FRAG(fa[q], fb[q], cur, cur, kk + 1, FM);
         __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-          for (int j = 0; j < FN; ++j)
-            acc[i][j] =
-                __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[p][i], fb[p][j], acc[i][j], 0, 0, 0);
+        static_for<NM>([&](auto m) {
+          if (p == 0) mfma_one(ic<0>{}, m); else mfma_one(ic<1>{}, m);
+        });
         __builtin_amdgcn_sched_barrier(0);
       }
+    };
+
+    static_for<STAGES - 1>([&](auto st) {
+      constexpr int S = decltype(st)::value;
+      static_for<PER>([&](auto d) { dma_one(min(S, nk - 1), S, d); });
+    });
+    // stage 0 landed when at most the later prologue stages are outstanding
+    wait_vmcnt<(STAGES - 2) * PER>();
+    __builtin_amdgcn_s_barrier();
+    CEP_LOAD_FRAG(fa[0], fb[0], 0, 0, 0, FM);
+    for (int kt = 0; kt + 1 < nk; ++kt) {
+      const int cur = kt % STAGES, nxt = (kt + 1) % STAGES;
+      const int ks = min(kt + STAGES - 1, nk - 1), kbuf = (kt + STAGES - 1) % STAGES;
+      early_subs(cur);
+      mfma_one(ic<PL>{}, ic<0>{});
+      __builtin_amdgcn_sched_barrier(0);
+      // this thread's loads of stage kt+1 are done when at most the
+      // STAGES-3 stages issued after it are outstanding
+      wait_vmcnt<(STAGES - 3) * PER>();
+      mfma_one(ic<PL>{}, ic<1>{});
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_barrier();  // stage kt+1 landed; step kt-1's buffer free
+      __builtin_amdgcn_sched_barrier(0);
+      // the next step's first fragments first: the four waves' reads queue
+      // on the LDS together, and the most MFMAs of this sub-step cover them
+      static_for<NR / 2>([&](auto r) {
+        constexpr int R = decltype(r)::value;
+        mfma_one(ic<PL>{}, ic<2 + R>{});
+        __builtin_amdgcn_sched_barrier(0);
+        read_one(ic<QL>{}, nxt, ic<2 * R>{});
+        read_one(ic<QL>{}, nxt, ic<2 * R + 1>{});
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      constexpr int M1 = 2 + NR / 2;
+      static_for<PER>([&](auto d) {
+        mfma_one(ic<PL>{}, ic<M1 + decltype(d)::value>{});
+        __builtin_amdgcn_sched_barrier(0);
+        dma_one(ks, kbuf, d);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      static_for<NM - M1 - PER>(
+          [&](auto m) { mfma_one(ic<PL>{}, ic<M1 + PER + decltype(m)::value>{}); });
+      __builtin_amdgcn_sched_barrier(0);
     }
+    // the last step: no loads, no barrier
+    early_subs((nk - 1) % STAGES);
+    static_for<NM>([&](auto m) { mfma_one(ic<PL>{}, m); });
+    // the tail's reloads must land before the workgroup's LDS is released
+    wait_vmcnt<0>();
   } else {
     // NFA A fragments per wave and NAL_ A loads per wave and step (all of
     // them, or for a VAR half tile those of its first BM/2 rows); every wave
@@ -279,6 +367,62 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
 
   // 32x32 accumulator layout: lane l, element r -> column l%32,
   // row 8*(r/4) + 4*(l/32) + r%4.
+  if constexpr (PIPE) {
+    // The output tile goes through LDS: each wave writes its bf16 results
+    // into the (now idle) operand ring, rows of wave row 0 in sA and of wave
+    // row 1 in sB, then the workgroup writes whole rows with 16-byte stores
+    // (a store instruction covers two to four full rows instead of 64
+    // two-byte pieces).  Chunk c of a staged row r sits at c ^ (4 * ((r/4) % 4)),
+    // so the two half-waves of one element write (rows r and r+4) use
+    // different banks.
+    static_assert(WGM == 2 && !VAR, "staged epilogue: two wave rows");
+    constexpr int CB = SWIGLU ? BN / 2 : BN;  // output columns of the tile
+    constexpr int CPR = CB / 8;               // 16-byte chunks per output row
+    constexpr int WCB = SWIGLU ? WN / 2 : WN; // output columns of one wave
+    static_assert(WM * CB * 2 <= (int)sizeof(sA) && WM * CB * 2 <= (int)sizeof(sB),
+                  "a wave row's outputs fit one operand ring");
+    static_assert(CPR % 4 == 0 && CPR >= 16, "swizzle stays inside the row");
+    // every wave's tail loads landed (wait_vmcnt<0> above) and its last
+    // operand reads completed: the ring is free
+    __syncthreads();
+    __bf16 *st = (__bf16 *)(wm == 0 ? (void *)&sA[0][0] : (void *)&sB[0][0]);
+    auto soff = [](int r, int c) {
+      return r * CB + ((((c >> 3) ^ (((r >> 2) & 3) << 2))) << 3) + (c & 7);
+    };
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int lr = i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (SWIGLU) {
+          // fragment pairs (2*j2, 2*j2+1) are the gate and up columns of h
+          // columns wn*WCB + j2*32 + [0, 32) of the tile
+#pragma unroll
+          for (int j2 = 0; j2 < FN / 2; ++j2)
+            st[soff(lr, wn * WCB + j2 * 32 + (lane & 31))] =
+                (__bf16)silu_mul(acc[i][2 * j2][r], acc[i][2 * j2 + 1][r]);
+        } else {
+          // padding rows read a stale coefficient; they are never stored
+          const float w = g.wrow[(size_t)t.row0 + wm * WM + lr];
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            st[soff(lr, wn * WCB + j * 32 + (lane & 31))] = (__bf16)(acc[i][j][r] * w);
+        }
+      }
+    }
+    __syncthreads();
+    const size_t ldo = SWIGLU ? g.N / 2 : g.N;
+    __bf16 *O = (__bf16 *)g.out + (size_t)t.row0 * ldo + (size_t)nt * CB;
+#pragma unroll 4
+    for (int q = tid; q < BM * CPR; q += 64 * NW) {
+      const int row = q / CPR, c = q % CPR;
+      if (row >= t.rows) break;  // q grows with the row
+      const int lr = row % WM;
+      const u32x4 *src = row < WM ? &sA[0][0] : &sB[0][0];
+      *(u32x4 *)(O + (size_t)row * ldo + c * 8) = src[lr * CPR + (c ^ (((lr >> 2) & 3) << 2))];
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
     if (half && i > 0) break;
