@@ -21,13 +21,19 @@ constexpr int kRouteThreads = 256;   // threads per routing block
 constexpr int kRoutePairs = 2048;    // flat pairs per routing block (8 rounds of 256)
 constexpr int kInterleave = 32;           // gate/up column interleave of the packed W1
 // Packed bf16 weights ([N][K], K contiguous per output column n) are stored
-// in 1 KB blocks of 16 columns x 32 K: block (n/16, k/32) at element
-// ((n/16)*(K/32) + k/32)*512, column n%16 at 32 elements, k%32 within it.  A
-// GEMM's 1 KB direct-to-LDS load then reads one contiguous block (or two
-// 512-byte halves) instead of sixteen 64-byte pieces K*2 bytes apart.
+// in 16 KB blocks of 128 columns x 64 K, block (n/128, k/64) at element
+// ((n/128)*(K/64) + k/64)*8192; inside a block the 32-wide K half
+// (k/32)%2 takes 8 KB, each 16-column group (n/16)%8 of it 1 KB, column
+// n%16 32 elements, k%32 within it.  A weight-streaming workgroup (128
+// columns, 64 K per step) then reads one contiguous 16 KB run per step and
+// a 256-column tile two 8 KB runs (32 K per step); each 1 KB direct-to-LDS
+// load is one contiguous piece.  Requires N % 128 == 0 and K % 64 == 0.
 __host__ __device__ inline size_t bf16_block_index(int n, int k, int K) {
-  return ((size_t)(n >> 4) * (K >> 5) + (k >> 5)) * 512 + (n & 15) * 32 + (k & 31);
+  return ((size_t)(n >> 7) * (K >> 6) + (k >> 6)) * 8192 + ((k >> 5) & 1) * 4096 +
+         ((n >> 4) & 7) * 512 + (n & 15) * 32 + (k & 31);
 }
+// K-step stride of bf16_block_index: K advancing by 32 moves 8 KB
+constexpr int kBf16BlockStepBytes = 8192;
 // batches up to this many flat (row, slot) entries route in one block (ids
 // in LDS); beyond it the three-kernel path is faster (one block's scatter
 // grows with the entries, the other path's cost is mostly its launches:

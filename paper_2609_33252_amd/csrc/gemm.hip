@@ -31,7 +31,7 @@ hipError_t launch_any(const GemmArgs &g, int grid_tiles, int split_tiles, int al
   r.tiles = sc.tiles + (size_t)(2 * which + 1) * list_cap;
   r.n_tiles = sc.n_tiles + 2 * which + 1;
   r.max_tiles = split_tiles;
-  return launch_bf16<SWIGLU>(r, split_tiles, kBf16SmallTileM, s);
+  return launch_bf16_rem<SWIGLU>(r, split_tiles, s);
 }
 
 // the scan's second list of `which`: the batch's 128-row tiles

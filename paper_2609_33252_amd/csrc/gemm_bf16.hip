@@ -100,7 +100,8 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
   ((uint32_t)((seg) * RPS + seg_row) * K * 2 +                                      \
    (uint32_t)(((lane % CH) ^ ((((seg) * RPS + seg_row) >> SH) & (CH - 1))) * 16))
   // B (packed weights, bf16_block_index layout): the byte offset of the
-  // lane's chunk of segment seg in K step 0; step kt adds kt * BK/32 blocks.
+  // lane's chunk of segment seg in K step 0; step kt adds kt * BK/32 times
+  // the layout's 8 KB per 32 K.
   auto b_lane_off = [&](int seg) -> size_t {
     const int tr = seg * RPS + seg_row, n = nt * BN + tr;
     const int kc = ((lane % CH) ^ ((tr >> SH) & (CH - 1))) * 8;  // K element of the chunk
@@ -134,7 +135,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
     const int buf_ = (kt) % STAGES;                                                 \
     _Pragma("unroll") for (int i = 0; i < B_LD; ++i) {                              \
       const int seg = wid * B_LD + i;                                               \
-      dma16(Bg + b_lane_off(seg) + (size_t)(kt) * (BK / 32) * 1024,                 \
+      dma16(Bg + b_lane_off(seg) + (size_t)(kt) * (BK / 32) * kBf16BlockStepBytes,                 \
             __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf_][seg * 64])));       \
     }                                                                               \
   }
@@ -220,7 +221,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
               __builtin_amdgcn_readfirstlane(lds_offset(&sA[buf][seg * 64])));
       } else {
         const int seg = wid * B_LD + (idx - A_LD);
-        dma16(Bg + b_lane_off(seg) + (size_t)ks * (BK / 32) * 1024,
+        dma16(Bg + b_lane_off(seg) + (size_t)ks * (BK / 32) * kBf16BlockStepBytes,
               __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf][seg * 64])));
       }
     };
@@ -472,6 +473,34 @@ hipError_t launch_bf16_as(const GemmArgs &g, int grid_tiles, int align, hipStrea
   }
   return hipGetLastError();
 }
+
+// Remainder tiles run alone after the 256-row launch and touch one or two
+// experts, so few workgroups stream their weights; each CU's streaming rate
+// is bounded, so the down projection (no gate/up pairing) uses 64-column
+// tiles: twice the workgroups, half the weight bytes each.
+template <bool SWIGLU, bool GATHER>
+hipError_t launch_bf16_rem_as(const GemmArgs &g, int grid_tiles, hipStream_t s) {
+  constexpr int BN = SWIGLU ? 128 : 64;
+  if (g.N % BN || g.K % 64) return hipErrorInvalidValue;
+  const int grid = balanced_grid(grid_tiles, kGroupM, g.N / BN);
+  hipLaunchKernelGGL(
+      (k_gemm_bf16<kBf16SmallTileM, BN, 64, 3, 2, false, SWIGLU, 2, 4, kGroupM, GATHER>),
+      dim3(grid), dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+
+template <bool SWIGLU>
+hipError_t launch_bf16_rem(const GemmArgs &g, int grid_tiles, hipStream_t s) {
+  if constexpr (SWIGLU) {
+    if (g.A == nullptr) {
+      if (!g.xrow || !g.perm || g.k < 1) return hipErrorInvalidValue;
+      return launch_bf16_rem_as<true, true>(g, grid_tiles, s);
+    }
+  }
+  return launch_bf16_rem_as<SWIGLU, false>(g, grid_tiles, s);
+}
+template hipError_t launch_bf16_rem<true>(const GemmArgs &, int, hipStream_t);
+template hipError_t launch_bf16_rem<false>(const GemmArgs &, int, hipStream_t);
 
 template <bool SWIGLU>
 hipError_t launch_bf16(const GemmArgs &g, int grid_tiles, int align, hipStream_t s) {

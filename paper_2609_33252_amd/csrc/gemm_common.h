@@ -148,6 +148,9 @@ __device__ inline void wait_stages(int r) {
 // Launchers of the two kernel families (grid from the tile bound).
 template <bool SWIGLU>
 hipError_t launch_bf16(const GemmArgs &g, int grid_tiles, int align, hipStream_t s);
+// bf16 GEMM over the scan's 64-row remainder tiles
+template <bool SWIGLU>
+hipError_t launch_bf16_rem(const GemmArgs &g, int grid_tiles, hipStream_t s);
 // bf16 GEMM over a list of 128-row and 64-row (half) tiles
 template <bool SWIGLU>
 hipError_t launch_bf16_var(const GemmArgs &g, int grid_tiles, hipStream_t s);

@@ -563,7 +563,7 @@ __global__ __launch_bounds__(256) void k_combine(Arena a, Scratch sc, int row0, 
 // out[map(c)][r] = in[r][c] for a [rows][cols] matrix, 64x64 tiles via LDS.
 // MAP 0: identity; MAP 1: gate half of the W1 interleave; MAP 2: up half.
 // e4m3 outputs are row-major [cols][rows]; bf16 outputs are stored in the
-// blocked layout of bf16_block_index (1 KB blocks of 16 rows x 32 K).
+// blocked layout of bf16_block_index (16 KB blocks of 128 rows x 64 K).
 template <typename TI, typename TO, int MAP>
 __global__ __launch_bounds__(256) void k_transpose(const TI *__restrict__ in, TO *__restrict__ out,
                                                    int rows, int cols) {
