@@ -18,7 +18,7 @@ constexpr int kBf16TileN = 256;
 constexpr int kFp8TileM = 128;       // e4m3 / MXFP4 grouped GEMM tile (4 waves)
 constexpr int kFp8LargeTileM = 256;  // e4m3 / MXFP4 tile for large batches (8 waves)
 constexpr int kRouteThreads = 256;   // threads per routing block
-constexpr int kRoutePairs = 2048;    // flat pairs per routing block (8 rounds of 256)
+constexpr int kRoutePairs = 1024;    // flat pairs per routing block (4 rounds of 256)
 constexpr int kInterleave = 32;           // gate/up column interleave of the packed W1
 // Packed bf16 weights ([N][K], K contiguous per output column n) are stored
 // in 16 KB blocks of 128 columns x 64 K, block (n/128, k/64) at element
@@ -172,7 +172,6 @@ struct Arena {
 // Per-stream-slot scratch of one grouped invocation.
 struct Scratch {
   int32_t *blk_cnt;    // [max_blocks][E] pairs per (routing block, expert)
-  int32_t *blk_base;   // [max_blocks][E] first grouped row of each block's pairs
   int32_t *cnt;        // [E]
   int32_t *off;        // [E+1]
   int32_t *off_pad;    // [E+1]

@@ -49,26 +49,42 @@ __global__ __launch_bounds__(256) void k_ingest(Arena a, IngestGroup grp, int k,
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= c.n_rows) return;
   const int row = c.row0 + i;
+  // every load of the row first (one memory latency), the checks after; the
+  // error flags are raised once per row
   const int t = c.token_idx[i];
+  int idv[kMaxTopK];
+  float wv[kMaxTopK];
+#pragma unroll
+  for (int s = 0; s < kMaxTopK; ++s) {
+    if (s < k) {
+      idv[s] = c.topk_id[(size_t)i * k + s];
+      wv[s] = c.topk_w[(size_t)i * k + s];
+    }
+  }
+  uint32_t bad = 0;
   int dst = -1;
   if (t >= 0 && t < t_max) dst = c.replica * t_max + t;
-  else atomicOr(err, kErrBadToken);
+  else bad |= kErrBadToken;
   a.dst[row] = dst;
   a.xrow[row] = (const char *)c.x + (size_t)i * x_row_bytes;
-  for (int s = 0; s < k; ++s) {
-    int id = c.topk_id[(size_t)i * k + s];
-    if (id < -1 || id >= E) {
-      atomicOr(err, kErrBadId);
-      id = -1;
+#pragma unroll
+  for (int s = 0; s < kMaxTopK; ++s) {
+    if (s < k) {
+      int id = idv[s];
+      if (id < -1 || id >= E) {
+        bad |= kErrBadId;
+        id = -1;
+      }
+      if (dst < 0) id = -1;
+      a.ids[(size_t)row * k + s] = id;
+      a.w[(size_t)row * k + s] = wv[s];
     }
-    if (dst < 0) id = -1;
-    a.ids[(size_t)row * k + s] = id;
-    a.w[(size_t)row * k + s] = c.topk_w[(size_t)i * k + s];
   }
+  if (bad) atomicOr(err, bad);
 }
 
 // ------------------------------------------------------------ histogram
-// Block b counts the valid pairs of flat pairs [b*2048, (b+1)*2048) per
+// Block b counts the valid pairs of flat pairs [b*1024, (b+1)*1024) per
 // expert.  Each wave resolves its 64 ids with seven ballots (the lanes
 // sharing each lane's id); the lowest lane of each id adds the group's size.
 __global__ __launch_bounds__(kRouteThreads) void k_route_count(const int32_t *__restrict__ ids,
@@ -217,46 +233,6 @@ __device__ void plan_batch(const Scratch &sc, PlanLds &L, const PlanArgs &a, int
   }
 }
 
-// ------------------------------------------------------------------ scan
-// One block: per-expert totals over the routing blocks' counts, the tile
-// plan, and the first grouped row of every routing block's pairs of every
-// expert.  Thread t serves expert t % E over a contiguous range of routing
-// blocks (group t / E), so the block counts are read in parallel and
-// scanned in LDS.
-__global__ __launch_bounds__(256) void k_route_scan(Scratch sc, int n_blocks, PlanArgs pa) {
-  __shared__ int s_part[256];  // [group][expert]: range sum, then exclusive prefix
-  __shared__ PlanLds L;
-  const int tid = threadIdx.x, E = pa.E;
-  const int G = 256 / E, e = tid % E, grp = tid / E;
-  const bool mine = grp < G;
-  const int span = (n_blocks + G - 1) / G;
-  const int b0 = min(grp * span, n_blocks), b1 = min(b0 + span, n_blocks);
-  if (mine) {
-    int part = 0;
-    for (int b = b0; b < b1; ++b) part += sc.blk_cnt[b * E + e];
-    s_part[grp * E + e] = part;
-  }
-  __syncthreads();
-  if (tid < E) {
-    int run = 0;
-    for (int q = 0; q < G; ++q) {
-      const int v = s_part[q * E + tid];
-      s_part[q * E + tid] = run;
-      run += v;
-    }
-    L.cnt[tid] = run;
-  }
-  __syncthreads();
-  plan_batch(sc, L, pa, tid, 256);
-  if (mine) {
-    int run = L.pad[e] + s_part[grp * E + e];
-    for (int b = b0; b < b1; ++b) {
-      sc.blk_base[b * E + e] = run;
-      run += sc.blk_cnt[b * E + e];
-    }
-  }
-}
-
 // ---------------------------------------------------- fused (one block)
 // Histogram, scan, tile plan and stable scatter of a batch in one block of
 // 16 waves, for batches whose ids fit in LDS: one coalesced pass stages the
@@ -325,24 +301,76 @@ __global__ __launch_bounds__(64 * kFusedWaves) void k_route_fused(Arena a, Scrat
   }
 }
 
-// -------------------------------------------------------------- permute
-// Same block decomposition as k_route_count.  Each pair's grouped row is the
-// block's first row for its expert, plus pairs of that expert in earlier
-// rounds of this block, in earlier waves of this round, and in lower lanes
-// of this wave (stable in canonical order).  Writes the inverse map (grouped
-// row of each pair), the permutation (pair of each grouped row) and each
-// grouped row's routing coefficient.
-__global__ __launch_bounds__(kRouteThreads) void k_route_scatter(Arena a, Scratch sc, int row0,
-                                                                 int n_flat, int k, int E,
-                                                                 int max_mpad) {
+// ------------------------------------------------------- scan + permute
+// Same block decomposition as k_route_count.  Every block first reads all
+// blocks' counts (thread t serves expert t % E over a contiguous range of
+// blocks, group t / E) and scans them in LDS: the per-expert totals give the
+// tile-aligned expert offsets, and the counts of the blocks before it give
+// this block's first grouped row per expert.  One extra block (the last)
+// publishes the tile plan (plan_batch) instead.  Then each pair's grouped row is that first row
+// for its expert, plus pairs of that expert in earlier rounds of this block,
+// in earlier waves of this round, and in lower lanes of this wave (stable in
+// canonical order).  Writes the inverse map (grouped row of each pair), the
+// permutation (pair of each grouped row) and each grouped row's routing
+// coefficient.
+__global__ __launch_bounds__(kRouteThreads) void k_route_scan_scatter(Arena a, Scratch sc, int row0,
+                                                                      int n_flat, int k,
+                                                                      int n_blocks, PlanArgs pa) {
+  static_assert(kRouteThreads == 256, "one thread per (group, expert) of the count scan");
+  __shared__ int s_part[kRouteThreads];  // [group][expert]: range sum, then exclusive prefix
+  __shared__ PlanLds L;
   __shared__ int running[kMaxExperts];
   __shared__ int wave_cnt[kRouteThreads / 64][kMaxExperts];
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, E = pa.E;
   const int b = blockIdx.x;
-  if (tid < E) running[tid] = sc.blk_base[b * E + tid];
+  const int G = kRouteThreads / E, e = tid % E, grp = tid / E;
+  const bool mine = grp < G;
+  const int span = (n_blocks + G - 1) / G;
+  {
+    const int b0 = min(grp * span, n_blocks), b1 = min(b0 + span, n_blocks);
+    if (mine) {
+      int part = 0;
+      for (int q = b0; q < b1; ++q) part += sc.blk_cnt[q * E + e];
+      s_part[grp * E + e] = part;
+    }
+  }
   for (int i = tid; i < (kRouteThreads / 64) * kMaxExperts; i += kRouteThreads)
     (&wave_cnt[0][0])[i] = 0;
   __syncthreads();
+  if (tid < E) {
+    int run = 0;
+    for (int q = 0; q < G; ++q) {
+      const int v = s_part[q * E + tid];
+      s_part[q * E + tid] = run;
+      run += v;
+    }
+    L.cnt[tid] = run;
+  }
+  __syncthreads();
+  if (b == n_blocks) {
+    // the extra block publishes the tile plan while the others scatter
+    plan_batch(sc, L, pa, tid, kRouteThreads);
+    return;
+  }
+  {
+    if (tid == 0) {
+      int op = 0;
+      for (int x = 0; x < E; ++x) {
+        L.pad[x] = op;
+        op += (L.cnt[x] + pa.align - 1) / pa.align * pa.align;
+      }
+    }
+    __syncthreads();
+  }
+  if (tid < E) {
+    // blocks before b: whole groups, then the blocks of b's group before it
+    const int gb = b / span;
+    int run = L.pad[tid] + s_part[gb * E + tid];
+    for (int q = gb * span; q < b; ++q) run += sc.blk_cnt[q * E + tid];
+    running[tid] = run;
+  }
+  __syncthreads();
+  const int max_mpad = pa.max_mpad;
   const int32_t *ids = a.ids + (size_t)row0 * k;
   const int base = b * kRoutePairs;
   constexpr int R = kRoutePairs / kRouteThreads;
@@ -735,9 +763,8 @@ hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows,
   } else {
     hipLaunchKernelGGL(k_route_count, dim3(nb), dim3(kRouteThreads), 0, s,
                        a.ids + (size_t)row0 * k, n_flat, E, sc.blk_cnt);
-    hipLaunchKernelGGL(k_route_scan, dim3(1), dim3(256), 0, s, sc, nb, pa);
-    hipLaunchKernelGGL(k_route_scatter, dim3(nb), dim3(kRouteThreads), 0, s, a, sc, row0,
-                       n_flat, k, E, max_mpad);
+    hipLaunchKernelGGL(k_route_scan_scatter, dim3(nb + 1), dim3(kRouteThreads), 0, s, a, sc,
+                       row0, n_flat, k, nb, pa);
   }
   // grouped rows: at most every pair plus one partial tile per expert
   const long long bound = ((long long)(expected_pairs + align - 1) / align + E) * align;

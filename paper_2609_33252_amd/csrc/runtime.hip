@@ -96,6 +96,9 @@ struct cep_ctx {
   // sync-only events, one set per slot (re-recorded per batch)
   hipEvent_t ev_ingest[8] = {}, ev_routed[8] = {}, ev_helper[8] = {};
   hipEvent_t ev_layer_done = nullptr, ev_layer_ingest = nullptr;
+  // the last event recorded on the ingest stream with no kernel after it
+  // (the end event of a batch that ran there), or null
+  hipEvent_t ingest_tail = nullptr;
   std::vector<hipEvent_t> timing_pool[2];  // [fenced]
   size_t timing_used[2] = {0, 0};
 };
@@ -211,6 +214,7 @@ int stage_chunks(cep_ctx *c, int64_t upto, hipStream_t s) {
     }
     HIPCHK(c, launch_ingest(c->arena, g, c->cfg.top_k, c->cfg.n_local_experts,
                             c->cfg.max_tokens_per_replica, xrb, c->d_err, s));
+    if (s == c->ingest) c->ingest_tail = nullptr;
   }
   return CEP_OK;
 }
@@ -321,6 +325,7 @@ int launch_pending(cep_ctx *c) {
                              hipMemcpyDeviceToHost, s));
   }
   HIPCHK(c, hipEventRecord(b.ev_end, s));
+  if (s == c->ingest) c->ingest_tail = b.ev_end;
   c->batches.push_back(b);
   c->pending_first = c->chunks.size();
   c->pending_pairs = c->pending_rows = 0;
@@ -434,7 +439,6 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
   for (int i = 0; i < cfg->n_streams; ++i) {
     Scratch &sc = c->sc[i];
     sc.blk_cnt = (int32_t *)A(sizeof(int32_t) * c->max_blocks * E);
-    sc.blk_base = (int32_t *)A(sizeof(int32_t) * c->max_blocks * E);
     sc.cnt = (int32_t *)A(sizeof(int32_t) * E);
     sc.off = (int32_t *)A(sizeof(int32_t) * (E + 1));
     sc.off_pad = (int32_t *)A(sizeof(int32_t) * (E + 1));
@@ -546,6 +550,7 @@ CEP_API int cep_begin_layer(cep_ctx *c, uint32_t generation, int n_replicas,
   c->pending_first = 0;
   c->pending_pairs = c->pending_rows = 0;
   HIPCHK(c, hipEventRecord(c->ev_origin, c->ingest));  // clock origin of this layer's stats
+  c->ingest_tail = nullptr;
   c->origin_set = true;
   c->fetched = false;
   c->fetched_mask = 0;
@@ -668,8 +673,10 @@ CEP_API int cep_combine(cep_ctx *c, hipStream_t s, hipEvent_t *done) {
     }
   }
   if (s != c->ingest) {
-    HIPCHK(c, hipEventRecord(c->ev_layer_ingest, c->ingest));
-    HIPCHK(c, hipStreamWaitEvent(s, c->ev_layer_ingest, 0));
+    // a batch end event with no kernel after it already marks the end of
+    // the ingest stream's work: one marker fewer between layers
+    if (!c->ingest_tail) HIPCHK(c, hipEventRecord(c->ev_layer_ingest, c->ingest));
+    HIPCHK(c, hipStreamWaitEvent(s, c->ingest_tail ? c->ingest_tail : c->ev_layer_ingest, 0));
   }
   HIPCHK(c, hipEventRecord(c->ev_layer_done, s));
   if (done) *done = c->ev_layer_done;
