@@ -41,9 +41,9 @@ GEMM_SOURCES = {
     "mxfp4": ["paper_2609_33252_amd/csrc/gemm_mx.hip", "paper_2609_33252_amd/csrc/gemm_common.h"],
 }
 TRAFFIC_BYTES = {  # workload -> (GEMM family, sha1 prefix of its sources, bytes per batch)
-    "sync_d4096": ("bf16", "f0d29f88cdb3", 504216716),
-    "zipf_imbalanced_d7168/per_chunk": ("bf16", "f0d29f88cdb3", 474052337),
-    "mxfp4_dsv4flash_d4096": ("mxfp4", "8088fc7a9bba", 1368735515),
+    "sync_d4096": ("bf16", "1d3033ba4be0", 504322048),
+    "zipf_imbalanced_d7168/per_chunk": ("bf16", "1d3033ba4be0", 473709568),
+    "mxfp4_dsv4flash_d4096": ("mxfp4", "52e124864ab3", 1369075712),
 }
 
 
