@@ -185,11 +185,13 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
     // and the loop body is one basic block: steps past the end reload the
     // last K step into a buffer nobody reads again.  Sub-steps 0 .. KK-2 of
     // step kt read the fragments of the next sub-step, then multiply the
-    // current ones.  The last sub-step multiplies while it waits for stage
-    // kt+1, passes the barrier, reads the first fragments of kt+1 and issues
-    // the loads of stage kt+STAGES-1: those instructions sit between its
-    // MFMAs, so the matrix pipe always has the next MFMA queued, and the
-    // LDS-read wait before an MFMA never counts the reads issued after it.
+    // current ones; sub-step 0 also issues the loads of stage kt+STAGES-1
+    // into the buffer of step kt-1, which every wave stopped reading before
+    // the previous step's barrier.  The last sub-step multiplies while it
+    // waits for stage kt+1, passes the barrier and reads the first fragments
+    // of kt+1.  Loads, waits, the barrier and reads sit between MFMAs, so the
+    // matrix pipe always has the next MFMA queued, and the LDS-read wait
+    // before an MFMA never counts the reads issued after it.
     bf16x8 fa[2][FM], fb[2][FN];
     constexpr int NM = FM * FN;   // MFMAs per sub-step
     constexpr int NR = FM + FN;   // fragment reads per sub-step
@@ -226,15 +228,31 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
       }
     };
     // sub-steps 0 .. KK-2 of the step in buffer cur
-    auto early_subs = [&](int cur) {
+    // sub-steps 0 .. KK-2 of the step in buffer cur; with DMA, sub-step 0
+    // also issues the loads of K step ks into buffer kbuf between its MFMAs
+    auto early_subs = [&](int cur, auto dma_c, int ks, int kbuf) {
+      constexpr bool DMA = decltype(dma_c)::value;
 #pragma unroll
       for (int kk = 0; kk + 1 < KK; ++kk) {
         const int p = kk & 1, q = p ^ 1;
         CEP_LOAD_FRAG(fa[q], fb[q], cur, cur, kk + 1, FM);
         __builtin_amdgcn_sched_barrier(0);
-        static_for<NM>([&](auto m) {
-          if (p == 0) mfma_one(ic<0>{}, m); else mfma_one(ic<1>{}, m);
-        });
+        if (DMA && kk == 0) {
+          static_for<PER>([&](auto d) {
+            if (p == 0) mfma_one(ic<0>{}, d); else mfma_one(ic<1>{}, d);
+            __builtin_amdgcn_sched_barrier(0);
+            dma_one(ks, kbuf, d);
+            __builtin_amdgcn_sched_barrier(0);
+          });
+          static_for<NM - PER>([&](auto m) {
+            constexpr int M = PER + decltype(m)::value;
+            if (p == 0) mfma_one(ic<0>{}, ic<M>{}); else mfma_one(ic<1>{}, ic<M>{});
+          });
+        } else {
+          static_for<NM>([&](auto m) {
+            if (p == 0) mfma_one(ic<0>{}, m); else mfma_one(ic<1>{}, m);
+          });
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
     };
@@ -250,18 +268,16 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
     for (int kt = 0; kt + 1 < nk; ++kt) {
       const int cur = kt % STAGES, nxt = (kt + 1) % STAGES;
       const int ks = min(kt + STAGES - 1, nk - 1), kbuf = (kt + STAGES - 1) % STAGES;
-      early_subs(cur);
+      early_subs(cur, std::true_type{}, ks, kbuf);
       mfma_one(ic<PL>{}, ic<0>{});
       __builtin_amdgcn_sched_barrier(0);
       // this thread's loads of stage kt+1 are done when at most the
-      // STAGES-3 stages issued after it are outstanding
-      wait_vmcnt<(STAGES - 3) * PER>();
+      // STAGES-2 stages issued after it are outstanding
+      wait_vmcnt<(STAGES - 2) * PER>();
       mfma_one(ic<PL>{}, ic<1>{});
       __builtin_amdgcn_sched_barrier(0);
-      __builtin_amdgcn_s_barrier();  // stage kt+1 landed; step kt-1's buffer free
+      __builtin_amdgcn_s_barrier();  // stage kt+1 landed; step kt's buffer free
       __builtin_amdgcn_sched_barrier(0);
-      // the next step's first fragments first: the four waves' reads queue
-      // on the LDS together, and the most MFMAs of this sub-step cover them
       static_for<NR / 2>([&](auto r) {
         constexpr int R = decltype(r)::value;
         mfma_one(ic<PL>{}, ic<2 + R>{});
@@ -270,19 +286,12 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
         read_one(ic<QL>{}, nxt, ic<2 * R + 1>{});
         __builtin_amdgcn_sched_barrier(0);
       });
-      constexpr int M1 = 2 + NR / 2;
-      static_for<PER>([&](auto d) {
-        mfma_one(ic<PL>{}, ic<M1 + decltype(d)::value>{});
-        __builtin_amdgcn_sched_barrier(0);
-        dma_one(ks, kbuf, d);
-        __builtin_amdgcn_sched_barrier(0);
-      });
-      static_for<NM - M1 - PER>(
-          [&](auto m) { mfma_one(ic<PL>{}, ic<M1 + PER + decltype(m)::value>{}); });
+      static_for<NM - 2 - NR / 2>(
+          [&](auto m) { mfma_one(ic<PL>{}, ic<2 + NR / 2 + decltype(m)::value>{}); });
       __builtin_amdgcn_sched_barrier(0);
     }
     // the last step: no loads, no barrier
-    early_subs((nk - 1) % STAGES);
+    early_subs((nk - 1) % STAGES, std::false_type{}, 0, 0);
     static_for<NM>([&](auto m) { mfma_one(ic<PL>{}, m); });
     // the tail's reloads must land before the workgroup's LDS is released
     wait_vmcnt<0>();
