@@ -76,7 +76,12 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
   constexpr int A_LD = BM * BK * 2 / 1024 / NW, B_LD = BN * BK * 2 / 1024 / NW;  // per wave
   static_assert(A_LD * NW * 1024 == BM * BK * 2 && B_LD * NW * 1024 == BN * BK * 2,
                 "loads split evenly over the waves");
-  static_assert(!SWIGLU || (BN / WGN) % 64 == 0, "a wave's columns hold whole gate/up pairs");
+  // SwiGLU: a wave's columns hold whole gate/up pairs of 32, or (XCH, two
+  // wave columns of 32) wave column 0 holds the gate and 1 the up columns
+  // and they meet in LDS after the K loop
+  constexpr bool XCH = SWIGLU && !PIPE && WGN == 2 && WN == 32;
+  static_assert(!SWIGLU || XCH || (BN / WGN) % 64 == 0,
+                "a wave's columns hold whole gate/up pairs");
   constexpr int PER = A_LD + B_LD;            // loads per thread per step
   int mt, nt;
   if (!balanced_tile<GM>(*g.n_tiles, g.N / BN, &mt, &nt)) return;
@@ -433,6 +438,38 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
     }
     return;
   }
+  if constexpr (XCH) {
+    // the up waves hand their accumulators to the gate waves through the
+    // idle A ring (every load of the K loop landed: the last step waited
+    // for all of them)
+    static_assert(FN == 1 && WGM * FM * 16 * 64 * 4 <= (int)sizeof(sA), "exchange fits the A ring");
+    float *xch = (float *)&sA[0][0];
+    __syncthreads();  // every wave's last operand reads completed
+    if (wn == 1) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) xch[((wm * FM + i) * 16 + r) * 64 + lane] = acc[i][0][r];
+    }
+    __syncthreads();
+    if (wn == 1) return;
+    __bf16 *H = (__bf16 *)g.out;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      if (half && i > 0) break;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rt = frow(i) + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (rt >= t.rows) continue;
+        const size_t row = (size_t)t.row0 + rt;
+        // gate columns nt*BN + [0, 32) and up columns nt*BN + [32, 64) are
+        // h columns nt*BN/2 + [0, 32)
+        H[row * (g.N / 2) + nt * BN / 2 + (lane & 31)] =
+            (__bf16)silu_mul(acc[i][0][r], xch[((wm * FM + i) * 16 + r) * 64 + lane]);
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
     if (half && i > 0) break;
@@ -485,11 +522,12 @@ hipError_t launch_bf16_as(const GemmArgs &g, int grid_tiles, int align, hipStrea
 
 // Remainder tiles run alone after the 256-row launch and touch one or two
 // experts, so few workgroups stream their weights; each CU's streaming rate
-// is bounded, so the down projection (no gate/up pairing) uses 64-column
-// tiles: twice the workgroups, half the weight bytes each.
+// is bounded, so they use 64-column tiles: twice the workgroups of the
+// streaming tile, half the weight bytes each (GEMM1's gate and up halves
+// meet in LDS).
 template <bool SWIGLU, bool GATHER>
 hipError_t launch_bf16_rem_as(const GemmArgs &g, int grid_tiles, hipStream_t s) {
-  constexpr int BN = SWIGLU ? 128 : 64;
+  constexpr int BN = 64;
   if (g.N % BN || g.K % 64) return hipErrorInvalidValue;
   const int grid = balanced_grid(grid_tiles, kGroupM, g.N / BN);
   hipLaunchKernelGGL(
