@@ -526,6 +526,12 @@ CEP_API int cep_begin_layer(cep_ctx *c, uint32_t generation, int n_replicas,
     if (chunks_per_replica[r] < 0) return fail(c, CEP_EINVAL, "negative chunk count");
     tot += chunks_per_replica[r];
   }
+  // The previous layer's last batch end event, when nothing was enqueued on
+  // the ingest stream after it and it is still pending, already marks where
+  // this layer's ingest work can start: it becomes the clock origin (its
+  // event object trades places with the origin's in the timing pool) and
+  // the stream carries one marker fewer between layers.
+  hipEvent_t prev_tail = (c->used_st | c->used_helper) == 0 ? c->ingest_tail : nullptr;
   // the previous layer's batches may still read the arena: stage after them
   for (int i = 0; i < c->cfg.n_streams; ++i) {
     if ((c->used_st >> i) & 1) {
@@ -549,7 +555,22 @@ CEP_API int cep_begin_layer(cep_ctx *c, uint32_t generation, int n_replicas,
   c->chunks.clear();
   c->pending_first = 0;
   c->pending_pairs = c->pending_rows = 0;
-  HIPCHK(c, hipEventRecord(c->ev_origin, c->ingest));  // clock origin of this layer's stats
+  bool aliased = false;
+  if (prev_tail) {
+    const hipError_t q = hipEventQuery(prev_tail);
+    (void)hipGetLastError();  // a pending event's status is not an error
+    if (q == hipErrorNotReady) {
+      for (hipEvent_t &e : c->timing_pool[0]) {
+        if (e == prev_tail) {
+          std::swap(e, c->ev_origin);
+          aliased = true;
+          break;
+        }
+      }
+    }
+  }
+  // clock origin of this layer's stats
+  if (!aliased) HIPCHK(c, hipEventRecord(c->ev_origin, c->ingest));
   c->ingest_tail = nullptr;
   c->origin_set = true;
   c->fetched = false;
@@ -578,7 +599,10 @@ CEP_API int cep_submit_chunk(cep_ctx *c, uint32_t generation, int replica, int n
     return fail(c, CEP_ENOMEM, "chunk pairs %d exceed max_pairs_per_batch %d", n_pairs, c->max_pairs);
   // readiness: later work on the ingest stream (and every batch, which
   // follows it) runs after the chunk's arrival
-  if (arrival) HIPCHK(c, hipStreamWaitEvent(c->ingest, arrival, 0));
+  if (arrival) {
+    HIPCHK(c, hipStreamWaitEvent(c->ingest, arrival, 0));
+    c->ingest_tail = nullptr;
+  }
   ChunkRec ch{replica, c->rows_used, n_rows, n_pairs, arrival, token_idx, x, topk_id, topk_w};
   c->rows_used += n_rows;
   const int64_t id = (int64_t)c->chunks.size();
