@@ -24,6 +24,7 @@
 // permutation (the layout transform's row pack reduced to an address lookup).
 #include "gemm_common.h"
 
+#include <algorithm>
 #include <type_traits>
 #include <utility>
 
@@ -40,6 +41,40 @@ __device__ inline void static_for_impl(F &&f, std::integer_sequence<int, I...>) 
 template <int N, class F>
 __device__ inline void static_for(F &&f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// Work item it of this workgroup, balanced over the XCDs as balanced_tile:
+// the live work W = n_live x N tiles is cut into 8 contiguous shares, one per
+// XCD.  A persistent grid (one workgroup per CU, gridDim.x a multiple of 8)
+// takes items j, j + gridDim.x/8, ... of its XCD's share; otherwise a
+// workgroup takes item blockIdx.x/8 only.
+template <int GM, bool PERSIST>
+__device__ inline bool work_item(int it, int n_live, int n_tiles_n, int *mt, int *nt) {
+  if (!PERSIST && it > 0) return false;
+  const int W = n_live * n_tiles_n;
+  const int C = (W + 7) / 8;
+  const int x = blockIdx.x & 7, j = (blockIdx.x >> 3) + it * (int)(gridDim.x >> 3);
+  const int L = x * C + j;
+  if (j >= C || L >= W) return false;
+  tile_of<GM>(L, n_live, n_tiles_n, mt, nt);
+  return true;
+}
+
+// s_waitcnt lgkmcnt(0) alone (vmcnt and expcnt at their "do not wait" maxima)
+__device__ inline void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xF | (7 << 4) | (3 << 14)); }
+
+// One workgroup per CU of the current device, a multiple of 8 (the XCDs).
+inline int persistent_grid() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cached[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 8)
+      n = 256;
+    cached[dev] = n / 8 * 8;
+  }
+  return cached[dev];
 }
 
 // BM x BN output tile, NW waves as WGM x (NW/WGM), each wave owning a
@@ -83,8 +118,13 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
   static_assert(!SWIGLU || XCH || (BN / WGN) % 64 == 0,
                 "a wave's columns hold whole gate/up pairs");
   constexpr int PER = A_LD + B_LD;            // loads per thread per step
+  // PIPE workgroups are persistent (one per CU) and take every grid-th work
+  // item of their XCD's share: the next tile's first loads then start while
+  // the previous tile's output stores drain.  Others take one work item.
+  const int n_live = *g.n_tiles;
+  for (int it = 0;; ++it) {
   int mt, nt;
-  if (!balanced_tile<GM>(*g.n_tiles, g.N / BN, &mt, &nt)) return;
+  if (!work_item<GM, PIPE>(it, n_live, g.N / BN, &mt, &nt)) return;
   const Tile t = g.tiles[mt];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -436,7 +476,11 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
       const u32x4 *src = row < WM ? &sA[0][0] : &sB[0][0];
       *(u32x4 *)(O + (size_t)row * ldo + c * 8) = src[lr * CPR + (c ^ (((lr >> 2) & 3) << 2))];
     }
-    return;
+    // every wave's reads of the staged rows completed: the ring is free for
+    // the next tile's loads (the stores may still be in flight)
+    wait_lgkm0();
+    __builtin_amdgcn_s_barrier();
+    continue;
   }
   if constexpr (XCH) {
     // the up waves hand their accumulators to the gate waves through the
@@ -495,6 +539,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
       }
     }
   }
+  }  // work items
 }
 
 }  // namespace
@@ -504,7 +549,7 @@ hipError_t launch_bf16_as(const GemmArgs &g, int grid_tiles, int align, hipStrea
   if (align == kBf16TileM) {
     constexpr int BN = 256;
     if (g.N % BN) return hipErrorInvalidValue;
-    const int grid = balanced_grid(grid_tiles, kGroupM, g.N / BN);
+    const int grid = std::min(balanced_grid(grid_tiles, kGroupM, g.N / BN), persistent_grid());
     hipLaunchKernelGGL((k_gemm_bf16<kBf16TileM, BN, 32, 4, 1, true, SWIGLU, 2, 4, kGroupM, GATHER>),
                        dim3(grid), dim3(256), 0, s, g);
   } else if (align == kBf16SmallTileM) {
