@@ -41,8 +41,8 @@ GEMM_SOURCES = {
     "mxfp4": ["paper_2609_33252_amd/csrc/gemm_mx.hip", "paper_2609_33252_amd/csrc/gemm_common.h"],
 }
 TRAFFIC_BYTES = {  # workload -> (GEMM family, sha1 prefix of its sources, bytes per batch)
-    "sync_d4096": ("bf16", "c1df66086b2f", 504334336),
-    "zipf_imbalanced_d7168/per_chunk": ("bf16", "c1df66086b2f", 473560064),
+    "sync_d4096": ("bf16", "c3b56bd685eb", 504303616),
+    "zipf_imbalanced_d7168/per_chunk": ("bf16", "c3b56bd685eb", 473822208),
     "mxfp4_dsv4flash_d4096": ("mxfp4", "52e124864ab3", 1369075712),
 }
 
