@@ -544,16 +544,18 @@ __global__ __launch_bounds__(256) void k_combine(Arena a, Scratch sc, int row0, 
   __shared__ int s_pos[kMaxTopK];
   __shared__ int s_n;
   const int i = blockIdx.x;
+  // the row's slot positions load beside its destination (one memory
+  // latency, not two); lane s of wave 0 holds slot s, and a ballot keeps the
+  // valid ones in slot order
+  static_assert(kMaxTopK <= 64, "a row's slots fit one wave");
+  int ps = -1;
+  if (threadIdx.x < k) ps = sc.pos_of[(size_t)i * k + threadIdx.x];
   const int dst = a.dst[row0 + i];
-  if (dst < 0) return;
-  if (threadIdx.x == 0) {
-    const int32_t *pos = sc.pos_of + (size_t)i * k;
-    int n = 0;
-    for (int s = 0; s < k; ++s) {
-      const int ps = pos[s];
-      if (ps >= 0) s_pos[n++] = ps;
-    }
-    s_n = n;
+  if (dst < 0) return;  // the same for the whole block
+  if (threadIdx.x < 64) {
+    const uint64_t m = __ballot(ps >= 0);
+    if (ps >= 0) s_pos[lanemask_lt_popc(m)] = ps;
+    if (threadIdx.x == 0) s_n = (int)__popcll(m);
   }
   __syncthreads();
   const int n = s_n, d4 = d / 4;
