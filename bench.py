@@ -440,7 +440,7 @@ def main():
         print(json.dumps({"calibrate_copy_bytes": n, "copies": args.steps}))
         return
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: this build has no multi-GPU path "
+        print(f"bench.py runs on one GPU only: the library has no multi-GPU path "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
         sys.exit(2)
 
