@@ -35,10 +35,12 @@ __host__ __device__ inline size_t bf16_block_index(int n, int k, int K) {
 // K-step stride of bf16_block_index: K advancing by 32 moves 8 KB
 constexpr int kBf16BlockStepBytes = 8192;
 // batches up to this many flat (row, slot) entries route in one block (ids
-// in LDS); beyond it the three-kernel path is faster (one block's scatter
-// grows with the entries, the other path's cost is mostly its launches:
-// equal at ~24 K entries with 8 experts, 11 us faster at ~30 K with 32)
-constexpr int kFusedRoutePairs = 1 << 14;
+// in LDS); beyond it the two-kernel path (count, then scan + scatter) is
+// faster: one block's scatter grows with the entries, the other path's cost
+// is mostly its two launches (staging and routing per batch, straggler
+// workload: batches of ~2 K pairs 31 -> 22 us, of ~1 K pairs 19.3 -> 18.4 us
+// against a 16 K crossover)
+constexpr int kFusedRoutePairs = 1 << 12;
 constexpr int kMxBlock = 32;               // MX scale block along K
 
 // Expert weight format of a context (from cep_config.w_dtype).
