@@ -1,20 +1,36 @@
 """Benchmark of the streamFFN routed-expert path on one MI355X.
 
-Workload (the synchronous-EP shape): d_model 4096, expert d_ff 2048, 8 local
-experts, 4 replicas x 2048 tokens routed top-8 over 64 experts uniformly, one
-chunk per replica, all arriving together, bf16 weights and tokens.  One step
-is one layer through the whole path: open the layer, submit every chunk (the
-launch policy forms the batch), histogram/scan/permute, grouped GEMM1 with
-SwiGLU, grouped GEMM2, combine, layer barrier.  Inputs are resident in HBM
-before the timed region.
+Default run (one JSON line), every input seeded, synthetic and resident in
+HBM before the timed region:
 
-value = routed-expert FFN TFLOP/s = 6 * d_model * d_ff * (local pairs) per
-step / time per step.  The JSON line also carries the roofline of the
-dominant kernel (grouped GEMM1, timed with HIP events on its own stream) and
-the CPU oracle's throughput on a bounded sample.
+* headline -- the e4m3 workload: d_model 6144, expert d_ff 2560, 16 local
+  experts of 160, top-8 with Zipf(1.5) popularity, 8 replicas x 8192 tokens
+  (bf16 rows), e4m3 weights with 128x128 float32 block scales, 4 of the 16
+  experts resident only in a donor region and copied once per layer on a
+  side stream (their tiles gated by the copy).  One step is one layer
+  through the whole path: open the layer, issue the weight fetch, submit
+  every chunk (wait-all: one batch), histogram/scan/permute and e4m3 row
+  quantisation, grouped GEMM1 with SwiGLU and h re-quantisation, grouped
+  GEMM2, combine, layer barrier.  value = routed-expert FFN TFLOP/s =
+  6 * d_model * d_ff * (local pairs) per step / time per step;
+* roofline of the dominant kernel (the e4m3 grouped GEMM1, both launches of
+  a layer: the resident experts' and, after the copy, the fetched
+  experts'), from HIP events around each launch on the batch stream;
+* fetch: the same layer with the copy in flight against the same layer whose
+  copy finished before its batch started (same launches): the copy's
+  exposed time;
+* the 4096-wide bf16 workload (4 replicas x 2048 tokens, top-8 of 64, 8
+  local experts, all chunks at once): TFLOP/s and its GEMM1 roofline;
+* the straggler workload (d_model 7168, 8 replicas x 4096 tokens in 64
+  chunks with lognormal gaps, replica 0 finishing 2x later): time to last
+  chunk done and exposed tail under wait-all and under the threshold
+  theta(0.9) on timed arrivals;
+* the CPU oracle (float64 numpy) on a bounded sample of every workload, on
+  all host threads and on one.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
-       [--workload NAME] [--policy wait_all|per_chunk|threshold --theta N --streams S]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
+       python bench.py --workload NAME [--policy wait_all|per_chunk|threshold --theta N
+                       --streams S]       (one workload only)
        python bench.py --sweep | --matched-work | --calibrate-theta | --oewf-sim
 """
 import argparse
@@ -28,22 +44,24 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "routed-expert FFN TFLOP/s (% MFMA peak) + time-to-last-chunk-done, 1 GPU"
+HEADLINE = "fp8_fetch_d6144"
 # dense MFMA TFLOP/s, MI355X.  MXFP4 weights meet MXFP8 activations in one
 # block-scaled MFMA, which issues at the fp8 rate when either operand is e4m3.
 PEAK = {"bf16": 2500.0, "fp8": 5000.0, "mxfp4": 5000.0}
 HBM_PEAK_GBS = 8000.0
-# Measured HBM traffic of the dominant kernel (GEMM1) per batch: rocprofv3
+# launch threshold theta(0.9) of the straggler workload, from the calibration
+# (bench.py --calibrate-theta: the smallest profiled count at 0.9 of peak)
+THETA_09 = 8192
+# Measured HBM traffic of the dominant kernel (GEMM1) per launch: rocprofv3
 # FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0 KiB (factors from a 1 GiB copy), keyed
 # by workload, valid only while the GEMM sources hash to the recorded sha1
 # prefix (the report is null once the kernel changes).
 GEMM_SOURCES = {
     "bf16": ["paper_2609_33252_amd/csrc/gemm_bf16.hip", "paper_2609_33252_amd/csrc/gemm_common.h"],
+    "fp8": ["paper_2609_33252_amd/csrc/gemm_fp8.hip", "paper_2609_33252_amd/csrc/gemm_common.h"],
     "mxfp4": ["paper_2609_33252_amd/csrc/gemm_mx.hip", "paper_2609_33252_amd/csrc/gemm_common.h"],
 }
-TRAFFIC_BYTES = {  # workload -> (GEMM family, sha1 prefix of its sources, bytes per batch)
-    "sync_d4096": ("bf16", "c3b56bd685eb", 504303616),
-    "zipf_imbalanced_d7168/per_chunk": ("bf16", "c3b56bd685eb", 473822208),
-    "mxfp4_dsv4flash_d4096": ("mxfp4", "52e124864ab3", 1369075712),
+TRAFFIC_BYTES = {  # workload -> (GEMM family, sha1 prefix of its sources, bytes per launch)
 }
 
 
@@ -63,6 +81,7 @@ def measured_traffic(workload):
     dtype, sha, nbytes = entry
     return nbytes if gemm_source_hash(dtype) == sha else None
 
+
 POLICIES = {"wait_all": 0, "per_chunk": 1, "threshold": 2}
 
 
@@ -70,14 +89,36 @@ def describe(cfg, name):
     return (f"{name}: d_model={cfg['d']}, d_ff={cfg['I']}, {cfg['E']} local experts of "
             f"{cfg['Eg']}, top-{cfg['k']} {'uniform' if cfg['zipf'] is None else 'Zipf(%s)' % cfg['zipf']}, "
             f"{cfg['R']} replicas x {cfg['T']} tokens, {cfg['R'] * cfg['cpr']} chunks, "
-            f"{cfg['w']} weights")
+            f"{cfg['w']} weights" + (f", {len(cfg.get('_fetched', []))} experts fetched"
+                                     if cfg.get('_fetched') else ""))
 
 
-def cpu_baseline(wl, budget_s=12.0):
-    """The CPU oracle as it stands, on a bounded sample of the same workload's
-    delivered tokens; returns TFLOP/s over the pairs it computed."""
+def dtype_of(wl):
+    from paper_2609_33252_amd import workload as W
+    return {W.FP8: "fp8", W.MXFP4: "mxfp4"}.get(wl.cfg["w"], "bf16")
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+_BANKS = {}
+
+
+def cpu_oracle_rate(wl, budget_s, threads=None):
+    """The CPU oracle as it stands (float64 numpy, the plain definition) on a
+    bounded sample of the workload's delivered tokens (seeded order, batches
+    doubling from 64 tokens, until budget_s of oracle time); threads: BLAS
+    threads (None = all).  Returns the cpu_baseline record in TFLOP/s."""
     import numpy as np
-    from threadpoolctl import threadpool_info
+    from threadpoolctl import threadpool_info, threadpool_limits
     from oracle import ffn
     import torch
 
@@ -87,8 +128,12 @@ def cpu_baseline(wl, budget_s=12.0):
         return None if t is None else (t.view(torch.int16).numpy().view(np.uint16)
                                        if t.dtype == torch.bfloat16 else t.numpy())
     kind = {"f32": "f32", "bf16": "bf16", "fp8_e4m3_b128": "fp8", "mxfp4": "mxfp4"}[c["w"]]
-    bank = ffn.ExpertBank(kind, bits(wl.w_gate), bits(wl.w_up), bits(wl.w_down),
-                          bits(wl.s_gate), bits(wl.s_up), bits(wl.s_down))
+    # one decoded copy of the weights per workload (decoding is not timed)
+    bank = _BANKS.get(id(wl))
+    if bank is None:
+        bank = _BANKS[id(wl)] = ffn.ExpertBank(
+            kind, bits(wl.w_gate), bits(wl.w_up), bits(wl.w_down), bits(wl.s_gate),
+            bits(wl.s_up), bits(wl.s_down))
     h_mode = {"f32": None, "bf16": "bf16", "fp8": "fp8", "mxfp4": "mxfp8"}[kind]
     x_mode = {"fp8": "fp8", "mxfp4": "mxfp8"}.get(kind)
     deliv = np.argwhere(wl.delivered)
@@ -96,25 +141,33 @@ def cpu_baseline(wl, budget_s=12.0):
     deliv = deliv[rng.permutation(len(deliv))]
     for e in range(c["E"]):      # decode weights outside the timed sample
         bank(e)
-    done_pairs, t_total, n_tok, step = 0, 0.0, 0, 64
-    while t_total < budget_s and n_tok < len(deliv):
-        sel = deliv[n_tok:n_tok + step]
-        xb = bits(wl.x)[sel[:, 0], sel[:, 1]]
-        ids = wl.topk_local[sel[:, 0], sel[:, 1]]
-        w = wl.topk_w[sel[:, 0], sel[:, 1]]
-        t0 = time.perf_counter()
-        x = ffn.decode_rows(xb, "bf16" if c["x"] == "bf16" else "f32")
-        ffn.routed_output(x, ids, w, bank, c["E"], h_mode=h_mode, x_mode=x_mode, y_mode="bf16")
-        t_total += time.perf_counter() - t0
-        done_pairs += int((ids >= 0).sum())
-        n_tok += len(sel)
-        step = min(step * 2, 1024)
+    # one untimed call first: starts the BLAS threads
+    sel = deliv[:8]
+    ffn.routed_output(ffn.decode_rows(bits(wl.x)[sel[:, 0], sel[:, 1]],
+                                      "bf16" if c["x"] == "bf16" else "f32"),
+                      wl.topk_local[sel[:, 0], sel[:, 1]], wl.topk_w[sel[:, 0], sel[:, 1]], bank,
+                      c["E"], h_mode=h_mode, x_mode=x_mode)
+    from contextlib import nullcontext
+    with (threadpool_limits(limits=threads) if threads else nullcontext()):
+        used = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        done_pairs, t_total, n_tok, step = 0, 0.0, 0, 64
+        while t_total < budget_s and n_tok < len(deliv):
+            sel = deliv[n_tok:n_tok + step]
+            xb = bits(wl.x)[sel[:, 0], sel[:, 1]]
+            ids = wl.topk_local[sel[:, 0], sel[:, 1]]
+            w = wl.topk_w[sel[:, 0], sel[:, 1]]
+            t0 = time.perf_counter()
+            x = ffn.decode_rows(xb, "bf16" if c["x"] == "bf16" else "f32")
+            ffn.routed_output(x, ids, w, bank, c["E"], h_mode=h_mode, x_mode=x_mode)
+            t_total += time.perf_counter() - t0
+            done_pairs += int((ids >= 0).sum())
+            n_tok += len(sel)
+            step = min(step * 2, 1024)
     flops = 6.0 * c["d"] * c["I"] * done_pairs
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    return {"value": flops / t_total / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+    return {"value": round(flops / t_total / 1e12, 5), "unit": "TFLOP/s", "cores": int(used),
             "kind": "oracle",
-            "sample": f"{n_tok} delivered tokens ({done_pairs} pairs) of the same workload, "
-                      f"float64 numpy, {t_total:.1f} s"}
+            "sample": f"{n_tok} delivered tokens ({done_pairs} pairs) of {wl.name}, float64 "
+                      f"numpy, {t_total:.1f} s"}
 
 
 def sweep(args):
@@ -368,16 +421,287 @@ def oewf_sim(args):
     prof.close()
 
 
+# ------------------------------------------------------------- default run
+def batch_pairs(wl, st, fetched):
+    """(pairs of resident experts, pairs of fetched experts, experts touched
+    by each) of every batch of one layer's statistics."""
+    import numpy as np
+    out = []
+    fset = np.asarray(sorted(fetched), dtype=np.int64)
+    for b in st["batches"]:
+        ids = np.concatenate([
+            wl.topk_local[wl.chunks[c].replica][wl.chunks[c].token_idx].ravel()
+            for c in range(b["first_chunk"], b["first_chunk"] + b["n_chunks"])])
+        ids = ids[ids >= 0]
+        is_f = np.isin(ids, fset) if (b["fetched"] and len(fset)) else np.zeros(len(ids), bool)
+        out.append((int((~is_f).sum()), int(is_f.sum()),
+                    len(np.unique(ids[~is_f])), len(np.unique(ids[is_f]))))
+    return out
+
+
+def gemm1_roofline(wl, stats, fetched, dtype, workload_key):
+    """Roofline of the grouped GEMM1 over every GEMM1 launch of the layers in
+    `stats` (the resident experts', and the fetched experts' after the copy,
+    both on the batch stream and never overlapping): achieved = mean
+    algorithmic work per launch / mean launch duration (HIP events around
+    the launches on the batch stream)."""
+    from paper_2609_33252_amd import workload as W
+    c = wl.cfg
+    elem = {W.BF16: 2, W.F32: 2, W.FP8: 1}.get(c["w"], 0.5)
+    xel = 2 if dtype == "bf16" else 1
+    flops = bytes_ = dur = 0.0
+    n = 0
+    for st in stats:
+        for b, (pr, pf, er, ef) in zip(st["batches"], batch_pairs(wl, st, fetched)):
+            for pairs, experts, ms in ((pr, er, b["gemm1_ms"]),
+                                       (pf, ef, b["fetched_gemm1_ms"] if b["fetched"] else -1)):
+                if ms < 0:
+                    continue
+                flops += 4.0 * c["d"] * c["I"] * pairs
+                # gate/up weights of every expert the launch touches (each
+                # streamed once), the launch's rows in and h out
+                bytes_ += experts * 2.0 * c["I"] * c["d"] * elem + pairs * (c["d"] + c["I"]) * xel
+                dur += ms
+                n += 1
+    f1, b1, ms1 = flops / n, bytes_ / n, dur / n
+    hbm = b1 / (HBM_PEAK_GBS * 1e9) > f1 / (PEAK[dtype] * 1e12)
+    kern = {"bf16": "k_gemm_bf16", "fp8": "k_gemm_fp8", "mxfp4": "k_gemm_mx"}[dtype]
+    r = {"kernel": f"{kern}<SwiGLU> (grouped gate/up GEMM, every launch of the layer)",
+         "launches": n, "launch_ms": round(ms1, 4), "traffic": measured_traffic(workload_key)}
+    if hbm:
+        a = b1 / (ms1 * 1e-3) / 1e9
+        r.update(bound="hbm", achieved=round(a, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                 frac=round(a / HBM_PEAK_GBS, 4), bytes_per_launch=round(b1))
+    else:
+        a = f1 / (ms1 * 1e-3) / 1e12
+        r.update(bound="mfma", achieved=round(a, 2), peak=PEAK[dtype], unit="TFLOP/s",
+                 frac=round(a / PEAK[dtype], 4), flop_per_launch=f1)
+    return {k: r[k] for k in ("bound", "achieved", "peak", "unit", "frac", "traffic", "kernel",
+                              "launches", "launch_ms") + (("bytes_per_launch",) if hbm else
+                                                          ("flop_per_launch",))}
+
+
+def timed_layers(run, warmup, steps, **kw):
+    """Wall time per layer (ms) of `steps` layers after `warmup`, bracketed
+    by device synchronisation; per-phase events off."""
+    import torch
+    from paper_2609_33252_amd import cep
+    cep.cep_set_phase_timing(run.ctx, False)
+    for _ in range(warmup):
+        run.run(**kw)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        run.run(**kw)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) / steps * 1e3
+    from paper_2609_33252_amd import cep as _c
+    _c.cep_get_status(run.ctx)
+    cep.cep_set_phase_timing(run.ctx, True)
+    return ms
+
+
+def phase_layers(run, steps, **kw):
+    """Statistics of `steps` layers with per-phase events."""
+    out = []
+    for _ in range(steps):
+        run.run(**kw)
+        out.append(run.stats())
+    return out
+
+
+def mean(v):
+    return sum(v) / len(v)
+
+
+def full_bench(args):
+    import torch
+    from paper_2609_33252_amd import cep, harness, streaming, workload as W
+
+    torch.cuda.set_device(0)
+    K, Wm = args.steps, args.warmup
+    line = {}
+
+    # ---- headline: e4m3 workload with the weight fetch, wait-all
+    wl = W.generate(HEADLINE, 0)
+    c = wl.cfg
+    run = harness.Runner(wl, n_streams=1)
+    P = run.n_pairs
+    flops = 6.0 * c["d"] * c["I"] * P
+    kw = dict(policy=cep.CEP_WAIT_ALL, inputs_ready=True)
+    ms = timed_layers(run, Wm, K, **kw)
+    value = flops / (ms * 1e-3) / 1e12
+    st = phase_layers(run, K, **kw)
+    fetched = list(wl.fetched)
+    phases = {k: round(mean([sum(b[k] for b in s["batches"]) for s in st]), 4)
+              for k in ("route_ms", "gemm1_ms", "gemm2_ms", "combine_ms", "fetched_gemm1_ms",
+                        "fetched_gemm2_ms")}
+    span_copy = [max(b["end_ms"] for b in s["batches"]) -
+                 min(min(b["start_ms"] for b in s["batches"]), s["fetch"]["start_ms"])
+                 for s in st]
+    copy_ms = [s["fetch"]["end_ms"] - s["fetch"]["start_ms"] for s in st]
+    fbytes = st[0]["fetch"]["bytes"]
+    roof = gemm1_roofline(wl, st, fetched, "fp8", HEADLINE)
+    # the same layer with its copy finished before the batch starts
+    stp = phase_layers(run, K, prefetch=True, **kw)
+    span_pre = [max(b["end_ms"] for b in s["batches"]) - min(b["start_ms"] for b in s["batches"])
+                for s in stp]
+    cep.cep_get_status(run.ctx)
+    run.close()
+    del run
+    c = dict(c, _fetched=fetched)
+    line.update({
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": K, "warmup": Wm, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "fp8", "data": "synthetic",
+        "config": {"workload": describe(c, HEADLINE), "local_pairs": P, "policy": "wait_all",
+                   "streams": 1, "global_batch": c["R"] * c["T"], "seq_len": c["T"],
+                   "parallelism": "ep_share_1gpu"},
+        "pct_mfma_peak": round(100 * value / PEAK["fp8"], 2),
+        "phases_ms": phases,
+        "roofline": roof,
+        "fetch": {"experts": len(fetched), "bytes": fbytes,
+                  "copy_ms": round(mean(copy_ms), 4),
+                  "copy_gbps": round(fbytes / (mean(copy_ms) * 1e-3) / 1e9, 1),
+                  "layer_ms_copy_in_flight": round(mean(span_copy), 4),
+                  "layer_ms_prefetched": round(mean(span_pre), 4),
+                  "exposed_copy_ms": round(mean(span_copy) - mean(span_pre), 4),
+                  "note": "GPU spans (HIP events) of the layer with the copy issued with the "
+                          "batch vs issued and finished before it; same launches"},
+    })
+    print(json.dumps({"progress": "headline", "value": line["value"]}), file=sys.stderr,
+          flush=True)
+
+    # ---- 4096-wide bf16 workload, all chunks at once
+    wl2 = W.generate("sync_d4096", 0)
+    c2 = wl2.cfg
+    run = harness.Runner(wl2, n_streams=1)
+    ms2 = timed_layers(run, Wm, K, **kw)
+    st2 = phase_layers(run, K, **kw)
+    f2 = 6.0 * c2["d"] * c2["I"] * run.n_pairs
+    cep.cep_get_status(run.ctx)
+    line["sync_d4096"] = {
+        "workload": describe(c2, "sync_d4096"), "local_pairs": run.n_pairs,
+        "ms_per_layer": round(ms2, 4), "tflops": round(f2 / (ms2 * 1e-3) / 1e12, 2),
+        "pct_mfma_peak": round(100 * f2 / (ms2 * 1e-3) / 1e12 / PEAK["bf16"], 2),
+        "phases_ms": {k: round(mean([sum(b[k] for b in s["batches"]) for s in st2]), 4)
+                      for k in ("route_ms", "gemm1_ms", "gemm2_ms", "combine_ms")},
+        "roofline": gemm1_roofline(wl2, st2, [], "bf16", "sync_d4096")}
+    run.close()
+    del run
+    print(json.dumps({"progress": "sync_d4096"}), file=sys.stderr, flush=True)
+
+    # ---- straggler workload on timed arrivals: wait-all vs theta(0.9)
+    wl4 = W.generate("zipf_imbalanced_d7168", 0)
+    c4 = wl4.cfg
+    run = harness.Runner(wl4, n_streams=2)
+    f4 = 6.0 * c4["d"] * c4["I"] * run.n_pairs
+    res = {}
+    for name, pol, theta, ns in (("wait_all", cep.CEP_WAIT_ALL, 1, 1),
+                                 (f"theta_{THETA_09}", cep.CEP_THRESHOLD, THETA_09, 2)):
+        ms_ = []
+        for i in range(1 + args.timed_layers):
+            run.run(policy=pol, theta=theta, n_streams=ns, timed=True)
+            torch.cuda.synchronize()
+            if i:
+                ms_.append(streaming.layer_metrics(run.stats(), f4))
+        m = streaming.mean_metrics(ms_)
+        res[name] = {"batches": m["batches"],
+                     "time_to_last_chunk_done_ms": round(m["time_to_last_chunk_done_ms"], 4),
+                     "last_arrival_ms": round(m["last_arrival_ms"], 4),
+                     "exposed_tail_ms": round(m["exposed_tail_ms"], 4),
+                     "chunk_latency_p50_ms": round(m["chunk_latency_ms"]["p50"], 4),
+                     "chunk_latency_p95_ms": round(m["chunk_latency_ms"]["p95"], 4),
+                     "busy_tflops": round(m["busy_tflops"], 2)}
+    cep.cep_get_status(run.ctx)
+    run.close()
+    del run
+    wa, th = res["wait_all"], res[f"theta_{THETA_09}"]
+    line["time_to_last_chunk_done"] = {
+        "workload": describe(c4, "zipf_imbalanced_d7168"), "local_pairs": wl4.n_pairs,
+        "arrivals": "timed: lognormal(0, 0.5) ms gaps, replica 0 scaled 2x, others U[1, 1.5]x",
+        "layers": args.timed_layers, **res,
+        "exposed_tail_ratio": round(th["exposed_tail_ms"] / wa["exposed_tail_ms"], 4),
+        "busy_tflops_ratio": round(th["busy_tflops"] / wa["busy_tflops"], 4)}
+    print(json.dumps({"progress": "straggler"}), file=sys.stderr, flush=True)
+
+    # ---- targets of the path, as measured here
+    line["targets"] = {
+        "bf16_gemm1_mfma_frac_ge_0.60": line["sync_d4096"]["roofline"]["frac"] >= 0.60,
+        "fp8_gemm1_mfma_frac": roof["frac"],
+        "streaming_lowers_exposed_tail": th["exposed_tail_ms"] < wa["exposed_tail_ms"]}
+
+    # ---- the CPU oracle
+    if not args.no_cpu:
+        per = {}
+        gens = {HEADLINE: wl, "sync_d4096": wl2, "zipf_imbalanced_d7168": wl4}
+        for name in W.CONFIG_ORDER:
+            w_ = gens.get(name) or W.generate(name, 0)
+            per[name] = {"all_threads": cpu_oracle_rate(w_, args.cpu_budget),
+                         "one_thread": cpu_oracle_rate(w_, args.cpu_budget / 2, threads=1)}
+            _BANKS.clear()
+        line["cpu_baseline"] = per[HEADLINE]["all_threads"]
+        line["cpu_baseline_per_config"] = {
+            "cpu_model": cpu_model(), "affinity_cpus": len(os.sched_getaffinity(0)), **per}
+    print(json.dumps(line), flush=True)
+
+
+def single_workload(args):
+    """One workload (--workload): the line of full_bench's headline for it."""
+    import torch
+    from paper_2609_33252_amd import cep, harness, workload as W
+
+    torch.cuda.set_device(0)
+    wl = W.generate(args.workload, 0)
+    c = wl.cfg
+    run = harness.Runner(wl, n_streams=max(1, args.streams), use_fetch=not args.no_fetch)
+    pol = POLICIES[args.policy]
+    dtype = dtype_of(wl)
+    kw = dict(policy=pol, theta=args.theta, n_streams=args.streams, inputs_ready=True)
+    ms = timed_layers(run, args.warmup, args.steps, **kw)
+    flops = 6.0 * c["d"] * c["I"] * run.n_pairs
+    value = flops / (ms * 1e-3) / 1e12
+    st = phase_layers(run, args.steps, **kw)
+    fetched = list(wl.fetched) if run.use_fetch else []
+    key = args.workload if args.policy == "wait_all" else f"{args.workload}/{args.policy}"
+    line = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
+        "data": "synthetic",
+        "config": {"workload": describe(dict(c, _fetched=fetched), args.workload),
+                   "local_pairs": run.n_pairs, "policy": args.policy, "theta": args.theta,
+                   "streams": args.streams, "global_batch": c["R"] * c["T"], "seq_len": c["T"],
+                   "parallelism": "ep_share_1gpu"},
+        "pct_mfma_peak": round(100 * value / PEAK[dtype], 2),
+        "phases_ms": {k: round(mean([sum(b[k] for b in s["batches"]) for s in st]), 4)
+                      for k in ("route_ms", "gemm1_ms", "gemm2_ms", "combine_ms")},
+        "roofline": gemm1_roofline(wl, st, fetched, dtype, key),
+    }
+    cep.cep_get_status(run.ctx)
+    run.close()
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_oracle_rate(wl, args.cpu_budget)
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="sync_d4096")
+    ap.add_argument("--workload", default=None,
+                    help="run one workload only (default: the full run described above)")
     ap.add_argument("--policy", default="wait_all", choices=list(POLICIES))
     ap.add_argument("--theta", type=int, default=1)
     ap.add_argument("--streams", type=int, default=1)
+    ap.add_argument("--no-fetch", action="store_true",
+                    help="--workload: keep every expert resident")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-budget", type=float, default=2.0,
+                    help="seconds of oracle time per workload and thread setting")
+    ap.add_argument("--timed-layers", type=int, default=3,
+                    help="timed-arrival layers per policy of the straggler workload")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run device-to-device copies of MIB MiB (counter calibration)")
     ap.add_argument("--sweep", action="store_true",
@@ -400,35 +724,10 @@ def main():
     ap.add_argument("--fetch-experts", type=int, default=4,
                     help="fetch buffer capacity in experts (byte budget B_h)")
     args = ap.parse_args()
-    if args.oewf_sim:
-        if args.workload == "sync_d4096":
-            args.workload = "zipf_imbalanced_d7168"
-        oewf_sim(args)
-        return
-    if args.calibrate_theta:
-        if args.gpus != 1:
-            print("bench.py runs on one GPU only", file=sys.stderr)
-            sys.exit(2)
-        if args.workload == "sync_d4096":
-            args.workload = "zipf_imbalanced_d7168"
-        calibrate_theta(args)
-        return
-    if args.matched_work:
-        if args.gpus != 1:
-            print("bench.py runs on one GPU only", file=sys.stderr)
-            sys.exit(2)
-        if args.workload == "sync_d4096":
-            args.workload = "zipf_imbalanced_d7168"
-        matched_work(args)
-        return
-    if args.sweep:
-        if args.gpus != 1:
-            print("bench.py runs on one GPU only", file=sys.stderr)
-            sys.exit(2)
-        if args.workload == "sync_d4096":
-            args.workload = "zipf_imbalanced_d7168"
-        sweep(args)
-        return
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the library has no multi-GPU path "
+              f"(--gpus {args.gpus} requested)", file=sys.stderr)
+        sys.exit(2)
     if args.calibrate_copy:
         import torch
         n = args.calibrate_copy << 20
@@ -439,108 +738,24 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": n, "copies": args.steps}))
         return
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: the library has no multi-GPU path "
-              f"(--gpus {args.gpus} requested)", file=sys.stderr)
-        sys.exit(2)
 
-    import torch
-    from paper_2609_33252_amd import cep, harness, workload as W
-
+    from paper_2609_33252_amd import cep
     if not os.path.exists(cep.LIB_PATH):
         from paper_2609_33252_amd import build
         build.build()
+    import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
-    torch.cuda.set_device(0)
-
-    wl = W.generate(args.workload, 0)
-    c = wl.cfg
-    run = harness.Runner(wl, n_streams=max(1, args.streams))
-    pol = POLICIES[args.policy]
-    flops_step = 6.0 * c["d"] * c["I"] * run.n_pairs
-    dtype = {W.FP8: "fp8", W.MXFP4: "mxfp4"}.get(c["w"], "bf16")
-
-    # the chunk inputs are generated once and resident in HBM: steady-state
-    # layers carry no arrival events (the library orders each layer after the
-    # previous one's batches itself)
-    def step():
-        run.run(policy=pol, theta=args.theta, n_streams=args.streams, inputs_ready=True)
-
-    # timed steps without per-phase events (instrumentation, not work); the
-    # phase pass below turns them back on
-    cep.cep_set_phase_timing(run.ctx, False)
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    cep.cep_get_status(run.ctx)
-    cep.cep_set_phase_timing(run.ctx, True)
-    ms_step = elapsed / args.steps * 1e3
-    value = flops_step / (elapsed / args.steps) / 1e12
-
-    # kernel phases of each step, from HIP events on the batch stream
-    ph = {"route_ms": [], "gemm1_ms": [], "gemm2_ms": [], "combine_ms": [], "last_done_ms": []}
-    for _ in range(args.steps):
-        step()
-        st = run.stats()
-        for key in ("route_ms", "gemm1_ms", "gemm2_ms", "combine_ms"):
-            ph[key].append(sum(b[key] for b in st["batches"]))
-        ph["last_done_ms"].append(max(b["end_ms"] for b in st["batches"]))
-    avg = {k: sum(v) / len(v) for k, v in ph.items()}
-    n_launch = len(st["batches"])
-    g1_flops = 4.0 * c["d"] * c["I"] * run.n_pairs / n_launch
-    g1_ms = avg["gemm1_ms"] / n_launch
-    # algorithmic bytes of GEMM1 per launch: the gate/up weights of every
-    # local expert a batch touches (each streamed once), the batch's rows in
-    # and h out
-    import numpy as np
-    elem = {W.BF16: 2, W.F32: 2, W.FP8: 1}.get(c["w"], 0.5)
-    xel = 2 if dtype == "bf16" else 1
-    touched = [set(int(e) for e in np.unique(wl.topk_local[ch.replica][ch.token_idx]) if e >= 0)
-               for ch in wl.chunks]
-    g1_bytes = sum(len(set().union(*touched[b["first_chunk"]:b["first_chunk"] + b["n_chunks"]]))
-                   for b in st["batches"]) * 2.0 * c["I"] * c["d"] * elem / n_launch
-    g1_bytes += run.n_pairs * (c["d"] + c["I"]) * xel / n_launch
-    # the roofline that bounds a launch: MFMA time vs HBM time at peak
-    hbm_bound = g1_bytes / (HBM_PEAK_GBS * 1e9) > g1_flops / (PEAK[dtype] * 1e12)
-    traffic = measured_traffic(args.workload if args.policy == "wait_all"
-                               else f"{args.workload}/{args.policy}")
-    kernel = ("k_gemm_%s<SwiGLU> (grouped gate/up GEMM; %s)" %
-              ({"mxfp4": "mx"}.get(dtype, dtype),
-               "64-row weight-streaming tiles" if hbm_bound else
-               "256-row tiles, bf16 plus 64-row remainder tiles when planned"))
-    if hbm_bound:
-        achieved = g1_bytes / (g1_ms * 1e-3) / 1e9
-        roofline = {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 1),
-                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": traffic, "launch_ms": round(g1_ms, 4),
-                    "bytes_per_launch": round(g1_bytes)}
-    else:
-        achieved = g1_flops / (g1_ms * 1e-3) / 1e12
-        roofline = {"bound": "mfma", "kernel": kernel, "achieved": round(achieved, 2),
-                    "peak": PEAK[dtype], "unit": "TFLOP/s", "frac": round(achieved / PEAK[dtype], 4),
-                    "traffic": traffic, "launch_ms": round(g1_ms, 4), "flop_per_launch": g1_flops}
-    line = {
-        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
-        "data": "synthetic",
-        "config": {"workload": describe(c, args.workload), "local_pairs": run.n_pairs,
-                   "policy": args.policy, "theta": args.theta, "streams": args.streams,
-                   "global_batch": c["R"] * c["T"], "seq_len": c["T"], "parallelism": "ep_share_1gpu"},
-        "pct_mfma_peak": round(100 * value / PEAK[dtype], 2),
-        "time_to_last_chunk_done_ms": round(avg["last_done_ms"], 4),
-        "phases_ms": {k: round(v, 4) for k, v in avg.items() if k != "last_done_ms"},
-        "roofline": roofline,
-    }
-    run.close()
-    if not args.no_cpu:
-        line["cpu_baseline"] = cpu_baseline(wl)
-    print(json.dumps(line), flush=True)
+    if args.sweep or args.matched_work or args.calibrate_theta or args.oewf_sim:
+        if args.workload is None:
+            args.workload = "zipf_imbalanced_d7168"
+        fn = (oewf_sim if args.oewf_sim else calibrate_theta if args.calibrate_theta
+              else matched_work if args.matched_work else sweep)
+        fn(args)
+        return
+    if args.workload is not None:
+        single_workload(args)
+        return
+    full_bench(args)
 
 
 if __name__ == "__main__":

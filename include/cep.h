@@ -23,9 +23,9 @@
  *
  * The single-GPU part of opportunistic expert weight fetching (Section 3.3;
  * Appendix C, "One-shot weight fetching") is a side-stream device-to-device
- * copy of whole expert weight blobs into a preallocated buffer; the work of
- * fetched experts runs as a separate grouped invocation on a helper stream
- * gated by the copy.
+ * copy of whole expert weight blobs into a preallocated buffer; the fetched
+ * experts' grouped GEMMs of a batch run after its resident experts' GEMMs,
+ * gated by the copy, so the copy overlaps the resident work.
  *
  * Conventions for every entry point:
  *   - Return value: CEP_OK or a negative cep_status.  Nothing aborts or
@@ -67,6 +67,18 @@ enum cep_dtype {
   CEP_MXFP4 = 3          /* weights only: OCP MXFP4 (e2m1 codes, one E8M0 scale
                            per 32 along K; Section 4.1's DeepSeek-V4 experts);
                            activations and h run as MXFP8 inside the library */
+};
+
+/* How cep_weight_fetch brings a fetched expert's weights (Appendix C,
+ * "One-shot weight fetching"; "FFN reassignment commit and fallback"). */
+enum cep_fetch_mode {
+  CEP_FETCH_COPY = 0,      /* copy the blobs into the fetch buffer on the side
+                              stream; the experts' tiles wait for the copy.  A
+                              copy that fails to start falls back to IN_PLACE */
+  CEP_FETCH_IN_PLACE = 1,  /* no copy: the experts' tiles read the donor blobs
+                              where they are (a peer region read in place)    */
+  CEP_FETCH_FAIL_COPY = 2  /* test aid: behave as if the first copy failed to
+                              start, which takes the fallback of COPY          */
 };
 
 enum cep_policy {
@@ -121,10 +133,17 @@ int cep_pack_experts(const cep_config *cfg, const cep_weights *w, int first, int
 
 /* Create a context: validates cfg, allocates every scratch buffer, the chunk
  * arena and the fetch buffer, creates the streams, and packs the weights of
- * resident experts into library-owned memory.  resident: host [E] flags,
- * NULL = all resident; an expert with flag 0 has no local weights and its
- * work can only run after cep_weight_fetch brings them (w is not read for
- * it).  Synchronises s before returning, so the caller may free w after. */
+ * resident experts into library-owned memory.  These are the expert weights
+ * every grouped invocation reads (Appendix C, "Grouped FFN invocations"),
+ * and the preallocated temporary weight buffer of a helper (Appendix C,
+ * "One-shot weight fetching": its capacity bounds the fetch byte budget).
+ * resident: host [E] flags, NULL = all resident; an expert with flag 0 has
+ * no local weights (its weights live with a donor, Section 3.3) and its work
+ * can only run after cep_weight_fetch brings them (w is not read for it).
+ * Synchronises s before returning, so the caller may free w after.  Errors:
+ * CEP_EINVAL for a bad cfg or NULL weights, CEP_ENOMEM when a device
+ * allocation fails, CEP_EHIP; *out is NULL then (message in
+ * cep_last_error(NULL)). */
 int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_weights *w,
                      const uint8_t *resident, hipStream_t s);
 
@@ -133,13 +152,20 @@ int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_weights *w,
  * n_streams in 1..cfg.n_streams.  Only between layers (CEP_ESTATE otherwise). */
 int cep_set_policy(cep_ctx *ctx, int policy, int threshold_pairs, int n_streams);
 
-/* Open layer `generation`.  n_replicas <= R_max; chunks_per_replica: host
- * [n_replicas], the number of chunks each replica will submit (the final
- * flush fires after the last of them).  out: device float32
- * [n_replicas][T_max][d]; the combine step writes the rows of delivered
- * tokens, other rows are left untouched (pass zeroed memory for y = 0 there).
- * `out` must stay valid until cep_combine's event completes.  The previous
- * layer must have been combined (CEP_ESTATE otherwise). */
+/* Open layer `generation` (Appendix C, "Asynchronous dispatch": each
+ * dispatch instance carries a generation tag, and every chunk submitted for
+ * this layer must carry it; "Output return and combine": the next layer is
+ * admitted only after the previous one's outputs are in, so the previous
+ * layer must have been combined, CEP_ESTATE otherwise).  n_replicas <= R_max;
+ * chunks_per_replica: host [n_replicas], the number of chunks each replica
+ * will submit (the final flush of Section 3.2, "Launch threshold", fires
+ * after the last of them).  out: device float32 [n_replicas][T_max][d],
+ * caller-owned; the combine writes each delivered token's row once (its sum
+ * over local slots) and leaves the rows of tokens never delivered untouched
+ * (pass zeroed memory for y = 0 there; a zero fill of every row would cost as
+ * much HBM traffic as the combine itself).  `out` must stay valid until
+ * cep_combine's event completes.  Errors: CEP_EINVAL for a bad n_replicas,
+ * a negative chunk count or a NULL pointer. */
 int cep_begin_layer(cep_ctx *ctx, uint32_t generation, int n_replicas,
                     const int *chunks_per_replica, float *out);
 
@@ -155,47 +181,72 @@ int cep_begin_layer(cep_ctx *ctx, uint32_t generation, int n_replicas,
  *   topk_id   [n_rows][k] int32 local expert id in [0, E) or -1 (remote slot)
  *   topk_w    [n_rows][k] float32 routing coefficients
  * n_pairs: host-known count of valid (id >= 0) entries.  arrival: event after
- * which the data is valid (NULL: valid now); the wait is enqueued here, so
- * the event may be recorded again afterwards.  The chunk's metadata is read
- * when its batch launches (all chunks of a batch in one staging launch).
- * May launch batches per policy; never blocks.  chunk_id (optional) receives the chunk's sequence number.
+ * which the data is valid (NULL: valid now).  The wait is enqueued here, on
+ * the stream of the batch that will hold this chunk, so that only that
+ * batch waits for it (a chunk becomes eligible on its own signal, not behind
+ * other replicas' chunks); the event may be recorded again afterwards.  The
+ * chunk's metadata is read when its batch launches (all chunks of a batch in
+ * one staging launch).  May launch batches per policy; never blocks.
+ * chunk_id (optional) receives the chunk's sequence number.
  * Errors: CEP_ESTATE for a wrong generation or a closed layer, CEP_EINVAL
  * for bad sizes, CEP_ENOMEM if the layer's rows exceed the arena
- * (R_max * T_max rows) or n_pairs exceeds max_pairs_per_batch.  Ids outside
- * [-1, E) or a wrong n_pairs are detected on the device and reported by
- * cep_get_status. */
+ * (R_max * T_max rows) or n_pairs exceeds max_pairs_per_batch; nothing of
+ * the chunk is recorded then.  CEP_ESTATE also when a batch would launch
+ * while an expert without resident weights has no fetch this layer: the
+ * chunk is recorded and stays pending (cep_weight_fetch, then cep_flush,
+ * launch it).  Ids outside [-1, E) or a wrong n_pairs are detected on the
+ * device and reported by cep_get_status. */
 int cep_submit_chunk(cep_ctx *ctx, uint32_t generation, int replica, int n_rows, int n_pairs,
                      const int32_t *token_idx, const void *x, const int32_t *topk_id,
                      const float *topk_w, hipEvent_t arrival, int64_t *chunk_id);
 
 /* Launch everything pending now (explicit final flush, Section 3.2).
- * No-op when nothing is pending. */
+ * No-op when nothing is pending.  CEP_ESTATE as for cep_submit_chunk when an
+ * expert without resident weights has no fetch this layer. */
 int cep_flush(cep_ctx *ctx);
 
 /* One-shot weight fetch (Section 3.3, Algorithm 1's AsyncFetch; Appendix C,
  * "One-shot weight fetching").  Copies the packed blobs src_blobs[i] (device
  * pointers, each cep_packed_expert_bytes, e.g. from cep_pack_experts) of local
  * experts ids[i] into the context's fetch buffer on stream `side` and returns
- * a library-owned event `ready` that completes with the copy.  Grouped FFN
- * work of these experts in later batches of this layer runs on a helper
- * stream that waits for `ready`; other experts are not delayed.  One fetch
- * per layer: a second call returns CEP_EBUSY.  Total bytes above
- * fetch_buffer_bytes: CEP_ENOMEM and nothing is copied.  Duplicate or
- * out-of-range ids: CEP_EINVAL.  Batches launched before the fetch use the
- * resident weights.  src_blobs must stay valid until `ready` completes. */
+ * a library-owned event `ready` that completes with the copy (side NULL: a
+ * library stream).  In later batches of this layer, the grouped GEMMs of
+ * these experts run after the batch's resident experts' GEMMs and wait for
+ * `ready`; the resident experts' work is not delayed.  When the
+ * fetch mode is CEP_FETCH_IN_PLACE, or a copy fails to start (Appendix C,
+ * "FFN reassignment commit and fallback": a failed copy leaves the work
+ * where it can run and triggers no new decision), nothing is copied: the
+ * experts' tiles read src_blobs in place, *ready is NULL, and cep_get_stats
+ * reports the fetch as in place (with "fallback" after a failed copy).  The
+ * output is the same, bit for bit, in every mode.  One fetch per layer: a
+ * second call returns CEP_EBUSY.  Total bytes above fetch_buffer_bytes:
+ * CEP_ENOMEM and nothing is copied.  Duplicate or out-of-range ids:
+ * CEP_EINVAL.  Batches launched before the fetch use the resident weights;
+ * an expert without resident weights must be fetched before the first batch
+ * of the layer launches.  src_blobs must stay valid until cep_combine's
+ * `done` event completes (the layer barrier also waits for the copy). */
 int cep_weight_fetch(cep_ctx *ctx, const int *ids, int n, const void *const *src_blobs,
                      hipStream_t side, hipEvent_t *ready);
 
+/* Fetch mode of the following layers' cep_weight_fetch (enum cep_fetch_mode).
+ * Only between layers (CEP_ESTATE otherwise); CEP_EINVAL for an unknown mode. */
+int cep_set_fetch_mode(cep_ctx *ctx, int mode);
+
 /* Layer barrier (Appendix C, "Output return and combine": the next layer is
  * admitted only after all outputs are in).  Flushes pending chunks, makes
- * stream s wait for every batch of the layer, and returns a library-owned
- * event `done` (may be NULL) recorded on s after which `out` is final.
+ * stream s wait for every batch of the layer (and for the layer's weight
+ * copy), and returns a library-owned event `done` (may be NULL) recorded on
+ * s after which `out` is final.
  * Closes the layer.  CEP_ESTATE if the layer is not open or chunks are still
  * expected (call cep_flush first to end a layer early). */
 int cep_combine(cep_ctx *ctx, hipStream_t s, hipEvent_t *done);
 
-/* Routing metadata of batch `batch` of the last layer (requires
- * cfg.record_routing; waits for that batch).  Host outputs, any may be NULL:
+/* Routing metadata of batch `batch` of the last layer: the per-expert row
+ * counts, the tile-aligned offsets and the inverse map of one grouped
+ * invocation (Appendix C, "Grouped FFN invocations"), for checking against a
+ * reference (requires cfg.record_routing; waits for that batch).  CEP_EINVAL
+ * for an unknown batch, CEP_ESTATE if record_routing is off and an array
+ * was asked for.  Host outputs, any may be NULL:
  *   align [1]: M-tile alignment A;  n_pairs [1]; n_rows [1]
  *   cnt [E]; off [E+1] unpadded; off_pad [E+1] A-aligned
  *   perm_src [n_pairs]: flat pair index (row_in_batch * k + slot) of each
@@ -217,13 +268,19 @@ int cep_set_phase_timing(cep_ctx *ctx, int on);
 /* Number of batches launched in the current (or last) layer. */
 int cep_get_batch_count(const cep_ctx *ctx);
 
-/* Waits for the layer's work and writes a JSON object to buf (host, cap
- * bytes, NUL-terminated; CEP_ENOMEM if too small): per batch its chunks,
+/* Timing of the last layer, for the measurements of Section 4.3 (per-chunk
+ * latency, FFN throughput of streamed against synchronous launches) and the
+ * readiness timing of Appendix A ("Timing and readiness gaps": when each
+ * replica's inputs arrived).  Waits for the layer's work and writes a JSON
+ * object to buf (host, cap bytes, NUL-terminated; CEP_ENOMEM if too small;
+ * CEP_EINVAL for NULL): per batch its chunks,
  * rows, pairs, stream slot, start/end in ms from the layer's origin
  * (cep_begin_layer) and the durations of its routing, GEMM1, GEMM2 and
- * combine phases (HIP events on the batch stream between the launches); per
+ * combine phases (HIP events on the batch stream between the launches; for
+ * a batch with fetched experts also when its fetched experts' GEMMs started,
+ * after the copy, and their GEMM1 and GEMM2 durations, -1 otherwise); per
  * chunk its arrival (when a timing event was given, else -1) in the same
- * clock; and the fetch interval. */
+ * clock; and the fetch (interval, bytes copied, experts, in place or not). */
 int cep_get_stats(cep_ctx *ctx, char *buf, size_t cap);
 
 /* Waits for all work and reads the device-side error word: CEP_OK, or

@@ -95,5 +95,19 @@ def dequantize_weight(codes: np.ndarray, scale: np.ndarray) -> np.ndarray:
     """float64 values of one [rows][cols] weight matrix with one scale per
     128x128 block (scale shape [rows/128][cols/128])."""
     r, c = codes.shape
-    v = decode(codes).reshape(r // BLOCK, BLOCK, c // BLOCK, BLOCK)
+    # the values of all 256 codes, looked up per element (the same values as
+    # decode() of each code; a weight matrix has tens of millions of codes)
+    v = _code_values()[np.asarray(codes, dtype=np.uint8)].reshape(r // BLOCK, BLOCK,
+                                                                 c // BLOCK, BLOCK)
     return (v * scale.astype(np.float64)[:, None, :, None]).reshape(r, c)
+
+
+_VALUES = None
+
+
+def _code_values() -> np.ndarray:
+    """decode() of codes 0..255, computed once."""
+    global _VALUES
+    if _VALUES is None:
+        _VALUES = decode(np.arange(256, dtype=np.uint8))
+    return _VALUES

@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(_HERE, "libcep.so")
 CEP_OK, CEP_EINVAL, CEP_ENOMEM, CEP_EHIP, CEP_ESTATE, CEP_EBUSY = 0, -1, -2, -3, -4, -5
 CEP_F32, CEP_BF16, CEP_FP8_E4M3_B128, CEP_MXFP4 = 0, 1, 2, 3
 CEP_WAIT_ALL, CEP_PER_CHUNK, CEP_THRESHOLD = 0, 1, 2
+CEP_FETCH_COPY, CEP_FETCH_IN_PLACE, CEP_FETCH_FAIL_COPY = 0, 1, 2
 STATUS_NAMES = {0: "CEP_OK", -1: "CEP_EINVAL", -2: "CEP_ENOMEM", -3: "CEP_EHIP",
                 -4: "CEP_ESTATE", -5: "CEP_EBUSY"}
 
@@ -23,6 +24,7 @@ EXPORTED = ["cep_packed_expert_bytes", "cep_pack_experts", "cep_init_experts", "
             "cep_begin_layer", "cep_submit_chunk", "cep_flush", "cep_weight_fetch",
             "cep_combine", "cep_get_batch_routing", "cep_get_batch_count", "cep_get_stats",
             "cep_get_status", "cep_last_error", "cep_destroy", "cep_set_phase_timing",
+            "cep_set_fetch_mode",
             "cep_profile_create",
             "cep_profile_peak", "cep_profile_theta", "cep_profile_eta", "cep_profile_latency",
             "cep_profile_destroy", "cep_oewf_create", "cep_oewf_begin_layer", "cep_oewf_set_rank",
@@ -100,6 +102,7 @@ def lib():
         L.cep_last_error.restype = ctypes.c_char_p
         L.cep_destroy.argtypes = [vp]
         L.cep_set_phase_timing.argtypes = [vp, i32]
+        L.cep_set_fetch_mode.argtypes = [vp, i32]
         i64, f64 = ctypes.c_int64, ctypes.c_double
         L.cep_profile_create.argtypes = [P(i64), P(f64), i32, P(vp)]
         L.cep_profile_peak.argtypes = [vp]
@@ -273,6 +276,10 @@ def cep_get_stats(ctx) -> dict:
 
 def cep_set_phase_timing(ctx, on=True):
     _check(ctx, lib().cep_set_phase_timing(ctx, 1 if on else 0))
+
+
+def cep_set_fetch_mode(ctx, mode):
+    _check(ctx, lib().cep_set_fetch_mode(ctx, mode))
 
 
 def cep_get_status(ctx):

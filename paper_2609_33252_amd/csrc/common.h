@@ -54,23 +54,15 @@ struct Tile {
   int pad;
 };
 
-// Where each expert's packed weight blob lives: resident experts at
-// res + e * bytes; fetched experts (bit e of fetched set) in the fetch
-// buffer at slot = number of fetched experts with a smaller id.
+// Where each expert's packed weight blob lives for one grouped invocation:
+// resident experts in the context's region, fetched experts in the fetch
+// buffer (or, after a failed or skipped copy, in the donor region itself),
+// experts without weights null (the host never launches tiles for them).
 struct BlobTable {
-  const uint8_t *res;
-  const uint8_t *fetch;
-  size_t bytes;
-  uint64_t fetched;
+  const uint8_t *blob[kMaxExperts];
 };
 
-__host__ __device__ inline const uint8_t *blob_of(const BlobTable &t, int e) {
-  if ((t.fetched >> e) & 1) {
-    const uint64_t below = t.fetched & ((1ull << e) - 1);
-    return t.fetch + (size_t)__builtin_popcountll(below) * t.bytes;
-  }
-  return t.res + (size_t)e * t.bytes;
-}
+__host__ __device__ inline const uint8_t *blob_of(const BlobTable &t, int e) { return t.blob[e]; }
 
 // Packed blob layout of one expert (byte offsets from the blob start).
 //   bf16: W1p [2I][d] bf16, W2p [d][I] bf16, in bf16_block_index order
@@ -190,7 +182,11 @@ struct Scratch {
   void *h;             // [max_mpad][I] bf16 or e4m3
   float *hs;           // scales of h, laid out like xs (K = I)
   int s_ld;            // row stride of xs / hs (= max_mpad, a multiple of 256)
-  __bf16 *y;           // [max_mpad][d] bf16, already scaled by the coefficient
+  void *y;             // [max_mpad][d] expert outputs already scaled by the
+                       // coefficient: float32 with bf16 weights (the combine
+                       // then sums exactly the float32 products), bf16 with
+                       // e4m3 / MXFP4 weights (their h quantisation error is
+                       // ~2^-4, a bf16 rounding ~2^-9 adds nothing measurable)
 };
 
 // Device error word bits.
@@ -235,8 +231,9 @@ hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows,
                         int align, int expected_pairs, int max_mpad, int max_tiles,
                         uint64_t fetched_mask, int x_dtype, int wk, int d, int split_cu,
                         int n_tiles_n, bool var, uint32_t *err, hipStream_t s);
+// y_f32: the grouped outputs are float32 (bf16 weights), else bf16
 hipError_t launch_combine(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int d,
-                          float *out, hipStream_t s);
+                          bool y_f32, float *out, hipStream_t s);
 
 // grouped GEMMs over the tile lists of `which` (0 resident, 1 fetched) of a
 // scratch whose lists hold list_cap tiles each; the grid covers grid_tiles

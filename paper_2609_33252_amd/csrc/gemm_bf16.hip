@@ -216,16 +216,10 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
     const char *arow[NAL_];
     CEP_AROWS(arow)
     // Stage s is issued at the barrier of step s - STAGES + 1 (the prologue
-    // issues stages 0 .. STAGES-2), into the buffer of stage s - STAGES,
+    // below issues stages 0 .. STAGES-2), into the buffer of stage s - STAGES,
     // whose last fragment reads completed before the MFMAs of step
     // s - STAGES.
-#pragma unroll
-    for (int s = 0; s < STAGES - 1; ++s)
-      if (s < nk) CEP_DMA_STAGE(s);
-    // stage 0 landed when at most the later prologue stages are outstanding
-    wait_stages<PER, STAGES - 2>(min(nk - 1, STAGES - 2));
-    __builtin_amdgcn_s_barrier();
-
+    //
     // Every step issues one stage of loads, so the vmcnt waits are constants
     // and the loop body is one basic block: steps past the end reload the
     // last K step into a buffer nobody reads again.  Sub-steps 0 .. KK-2 of
@@ -422,8 +416,32 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
 
   // 32x32 accumulator layout: lane l, element r -> column l%32,
   // row 8*(r/4) + 4*(l/32) + r%4.
+  if constexpr (PIPE && !SWIGLU) {
+    // float32 outputs straight from the accumulators: one store instruction
+    // writes 32 consecutive columns (128 bytes) of two rows
+    static_assert(WGM == 2 && !VAR, "two wave rows");
+    float *Y = (float *)g.out;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int lr = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (lr >= t.rows) continue;
+        const size_t row = (size_t)t.row0 + lr;
+        const float w = g.wrow[row];
+        const size_t ybase = row * g.N + nt * BN + wn * WN + (lane & 31);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) Y[ybase + j * 32] = acc[i][j][r] * w;
+      }
+    }
+    // every wave's last operand reads completed: the ring is free for the
+    // next tile's loads (the stores may still be in flight)
+    wait_lgkm0();
+    __builtin_amdgcn_s_barrier();
+    continue;
+  }
   if constexpr (PIPE) {
-    // The output tile goes through LDS: each wave writes its bf16 results
+    // The h tile goes through LDS: each wave writes its bf16 results
     // into the (now idle) operand ring, rows of wave row 0 in sA and of wave
     // row 1 in sB, then the workgroup writes whole rows with 16-byte stores
     // (a store instruction covers two to four full rows instead of 64
@@ -431,9 +449,9 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
     // so the two half-waves of one element write (rows r and r+4) use
     // different banks.
     static_assert(WGM == 2 && !VAR, "staged epilogue: two wave rows");
-    constexpr int CB = SWIGLU ? BN / 2 : BN;  // output columns of the tile
-    constexpr int CPR = CB / 8;               // 16-byte chunks per output row
-    constexpr int WCB = SWIGLU ? WN / 2 : WN; // output columns of one wave
+    constexpr int CB = BN / 2;   // h columns of the tile
+    constexpr int CPR = CB / 8;  // 16-byte chunks per output row
+    constexpr int WCB = WN / 2;  // h columns of one wave
     static_assert(WM * CB * 2 <= (int)sizeof(sA) && WM * CB * 2 <= (int)sizeof(sB),
                   "a wave row's outputs fit one operand ring");
     static_assert(CPR % 4 == 0 && CPR >= 16, "swizzle stays inside the row");
@@ -449,24 +467,16 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int lr = i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (SWIGLU) {
-          // fragment pairs (2*j2, 2*j2+1) are the gate and up columns of h
-          // columns wn*WCB + j2*32 + [0, 32) of the tile
+        // fragment pairs (2*j2, 2*j2+1) are the gate and up columns of h
+        // columns wn*WCB + j2*32 + [0, 32) of the tile
 #pragma unroll
-          for (int j2 = 0; j2 < FN / 2; ++j2)
-            st[soff(lr, wn * WCB + j2 * 32 + (lane & 31))] =
-                (__bf16)silu_mul(acc[i][2 * j2][r], acc[i][2 * j2 + 1][r]);
-        } else {
-          // padding rows read a stale coefficient; they are never stored
-          const float w = g.wrow[(size_t)t.row0 + wm * WM + lr];
-#pragma unroll
-          for (int j = 0; j < FN; ++j)
-            st[soff(lr, wn * WCB + j * 32 + (lane & 31))] = (__bf16)(acc[i][j][r] * w);
-        }
+        for (int j2 = 0; j2 < FN / 2; ++j2)
+          st[soff(lr, wn * WCB + j2 * 32 + (lane & 31))] =
+              (__bf16)silu_mul(acc[i][2 * j2][r], acc[i][2 * j2 + 1][r]);
       }
     }
     __syncthreads();
-    const size_t ldo = SWIGLU ? g.N / 2 : g.N;
+    const size_t ldo = g.N / 2;
     __bf16 *O = (__bf16 *)g.out + (size_t)t.row0 * ldo + (size_t)nt * CB;
 #pragma unroll 4
     for (int q = tid; q < BM * CPR; q += 64 * NW) {
@@ -532,10 +542,10 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
           H[hbase + j2 * 32] = (__bf16)silu_mul(acc[i][2 * j2][r], acc[i][2 * j2 + 1][r]);
       } else {
         const float w = g.wrow[row];
-        __bf16 *Y = (__bf16 *)g.out;
+        float *Y = (float *)g.out;
         const size_t ybase = row * g.N + nt * BN + wn * WN + (lane & 31);
 #pragma unroll
-        for (int j = 0; j < FN; ++j) Y[ybase + j * 32] = (__bf16)(acc[i][j][r] * w);
+        for (int j = 0; j < FN; ++j) Y[ybase + j * 32] = acc[i][j][r] * w;
       }
     }
   }

@@ -29,7 +29,8 @@ struct GemmArgs {
   int K, N;               // contraction length, packed output columns
   size_t b_off, bs_off;   // offsets of B and its scales in each blob
   BlobTable bt;
-  void *out;              // H [mpad][N/2] (GEMM1) or Y [mpad][N] bf16 (GEMM2)
+  void *out;              // H [mpad][N/2] (GEMM1) or Y [mpad][N] (GEMM2: float32
+                          // with bf16 weights, bf16 with e4m3 / MXFP4 weights)
   float *out_s;           // quantised GEMM1: h scales (layout of As, K = N/2)
   const float *wrow;      // GEMM2: routing coefficient per grouped row
   // bf16 GEMM1 with A == nullptr: grouped row r is the batch's input row

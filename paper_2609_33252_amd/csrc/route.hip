@@ -533,12 +533,13 @@ __global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0
 
 // --------------------------------------------------------------- combine
 // One block per batch row: out[dst] = sum over its valid slots, in slot
-// order, of the grouped output rows (bf16, already scaled by their
-// coefficient), accumulated in float32.
+// order, of the grouped output rows (already scaled by their coefficient;
+// float32, or bf16 with YF32 false), accumulated in float32.
 // The row's valid slot positions are gathered once into LDS; each thread
 // then issues the loads of all its columns before summing, slot by slot.
 constexpr int kCombineCols = 4;  // float4 columns per thread per pass
 
+template <bool YF32>
 __global__ __launch_bounds__(256) void k_combine(Arena a, Scratch sc, int row0, int k, int d,
                                                  float *__restrict__ out) {
   __shared__ int s_pos[kMaxTopK];
@@ -560,12 +561,31 @@ __global__ __launch_bounds__(256) void k_combine(Arena a, Scratch sc, int row0, 
   __syncthreads();
   const int n = s_n, d4 = d / 4;
   float4 *o = (float4 *)(out + (size_t)dst * d);
-  const uint2 *y = (const uint2 *)sc.y;  // four bf16 per column group
   for (int c0 = threadIdx.x; c0 < d4; c0 += blockDim.x * kCombineCols) {
     float4 acc[kCombineCols];
 #pragma unroll
     for (int u = 0; u < kCombineCols; ++u) acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int j = 0; j < n; ++j) {
+    if constexpr (YF32) {
+      const float4 *y = (const float4 *)sc.y;
+      for (int j = 0; j < n; ++j) {
+        const float4 *yr = y + (size_t)s_pos[j] * d4;
+        float4 v[kCombineCols];
+#pragma unroll
+        for (int u = 0; u < kCombineCols; ++u) {
+          const int c = c0 + u * blockDim.x;
+          v[u] = c < d4 ? yr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < kCombineCols; ++u) {
+          acc[u].x += v[u].x;
+          acc[u].y += v[u].y;
+          acc[u].z += v[u].z;
+          acc[u].w += v[u].w;
+        }
+      }
+    }
+    const uint2 *y = (const uint2 *)sc.y;  // four bf16 per column group
+    for (int j = 0; !YF32 && j < n; ++j) {
       const uint2 *yr = y + (size_t)s_pos[j] * d4;
       uint2 v[kCombineCols];
 #pragma unroll
@@ -783,9 +803,12 @@ hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows,
 }
 
 hipError_t launch_combine(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int d,
-                          float *out, hipStream_t s) {
+                          bool y_f32, float *out, hipStream_t s) {
   if (n_rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_combine, dim3(n_rows), dim3(256), 0, s, a, sc, row0, k, d, out);
+  if (y_f32)
+    hipLaunchKernelGGL(k_combine<true>, dim3(n_rows), dim3(256), 0, s, a, sc, row0, k, d, out);
+  else
+    hipLaunchKernelGGL(k_combine<false>, dim3(n_rows), dim3(256), 0, s, a, sc, row0, k, d, out);
   return hipGetLastError();
 }
 

@@ -37,11 +37,14 @@ struct BatchRec {
   int row0, n_rows, n_pairs;
   int slot;
   int align;  // per-expert row alignment of the grouped layout (GEMM M tile)
-  bool helper;
+  bool fetched;  // the batch has fetched experts' tiles (run after the copy)
   hipEvent_t ev_start, ev_end;
   // on the batch stream after: routing, GEMM1, GEMM2, combine
   hipEvent_t ev_phase[4];
-  bool phases;  // ev_phase recorded (phase timing on at launch)
+  // fetched experts' GEMMs, on the batch stream after the resident experts'
+  // GEMMs: after the wait for the copy, after GEMM1, after GEMM2
+  hipEvent_t ev_fphase[3];
+  bool phases;  // ev_phase (and ev_fphase for batches with fetched tiles) recorded
   // recorded routing (record_routing only), pinned host memory
   int32_t *h_cnt = nullptr, *h_off = nullptr, *h_off_pad = nullptr, *h_perm = nullptr,
           *h_pos = nullptr;
@@ -60,17 +63,20 @@ struct cep_ctx {
   BlobLayout L{};
   uint8_t *w_res = nullptr;  // E blobs
   std::vector<uint8_t> resident;
+  uint64_t nonres_mask = 0;  // experts without resident weights
   uint8_t *fetch_buf = nullptr;
+  int fetch_mode = CEP_FETCH_COPY;
   Arena arena{};
   int arena_cap = 0;
   uint32_t *d_err = nullptr;
   int max_pairs = 0, max_mpad = 0, max_tiles = 0, max_blocks = 0, max_rows = 0;
   int n_cu = 0;  // compute units of the device (tile-plan makespan estimate)
   hipStream_t ingest = nullptr;
-  hipStream_t st[8] = {}, helper[8] = {};
-  // slot streams and helper streams that ran batches since the last layer
-  // barrier; the next layer's staging waits for exactly these
-  unsigned used_st = 0, used_helper = 0;
+  hipStream_t st[8] = {};
+  hipStream_t copy = nullptr;  // the fetch's copies when the caller gives no stream
+  // slot streams that ran batches (or hold arrival waits) since the last
+  // layer barrier; the next layer's staging waits for exactly these
+  unsigned used_st = 0;
   Scratch sc[8] = {};
   std::vector<void *> allocs;
   // policy
@@ -89,12 +95,19 @@ struct cep_ctx {
   std::vector<BatchRec> batches;
   bool origin_set = false;
   hipEvent_t ev_origin = nullptr;
-  // fetch
+  // fetch: the one decision of this layer; fetched_mask = experts whose
+  // copies gate their tiles, inplace_mask = experts read from the donor
+  // region in place (no copy, or a copy that failed to start)
   bool fetched = false;
-  uint64_t fetched_mask = 0;
+  uint64_t fetched_mask = 0, inplace_mask = 0;
+  bool fetch_copy_issued = false;  // a copy was enqueued (this layer)
+  bool fetch_copy_prev = false;    // ev_fetch_ready holds an earlier layer's copy
+  bool fetch_fallback = false;     // this layer's copy failed: read in place
+  // where each expert's weights are read from in this layer (null: none)
+  const uint8_t *blob_ptr[kMaxExperts] = {};
   hipEvent_t ev_fetch_start = nullptr, ev_fetch_ready = nullptr;
   // sync-only events, one set per slot (re-recorded per batch)
-  hipEvent_t ev_ingest[8] = {}, ev_routed[8] = {}, ev_helper[8] = {};
+  hipEvent_t ev_ingest[8] = {};
   hipEvent_t ev_layer_done = nullptr, ev_layer_ingest = nullptr;
   // the last event recorded on the ingest stream with no kernel after it
   // (the end event of a batch that ran there), or null
@@ -219,6 +232,20 @@ int stage_chunks(cep_ctx *c, int64_t upto, hipStream_t s) {
   return CEP_OK;
 }
 
+// Stream slot and stream of the batch that will hold the chunks pending now
+// (the next batch to launch).  With one stream, batches run on the ingest
+// stream itself.
+int pending_slot(const cep_ctx *c) { return (int)(c->batches.size() % c->n_streams); }
+hipStream_t pending_stream(const cep_ctx *c) {
+  return c->n_streams == 1 ? c->ingest : c->st[pending_slot(c)];
+}
+
+// Experts that have pairs routed to them but no weights this layer: neither
+// resident nor fetched (copied or read in place).
+uint64_t missing_experts(const cep_ctx *c) {
+  return c->nonres_mask & ~(c->fetched_mask | c->inplace_mask);
+}
+
 // Launch all pending chunks as one grouped invocation on the next stream slot.
 int launch_pending(cep_ctx *c) {
   const int64_t nch = (int64_t)c->chunks.size() - c->pending_first;
@@ -229,10 +256,13 @@ int launch_pending(cep_ctx *c) {
   }
   const cep_config &cfg = c->cfg;
   const int E = cfg.n_local_experts, k = cfg.top_k, d = cfg.d_model, I = cfg.d_ff;
-  // every expert whose weights are not resident must have been fetched
-  for (int e = 0; e < E; ++e)
-    if (!c->resident[e] && !((c->fetched_mask >> e) & 1))
-      return fail(c, CEP_ESTATE, "expert %d has no resident weights and no fetch this layer", e);
+  // every expert without resident weights must have been fetched (copied or
+  // read in place) before a batch launches
+  if (const uint64_t miss = missing_experts(c))
+    return fail(c, CEP_ESTATE,
+                "expert %d has no resident weights and no fetch this layer; the chunk stays "
+                "pending (cep_weight_fetch, then cep_flush)",
+                __builtin_ctzll(miss));
 
   BatchRec b{};
   b.first_chunk = c->pending_first;
@@ -240,11 +270,11 @@ int launch_pending(cep_ctx *c) {
   b.row0 = c->chunks[c->pending_first].row0;
   b.n_rows = c->pending_rows;
   b.n_pairs = c->pending_pairs;
-  b.slot = (int)(c->batches.size() % c->n_streams);
+  b.slot = pending_slot(c);
   const int slot = b.slot;
   // one stream: batches run on the ingest stream itself, in submission
   // order after their chunks' staging, without a cross-stream hop
-  hipStream_t s = c->n_streams == 1 ? c->ingest : c->st[slot];
+  hipStream_t s = pending_stream(c);
   if (s != c->ingest) c->used_st |= 1u << slot;
   const Scratch &sc = c->sc[slot];
   const int P = b.n_pairs;
@@ -256,13 +286,18 @@ int launch_pending(cep_ctx *c) {
   b.phases = c->phase_timing;
   b.ev_start = b.phases ? timing_event(c, false) : nullptr;
   b.ev_end = timing_event(c, cfg.record_routing != 0);
+  b.fetched = c->fetched_mask != 0;
   for (hipEvent_t &e : b.ev_phase) e = b.phases ? timing_event(c, false) : nullptr;
+  for (hipEvent_t &e : b.ev_fphase) e = b.phases && b.fetched ? timing_event(c, false) : nullptr;
   if ((b.phases && !b.ev_start) || !b.ev_end ||
-      (b.phases && (!b.ev_phase[0] || !b.ev_phase[1] || !b.ev_phase[2] || !b.ev_phase[3])))
+      (b.phases && (!b.ev_phase[0] || !b.ev_phase[1] || !b.ev_phase[2] || !b.ev_phase[3])) ||
+      (b.phases && b.fetched && (!b.ev_fphase[0] || !b.ev_fphase[1] || !b.ev_fphase[2])))
     return fail(c, CEP_EHIP, "hipEventCreate failed");
 
-  // the chunks' arrival waits sit on the ingest stream: the batch stream
-  // follows it, then stages every chunk submitted so far (the batch's, and
+  // the batch's chunks' arrival waits already sit on this stream (enqueued
+  // at submit); the ingest stream carries the layer's start (after the
+  // previous layer's batches, which read the arena), which the batch stream
+  // follows; then it stages every chunk submitted so far (the batch's, and
   // chunks without local pairs before it) in one launch per group
   if (s != c->ingest) {
     HIPCHK(c, hipEventRecord(c->ev_ingest[slot], c->ingest));
@@ -284,29 +319,30 @@ int launch_pending(cep_ctx *c) {
                          2 * I / kBf16TileN, var, c->d_err, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[0], s));
 
-  BlobTable bt{c->w_res, c->fetch_buf, c->L.bytes, c->fetched_mask};
+  BlobTable bt{};
+  for (int e = 0; e < E; ++e) bt.blob[e] = c->blob_ptr[e];
   // bf16 rows with bf16 weights are not packed: GEMM1 reads them in place
   const Arena *gather = c->wk == kWBf16 && cfg.x_dtype == CEP_BF16 ? &c->arena : nullptr;
 
-  b.helper = c->fetched_mask != 0;
-  if (b.helper) {
-    hipStream_t h = c->helper[slot];
-    c->used_helper |= 1u << slot;
-    HIPCHK(c, hipEventRecord(c->ev_routed[slot], s));
-    HIPCHK(c, hipStreamWaitEvent(h, c->ev_routed[slot], 0));
-    HIPCHK(c, hipStreamWaitEvent(h, c->ev_fetch_ready, 0));
-    HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
-                           gather, b.row0, k, h));
-    HIPCHK(c, launch_gemm2(sc, 1, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I, h));
-    HIPCHK(c, hipEventRecord(c->ev_helper[slot], h));
-  }
   HIPCHK(c, launch_gemm1(sc, 0, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
                          gather, b.row0, k, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[1], s));
   HIPCHK(c, launch_gemm2(sc, 0, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[2], s));
-  if (b.helper) HIPCHK(c, hipStreamWaitEvent(s, c->ev_helper[slot], 0));
-  HIPCHK(c, launch_combine(c->arena, sc, b.row0, b.n_rows, k, d, c->out, s));
+  // fetched experts' tiles (the scan's second tile lists) run after the
+  // resident experts' GEMMs, once their weights are in: the copy overlaps
+  // the resident work and delays nothing before it (Appendix C, "One-shot
+  // weight fetching": the donor-side work does not wait for the copy)
+  if (b.fetched) {
+    HIPCHK(c, hipStreamWaitEvent(s, c->ev_fetch_ready, 0));
+    if (b.phases) HIPCHK(c, hipEventRecord(b.ev_fphase[0], s));
+    HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
+                           gather, b.row0, k, s));
+    if (b.phases) HIPCHK(c, hipEventRecord(b.ev_fphase[1], s));
+    HIPCHK(c, launch_gemm2(sc, 1, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I, s));
+    if (b.phases) HIPCHK(c, hipEventRecord(b.ev_fphase[2], s));
+  }
+  HIPCHK(c, launch_combine(c->arena, sc, b.row0, b.n_rows, k, d, c->wk == kWBf16, c->out, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[3], s));
 
   if (cfg.record_routing) {
@@ -413,6 +449,8 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
   c->resident.assign(E, 1);
   if (resident)
     for (int e = 0; e < E; ++e) c->resident[e] = resident[e] ? 1 : 0;
+  for (int e = 0; e < E; ++e)
+    if (!c->resident[e]) c->nonres_mask |= 1ull << e;
   c->arena_cap = cfg->max_replicas * cfg->max_tokens_per_replica;
   c->max_rows = c->arena_cap;
   const long long def_pairs = (long long)c->arena_cap * k;
@@ -450,7 +488,7 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
     // bf16 rows with bf16 weights are read in place by GEMM1 (no packed copy)
     if (!(c->wk == kWBf16 && cfg->x_dtype == CEP_BF16)) sc.xg = A(xes * c->max_mpad * d);
     sc.h = A(xes * c->max_mpad * I);
-    sc.y = (__bf16 *)A(sizeof(__bf16) * c->max_mpad * d);
+    sc.y = A((c->wk == kWBf16 ? 4 : 2) * (size_t)c->max_mpad * d);
     if (c->wk != kWBf16) {  // e4m3 float scales per 128, or E8M0 bytes per 32: same size
       sc.xs = (float *)A(sizeof(float) * c->max_mpad * (d / 128));
       sc.hs = (float *)A(sizeof(float) * c->max_mpad * (I / 128));
@@ -466,11 +504,10 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
   bool ok = hipStreamCreateWithFlags(&c->ingest, hipStreamNonBlocking) == hipSuccess;
   for (int i = 0; i < cfg->n_streams && ok; ++i) {
     ok = hipStreamCreateWithFlags(&c->st[i], hipStreamNonBlocking) == hipSuccess &&
-         hipStreamCreateWithFlags(&c->helper[i], hipStreamNonBlocking) == hipSuccess &&
-         hipEventCreateWithFlags(&c->ev_ingest[i], kDepEvent) == hipSuccess &&
-         hipEventCreateWithFlags(&c->ev_routed[i], kDepEvent) == hipSuccess &&
-         hipEventCreateWithFlags(&c->ev_helper[i], kDepEvent) == hipSuccess;
+         hipEventCreateWithFlags(&c->ev_ingest[i], kDepEvent) == hipSuccess;
   }
+  if (ok && cfg->fetch_buffer_bytes)
+    ok = hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking) == hipSuccess;
   ok = ok && hipEventCreateWithFlags(&c->ev_origin, hipEventDisableSystemFence) == hipSuccess &&
        hipEventCreateWithFlags(&c->ev_fetch_start, hipEventDisableSystemFence) == hipSuccess &&
        hipEventCreate(&c->ev_fetch_ready) == hipSuccess &&
@@ -531,19 +568,15 @@ CEP_API int cep_begin_layer(cep_ctx *c, uint32_t generation, int n_replicas,
   // this layer's ingest work can start: it becomes the clock origin (its
   // event object trades places with the origin's in the timing pool) and
   // the stream carries one marker fewer between layers.
-  hipEvent_t prev_tail = (c->used_st | c->used_helper) == 0 ? c->ingest_tail : nullptr;
+  hipEvent_t prev_tail = c->used_st == 0 ? c->ingest_tail : nullptr;
   // the previous layer's batches may still read the arena: stage after them
   for (int i = 0; i < c->cfg.n_streams; ++i) {
     if ((c->used_st >> i) & 1) {
       HIPCHK(c, hipEventRecord(c->ev_ingest[i], c->st[i]));
       HIPCHK(c, hipStreamWaitEvent(c->ingest, c->ev_ingest[i], 0));
     }
-    if ((c->used_helper >> i) & 1) {
-      HIPCHK(c, hipEventRecord(c->ev_routed[i], c->helper[i]));
-      HIPCHK(c, hipStreamWaitEvent(c->ingest, c->ev_routed[i], 0));
-    }
   }
-  c->used_st = c->used_helper = 0;
+  c->used_st = 0;
   free_batch_records(c);
   c->timing_used[0] = c->timing_used[1] = 0;
   c->gen = generation;
@@ -574,7 +607,12 @@ CEP_API int cep_begin_layer(cep_ctx *c, uint32_t generation, int n_replicas,
   c->ingest_tail = nullptr;
   c->origin_set = true;
   c->fetched = false;
-  c->fetched_mask = 0;
+  c->fetched_mask = c->inplace_mask = 0;
+  c->fetch_copy_prev = c->fetch_copy_prev || c->fetch_copy_issued;
+  c->fetch_copy_issued = false;
+  c->fetch_fallback = false;
+  for (int e = 0; e < c->cfg.n_local_experts; ++e)
+    c->blob_ptr[e] = c->resident[e] ? c->w_res + (size_t)e * c->L.bytes : nullptr;
   c->state = kOpen;
   return CEP_OK;
 }
@@ -597,22 +635,29 @@ CEP_API int cep_submit_chunk(cep_ctx *c, uint32_t generation, int replica, int n
     return fail(c, CEP_ENOMEM, "layer rows exceed max_replicas * max_tokens_per_replica");
   if (n_pairs > c->max_pairs)
     return fail(c, CEP_ENOMEM, "chunk pairs %d exceed max_pairs_per_batch %d", n_pairs, c->max_pairs);
-  // readiness: later work on the ingest stream (and every batch, which
-  // follows it) runs after the chunk's arrival
+  // a chunk that would overflow a batch first launches what is pending,
+  // before anything of this chunk is recorded (a failure leaves the layer as
+  // it was before the call)
+  if (n_pairs > 0 && c->pending_pairs > 0 && c->pending_pairs + n_pairs > c->max_pairs) {
+    int rc = launch_pending(c);
+    if (rc != CEP_OK) return rc;
+  }
+  // readiness (Appendix C, "Asynchronous dispatch": a lane's inputs become
+  // eligible on its own signal): the wait goes on the stream of the batch
+  // that will hold this chunk, ahead of that batch's staging, so no other
+  // batch waits for this chunk's arrival
   if (arrival) {
-    HIPCHK(c, hipStreamWaitEvent(c->ingest, arrival, 0));
-    c->ingest_tail = nullptr;
+    hipStream_t s = pending_stream(c);
+    HIPCHK(c, hipStreamWaitEvent(s, arrival, 0));
+    if (s == c->ingest)
+      c->ingest_tail = nullptr;
+    else
+      c->used_st |= 1u << pending_slot(c);
   }
   ChunkRec ch{replica, c->rows_used, n_rows, n_pairs, arrival, token_idx, x, topk_id, topk_w};
   c->rows_used += n_rows;
   const int64_t id = (int64_t)c->chunks.size();
   if (chunk_id) *chunk_id = id;
-
-  // a chunk that would overflow a batch first launches what is pending
-  if (n_pairs > 0 && c->pending_pairs > 0 && c->pending_pairs + n_pairs > c->max_pairs) {
-    int rc = launch_pending(c);
-    if (rc != CEP_OK) return rc;
-  }
   c->chunks.push_back(ch);
   if (n_pairs > 0) {
     if (c->pending_pairs == 0) c->pending_first = id;
@@ -623,6 +668,8 @@ CEP_API int cep_submit_chunk(cep_ctx *c, uint32_t generation, int replica, int n
   }
   const bool last = (int)c->chunks.size() == c->expected_chunks;
   const bool thresh = c->policy != CEP_WAIT_ALL && c->pending_pairs >= c->theta && c->pending_pairs > 0;
+  // a launch that fails here (an expert without weights) leaves the chunk
+  // pending: cep_weight_fetch and then cep_flush launch it
   if (thresh || last) return launch_pending(c);
   return CEP_OK;
 }
@@ -653,26 +700,63 @@ CEP_API int cep_weight_fetch(cep_ctx *c, const int *ids, int n, const void *cons
     return fail(c, CEP_ENOMEM, "fetch of %zu bytes exceeds the %zu-byte buffer", need,
                 c->cfg.fetch_buffer_bytes);
   c->fetched = true;  // one decision per layer, also when it copies nothing
-  if (n == 0) {
-    if (ready) *ready = nullptr;
+  if (ready) *ready = nullptr;
+  if (n == 0) return CEP_OK;
+  bool in_place = c->fetch_mode == CEP_FETCH_IN_PLACE;
+  if (!in_place) {
+    hipStream_t s = side ? side : c->copy;
+    // do not overwrite the buffer while an earlier layer's batches may still
+    // read it (the earlier layer's barrier event covers all of them), nor
+    // while an earlier layer's copy may still write it
+    if (c->fetch_copy_prev) {
+      HIPCHK(c, hipStreamWaitEvent(s, c->ev_layer_done, 0));
+      HIPCHK(c, hipStreamWaitEvent(s, c->ev_fetch_ready, 0));
+    }
+    HIPCHK(c, hipEventRecord(c->ev_fetch_start, s));
+    // expert e goes to slot = number of fetched experts with a smaller id.  A
+    // copy that fails to start ends the copying; the fetch then falls back to
+    // reading the donor blobs in place (Appendix C, "FFN reassignment commit
+    // and fallback": a failed copy never triggers another fetch decision)
+    for (int i = 0; i < n && !in_place; ++i) {
+      const int slot = __builtin_popcountll(mask & ((1ull << ids[i]) - 1));
+      uint8_t *dst = c->fetch_buf + (size_t)slot * c->L.bytes;
+      const hipError_t e =
+          c->fetch_mode == CEP_FETCH_FAIL_COPY
+              ? hipErrorInvalidValue
+              : hipMemcpyAsync(dst, src_blobs[i], c->L.bytes, hipMemcpyDeviceToDevice, s);
+      if (e != hipSuccess) {
+        (void)hipGetLastError();
+        in_place = true;
+        c->fetch_fallback = true;
+      }
+    }
+    // the copies already enqueued finish before `ready`, which the layer
+    // barrier also waits for
+    HIPCHK(c, hipEventRecord(c->ev_fetch_ready, s));
+    c->fetch_copy_issued = true;
+  }
+  if (in_place) {
+    // fetched experts read their donor blobs where they are: no copy to wait
+    // for, so their tiles run with the resident experts' tiles
+    for (int i = 0; i < n; ++i) c->blob_ptr[ids[i]] = (const uint8_t *)src_blobs[i];
+    c->inplace_mask = mask;
     return CEP_OK;
   }
-  hipStream_t s = side ? side : c->helper[0];
-  // do not overwrite the buffer while an earlier layer may still read it
-  for (int i = 0; i < c->cfg.n_streams; ++i) {
-    HIPCHK(c, hipEventRecord(c->ev_routed[i], c->helper[i]));
-    HIPCHK(c, hipStreamWaitEvent(s, c->ev_routed[i], 0));
-  }
-  HIPCHK(c, hipEventRecord(c->ev_fetch_start, s));
-  // expert e goes to slot = number of fetched experts with a smaller id
   for (int i = 0; i < n; ++i) {
     const int slot = __builtin_popcountll(mask & ((1ull << ids[i]) - 1));
-    uint8_t *dst = c->fetch_buf + (size_t)slot * c->L.bytes;
-    HIPCHK(c, hipMemcpyAsync(dst, src_blobs[i], c->L.bytes, hipMemcpyDeviceToDevice, s));
+    c->blob_ptr[ids[i]] = c->fetch_buf + (size_t)slot * c->L.bytes;
   }
-  HIPCHK(c, hipEventRecord(c->ev_fetch_ready, s));
   c->fetched_mask = mask;
   if (ready) *ready = c->ev_fetch_ready;
+  return CEP_OK;
+}
+
+CEP_API int cep_set_fetch_mode(cep_ctx *c, int mode) {
+  if (!c) return CEP_EINVAL;
+  if (c->state != kIdle) return fail(c, CEP_ESTATE, "cep_set_fetch_mode inside an open layer");
+  if (mode < CEP_FETCH_COPY || mode > CEP_FETCH_FAIL_COPY)
+    return fail(c, CEP_EINVAL, "unknown fetch mode %d", mode);
+  c->fetch_mode = mode;
   return CEP_OK;
 }
 
@@ -685,9 +769,18 @@ CEP_API int cep_combine(cep_ctx *c, hipStream_t s, hipEvent_t *done) {
   int rc = launch_pending(c);
   if (rc != CEP_OK) return rc;
   // chunks after the last batch (no local pairs) are still staged, so their
-  // ids are validated and the caller may release them after `done`
-  rc = stage_chunks(c, (int64_t)c->chunks.size(), c->ingest);
-  if (rc != CEP_OK) return rc;
+  // ids are validated and the caller may release them after `done`; their
+  // arrival waits sit on the stream of the batch that would have held them
+  if (c->staged < (int64_t)c->chunks.size()) {
+    hipStream_t ps = pending_stream(c);
+    if (ps != c->ingest) {
+      HIPCHK(c, hipEventRecord(c->ev_ingest[pending_slot(c)], c->ingest));
+      HIPCHK(c, hipStreamWaitEvent(ps, c->ev_ingest[pending_slot(c)], 0));
+      c->used_st |= 1u << pending_slot(c);
+    }
+    rc = stage_chunks(c, (int64_t)c->chunks.size(), ps);
+    if (rc != CEP_OK) return rc;
+  }
   // every batch of the layer ran on a used slot stream or on the ingest
   // stream
   for (int i = 0; i < c->cfg.n_streams; ++i) {
@@ -702,6 +795,9 @@ CEP_API int cep_combine(cep_ctx *c, hipStream_t s, hipEvent_t *done) {
     if (!c->ingest_tail) HIPCHK(c, hipEventRecord(c->ev_layer_ingest, c->ingest));
     HIPCHK(c, hipStreamWaitEvent(s, c->ingest_tail ? c->ingest_tail : c->ev_layer_ingest, 0));
   }
+  // the layer's copy (also one no batch consumed) has finished reading the
+  // donor blobs and writing the fetch buffer before `done`
+  if (c->fetch_copy_issued) HIPCHK(c, hipStreamWaitEvent(s, c->ev_fetch_ready, 0));
   HIPCHK(c, hipEventRecord(c->ev_layer_done, s));
   if (done) *done = c->ev_layer_done;
   c->state = kIdle;
@@ -743,7 +839,7 @@ CEP_API int cep_get_batch_routing(cep_ctx *c, int batch, int *align, int *n_pair
 CEP_API int cep_get_stats(cep_ctx *c, char *buf, size_t cap) {
   if (!c || !buf) return CEP_EINVAL;
   std::string js = "{\"batches\":[";
-  char tmp[512];
+  char tmp[1024];
   for (size_t i = 0; i < c->batches.size(); ++i) {
     const BatchRec &b = c->batches[i];
     HIPCHK(c, hipEventSynchronize(b.ev_end));
@@ -755,12 +851,21 @@ CEP_API int cep_get_stats(cep_ctx *c, char *buf, size_t cap) {
       HIPCHK(c, hipEventElapsedTime(&ph[p], prev, b.ev_phase[p]));
       prev = b.ev_phase[p];
     }
+    // fetched experts' GEMMs sit between GEMM2 and the combine
+    float h0 = -1, hg1 = -1, hg2 = -1;
+    if (b.phases && b.fetched) {
+      HIPCHK(c, hipEventElapsedTime(&h0, c->ev_origin, b.ev_fphase[0]));
+      HIPCHK(c, hipEventElapsedTime(&hg1, b.ev_fphase[0], b.ev_fphase[1]));
+      HIPCHK(c, hipEventElapsedTime(&hg2, b.ev_fphase[1], b.ev_fphase[2]));
+      HIPCHK(c, hipEventElapsedTime(&ph[3], b.ev_fphase[2], b.ev_phase[3]));
+    }
     snprintf(tmp, sizeof tmp,
              "%s{\"first_chunk\":%lld,\"n_chunks\":%d,\"rows\":%d,\"pairs\":%d,\"slot\":%d,"
-             "\"helper\":%s,\"start_ms\":%.6f,\"end_ms\":%.6f,\"route_ms\":%.6f,"
-             "\"gemm1_ms\":%.6f,\"gemm2_ms\":%.6f,\"combine_ms\":%.6f}",
+             "\"fetched\":%s,\"start_ms\":%.6f,\"end_ms\":%.6f,\"route_ms\":%.6f,"
+             "\"gemm1_ms\":%.6f,\"gemm2_ms\":%.6f,\"combine_ms\":%.6f,"
+             "\"fetched_start_ms\":%.6f,\"fetched_gemm1_ms\":%.6f,\"fetched_gemm2_ms\":%.6f}",
              i ? "," : "", (long long)b.first_chunk, b.n_chunks, b.n_rows, b.n_pairs, b.slot,
-             b.helper ? "true" : "false", t0, t1, ph[0], ph[1], ph[2], ph[3]);
+             b.fetched ? "true" : "false", t0, t1, ph[0], ph[1], ph[2], ph[3], h0, hg1, hg2);
     js += tmp;
   }
   js += "],\"chunks\":[";
@@ -781,15 +886,22 @@ CEP_API int cep_get_stats(cep_ctx *c, char *buf, size_t cap) {
     js += tmp;
   }
   js += "]";
-  if (c->fetched && c->fetched_mask) {
-    float f0 = 0, f1 = 0;
-    HIPCHK(c, hipEventSynchronize(c->ev_fetch_ready));
-    if (c->origin_set) {
-      (void)hipEventElapsedTime(&f0, c->ev_origin, c->ev_fetch_start);
-      (void)hipEventElapsedTime(&f1, c->ev_origin, c->ev_fetch_ready);
+  if (c->fetched && (c->fetched_mask | c->inplace_mask)) {
+    float f0 = -1, f1 = -1;
+    if (c->fetch_copy_issued) {
+      HIPCHK(c, hipEventSynchronize(c->ev_fetch_ready));
+      if (c->origin_set) {
+        (void)hipEventElapsedTime(&f0, c->ev_origin, c->ev_fetch_start);
+        (void)hipEventElapsedTime(&f1, c->ev_origin, c->ev_fetch_ready);
+      }
     }
-    snprintf(tmp, sizeof tmp, ",\"fetch\":{\"start_ms\":%.6f,\"end_ms\":%.6f,\"bytes\":%zu}", f0,
-             f1, (size_t)__builtin_popcountll(c->fetched_mask) * c->L.bytes);
+    // bytes: what the copy moved into the fetch buffer (0 when read in place)
+    snprintf(tmp, sizeof tmp,
+             ",\"fetch\":{\"start_ms\":%.6f,\"end_ms\":%.6f,\"bytes\":%zu,\"experts\":%d,"
+             "\"in_place\":%s,\"fallback\":%s}",
+             f0, f1, (size_t)__builtin_popcountll(c->fetched_mask) * c->L.bytes,
+             __builtin_popcountll(c->fetched_mask | c->inplace_mask),
+             c->inplace_mask ? "true" : "false", c->fetch_fallback ? "true" : "false");
     js += tmp;
   }
   js += "}";
@@ -827,12 +939,10 @@ CEP_API int cep_destroy(cep_ctx *c) {
     if (e) (void)hipEventDestroy(e);
   for (int i = 0; i < 8; ++i) {
     if (c->ev_ingest[i]) (void)hipEventDestroy(c->ev_ingest[i]);
-    if (c->ev_routed[i]) (void)hipEventDestroy(c->ev_routed[i]);
-    if (c->ev_helper[i]) (void)hipEventDestroy(c->ev_helper[i]);
     if (c->st[i]) (void)hipStreamDestroy(c->st[i]);
-    if (c->helper[i]) (void)hipStreamDestroy(c->helper[i]);
   }
   if (c->ingest) (void)hipStreamDestroy(c->ingest);
+  if (c->copy) (void)hipStreamDestroy(c->copy);
   for (void *p : c->allocs) (void)hipFree(p);
   delete c;
   return CEP_OK;

@@ -30,12 +30,16 @@ class Runner:
     """One libcep context holding one workload's experts and chunks."""
 
     def __init__(self, wl: W.Workload, n_streams: int = 4, record_routing: bool = False,
-                 max_pairs: int = 0, use_fetch: bool = True, device: str = "cuda"):
+                 max_pairs=None, use_fetch: bool = True, device: str = "cuda"):
         self.wl = wl
         c = wl.cfg
         self.device = torch.device(device)
         self.use_fetch = use_fetch and bool(wl.fetched)
         scaled = c["w"] in (W.FP8, W.MXFP4)
+        # a batch never holds more pairs than the layer: size every stream
+        # slot's scratch for the layer's pairs (0 would size it for R*T*k)
+        if max_pairs is None:
+            max_pairs = max(1, wl.n_pairs)
         self.cfg = cep.make_config(
             d_model=c["d"], d_ff=c["I"], n_local_experts=c["E"], top_k=c["k"],
             max_replicas=c["R"], max_tokens_per_replica=c["T"], w_dtype=_DT[c["w"]],
@@ -102,7 +106,8 @@ class Runner:
         return sum(ch.n_pairs for ch in self.chunks)
 
     def run(self, policy=cep.CEP_WAIT_ALL, theta=1, n_streams=1, order=None, timed=False,
-            time_scale=1.0, arrival_events=False, out=None, stream=None, inputs_ready=False):
+            time_scale=1.0, arrival_events=False, out=None, stream=None, inputs_ready=False,
+            fetch_mode=None, prefetch=False):
         """Replay one layer; returns the library's done event handle.
 
         order: optional permutation of chunk indices (submission order).
@@ -110,17 +115,25 @@ class Runner:
         inputs_ready: the chunk inputs are resident and no work on the caller's
             stream writes them (steady-state replay of the same layer), so the
             chunks carry no arrival event.
+        fetch_mode: cep_fetch_mode of this and later layers (None: unchanged).
+        prefetch: wait on the host for the weight copy before submitting the
+            chunks (the layer then runs as if the copy had happened earlier).
         """
         out = self.out if out is None else out
         stream = torch.cuda.current_stream(self.device) if stream is None else stream
         ctx = self.ctx
         cep.cep_set_policy(ctx, policy, theta, n_streams)
+        if fetch_mode is not None:
+            cep.cep_set_fetch_mode(ctx, fetch_mode)
         self.gen += 1
         cep.cep_begin_layer(ctx, self.gen, self.chunks_per_replica, out)
         if self.use_fetch:
-            cep.cep_weight_fetch(ctx, list(self.wl.fetched),
-                                 [self.donor.data_ptr() + i * self.blob_bytes
-                                  for i in range(len(self.wl.fetched))], self.side)
+            self.fetch_ready = cep.cep_weight_fetch(
+                ctx, list(self.wl.fetched),
+                [self.donor.data_ptr() + i * self.blob_bytes for i in range(len(self.wl.fetched))],
+                self.side)
+            if prefetch:
+                torch.cuda.synchronize(self.device)
         seq = range(len(self.chunks)) if order is None else order
         # chunk inputs and `out` were written on the caller's stream: every
         # chunk becomes valid only after that work

@@ -1,5 +1,14 @@
 """Shared helpers for the parity tests: oracle references for a workload and
-the tolerance checks.  Inputs come from the seeded generator only."""
+the tolerance checks.  Inputs come from the seeded generator only.
+
+Every output check compares against the plain definition of the routed
+output (float64 expert FFNs, each weighted contribution summed in slot order
+in float64, one rounding to float32 at the end) with the target tolerance.
+A second, tighter regression bound follows: against the plain definition
+for bf16 weights (whose expert outputs reach the combine in float32), and
+against the oracle with each weighted expert output rounded to bf16 for
+e4m3 and MXFP4 weights (the library returns those in bf16).
+"""
 import numpy as np
 import torch
 
@@ -9,10 +18,14 @@ from paper_2609_33252_amd import workload as W
 # Elementwise bound for bf16 inputs with float32 accumulation, and the
 # relative-RMS bound for the e4m3 path (both from the target tolerance of the
 # routed-expert path); the MXFP4 path quantises activations and h to e4m3
-# like the e4m3 path and takes the same bound.
+# like the e4m3 path and takes the same bound, also per output row.
 BF16_ATOL, BF16_RTOL = 1e-2, 1e-2
 FP8_REL_RMS = 4e-2
 F32_REL_RMS = 1e-2
+# Regression bounds (relative RMS), a few times above what the library
+# measures: bf16 ~1e-4 (plain definition), f32 inputs 4.7e-3 (plain), e4m3
+# 1.6e-3 - 1.8e-3 and MXFP4 3.4e-4 - 8.4e-4 (bf16-rounded outputs mirrored).
+MIRROR_REL_RMS = {"bf16": 1e-3, "f32": 1e-2, "fp8": 1e-2, "mxfp4": 1e-2}
 
 
 def np_bits(t):
@@ -40,9 +53,10 @@ def bank(wl):
                           *[np_bits(t) for t in (wl.s_gate, wl.s_up, wl.s_down)])
 
 
-def reference(wl, tokens=None, bank_=None):
+def reference(wl, tokens=None, bank_=None, y_mode=None):
     """Oracle output.  tokens: None (all R*T rows, float32 [R][T][d]) or an
-    array of (replica, token) pairs (float32 [n][d])."""
+    array of (replica, token) pairs (float32 [n][d]).  y_mode None is the
+    plain definition; "bf16" mirrors the library's bf16 expert outputs."""
     c = wl.cfg
     kind, h_mode, x_mode = modes(wl)
     bank_ = bank_ or bank(wl)
@@ -52,25 +66,42 @@ def reference(wl, tokens=None, bank_=None):
         ids = wl.topk_local.reshape(-1, c["k"])
         w = wl.topk_w.reshape(-1, c["k"])
         out = ffn.routed_output(x, ids, w, bank_, c["E"], h_mode=h_mode, x_mode=x_mode,
-                                y_mode="bf16")
+                                y_mode=y_mode)
         return out.reshape(c["R"], c["T"], c["d"])
     tokens = np.asarray(tokens)
     r, t = tokens[:, 0], tokens[:, 1]
     xb = np_bits(wl.x)[r, t]
     x = ffn.decode_rows(xb, xk)
     return ffn.routed_output(x, wl.topk_local[r, t], wl.topk_w[r, t], bank_, c["E"],
-                             h_mode=h_mode, x_mode=x_mode, y_mode="bf16")
+                             h_mode=h_mode, x_mode=x_mode, y_mode=y_mode)
+
+
+def _rel(got, ref):
+    return float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30))
 
 
 def compare(wl, got, ref):
-    """Assert the target tolerance; returns (max abs err, relative RMS)."""
+    """Assert the target tolerance against the plain definition `ref`;
+    returns (max abs err, relative RMS)."""
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
     err = np.abs(got - ref)
-    rel = float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30))
+    rel = _rel(got, ref)
     kind, _, _ = modes(wl)
     if kind in ("fp8", "mxfp4"):
         assert rel <= FP8_REL_RMS, f"{kind} relative RMS {rel:.3e}"
+        # per output row as well: a localised error (one scale block, one
+        # wave's rows, one expert's tail tile) cannot hide in the whole
+        d = ref.shape[-1]
+        g2, r2 = got.reshape(-1, d), ref.reshape(-1, d)
+        rn = np.linalg.norm(r2, axis=1)
+        live = rn > 0
+        row_rel = np.linalg.norm(g2 - r2, axis=1)[live] / rn[live]
+        if row_rel.size:
+            worst = int(np.argmax(row_rel))
+            assert row_rel[worst] <= FP8_REL_RMS, (
+                f"{kind} row relative RMS {row_rel[worst]:.3e} (row {worst} of the live rows)")
+        assert not g2[~live].any(), "rows with an all-zero reference must be zero"
     else:
         bad = err > BF16_ATOL + BF16_RTOL * np.abs(ref)
         assert not bad.any(), (f"{int(bad.sum())} elements outside tolerance, max err "
@@ -78,3 +109,18 @@ def compare(wl, got, ref):
         if kind == "f32":
             assert rel <= F32_REL_RMS, f"relative RMS {rel:.3e}"
     return float(err.max()), rel
+
+
+def check(wl, got, tokens=None, bank_=None):
+    """Both checks: the target tolerance against the plain definition, then
+    the regression bound against the mirrored oracle.  Returns (max abs err,
+    relative RMS) against the plain definition."""
+    bank_ = bank_ or bank(wl)
+    ref = reference(wl, tokens=tokens, bank_=bank_)
+    mx, rel = compare(wl, got, ref)
+    kind, _, _ = modes(wl)
+    if kind in ("fp8", "mxfp4"):
+        ref = reference(wl, tokens=tokens, bank_=bank_, y_mode="bf16")
+    mrel = _rel(np.asarray(got, np.float64), np.asarray(ref, np.float64))
+    assert mrel <= MIRROR_REL_RMS[kind], f"{kind} relative RMS {mrel:.3e} (regression bound)"
+    return mx, rel

@@ -44,7 +44,7 @@ def test_most_experts_and_slots():
             assert np.array_equal(m[key], ref[key]), (b, key)
     got = run.out.cpu().numpy()
     run.close()
-    U.compare(wl, got, U.reference(wl))
+    U.check(wl, got)
 
 
 @pytest.mark.parametrize("d,I", [(MAX_DIM, 128), (256, MAX_DIM)])
@@ -53,7 +53,7 @@ def test_widest_dims_bf16(d, I):
     run = _run(wl)
     got = run.out.cpu().numpy()
     run.close()
-    mx, rel = U.compare(wl, got, U.reference(wl))
+    mx, rel = U.check(wl, got)
     print(f"bf16 d={d} I={I}: pairs={wl.n_pairs} max_abs={mx:.3e} rel={rel:.3e}")
 
 
@@ -67,7 +67,7 @@ def test_widest_dims_fp8_with_fetch(d, I):
     run = _run(wl, use_fetch=True)
     got = run.out.cpu().numpy()
     run.close()
-    mx, rel = U.compare(wl, got, U.reference(wl))
+    mx, rel = U.check(wl, got)
     print(f"e4m3 d={d} I={I}: pairs={wl.n_pairs} max_abs={mx:.3e} rel={rel:.3e}")
 
 
@@ -77,5 +77,5 @@ def test_widest_dims_mxfp4(d, I):
     run = _run(wl)
     got = run.out.cpu().numpy()
     run.close()
-    mx, rel = U.compare(wl, got, U.reference(wl))
+    mx, rel = U.check(wl, got)
     print(f"mxfp4 d={d} I={I}: pairs={wl.n_pairs} max_abs={mx:.3e} rel={rel:.3e}")

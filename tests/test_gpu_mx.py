@@ -45,8 +45,7 @@ def test_mxfp4_reduced_all_rows():
     aligns = {cep.cep_get_batch_routing(run.ctx, b, wl.cfg["E"], wl.cfg["k"])["align"]
               for b in range(cep.cep_get_batch_count(run.ctx))}
     run.close()
-    ref = U.reference(wl)
-    mx, rel = U.compare(wl, got, ref)
+    mx, rel = U.check(wl, got)
     assert not got[~wl.delivered].any()
     print(f"mxfp4 reduced: pairs={wl.n_pairs} aligns={sorted(aligns)} max_abs={mx:.3e} "
           f"rel_rms={rel:.3e}")
@@ -66,7 +65,7 @@ def test_mxfp4_large_and_small_m_tiles_agree_bitwise():
     assert cep.cep_get_batch_routing(run.ctx, 0, wl.cfg["E"], wl.cfg["k"])["align"] == 128
     run.close()
     assert np.array_equal(a, b)
-    U.compare(wl, a, U.reference(wl))
+    U.check(wl, a)
 
 
 def test_mxfp4_full_size_sampled_tokens():
@@ -82,8 +81,7 @@ def test_mxfp4_full_size_sampled_tokens():
     for e in (int(cnt.argmax()), int(np.argmin(np.where(cnt > 0, cnt, 1 << 30)))):
         rt = np.argwhere((wl.topk_local == e).any(axis=2))
         pick = np.vstack([pick, rt[-2:]])
-    ref = U.reference(wl, tokens=pick)
-    mx, rel = U.compare(wl, got[pick[:, 0], pick[:, 1]], ref)
+    mx, rel = U.check(wl, got[pick[:, 0], pick[:, 1]], tokens=pick)
     assert not got[~wl.delivered].any()
     print(f"mxfp4 full: pairs={wl.n_pairs} sampled={len(pick)} max_abs={mx:.3e} rel={rel:.3e}")
 
@@ -94,7 +92,7 @@ def test_mxfp4_fetched_experts_equal_resident_bitwise():
     a = harness.Runner(wl, n_streams=2, use_fetch=True)
     a.run(policy=cep.CEP_THRESHOLD, theta=500, n_streams=2)
     ga = _out(a)
-    assert all(b["helper"] for b in a.stats()["batches"])
+    assert all(b["fetched"] for b in a.stats()["batches"])
     a.close()
     b = harness.Runner(wl, n_streams=1, use_fetch=False)
     b.run(policy=cep.CEP_WAIT_ALL)

@@ -1,0 +1,185 @@
+"""Chunk readiness on each chunk's own signal (Section 3.2; Appendix C,
+"Asynchronous dispatch": a lane's inputs become eligible when its own
+completion signal fires, without waiting for other replicas).
+
+The chunk buffers start out poisoned (NaN rows and coefficients, expert ids
+and token slots out of range).  A dispatch stream writes each chunk's real
+data after a bounded device-side delay and records that chunk's arrival
+event; the host submits every chunk at once, before any of them has
+arrived, each with its own event.  The library must read every chunk only
+after its event: the output then equals the run on resident inputs, bit for
+bit, under every policy and stream count.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_33252_amd import cep, harness, workload as W
+
+from . import _util as U
+
+pytestmark = pytest.mark.gpu
+
+# spin of the delay kernel before each delivery (clock64 ticks: well under a
+# millisecond to tens of milliseconds, whatever the counter's rate)
+DELAY = 1_000_000
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    cep.lib()
+    torch.cuda.set_device(0)
+
+
+def _out(run):
+    torch.cuda.synchronize()
+    cep.cep_get_status(run.ctx)
+    return run.out.cpu().numpy()
+
+
+class Late:
+    """Real chunk data kept aside; poison and late delivery of the buffers
+    the library reads."""
+
+    def __init__(self, run):
+        self.run = run
+        self.src = [(ch.token_idx.clone(), ch.ids.clone(), ch.w.clone()) for ch in run.chunks]
+        self.x_src = run.recv.clone()
+        self.dispatch = torch.cuda.Stream()
+
+    def poison(self):
+        E = self.run.wl.cfg["E"]
+        self.run.recv.fill_(float("nan"))
+        for ch in self.run.chunks:
+            ch.token_idx.fill_(-5)
+            ch.ids.fill_(E + 5)
+            ch.w.fill_(float("nan"))
+        torch.cuda.synchronize()
+
+    def deliver(self, order, delay=DELAY):
+        """On the dispatch stream, in `order`: a delay, then the chunk's real
+        rows, ids, coefficients and token slots, then its arrival event.
+        Returns the events indexed by chunk."""
+        run = self.run
+        events = [None] * len(run.chunks)
+        r0s = np.cumsum([0] + [ch.n_rows for ch in run.chunks])
+        with torch.cuda.stream(self.dispatch):
+            for i in order:
+                ch = run.chunks[i]
+                if delay:
+                    torch.cuda._sleep(delay)
+                t, ids, w = self.src[i]
+                run.recv[r0s[i]:r0s[i + 1]].copy_(self.x_src[r0s[i]:r0s[i + 1]])
+                ch.token_idx.copy_(t)
+                ch.ids.copy_(ids)
+                ch.w.copy_(w)
+                ev = torch.cuda.Event(enable_timing=True)
+                ev.record(self.dispatch)
+                events[i] = ev
+        return events
+
+
+def _layer(run, events, policy, theta, streams):
+    """One layer whose chunks are all submitted at once, chunk i behind
+    events[i] (None: no event)."""
+    ctx = run.ctx
+    cep.cep_set_policy(ctx, policy, theta, streams)
+    run.gen += 1
+    cep.cep_begin_layer(ctx, run.gen, run.chunks_per_replica, run.out)
+    for i, ch in enumerate(run.chunks):
+        cep.cep_submit_chunk(ctx, run.gen, ch.replica, ch.n_rows, ch.n_pairs, ch.token_idx,
+                             ch.x, ch.ids, ch.w, events[i])
+    cep.cep_combine(ctx)
+
+
+def _workload():
+    return W.generate("zipf_stream_d7168", 5, d=1024, I=512, R=8, T=512, cpr=4)
+
+
+def test_each_chunk_waits_for_its_own_arrival():
+    wl = _workload()
+    run = harness.Runner(wl, n_streams=4)
+    run.run(policy=cep.CEP_WAIT_ALL)
+    ref = _out(run)
+    U.check(wl, ref)
+    late = Late(run)
+    n = len(run.chunks)
+    # deliveries in reverse submission order: the first chunk submitted is
+    # the last to arrive
+    order = list(range(n))[::-1]
+    for pol, theta, ns in ((cep.CEP_WAIT_ALL, 1, 1), (cep.CEP_PER_CHUNK, 1, 1),
+                           (cep.CEP_PER_CHUNK, 1, 4), (cep.CEP_THRESHOLD, 300, 2),
+                           (cep.CEP_THRESHOLD, 900, 3), (cep.CEP_THRESHOLD, 300, 4)):
+        late.poison()
+        run.out.zero_()
+        events = late.deliver(order)
+        _layer(run, events, pol, theta, ns)
+        got = _out(run)
+        assert np.array_equal(got, ref), (pol, theta, ns)
+        st = run.stats()
+        # every batch ended after the arrival of each of its chunks
+        arr = [c["arrival_ms"] for c in st["chunks"]]
+        for b in st["batches"]:
+            last = max(arr[b["first_chunk"]:b["first_chunk"] + b["n_chunks"]])
+            assert b["end_ms"] >= last, (pol, theta, ns, b)
+    run.close()
+
+
+def test_missing_waits_would_read_poison():
+    # the same late delivery submitted without events reads the poison: the
+    # check above is sensitive to a wait the library left out
+    wl = _workload()
+    run = harness.Runner(wl, n_streams=2)
+    run.run(policy=cep.CEP_WAIT_ALL)
+    ref = _out(run)
+    late = Late(run)
+    late.poison()
+    run.out.zero_()
+    late.deliver(range(len(run.chunks)))
+    _layer(run, [None] * len(run.chunks), cep.CEP_PER_CHUNK, 1, 2)
+    torch.cuda.synchronize()
+    failed = False
+    try:
+        cep.cep_get_status(run.ctx)
+    except cep.CepError:
+        failed = True
+    got = run.out.cpu().numpy()
+    run.close()
+    assert failed or not np.array_equal(got, ref)
+
+
+def test_late_chunk_blocks_only_its_own_batch():
+    # chunk 0 arrives long after all others; per-chunk batches on two
+    # streams: batch 0 (chunk 0) waits on stream slot 0, batches on slot 1
+    # run as soon as their own chunks are in, so they end before chunk 0
+    # arrives (no head-of-line blocking behind another replica's lane)
+    wl = _workload()
+    run = harness.Runner(wl, n_streams=2)
+    run.run(policy=cep.CEP_WAIT_ALL)
+    ref = _out(run)
+    late = Late(run)
+    late.poison()
+    run.out.zero_()
+    n = len(run.chunks)
+    slow = torch.cuda.Stream()
+    events = late.deliver(range(1, n), delay=0)
+    with torch.cuda.stream(slow):
+        torch.cuda._sleep(20 * DELAY)
+    late.dispatch, keep = slow, late.dispatch
+    events[0] = late.deliver([0], delay=0)[0]
+    late.dispatch = keep
+    _layer(run, events, cep.CEP_PER_CHUNK, 1, 2)
+    got = _out(run)
+    assert np.array_equal(got, ref)
+    st = run.stats()
+    a0 = st["chunks"][0]["arrival_ms"]
+    assert a0 > 0
+    nonempty = [b for b in st["batches"]]
+    assert nonempty[0]["first_chunk"] == 0 and nonempty[0]["slot"] == 0
+    early = [b for b in nonempty if b["slot"] == 1]
+    assert early, "per-chunk batches on the second stream slot"
+    for b in early:
+        assert b["end_ms"] < a0, (b, a0)
+    run.close()
