@@ -10,6 +10,7 @@ path runs in libcep's kernels.
 """
 from __future__ import annotations
 
+import ctypes
 import time
 
 import numpy as np
@@ -20,6 +21,19 @@ from . import workload as W
 
 _DT = {W.F32: cep.CEP_F32, W.BF16: cep.CEP_BF16, W.FP8: cep.CEP_FP8_E4M3_B128,
        W.MXFP4: cep.CEP_MXFP4}
+
+
+_HIP = None
+
+
+def _hip():
+    """The HIP runtime, for one stream-on-event wait the torch API has no
+    call for (the fetch's ready event is a raw hipEvent_t)."""
+    global _HIP
+    if _HIP is None:
+        _HIP = ctypes.CDLL("libamdhip64.so")
+        _HIP.hipStreamWaitEvent.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint]
+    return _HIP
 
 
 class DeviceChunk:
@@ -116,8 +130,10 @@ class Runner:
             stream writes them (steady-state replay of the same layer), so the
             chunks carry no arrival event.
         fetch_mode: cep_fetch_mode of this and later layers (None: unchanged).
-        prefetch: wait on the host for the weight copy before submitting the
-            chunks (the layer then runs as if the copy had happened earlier).
+        prefetch: every chunk arrives only after the weight copy (its arrival
+            event follows the fetch's ready event on the dispatch stream), so
+            the batch starts once the copy is done: the layer as if the copy
+            had happened before it, without a host round trip.
         """
         out = self.out if out is None else out
         stream = torch.cuda.current_stream(self.device) if stream is None else stream
@@ -132,12 +148,16 @@ class Runner:
                 ctx, list(self.wl.fetched),
                 [self.donor.data_ptr() + i * self.blob_bytes for i in range(len(self.wl.fetched))],
                 self.side)
-            if prefetch:
-                torch.cuda.synchronize(self.device)
         seq = range(len(self.chunks)) if order is None else order
         # chunk inputs and `out` were written on the caller's stream: every
         # chunk becomes valid only after that work
-        if inputs_ready and not (timed or arrival_events):
+        if prefetch and self.use_fetch and self.fetch_ready:
+            _hip().hipStreamWaitEvent(ctypes.c_void_p(self.dispatch.cuda_stream),
+                                      ctypes.c_void_p(self.fetch_ready), 0)
+            ready = torch.cuda.Event(enable_timing=True)
+            ready.record(self.dispatch)
+            self.arrival_events = [ready]
+        elif inputs_ready and not (timed or arrival_events):
             ready = None
             self.arrival_events = []
         else:
