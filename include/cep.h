@@ -296,6 +296,32 @@ const char *cep_last_error(const cep_ctx *ctx);
 /* Wait for all work, release every resource.  NULL is a no-op. */
 int cep_destroy(cep_ctx *ctx);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): one chunk
+ * of replica `replica` run as a one-batch layer, i.e. what cep_begin_layer,
+ * cep_submit_chunk (policy CEP_WAIT_ALL, arrival NULL) and cep_combine do,
+ * with the same kernels and the same bits in `out`, enqueued on stream s.
+ * Arguments as for cep_submit_chunk; out: device float32 [R_max][T_max][d]
+ * as for cep_begin_layer (delivered rows written, others untouched).  All
+ * scratch (the chunk's routing arrays, tile lists, grouped rows, h, expert
+ * outputs) lives in one 64 MiB device array of the library, one per device,
+ * so nothing is allocated or freed: CEP_ENOMEM (before any work) when the
+ * chunk needs more.  The need is about (2*d_ff + 4*d) bytes per grouped row
+ * with bf16 weights and rows ((2*d_ff + 6*d) with float32 rows, (d_ff + 3*d)
+ * with e4m3 or MXFP4 weights), for n_pairs rows
+ * plus up to one M tile (64 or 256 rows; 128 or 256 with e4m3 / MXFP4) of
+ * padding per expert: about 2 K pairs at d = 4096, d_ff = 2048, 8 experts.
+ * Every call on a device shares that array, and it keeps the last call's
+ * contents: calls that overlap on one device (on different streams, or with
+ * kernels of an earlier call still running on another stream) race.  Work of
+ * the context's layers uses its own buffers and does not conflict.  Needs
+ * every expert resident (CEP_ESTATE otherwise); n_pairs 0 does nothing.
+ * Device-side checks (ids, token slots, the pair count) are reported by
+ * cep_get_status. */
+int cep_ffn_noalloc(cep_ctx *ctx, int replica, int n_rows, int n_pairs, const int32_t *token_idx,
+                    const void *x, const int32_t *topk_id, const float *topk_w, float *out,
+                    hipStream_t s);
+
 /* ------------------------------------------------------------------------
  * FFN throughput profile (host only; no GPU work).
  *

@@ -24,7 +24,7 @@ EXPORTED = ["cep_packed_expert_bytes", "cep_pack_experts", "cep_init_experts", "
             "cep_begin_layer", "cep_submit_chunk", "cep_flush", "cep_weight_fetch",
             "cep_combine", "cep_get_batch_routing", "cep_get_batch_count", "cep_get_stats",
             "cep_get_status", "cep_last_error", "cep_destroy", "cep_set_phase_timing",
-            "cep_set_fetch_mode",
+            "cep_set_fetch_mode", "cep_ffn_noalloc",
             "cep_profile_create",
             "cep_profile_peak", "cep_profile_theta", "cep_profile_eta", "cep_profile_latency",
             "cep_profile_destroy", "cep_oewf_create", "cep_oewf_begin_layer", "cep_oewf_set_rank",
@@ -103,6 +103,7 @@ def lib():
         L.cep_destroy.argtypes = [vp]
         L.cep_set_phase_timing.argtypes = [vp, i32]
         L.cep_set_fetch_mode.argtypes = [vp, i32]
+        L.cep_ffn_noalloc.argtypes = [vp, i32, i32, i32, vp, vp, vp, vp, vp, vp]
         i64, f64 = ctypes.c_int64, ctypes.c_double
         L.cep_profile_create.argtypes = [P(i64), P(f64), i32, P(vp)]
         L.cep_profile_peak.argtypes = [vp]
@@ -280,6 +281,12 @@ def cep_set_phase_timing(ctx, on=True):
 
 def cep_set_fetch_mode(ctx, mode):
     _check(ctx, lib().cep_set_fetch_mode(ctx, mode))
+
+
+def cep_ffn_noalloc(ctx, replica, n_rows, n_pairs, token_idx, x, topk_id, topk_w, out,
+                    stream=None):
+    _check(ctx, lib().cep_ffn_noalloc(ctx, replica, n_rows, n_pairs, _ptr(token_idx), _ptr(x),
+                                      _ptr(topk_id), _ptr(topk_w), _ptr(out), _stream(stream)))
 
 
 def cep_get_status(ctx):

@@ -14,6 +14,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -426,6 +427,10 @@ CEP_API int cep_pack_experts(const cep_config *cfg, const cep_weights *w, int fi
   return pack_range(cfg, w, first, n, (uint8_t *)dst, s, nullptr, nullptr);
 }
 
+namespace {
+void scratch_setup(int dev);
+}  // namespace
+
 CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_weights *w,
                              const uint8_t *resident, hipStream_t s) {
   if (!out) return fail(nullptr, CEP_EINVAL, "cep_init_experts: out is NULL");
@@ -443,6 +448,8 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
     delete c;
     return fail(nullptr, CEP_EHIP, "cep_init_experts: device query failed");
   }
+  // the device's copy of the allocation-free call's scratch (once per device)
+  scratch_setup(c->device);
   const int E = cfg->n_local_experts, k = cfg->top_k, d = cfg->d_model, I = cfg->d_ff;
   c->wk = weight_kind(cfg->w_dtype);
   c->L = blob_layout(d, I, c->wk);
@@ -945,5 +952,141 @@ CEP_API int cep_destroy(cep_ctx *c) {
   if (c->copy) (void)hipStreamDestroy(c->copy);
   for (void *p : c->allocs) (void)hipFree(p);
   delete c;
+  return CEP_OK;
+}
+
+// ===================================================== allocation-free call
+// One grouped invocation whose scratch (arena, routing arrays, tile lists,
+// grouped rows, h and expert outputs) is carved from a file-scope device
+// array instead of the context's buffers, for callers that cannot allocate.
+// Each device holds its own copy of the array at its own address, found once
+// per device by cep_init_experts; every call on a device shares it.
+namespace {
+
+constexpr size_t kNoAllocBytes = (size_t)64 << 20;
+static __device__ __align__(256) uint8_t scratch[kNoAllocBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+hipError_t g_scratch_err[kMaxDevices] = {};
+
+// With device `dev` current: the device address of that device's copy of
+// `scratch`, looked up once.
+void scratch_setup(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev]) return;
+  void *p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e == hipSuccess && p) {
+    g_scratch_ptr[dev] = p;
+  } else {
+    g_scratch_err[dev] = e;
+    (void)hipGetLastError();
+  }
+}
+
+// Sub-allocation of `bytes` (256-byte aligned) from a carve cursor.
+struct Carver {
+  size_t used = 0;
+  uint8_t *base = nullptr;  // null: only count
+  void *take(size_t bytes) {
+    void *p = base ? base + used : nullptr;
+    used += align_up(std::max<size_t>(bytes, 1), 256);
+    return p;
+  }
+};
+
+}  // namespace
+
+CEP_API int cep_ffn_noalloc(cep_ctx *c, int replica, int n_rows, int n_pairs,
+                            const int32_t *token_idx, const void *x, const int32_t *topk_id,
+                            const float *topk_w, float *out, hipStream_t s) {
+  if (!c) return CEP_EINVAL;
+  const cep_config &cfg = c->cfg;
+  const int E = cfg.n_local_experts, k = cfg.top_k, d = cfg.d_model, I = cfg.d_ff;
+  if (replica < 0 || replica >= cfg.max_replicas)
+    return fail(c, CEP_EINVAL, "replica %d out of range", replica);
+  if (n_rows < 0 || n_rows > cfg.max_tokens_per_replica || n_pairs < 0 ||
+      (long long)n_pairs > (long long)n_rows * k)
+    return fail(c, CEP_EINVAL, "bad n_rows %d / n_pairs %d", n_rows, n_pairs);
+  if (n_rows > 0 && (!token_idx || !x || !topk_id || !topk_w || !out))
+    return fail(c, CEP_EINVAL, "NULL chunk array or output");
+  if (((uintptr_t)x & 15) != 0) return fail(c, CEP_EINVAL, "x must be 16-byte aligned");
+  if (c->nonres_mask)
+    return fail(c, CEP_ESTATE, "the allocation-free call needs every expert resident");
+  if (n_pairs == 0) return CEP_OK;
+  // capacities of this one invocation: its row alignment A is known here, so
+  // the grouped rows need at most P + E*(A-1) (each expert's last tile
+  // padded), rounded up to whole 256-row groups of the scale layouts
+  const int P = n_pairs;
+  const int A = batch_align(c->wk, P, E);
+  const int mpad = (int)align_up((size_t)P + (size_t)E * A, kMaxAlign);
+  const int tiles_cap = (P + kMinAlign - 1) / kMinAlign + E;
+  const int blocks = (int)(((long long)n_rows * k + kRoutePairs - 1) / kRoutePairs);
+  const size_t xes = c->wk != kWBf16 ? 1 : 2;
+  const bool packed = !(c->wk == kWBf16 && cfg.x_dtype == CEP_BF16);
+  Carver cv;
+  for (int pass = 0; pass < 2; ++pass) {
+    if (pass == 1) {
+      if (cv.used > kNoAllocBytes)
+        return fail(c, CEP_ENOMEM,
+                    "%d rows with %d pairs need %zu bytes of scratch; the allocation-free "
+                    "call has %zu",
+                    n_rows, n_pairs, cv.used, kNoAllocBytes);
+      const int dev = c->device;
+      if (dev < 0 || dev >= kMaxDevices || !g_scratch_ptr[dev])
+        return fail(c, CEP_EHIP, "scratch address of device %d unavailable: %s", dev,
+                    hipGetErrorString(dev >= 0 && dev < kMaxDevices ? g_scratch_err[dev]
+                                                                   : hipErrorInvalidDevice));
+      cv = Carver{};
+      cv.base = (uint8_t *)g_scratch_ptr[dev];
+    }
+    Arena a{};
+    a.ids = (int32_t *)cv.take(sizeof(int32_t) * (size_t)n_rows * k);
+    a.w = (float *)cv.take(sizeof(float) * (size_t)n_rows * k);
+    a.dst = (int32_t *)cv.take(sizeof(int32_t) * (size_t)n_rows);
+    a.xrow = (const void **)cv.take(sizeof(void *) * (size_t)n_rows);
+    Scratch sc{};
+    sc.blk_cnt = (int32_t *)cv.take(sizeof(int32_t) * (size_t)blocks * E);
+    sc.cnt = (int32_t *)cv.take(sizeof(int32_t) * E);
+    sc.off = (int32_t *)cv.take(sizeof(int32_t) * (E + 1));
+    sc.off_pad = (int32_t *)cv.take(sizeof(int32_t) * (E + 1));
+    sc.tiles = (Tile *)cv.take(sizeof(Tile) * 4 * (size_t)tiles_cap);
+    sc.n_tiles = (int32_t *)cv.take(sizeof(int32_t) * 4);
+    sc.pos_of = (int32_t *)cv.take(sizeof(int32_t) * (size_t)n_rows * k);
+    sc.perm = (int32_t *)cv.take(sizeof(int32_t) * (size_t)mpad);
+    sc.wrow = (float *)cv.take(sizeof(float) * (size_t)mpad);
+    if (packed) sc.xg = cv.take(xes * (size_t)mpad * d);
+    sc.h = cv.take(xes * (size_t)mpad * I);
+    sc.y = cv.take((c->wk == kWBf16 ? 4 : 2) * (size_t)mpad * d);
+    if (c->wk != kWBf16) {
+      sc.xs = (float *)cv.take(sizeof(float) * (size_t)mpad * (d / 128));
+      sc.hs = (float *)cv.take(sizeof(float) * (size_t)mpad * (I / 128));
+      sc.s_ld = mpad;
+    }
+    if (pass == 0) continue;
+
+    // the same kernels as a one-chunk wait-all layer, on stream s
+    IngestGroup g{};
+    g.c[0] = IngestChunk{token_idx, x, topk_id, topk_w, 0, n_rows, replica};
+    g.n = 1;
+    const size_t xrb = (size_t)d * (cfg.x_dtype == CEP_F32 ? 4 : 2);
+    HIPCHK(c, launch_ingest(a, g, k, E, cfg.max_tokens_per_replica, xrb, c->d_err, s));
+    const bool split = c->wk == kWBf16 && A == kBf16TileM;
+    const int split_tiles = split ? 2 * E : 0;
+    const bool var = batch_var_tiles(c->wk, A, P, E);
+    const int tiles = std::min(tiles_cap, (P + A - 1) / A + E);
+    HIPCHK(c, launch_route(a, sc, 0, n_rows, k, E, A, P, mpad, tiles_cap, 0, cfg.x_dtype, c->wk,
+                           d, split ? c->n_cu : 0, 2 * I / kBf16TileN, var, c->d_err, s));
+    BlobTable bt{};
+    for (int e = 0; e < E; ++e) bt.blob[e] = c->w_res + (size_t)e * c->L.bytes;
+    const Arena *gather = packed ? nullptr : &a;
+    HIPCHK(c, launch_gemm1(sc, 0, tiles_cap, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
+                           gather, 0, k, s));
+    HIPCHK(c, launch_gemm2(sc, 0, tiles_cap, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I, s));
+    HIPCHK(c, launch_combine(a, sc, 0, n_rows, k, d, c->wk == kWBf16, out, s));
+  }
   return CEP_OK;
 }
