@@ -13,8 +13,10 @@
  *   1. histogram of local expert ids over the batch's valid (token, slot) pairs
  *   2. exclusive scan -> per-expert row offsets, aligned to the GEMM M tile
  *   3. stable permute/pack of token rows into expert-contiguous order, with an
- *      inverse map (FP8: activations quantised per 1x128 block on the way)
- *   4. grouped gate/up GEMM with fused SwiGLU (FP8: h re-quantised per 1x128)
+ *      inverse map (e4m3 / MXFP4 weights: activations quantised to MXFP8 on
+ *      the way)
+ *   4. grouped gate/up GEMM with fused SwiGLU (e4m3 / MXFP4 weights: h
+ *      re-quantised to MXFP8)
  *   5. grouped down GEMM, scaled by the routing coefficient
  *   6. combine: each source token's local contributions summed in slot order
  *      and written to its (replica, token) row of the output
@@ -63,7 +65,8 @@ enum cep_dtype {
   CEP_F32 = 0,          /* float32 (converted to bf16 inside the library)     */
   CEP_BF16 = 1,         /* bfloat16                                            */
   CEP_FP8_E4M3_B128 = 2, /* weights only: OCP e4m3fn codes, one float32 scale
-                           per 128x128 block                                   */
+                           per 128x128 block; activations and h run as MXFP8
+                           (e4m3, one E8M0 scale per 32) inside the library */
   CEP_MXFP4 = 3          /* weights only: OCP MXFP4 (e2m1 codes, one E8M0 scale
                            per 32 along K; Section 4.1's DeepSeek-V4 experts);
                            activations and h run as MXFP8 inside the library */
@@ -216,7 +219,8 @@ int cep_flush(cep_ctx *ctx);
  * fetch mode is CEP_FETCH_IN_PLACE, or a copy fails to start (Appendix C,
  * "FFN reassignment commit and fallback": a failed copy leaves the work
  * where it can run and triggers no new decision), nothing is copied: the
- * experts' tiles read src_blobs in place, *ready is NULL, and cep_get_stats
+ * experts' tiles (still after the resident experts' GEMMs) read src_blobs
+ * in place, *ready is NULL, and cep_get_stats
  * reports the fetch as in place (with "fallback" after a failed copy).  The
  * output is the same, bit for bit, in every mode.  One fetch per layer: a
  * second call returns CEP_EBUSY.  Total bytes above fetch_buffer_bytes:

@@ -1,47 +1,67 @@
-// e4m3 (OCP fp8) grouped expert GEMMs for gfx950 (CDNA4) MFMA.
+// e4m3 (OCP fp8) grouped expert GEMMs for gfx950 (CDNA4) block-scaled MFMA.
 //
 // Expert weights arrive as e4m3 codes with one float32 scale per 128x128
-// block; activations are quantised per (row, 128 channels) by the pack step
-// and h per (row, 128 columns) in the GEMM1 epilogue (Appendix C, "Grouped
-// FFN invocations": the layout transform packs activations with their
-// quantisation metadata, and the activation and quantisation run between
-// the two expert GEMMs).  The hardware-scaled MFMA takes power-of-two
-// (E8M0) scales per 32 elements; these block scales are arbitrary float32,
-// so each 128-wide K block runs unscaled and is promoted in float32.
+// block.  Activations are quantised to MXFP8 (e4m3 codes, one E8M0
+// power-of-two scale per 32 channels) by the pack step and h to MXFP8 in the
+// GEMM1 epilogue (Appendix C, "Grouped FFN invocations": the layout
+// transform packs activations with their quantisation metadata, and the
+// activation and quantisation run between the two expert GEMMs).
+// v_mfma_scale_f32_16x16x128_f8f6f4 applies the activation scales itself
+// (E8M0 operands); the weight block scales are arbitrary float32, so each
+// 128-wide K block -- exactly one instruction -- is promoted into the float32
+// accumulator with one fused multiply-add by its block's scale, a value
+// shared by every element of the wave's 16-column fragment.  With float32
+// activation scales the promotion would need the product of a per-row and a
+// per-column scale for every element: a multiply on top of each FMA and a
+// row-scale read per row fragment.
+//
+// Operand layout of the instruction (lane l: row or column l%16, group
+// g = l/16): an e4m3 operand lane holds K [16g, 16g+16) in bytes 0-15 and
+// K [64+16g, 64+16g+16) in bytes 16-31; the A scale byte of lane l applies to
+// K block g of its row.
 #include "gemm_common.h"
 
 namespace cep {
 namespace {
 
-// BM x 256 output tile, K step 128 (one scale block).  NW waves: four
+// One e4m3 x e4m3 MFMA of a K block with the A operand's E8M0 scales (byte
+// oa of the word sa) and unit B scales; oa is a constant after the caller's
+// loop is unrolled, and the switch folds away.
+__device__ inline f32x4 f8_mfma(const i32x8 &a, const i32x8 &b, int oa, int sa) {
+  switch (oa) {
+    case 0: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, f32x4{}, 0, 0, 0, sa, 0, 127);
+    case 1: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, f32x4{}, 0, 0, 1, sa, 0, 127);
+    case 2: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, f32x4{}, 0, 0, 2, sa, 0, 127);
+    default: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, f32x4{}, 0, 0, 3, sa, 0, 127);
+  }
+}
+
+// BM x 256 output tile, K step 128 (one weight scale block).  NW waves: four
 // column groups of 64 x (NW/4) row groups of 128, each wave owning 128 rows x
-// 64 columns built from 8x4 v_mfma_scale_f32_16x16x128_f8f6f4 with unit
-// hardware scales.  Every instruction covers one whole K block, so its
-// result is promoted into the float32 accumulator with the product of the
-// row's activation scale and the weight block's scale: two VALU operations
-// per output element and K block, which is why each wave holds few column
-// scale blocks (GEMM1: the gate and the up block of its 32 h columns; GEMM2:
-// one) and few rows per lane.  With 8 waves (two per SIMD) one wave's
+// 64 columns = 8 x 4 16x16 fragments.  With 8 waves (two per SIMD) one wave's
 // promotion overlaps the other's MFMAs.
 //
 // Operands stream through a ring of STAGES LDS stages filled by direct
-// global->LDS loads issued STAGES-1 steps ahead ((BM + 256) x 128 codes + BM
-// row scales per stage).  An LDS row is 128 codes = eight 16-byte chunks;
-// chunk c of row r lives at slot c ^ ((r >> 1) & 7).  A lane reads chunks
-// g and g + 4 of its row (g = lane / 16): a 16-byte LDS read serves per
-// cycle the sixteen lanes of one half-wave whose quad index (lane bits 2-4)
-// has one parity, and those lanes then touch sixteen distinct slots of 256
-// bytes (reading chunks 2g, 2g + 1 instead measured two-way bank conflicts).
+// global->LDS loads issued STAGES-1 steps ahead ((BM + 256) x 128 codes plus
+// the BM x 4 row scales per stage).  The row-scale layout
+// (mx_row_scale_offset) gives each lane its eight row fragments' scales of
+// its K block as one 8-byte word.  The weight block scales of the tile's
+// columns go to LDS once.  An LDS row is 128 codes = eight 16-byte chunks;
+// chunk c of row r lives at slot c ^ ((r >> 1) & 7).  A lane reads chunks g
+// and g + 4 of its row (g = lane / 16): a 16-byte LDS read serves per cycle
+// the sixteen lanes of one half-wave whose quad index (lane bits 2-4) has
+// one parity, and those lanes then touch sixteen distinct slots of 256 bytes.
 //
-// GEMM1 epilogue: h = silu(gate) * up over the tile's 128 h columns, one
-// amax per row (lanes, then the four column waves via LDS), scale =
-// amax / 448, e4m3 codes of h / scale.
-template <int NW, int STAGES, bool SWIGLU>
-__global__ __launch_bounds__(64 * NW, 1) void k_gemm_fp8(GemmArgs g) {
+// GEMM1 epilogue: h = silu(gate) * up; each wave's 32 h columns of a row are
+// one MX block, so the block amax needs only a 16-lane reduction; the E8M0
+// scale is 2^(floor(log2 amax) - 8), the codes e4m3(h / scale) saturated at
+// 448.
+template <int NW, int STAGES, bool SWIGLU, int OCC = 1>
+__global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
   constexpr int BM = 128 * NW / 4, BN = 256, BK = 128, WN = BN / 4;
   constexpr int A_LD = BM * BK / 1024 / NW, B_LD = BN * BK / 1024 / NW;  // loads per wave
   constexpr int PER = A_LD + B_LD;  // per thread per step; wave 0 adds one (row scales)
-  static_assert(BM / 4 <= 64, "one load of BM row scales");
+  static_assert(BM * 4 <= 1024, "one load of the row scales");
   int mt, nt;
   if (!balanced_tile<kGroupM>(*g.n_tiles, g.N / BN, &mt, &nt)) return;
   const Tile t = g.tiles[mt];
@@ -52,13 +72,14 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_fp8(GemmArgs g) {
   const uint8_t *blob = blob_of(g.bt, t.expert);
   const char *Ag = (const char *)(g.A + (size_t)t.row0 * K);
   const char *Bg = (const char *)(blob + g.b_off + (size_t)nt * BN * K);
-  const char *Asg = (const char *)(g.As + t.row0);  // k-block kb at + kb * s_ld floats
+  // row scales of K step kb: 512 bytes per 128-row group, groups contiguous
+  const char *Asg = (const char *)g.As + (size_t)(t.row0 >> 7) * 512;
+  const size_t as_step = (size_t)(g.s_ld >> 7) * 512;
   const float *Bs = (const float *)(blob + g.bs_off);
 
   __shared__ u32x4 sA[STAGES][BM * 8];
   __shared__ u32x4 sB[STAGES][BN * 8];
-  __shared__ float sAs[STAGES][BM];
-  __shared__ float red[4][BM];
+  __shared__ u32x4 sAs[STAGES][BM / 4];
   __shared__ float sBs[8 * (kMaxDim / BK)];
 
   // lane l of a load fills slot l of a 1 KB segment (8 rows x 8 chunks)
@@ -80,7 +101,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_fp8(GemmArgs g) {
             __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf_][seg * 64])));      \
     }                                                                              \
     if (wid == 0 && lane < BM / 4)                                                 \
-      dma16(Asg + (size_t)(kb) * g.s_ld * 4 + lane * 16,                           \
+      dma16(Asg + (size_t)(kb) * as_step + lane * 16,                              \
             __builtin_amdgcn_readfirstlane(lds_offset(&sAs[buf_][0])));            \
   }
 
@@ -104,15 +125,18 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_fp8(GemmArgs g) {
   }
   __syncthreads();
 
-  const int rsw = ((lane & 15) >> 1) & 7;  // swizzle of every operand row this lane reads
-  // this lane's two chunks: K bytes [16g, 16g+16) and [64+16g, 64+16g+16),
-  // g = lane / 16, the instruction's own K order (A and B alike); reading the
-  // chunk pair (g, g + 4) keeps every 16-lane LDS cycle on distinct banks
-  const int c0 = lane >> 4, c1 = c0 + 4;
-  // scale rows of this wave's column blocks: GEMM1 blocks j = 0,1 (gate) use
-  // row 2*wn, j = 2,3 (up) row 2*wn + 1; GEMM2's 64 columns lie in row wn/2
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int rsw = (r16 >> 1) & 7;  // swizzle of every operand row this lane reads
+  // scale rows of this wave's column blocks: GEMM1 fragments j = 0,1 (gate)
+  // use row 2*wn, j = 2,3 (up) row 2*wn + 1; GEMM2's 64 columns lie in row
+  // wn/2
   const float *sb_row0 = &sBs[(SWIGLU ? 2 * wn : wn / 2) * nkb];
   const float *sb_row1 = &sBs[(SWIGLU ? 2 * wn + 1 : wn / 2) * nkb];
+  auto read_op = [&](const u32x4 *s, int row) {
+    const u32x4 lo = s[row * 8 + (grp ^ rsw)];
+    const u32x4 hi = s[row * 8 + ((grp + 4) ^ rsw)];
+    return __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
   for (int kb = 0; kb < nkb; ++kb) {
     // this wave's loads of step kb are done when at most the loads of the
     // steps issued after it are outstanding
@@ -126,31 +150,24 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_fp8(GemmArgs g) {
     if (kb + STAGES - 1 < nkb) CEP_F8_STAGE(kb + STAGES - 1);
     const int cur = kb % STAGES;
     const float sb0 = sb_row0[kb], sb1 = sb_row1[kb];
+    const uint2 sa = ((const uint2 *)&sAs[cur][0])[wm * 64 + grp * 16 + r16];
 
     i32x8 b[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int row = wn * WN + j * 16 + (lane & 15);
-      const u32x4 lo = sB[cur][row * 8 + (c0 ^ rsw)];
-      const u32x4 hi = sB[cur][row * 8 + (c1 ^ rsw)];
-      b[j] = __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-    }
+    for (int j = 0; j < 4; ++j) b[j] = read_op(sB[cur], wn * WN + j * 16 + r16);
+    // A fragments one row group ahead: the reads of group i+1 are issued
+    // before the MFMAs of group i, so LDS latency hides behind them
+    i32x8 a_next = read_op(sA[cur], wm * 128 + r16);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int row = wm * 128 + i * 16 + (lane & 15);
-      const u32x4 lo = sA[cur][row * 8 + (c0 ^ rsw)];
-      const u32x4 hi = sA[cur][row * 8 + (c1 ^ rsw)];
-      const i32x8 a =
-          __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      const i32x8 a = a_next;
+      if (i + 1 < 8) a_next = read_op(sA[cur], wm * 128 + (i + 1) * 16 + r16);
+      const int sai = (int)(i < 4 ? sa.x : sa.y);
       f32x4 p[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        p[j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b[j], f32x4{}, 0, 0, 0, 127,
-                                                               0, 127);
-      const f32x4 sa = *(const f32x4 *)&sAs[cur][wm * 128 + i * 16 + 4 * (lane >> 4)];
-      const f32x4 s0 = sa * sb0, s1 = sa * sb1;
+      for (int j = 0; j < 4; ++j) p[j] = f8_mfma(a, b[j], i & 3, sai);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] += p[j] * (j < 2 ? s0 : s1);
+      for (int j = 0; j < 4; ++j) acc[i][j] += p[j] * (j < 2 ? sb0 : sb1);
     }
   }
 #undef CEP_F8_STAGE
@@ -159,42 +176,31 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_fp8(GemmArgs g) {
   // 16x16 accumulator layout: lane l, element r -> column l%16,
   // row 4*(l/16) + r.
   if (SWIGLU) {
-    // h column nt*128 + wn*32 + jj*16 + l%16 = silu(gate block jj) * up block jj+2
-    float h[8][2][4];
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-#pragma unroll
-      for (int jj = 0; jj < 2; ++jj)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) h[i][jj][r] = silu_mul(acc[i][jj][r], acc[i][jj + 2][r]);
+    uint8_t *H = (uint8_t *)g.out;
+    uint8_t *Hs = (uint8_t *)g.out_s;
+    const int I = g.N / 2, hblk = nt * 4 + wn;  // this wave's MX block of h columns
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        float m = fmaxf(fabsf(h[i][0][r]), fabsf(h[i][1][r]));
+        // h column nt*128 + wn*32 + jj*16 + l%16 = silu(gate block jj) * up block jj+2
+        const float h0 = silu_mul(acc[i][0][r], acc[i][2][r]);
+        const float h1 = silu_mul(acc[i][1][r], acc[i][3][r]);
+        float m = fmaxf(fabsf(h0), fabsf(h1));
 #pragma unroll
         for (int sh = 1; sh < 16; sh <<= 1) m = fmaxf(m, __shfl_xor(m, sh, 16));
-        if ((lane & 15) == 0) red[wn][wm * 128 + i * 16 + 4 * (lane >> 4) + r] = m;
-      }
-    __syncthreads();
-    uint8_t *H = (uint8_t *)g.out;
-    const int I = g.N / 2;
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int rt = wm * 128 + i * 16 + 4 * (lane >> 4) + r;
+        const int rt = wm * 128 + i * 16 + 4 * grp + r;
         if (rt >= t.rows) continue;
-        const float amax = fmaxf(fmaxf(red[0][rt], red[1][rt]), fmaxf(red[2][rt], red[3][rt]));
-        const float scale = amax > 0.f ? amax / 448.0f : 1.0f;
+        const int code = max((int)((__float_as_uint(m) >> 23) & 0xff) - 8, 0);
+        const int e = 127 - code;  // h / 2^(code - 127), exact
+        const float q0 = fminf(fmaxf(ldexpf(h0, e), -448.0f), 448.0f);
+        const float q1 = fminf(fmaxf(ldexpf(h1, e), -448.0f), 448.0f);
+        const int q = __builtin_amdgcn_cvt_pk_fp8_f32(q0, q1, 0, false);
         const size_t row = (size_t)t.row0 + rt;
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-          const int col = nt * 128 + wn * 32 + jj * 16 + (lane & 15);
-          const int q = __builtin_amdgcn_cvt_pk_fp8_f32(h[i][jj][r] / scale, 0.f, 0, false);
-          H[row * I + col] = (uint8_t)(q & 0xff);
-        }
-        if (wn == 0 && (lane & 15) == 0) g.out_s[(size_t)nt * g.s_ld + row] = scale;
+        uint8_t *hrow = H + row * I + nt * 128 + wn * 32 + r16;
+        hrow[0] = (uint8_t)(q & 0xff);
+        hrow[16] = (uint8_t)((q >> 8) & 0xff);
+        if (r16 == 0) Hs[mx_row_scale_offset((int)row, hblk, g.s_ld)] = (uint8_t)code;
       }
   } else {
     __bf16 *Y = (__bf16 *)g.out;
@@ -202,13 +208,13 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_fp8(GemmArgs g) {
     for (int i = 0; i < 8; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int rt = wm * 128 + i * 16 + 4 * (lane >> 4) + r;
+        const int rt = wm * 128 + i * 16 + 4 * grp + r;
         if (rt >= t.rows) continue;
         const size_t row = (size_t)t.row0 + rt;
         const float w = g.wrow[row];
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          Y[row * g.N + nt * BN + wn * WN + j * 16 + (lane & 15)] = (__bf16)(acc[i][j][r] * w);
+          Y[row * g.N + nt * BN + wn * WN + j * 16 + r16] = (__bf16)(acc[i][j][r] * w);
       }
   }
 }
@@ -217,7 +223,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_gemm_fp8(GemmArgs g) {
 
 template <bool SWIGLU>
 hipError_t launch_fp8(const GemmArgs &g, int grid_tiles, int align, hipStream_t s) {
-  if (g.N % 256 || g.K % 128 || g.K > kMaxDim || g.s_ld % 4) return hipErrorInvalidValue;
+  if (g.N % 256 || g.K % 128 || g.K > kMaxDim || g.s_ld % 256) return hipErrorInvalidValue;
   const int grid = balanced_grid(grid_tiles, kGroupM, g.N / 256);
   if (align == kFp8TileM)
     hipLaunchKernelGGL((k_gemm_fp8<4, 3, SWIGLU>), dim3(grid), dim3(256), 0, s, g);

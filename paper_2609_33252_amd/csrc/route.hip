@@ -414,8 +414,8 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_scan_scatter(Arena a, S
 
 // ----------------------------------------------------------------- pack
 // One wave per grouped row (kPackRows rows per block): the pair's input row
-// is converted (f32 -> bf16) or quantised (e4m3, one scale per 128 channels;
-// or MXFP8, one E8M0 scale per 32 channels) into its grouped row.  Padding
+// is converted (f32 -> bf16) or quantised to MXFP8 (e4m3 codes, one E8M0
+// scale per 32 channels; for e4m3 and MXFP4 weights) into its grouped row.  Padding
 // rows (no pair) are skipped.  bf16 rows are not packed: the bf16 GEMM1
 // gathers them through the permutation.
 constexpr int kPackRows = 8;
@@ -440,27 +440,6 @@ __device__ inline uint2 e4m3x8(const float q[8]) {
   return make_uint2((uint32_t)lo, (uint32_t)hi);
 }
 
-// 16 lanes x 8 channels = one 128-channel block: scale = amax / 448 (1 for
-// an all-zero block), codes e4m3(x / scale); scales k-block major at
-// ds[b * s_ld].  Every lane takes part in the shuffles.
-__device__ inline void quant_e4m3_b128(const uint4 &in, bool ok, int lane, int c, uint8_t *dq,
-                                       float *ds, int s_ld) {
-  float v[8];
-  bf16x8_to_f32(in, v);
-  float amax = 0.f;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(v[j]));
-#pragma unroll
-  for (int sh = 1; sh < 16; sh <<= 1) amax = fmaxf(amax, __shfl_xor(amax, sh, 16));
-  const float scale = amax > 0.f ? amax / 448.0f : 1.0f;
-  if (!ok) return;
-  float q[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) q[j] = v[j] / scale;
-  *(uint2 *)(dq + c) = e4m3x8(q);
-  if ((lane & 15) == 0) ds[(size_t)(c / 128) * s_ld] = scale;
-}
-
 // 4 lanes x 8 channels = one 32-channel MX block: E8M0 scale
 // 2^(floor(log2 amax) - 8), codes e4m3(x / scale) saturated at 448.
 __device__ inline void quant_mx8(const uint4 &in, bool ok, int lane, int c, uint8_t *dq,
@@ -482,7 +461,7 @@ __device__ inline void quant_mx8(const uint4 &in, bool ok, int lane, int c, uint
   if ((lane & 3) == 0) ds[mx_row_scale_offset(pos, c / kMxBlock, s_ld)] = (uint8_t)code;
 }
 
-// 1: f32 -> bf16, 2: bf16 -> e4m3 + scales, 3: bf16 -> MXFP8
+// 1: f32 -> bf16, 3: bf16 -> MXFP8 (e4m3 and MXFP4 weights)
 template <int XMODE>
 __global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0, int k, int E,
                                                    int d, int n_rows_pad) {
@@ -521,10 +500,7 @@ __global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0
         for (int u = 0; u < kQuantPass; ++u) {
           if (p0 + u * 512 >= d) break;  // uniform over the wave
           const int c = p0 + u * 512 + lane * 8;
-          if (XMODE == 3)
-            quant_mx8(in[u], c < d, lane, c, dq, (uint8_t *)sc.xs, pos, sc.s_ld);
-          else
-            quant_e4m3_b128(in[u], c < d, lane, c, dq, sc.xs + pos, sc.s_ld);
+          quant_mx8(in[u], c < d, lane, c, dq, (uint8_t *)sc.xs, pos, sc.s_ld);
         }
       }
     }
@@ -792,10 +768,8 @@ hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows,
   const long long bound = ((long long)(expected_pairs + align - 1) / align + E) * align;
   const int n_pad = (int)std::min<long long>(bound, max_mpad);
   const dim3 pgrid((n_pad + kPackRows - 1) / kPackRows);
-  if (wk == kWMx)
+  if (wk == kWMx || wk == kWFp8)
     hipLaunchKernelGGL(k_pack_rows<3>, pgrid, dim3(256), 0, s, a, sc, row0, k, E, d, n_pad);
-  else if (wk == kWFp8)
-    hipLaunchKernelGGL(k_pack_rows<2>, pgrid, dim3(256), 0, s, a, sc, row0, k, E, d, n_pad);
   else if (x_dtype == 0)
     hipLaunchKernelGGL(k_pack_rows<1>, pgrid, dim3(256), 0, s, a, sc, row0, k, E, d, n_pad);
   // bf16 rows with bf16 weights: GEMM1 reads them in place

@@ -96,11 +96,14 @@ struct cep_ctx {
   std::vector<BatchRec> batches;
   bool origin_set = false;
   hipEvent_t ev_origin = nullptr;
-  // fetch: the one decision of this layer; fetched_mask = experts whose
-  // copies gate their tiles, inplace_mask = experts read from the donor
-  // region in place (no copy, or a copy that failed to start)
+  // fetch: the one decision of this layer; fetched_mask = the fetched
+  // experts, whose tiles run after the resident experts' GEMMs; copied: their
+  // weights come from the fetch buffer and their tiles wait for the copy
+  // (else they are read from the donor region in place: no copy, or a copy
+  // that failed to start)
   bool fetched = false;
-  uint64_t fetched_mask = 0, inplace_mask = 0;
+  uint64_t fetched_mask = 0;
+  bool copied = false;
   bool fetch_copy_issued = false;  // a copy was enqueued (this layer)
   bool fetch_copy_prev = false;    // ev_fetch_ready holds an earlier layer's copy
   bool fetch_fallback = false;     // this layer's copy failed: read in place
@@ -244,7 +247,7 @@ hipStream_t pending_stream(const cep_ctx *c) {
 // Experts that have pairs routed to them but no weights this layer: neither
 // resident nor fetched (copied or read in place).
 uint64_t missing_experts(const cep_ctx *c) {
-  return c->nonres_mask & ~(c->fetched_mask | c->inplace_mask);
+  return c->nonres_mask & ~c->fetched_mask;
 }
 
 // Launch all pending chunks as one grouped invocation on the next stream slot.
@@ -335,7 +338,7 @@ int launch_pending(cep_ctx *c) {
   // the resident work and delays nothing before it (Appendix C, "One-shot
   // weight fetching": the donor-side work does not wait for the copy)
   if (b.fetched) {
-    HIPCHK(c, hipStreamWaitEvent(s, c->ev_fetch_ready, 0));
+    if (c->copied) HIPCHK(c, hipStreamWaitEvent(s, c->ev_fetch_ready, 0));
     if (b.phases) HIPCHK(c, hipEventRecord(b.ev_fphase[0], s));
     HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
                            gather, b.row0, k, s));
@@ -614,7 +617,8 @@ CEP_API int cep_begin_layer(cep_ctx *c, uint32_t generation, int n_replicas,
   c->ingest_tail = nullptr;
   c->origin_set = true;
   c->fetched = false;
-  c->fetched_mask = c->inplace_mask = 0;
+  c->fetched_mask = 0;
+  c->copied = false;
   c->fetch_copy_prev = c->fetch_copy_prev || c->fetch_copy_issued;
   c->fetch_copy_issued = false;
   c->fetch_fallback = false;
@@ -743,10 +747,10 @@ CEP_API int cep_weight_fetch(cep_ctx *c, const int *ids, int n, const void *cons
     c->fetch_copy_issued = true;
   }
   if (in_place) {
-    // fetched experts read their donor blobs where they are: no copy to wait
-    // for, so their tiles run with the resident experts' tiles
+    // fetched experts read their donor blobs where they are: their tiles still
+    // run after the resident experts' GEMMs, with no copy to wait for
     for (int i = 0; i < n; ++i) c->blob_ptr[ids[i]] = (const uint8_t *)src_blobs[i];
-    c->inplace_mask = mask;
+    c->fetched_mask = mask;
     return CEP_OK;
   }
   for (int i = 0; i < n; ++i) {
@@ -754,6 +758,7 @@ CEP_API int cep_weight_fetch(cep_ctx *c, const int *ids, int n, const void *cons
     c->blob_ptr[ids[i]] = c->fetch_buf + (size_t)slot * c->L.bytes;
   }
   c->fetched_mask = mask;
+  c->copied = true;
   if (ready) *ready = c->ev_fetch_ready;
   return CEP_OK;
 }
@@ -893,7 +898,7 @@ CEP_API int cep_get_stats(cep_ctx *c, char *buf, size_t cap) {
     js += tmp;
   }
   js += "]";
-  if (c->fetched && (c->fetched_mask | c->inplace_mask)) {
+  if (c->fetched && c->fetched_mask) {
     float f0 = -1, f1 = -1;
     if (c->fetch_copy_issued) {
       HIPCHK(c, hipEventSynchronize(c->ev_fetch_ready));
@@ -906,9 +911,9 @@ CEP_API int cep_get_stats(cep_ctx *c, char *buf, size_t cap) {
     snprintf(tmp, sizeof tmp,
              ",\"fetch\":{\"start_ms\":%.6f,\"end_ms\":%.6f,\"bytes\":%zu,\"experts\":%d,"
              "\"in_place\":%s,\"fallback\":%s}",
-             f0, f1, (size_t)__builtin_popcountll(c->fetched_mask) * c->L.bytes,
-             __builtin_popcountll(c->fetched_mask | c->inplace_mask),
-             c->inplace_mask ? "true" : "false", c->fetch_fallback ? "true" : "false");
+             f0, f1, c->copied ? (size_t)__builtin_popcountll(c->fetched_mask) * c->L.bytes : 0,
+             __builtin_popcountll(c->fetched_mask), c->copied ? "false" : "true",
+             c->fetch_fallback ? "true" : "false");
     js += tmp;
   }
   js += "}";

@@ -10,7 +10,6 @@ path runs in libcep's kernels.
 """
 from __future__ import annotations
 
-import ctypes
 import time
 
 import numpy as np
@@ -21,19 +20,6 @@ from . import workload as W
 
 _DT = {W.F32: cep.CEP_F32, W.BF16: cep.CEP_BF16, W.FP8: cep.CEP_FP8_E4M3_B128,
        W.MXFP4: cep.CEP_MXFP4}
-
-
-_HIP = None
-
-
-def _hip():
-    """The HIP runtime, for one stream-on-event wait the torch API has no
-    call for (the fetch's ready event is a raw hipEvent_t)."""
-    global _HIP
-    if _HIP is None:
-        _HIP = ctypes.CDLL("libamdhip64.so")
-        _HIP.hipStreamWaitEvent.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint]
-    return _HIP
 
 
 class DeviceChunk:
@@ -121,7 +107,7 @@ class Runner:
 
     def run(self, policy=cep.CEP_WAIT_ALL, theta=1, n_streams=1, order=None, timed=False,
             time_scale=1.0, arrival_events=False, out=None, stream=None, inputs_ready=False,
-            fetch_mode=None, prefetch=False):
+            fetch_mode=None):
         """Replay one layer; returns the library's done event handle.
 
         order: optional permutation of chunk indices (submission order).
@@ -130,10 +116,6 @@ class Runner:
             stream writes them (steady-state replay of the same layer), so the
             chunks carry no arrival event.
         fetch_mode: cep_fetch_mode of this and later layers (None: unchanged).
-        prefetch: every chunk arrives only after the weight copy (its arrival
-            event follows the fetch's ready event on the dispatch stream), so
-            the batch starts once the copy is done: the layer as if the copy
-            had happened before it, without a host round trip.
         """
         out = self.out if out is None else out
         stream = torch.cuda.current_stream(self.device) if stream is None else stream
@@ -151,13 +133,7 @@ class Runner:
         seq = range(len(self.chunks)) if order is None else order
         # chunk inputs and `out` were written on the caller's stream: every
         # chunk becomes valid only after that work
-        if prefetch and self.use_fetch and self.fetch_ready:
-            _hip().hipStreamWaitEvent(ctypes.c_void_p(self.dispatch.cuda_stream),
-                                      ctypes.c_void_p(self.fetch_ready), 0)
-            ready = torch.cuda.Event(enable_timing=True)
-            ready.record(self.dispatch)
-            self.arrival_events = [ready]
-        elif inputs_ready and not (timed or arrival_events):
+        if inputs_ready and not (timed or arrival_events):
             ready = None
             self.arrival_events = []
         else:

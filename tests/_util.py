@@ -17,7 +17,7 @@ from paper_2609_33252_amd import workload as W
 
 # Elementwise bound for bf16 inputs with float32 accumulation, and the
 # relative-RMS bound for the e4m3 path (both from the target tolerance of the
-# routed-expert path); the MXFP4 path quantises activations and h to e4m3
+# routed-expert path); the MXFP4 path quantises activations and h to MXFP8
 # like the e4m3 path and takes the same bound, also per output row.
 BF16_ATOL, BF16_RTOL = 1e-2, 1e-2
 FP8_REL_RMS = 4e-2
@@ -39,7 +39,8 @@ def np_bits(t):
 def modes(wl):
     w = wl.cfg["w"]
     if w == W.FP8:
-        return "fp8", "fp8", "fp8"
+        # e4m3 weights with float32 block scales; activations and h in MXFP8
+        return "fp8", "mxfp8", "mxfp8"
     if w == W.MXFP4:
         return "mxfp4", "mxfp8", "mxfp8"
     if w == W.BF16:
