@@ -146,6 +146,86 @@ __device__ inline void wait_stages(int r) {
   wait_vmcnt<0>();
 }
 
+// Epilogues of the block-scaled 8 x 4-fragment wave tiles (e4m3 and MXFP4
+// weights).  With the weight fragment as the MFMA's first operand,
+// acc[i][j][r] is row wm*128 + i*16 + l%16 and column wn*64 + j*16 +
+// 4*(l/16) + r of the 256-column tile nt (lane l), so each lane holds four
+// consecutive outputs of a row.
+//
+// GEMM1: h = silu(gate) * up, quantised to MXFP8.  The wave's 64 columns are
+// 32 gate and 32 up columns (interleaved in groups of 32), so its 32 h
+// columns of a row -- one MX block -- lie in the four lanes of the row: the
+// block amax takes two cross-lane steps.  The E8M0 scale is
+// 2^(floor(log2 amax) - 8) (emax of e4m3), the codes e4m3(h / scale)
+// saturated at 448; each lane stores two runs of 4 codes.
+__device__ inline void store_h_mx(const f32x4 (&acc)[8][4], const GemmArgs &g, const Tile &t,
+                                  int nt, int wm, int wn, int lane) {
+  uint8_t *H = (uint8_t *)g.out;
+  uint8_t *Hs = (uint8_t *)g.out_s;
+  const int I = g.N / 2, hblk = nt * 4 + wn;  // this wave's MX block of h columns
+  const int r16 = lane & 15, grp = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    // h columns nt*128 + wn*32 + jj*16 + 4*grp + r = silu(gate fragment jj)
+    // * up fragment jj+2
+    float h[2][4];
+    float m = 0.0f;
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        h[jj][r] = silu_mul(acc[i][jj][r], acc[i][jj + 2][r]);
+        m = fmaxf(m, fabsf(h[jj][r]));
+      }
+    m = fmaxf(m, __shfl_xor(m, 16));
+    m = fmaxf(m, __shfl_xor(m, 32));
+    const int rt = wm * 128 + i * 16 + r16;
+    if (rt >= t.rows) continue;
+    const int code = max((int)((__float_as_uint(m) >> 23) & 0xff) - 8, 0);
+    const int e = 127 - code;  // h / 2^(code - 127), exact
+    uint32_t w[2];
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+      float q[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) q[r] = fminf(fmaxf(ldexpf(h[jj][r], e), -448.0f), 448.0f);
+      int v = __builtin_amdgcn_cvt_pk_fp8_f32(q[0], q[1], 0, false);
+      v = __builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], v, true);
+      w[jj] = (uint32_t)v;
+    }
+    const size_t row = (size_t)t.row0 + rt;
+    uint8_t *hrow = H + row * I + nt * 128 + wn * 32 + 4 * grp;
+    *(uint32_t *)hrow = w[0];
+    *(uint32_t *)(hrow + 16) = w[1];
+    if (grp == 0) Hs[mx_row_scale_offset((int)row, hblk, g.s_ld)] = (uint8_t)code;
+  }
+}
+
+// GEMM2: y = coefficient * acc in bf16, four consecutive columns (8 bytes)
+// per lane and row.
+__device__ inline void store_y_bf16(const f32x4 (&acc)[8][4], const GemmArgs &g, const Tile &t,
+                                    int nt, int wm, int wn, int lane) {
+  __bf16 *Y = (__bf16 *)g.out;
+  const int r16 = lane & 15, grp = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int rt = wm * 128 + i * 16 + r16;
+    if (rt >= t.rows) continue;
+    const size_t row = (size_t)t.row0 + rt;
+    const float wr = g.wrow[row];
+    __bf16 *yrow = Y + row * g.N + nt * 256 + wn * 64 + 4 * grp;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      uint32_t v[2];
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+        v[r] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[i][j][2 * r] * wr)) |
+               ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[i][j][2 * r + 1] * wr)) << 16);
+      *(uint2 *)(yrow + j * 16) = make_uint2(v[0], v[1]);
+    }
+  }
+}
+
 // Launchers of the two kernel families (grid from the tile bound).
 template <bool SWIGLU>
 hipError_t launch_bf16(const GemmArgs &g, int grid_tiles, int align, hipStream_t s);

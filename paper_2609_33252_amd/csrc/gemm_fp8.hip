@@ -17,22 +17,26 @@
 //
 // Operand layout of the instruction (lane l: row or column l%16, group
 // g = l/16): an e4m3 operand lane holds K [16g, 16g+16) in bytes 0-15 and
-// K [64+16g, 64+16g+16) in bytes 16-31; the A scale byte of lane l applies to
-// K block g of its row.
+// K [64+16g, 64+16g+16) in bytes 16-31; an operand's scale byte of lane l
+// applies to K block g of its row or column.
 #include "gemm_common.h"
 
 namespace cep {
 namespace {
 
-// One e4m3 x e4m3 MFMA of a K block with the A operand's E8M0 scales (byte
-// oa of the word sa) and unit B scales; oa is a constant after the caller's
-// loop is unrolled, and the switch folds away.
-__device__ inline f32x4 f8_mfma(const i32x8 &a, const i32x8 &b, int oa, int sa) {
-  switch (oa) {
-    case 0: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, f32x4{}, 0, 0, 0, sa, 0, 127);
-    case 1: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, f32x4{}, 0, 0, 1, sa, 0, 127);
-    case 2: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, f32x4{}, 0, 0, 2, sa, 0, 127);
-    default: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, f32x4{}, 0, 0, 3, sa, 0, 127);
+// One e4m3 x e4m3 MFMA of a K block: the weight fragment w is the
+// instruction's first operand (unit scales), the activation fragment x its
+// second, with E8M0 scales (byte ox of the word sx).  Output lane l then
+// holds activation row l%16 and the four consecutive weight columns
+// 4*(l/16) .. 4*(l/16)+3, so an epilogue stores 4 consecutive outputs of a
+// row per lane.  ox is a constant after the caller's loop is unrolled, and
+// the switch folds away.
+__device__ inline f32x4 f8_mfma(const i32x8 &w, const i32x8 &x, int ox, int sx) {
+  switch (ox) {
+    case 0: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(w, x, f32x4{}, 0, 0, 0, 127, 0, sx);
+    case 1: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(w, x, f32x4{}, 0, 0, 0, 127, 1, sx);
+    case 2: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(w, x, f32x4{}, 0, 0, 0, 127, 2, sx);
+    default: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(w, x, f32x4{}, 0, 0, 0, 127, 3, sx);
   }
 }
 
@@ -52,10 +56,7 @@ __device__ inline f32x4 f8_mfma(const i32x8 &a, const i32x8 &b, int oa, int sa) 
 // the sixteen lanes of one half-wave whose quad index (lane bits 2-4) has
 // one parity, and those lanes then touch sixteen distinct slots of 256 bytes.
 //
-// GEMM1 epilogue: h = silu(gate) * up; each wave's 32 h columns of a row are
-// one MX block, so the block amax needs only a 16-lane reduction; the E8M0
-// scale is 2^(floor(log2 amax) - 8), the codes e4m3(h / scale) saturated at
-// 448.
+// Epilogues: store_h_mx (GEMM1) and store_y_bf16 (GEMM2).
 template <int NW, int STAGES, bool SWIGLU, int OCC = 1>
 __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
   constexpr int BM = 128 * NW / 4, BN = 256, BK = 128, WN = BN / 4;
@@ -165,7 +166,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
       const int sai = (int)(i < 4 ? sa.x : sa.y);
       f32x4 p[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) p[j] = f8_mfma(a, b[j], i & 3, sai);
+      for (int j = 0; j < 4; ++j) p[j] = f8_mfma(b[j], a, i & 3, sai);
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] += p[j] * (j < 2 ? sb0 : sb1);
     }
@@ -173,50 +174,10 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
 #undef CEP_F8_STAGE
 #undef CEP_F8_OFF
 
-  // 16x16 accumulator layout: lane l, element r -> column l%16,
-  // row 4*(l/16) + r.
-  if (SWIGLU) {
-    uint8_t *H = (uint8_t *)g.out;
-    uint8_t *Hs = (uint8_t *)g.out_s;
-    const int I = g.N / 2, hblk = nt * 4 + wn;  // this wave's MX block of h columns
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        // h column nt*128 + wn*32 + jj*16 + l%16 = silu(gate block jj) * up block jj+2
-        const float h0 = silu_mul(acc[i][0][r], acc[i][2][r]);
-        const float h1 = silu_mul(acc[i][1][r], acc[i][3][r]);
-        float m = fmaxf(fabsf(h0), fabsf(h1));
-#pragma unroll
-        for (int sh = 1; sh < 16; sh <<= 1) m = fmaxf(m, __shfl_xor(m, sh, 16));
-        const int rt = wm * 128 + i * 16 + 4 * grp + r;
-        if (rt >= t.rows) continue;
-        const int code = max((int)((__float_as_uint(m) >> 23) & 0xff) - 8, 0);
-        const int e = 127 - code;  // h / 2^(code - 127), exact
-        const float q0 = fminf(fmaxf(ldexpf(h0, e), -448.0f), 448.0f);
-        const float q1 = fminf(fmaxf(ldexpf(h1, e), -448.0f), 448.0f);
-        const int q = __builtin_amdgcn_cvt_pk_fp8_f32(q0, q1, 0, false);
-        const size_t row = (size_t)t.row0 + rt;
-        uint8_t *hrow = H + row * I + nt * 128 + wn * 32 + r16;
-        hrow[0] = (uint8_t)(q & 0xff);
-        hrow[16] = (uint8_t)((q >> 8) & 0xff);
-        if (r16 == 0) Hs[mx_row_scale_offset((int)row, hblk, g.s_ld)] = (uint8_t)code;
-      }
-  } else {
-    __bf16 *Y = (__bf16 *)g.out;
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int rt = wm * 128 + i * 16 + 4 * grp + r;
-        if (rt >= t.rows) continue;
-        const size_t row = (size_t)t.row0 + rt;
-        const float w = g.wrow[row];
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          Y[row * g.N + nt * BN + wn * WN + j * 16 + r16] = (__bf16)(acc[i][j][r] * w);
-      }
-  }
+  if (SWIGLU)
+    store_h_mx(acc, g, t, nt, wm, wn, lane);
+  else
+    store_y_bf16(acc, g, t, nt, wm, wn, lane);
 }
 
 }  // namespace

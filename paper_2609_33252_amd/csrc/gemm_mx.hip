@@ -20,17 +20,20 @@
 namespace cep {
 namespace {
 
-// One e4m3 x e2m1 block-scaled MFMA; OB and oa pick the byte of the B and A
-// scale words (the instruction takes them as immediates: oa is a constant
-// after the caller's loop is unrolled, and the switch folds away).
-template <int OB>
-__device__ inline f32x4 mx_mfma(const i32x8 &a, const i32x8 &b, const f32x4 &c, int oa, int sa,
-                                int sb) {
-  switch (oa) {
-    case 0: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 4, 0, sa, OB, sb);
-    case 1: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 4, 1, sa, OB, sb);
-    case 2: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 4, 2, sa, OB, sb);
-    default: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 4, 3, sa, OB, sb);
+// One e2m1 x e4m3 block-scaled MFMA: the weight fragment w is the first
+// operand (scale byte OW of the word sw), the activation fragment x the
+// second (byte ox of sx), so that output lane l holds activation row l%16
+// and four consecutive weight columns.  The instruction takes the byte
+// selects as immediates: ox is a constant after the caller's loop is
+// unrolled, and the switch folds away.
+template <int OW>
+__device__ inline f32x4 mx_mfma(const i32x8 &w, const i32x8 &x, const f32x4 &c, int ox, int sx,
+                                int sw) {
+  switch (ox) {
+    case 0: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(w, x, c, 4, 0, OW, sw, 0, sx);
+    case 1: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(w, x, c, 4, 0, OW, sw, 1, sx);
+    case 2: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(w, x, c, 4, 0, OW, sw, 2, sx);
+    default: return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(w, x, c, 4, 0, OW, sw, 3, sx);
   }
 }
 
@@ -52,10 +55,7 @@ __device__ inline f32x4 mx_mfma(const i32x8 &a, const i32x8 &b, const f32x4 &c, 
 // with SQ_LDS_BANK_CONFLICT); with these swizzles each such group reads
 // sixteen distinct 16-byte slots of 256 bytes in both operand reads.
 //
-// GEMM1 epilogue: h = silu(gate) * up; each wave's 32 h columns of a row
-// are one MX block, so the block amax needs only a 16-lane reduction; the
-// E8M0 scale is 2^(floor(log2 amax) - 8), the codes e4m3(h / scale)
-// saturated at 448.
+// Epilogues: store_h_mx (GEMM1) and store_y_bf16 (GEMM2).
 __device__ inline int bsw_of(int r) { return (r & 1) | ((r >> 1) & 2); }
 
 
@@ -157,59 +157,19 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_mx(GemmArgs g) {
       if (i + 1 < 8) a_next = read_a(i + 1);
       __builtin_amdgcn_sched_barrier(0);
       const int sai = (int)(i < 4 ? sa.x : sa.y);
-      acc[i][0] = mx_mfma<0>(a, b[0], acc[i][0], i & 3, sai, (int)sb);
-      acc[i][1] = mx_mfma<1>(a, b[1], acc[i][1], i & 3, sai, (int)sb);
-      acc[i][2] = mx_mfma<2>(a, b[2], acc[i][2], i & 3, sai, (int)sb);
-      acc[i][3] = mx_mfma<3>(a, b[3], acc[i][3], i & 3, sai, (int)sb);
+      acc[i][0] = mx_mfma<0>(b[0], a, acc[i][0], i & 3, sai, (int)sb);
+      acc[i][1] = mx_mfma<1>(b[1], a, acc[i][1], i & 3, sai, (int)sb);
+      acc[i][2] = mx_mfma<2>(b[2], a, acc[i][2], i & 3, sai, (int)sb);
+      acc[i][3] = mx_mfma<3>(b[3], a, acc[i][3], i & 3, sai, (int)sb);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
 #undef CEP_MX_STAGE
 
-  // 16x16 accumulator layout: lane l, element r -> column l%16,
-  // row 4*(l/16) + r.
-  if (SWIGLU) {
-    uint8_t *H = (uint8_t *)g.out;
-    uint8_t *Hs = (uint8_t *)g.out_s;
-    const int I = g.N / 2, hblk = nt * 4 + wn;  // this wave's MX block of h columns
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        // h column nt*128 + wn*32 + jj*16 + l%16 = silu(gate block jj) * up block jj+2
-        const float h0 = silu_mul(acc[i][0][r], acc[i][2][r]);
-        const float h1 = silu_mul(acc[i][1][r], acc[i][3][r]);
-        float m = fmaxf(fabsf(h0), fabsf(h1));
-#pragma unroll
-        for (int sh = 1; sh < 16; sh <<= 1) m = fmaxf(m, __shfl_xor(m, sh, 16));
-        const int rt = wm * 128 + i * 16 + 4 * grp + r;
-        if (rt >= t.rows) continue;
-        const int code = max((int)((__float_as_uint(m) >> 23) & 0xff) - 8, 0);
-        const int e = 127 - code;  // h / 2^(code - 127), exact
-        const float q0 = fminf(fmaxf(ldexpf(h0, e), -448.0f), 448.0f);
-        const float q1 = fminf(fmaxf(ldexpf(h1, e), -448.0f), 448.0f);
-        const int q = __builtin_amdgcn_cvt_pk_fp8_f32(q0, q1, 0, false);
-        const size_t row = (size_t)t.row0 + rt;
-        uint8_t *hrow = H + row * I + nt * 128 + wn * 32 + r16;
-        hrow[0] = (uint8_t)(q & 0xff);
-        hrow[16] = (uint8_t)((q >> 8) & 0xff);
-        if (r16 == 0) Hs[mx_row_scale_offset((int)row, hblk, g.s_ld)] = (uint8_t)code;
-      }
-  } else {
-    __bf16 *Y = (__bf16 *)g.out;
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int rt = wm * 128 + i * 16 + 4 * grp + r;
-        if (rt >= t.rows) continue;
-        const size_t row = (size_t)t.row0 + rt;
-        const float w = g.wrow[row];
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          Y[row * g.N + nt * BN + wn * 64 + j * 16 + r16] = (__bf16)(acc[i][j][r] * w);
-      }
-  }
+  if (SWIGLU)
+    store_h_mx(acc, g, t, nt, wm, wn, lane);
+  else
+    store_y_bf16(acc, g, t, nt, wm, wn, lane);
 }
 
 }  // namespace
