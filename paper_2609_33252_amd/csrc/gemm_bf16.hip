@@ -416,23 +416,37 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
 
   // 32x32 accumulator layout: lane l, element r -> column l%32,
   // row 8*(r/4) + 4*(l/32) + r%4.
+  // GEMM2: routing coefficients of the 16 rows the lane holds in row group
+  // i.  The epilogues load group i+1's before storing group i's outputs, so
+  // that waiting for a group's coefficients never waits for earlier stores.
+  auto coef16 = [&](int i, float(&w)[16]) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int lr = frow(i) + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      w[r] = lr < t.rows ? g.wrow[(size_t)t.row0 + lr] : 0.0f;
+    }
+  };
   if constexpr (PIPE && !SWIGLU) {
     // float32 outputs straight from the accumulators: one store instruction
     // writes 32 consecutive columns (128 bytes) of two rows
     static_assert(WGM == 2 && !VAR, "two wave rows");
     float *Y = (float *)g.out;
+    float wc[16], wx[16];
+    coef16(0, wc);
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
+      if (i + 1 < FM) coef16(i + 1, wx);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int lr = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
         if (lr >= t.rows) continue;
         const size_t row = (size_t)t.row0 + lr;
-        const float w = g.wrow[row];
         const size_t ybase = row * g.N + nt * BN + wn * WN + (lane & 31);
 #pragma unroll
-        for (int j = 0; j < FN; ++j) Y[ybase + j * 32] = acc[i][j][r] * w;
+        for (int j = 0; j < FN; ++j) Y[ybase + j * 32] = acc[i][j][r] * wc[r];
       }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) wc[r] = wx[r];
     }
     // every wave's last operand reads completed: the ring is free for the
     // next tile's loads (the stores may still be in flight)
@@ -524,9 +538,12 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
     }
     return;
   }
+  float wc[16], wx[16];
+  if (!SWIGLU) coef16(0, wc);
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
     if (half && i > 0) break;
+    if (!SWIGLU && i + 1 < FM && !half) coef16(i + 1, wx);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int rt = frow(i) + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
@@ -541,12 +558,15 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
         for (int j2 = 0; j2 < FN / 2; ++j2)
           H[hbase + j2 * 32] = (__bf16)silu_mul(acc[i][2 * j2][r], acc[i][2 * j2 + 1][r]);
       } else {
-        const float w = g.wrow[row];
         float *Y = (float *)g.out;
         const size_t ybase = row * g.N + nt * BN + wn * WN + (lane & 31);
 #pragma unroll
-        for (int j = 0; j < FN; ++j) Y[ybase + j * 32] = acc[i][j][r] * w;
+        for (int j = 0; j < FN; ++j) Y[ybase + j * 32] = acc[i][j][r] * wc[r];
       }
+    }
+    if (!SWIGLU) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) wc[r] = wx[r];
     }
   }
   }  // work items

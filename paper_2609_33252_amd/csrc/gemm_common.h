@@ -201,10 +201,23 @@ __device__ inline void store_h_mx(const f32x4 (&acc)[8][4], const GemmArgs &g, c
   }
 }
 
+// GEMM2: the routing coefficients of the lane's eight rows, loaded before
+// the K loop so that their latency hides behind it (loaded in the epilogue,
+// each load's wait would also wait for the stores before it).
+__device__ inline void load_row_coef(const GemmArgs &g, const Tile &t, int wm, int lane,
+                                     float (&wr)[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int rt = wm * 128 + i * 16 + (lane & 15);
+    wr[i] = rt < t.rows ? g.wrow[(size_t)t.row0 + rt] : 0.0f;
+  }
+}
+
 // GEMM2: y = coefficient * acc in bf16, four consecutive columns (8 bytes)
 // per lane and row.
-__device__ inline void store_y_bf16(const f32x4 (&acc)[8][4], const GemmArgs &g, const Tile &t,
-                                    int nt, int wm, int wn, int lane) {
+__device__ inline void store_y_bf16(const f32x4 (&acc)[8][4], const float (&wrow)[8],
+                                    const GemmArgs &g, const Tile &t, int nt, int wm, int wn,
+                                    int lane) {
   __bf16 *Y = (__bf16 *)g.out;
   const int r16 = lane & 15, grp = lane >> 4;
 #pragma unroll
@@ -212,7 +225,7 @@ __device__ inline void store_y_bf16(const f32x4 (&acc)[8][4], const GemmArgs &g,
     const int rt = wm * 128 + i * 16 + r16;
     if (rt >= t.rows) continue;
     const size_t row = (size_t)t.row0 + rt;
-    const float wr = g.wrow[row];
+    const float wr = wrow[i];
     __bf16 *yrow = Y + row * g.N + nt * 256 + wn * 64 + 4 * grp;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {

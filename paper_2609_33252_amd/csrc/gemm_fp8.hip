@@ -126,6 +126,8 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
   }
   __syncthreads();
 
+  float wr[8];
+  if (!SWIGLU) load_row_coef(g, t, wm, lane, wr);
   const int r16 = lane & 15, grp = lane >> 4;
   const int rsw = (r16 >> 1) & 7;  // swizzle of every operand row this lane reads
   // scale rows of this wave's column blocks: GEMM1 fragments j = 0,1 (gate)
@@ -177,7 +179,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
   if (SWIGLU)
     store_h_mx(acc, g, t, nt, wm, wn, lane);
   else
-    store_y_bf16(acc, g, t, nt, wm, wn, lane);
+    store_y_bf16(acc, wr, g, t, nt, wm, wn, lane);
 }
 
 }  // namespace

@@ -119,6 +119,8 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_mx(GemmArgs g) {
   for (int s = 0; s < STAGES - 1; ++s)
     if (s < nkb) CEP_MX_STAGE(s);
 
+  float wr[8];
+  if (!SWIGLU) load_row_coef(g, t, wm, lane, wr);
   const int r16 = lane & 15, grp = lane >> 4;
   const int asw = (r16 >> 1) & 7;  // A swizzle of every row this lane reads
   const int bsw = bsw_of(r16);     // B swizzle of every row this lane reads
@@ -169,7 +171,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_mx(GemmArgs g) {
   if (SWIGLU)
     store_h_mx(acc, g, t, nt, wm, wn, lane);
   else
-    store_y_bf16(acc, g, t, nt, wm, wn, lane);
+    store_y_bf16(acc, wr, g, t, nt, wm, wn, lane);
 }
 
 }  // namespace

@@ -413,11 +413,11 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_scan_scatter(Arena a, S
 }
 
 // ----------------------------------------------------------------- pack
-// One wave per grouped row (kPackRows rows per block): the pair's input row
-// is converted (f32 -> bf16) or quantised to MXFP8 (e4m3 codes, one E8M0
-// scale per 32 channels; for e4m3 and MXFP4 weights) into its grouped row.  Padding
-// rows (no pair) are skipped.  bf16 rows are not packed: the bf16 GEMM1
-// gathers them through the permutation.
+// Input rows reach their grouped rows converted (f32 -> bf16, k_pack_rows)
+// or quantised to MXFP8 (e4m3 codes, one E8M0 scale per 32 channels, for
+// e4m3 and MXFP4 weights, k_pack_tokens).  Padding rows (no pair) are left
+// as they are: their outputs are never stored.  bf16 rows are not packed:
+// the bf16 GEMM1 gathers them through the permutation.
 constexpr int kPackRows = 8;
 
 constexpr int kQuantPass = 8;  // 512-channel groups loaded per pass of a quantised row
@@ -441,9 +441,9 @@ __device__ inline uint2 e4m3x8(const float q[8]) {
 }
 
 // 4 lanes x 8 channels = one 32-channel MX block: E8M0 scale
-// 2^(floor(log2 amax) - 8), codes e4m3(x / scale) saturated at 448.
-__device__ inline void quant_mx8(const uint4 &in, bool ok, int lane, int c, uint8_t *dq,
-                                 uint8_t *ds, int pos, int s_ld) {
+// 2^(floor(log2 amax) - 8), codes e4m3(x / scale) saturated at 448.  Returns
+// the lane's eight codes; *code gets the block's scale code.
+__device__ inline uint2 quant_mx8(const uint4 &in, int *code) {
   float v[8];
   bf16x8_to_f32(in, v);
   float amax = 0.f;
@@ -451,18 +451,15 @@ __device__ inline void quant_mx8(const uint4 &in, bool ok, int lane, int c, uint
   for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(v[j]));
   amax = fmaxf(amax, __shfl_xor(amax, 1, 4));
   amax = fmaxf(amax, __shfl_xor(amax, 2, 4));
-  if (!ok) return;
-  const int code = max((int)((__float_as_uint(amax) >> 23) & 0xff) - 8, 0);
-  const int e = 127 - code;
+  *code = max((int)((__float_as_uint(amax) >> 23) & 0xff) - 8, 0);
+  const int e = 127 - *code;
   float q[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) q[j] = fminf(fmaxf(ldexpf(v[j], e), -448.0f), 448.0f);
-  *(uint2 *)(dq + c) = e4m3x8(q);
-  if ((lane & 3) == 0) ds[mx_row_scale_offset(pos, c / kMxBlock, s_ld)] = (uint8_t)code;
+  return e4m3x8(q);
 }
 
-// 1: f32 -> bf16, 3: bf16 -> MXFP8 (e4m3 and MXFP4 weights)
-template <int XMODE>
+// f32 -> bf16 rows (one wave per grouped row).
 __global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0, int k, int E,
                                                    int d, int n_rows_pad) {
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
@@ -472,36 +469,54 @@ __global__ __launch_bounds__(256) void k_pack_rows(Arena a, Scratch sc, int row0
     if (pos >= end) return;
     const int p = sc.perm[pos];
     if (p < 0) continue;
-    const char *src = (const char *)a.xrow[row0 + p / k];
-    if (XMODE == 1) {
-      const float4 *s4 = (const float4 *)src;
-      uint4 *d4 = (uint4 *)((char *)sc.xg + (size_t)pos * d * 2);
-      for (int c = lane; c < d / 8; c += 64) {
-        const float4 lo = s4[2 * c], hi = s4[2 * c + 1];
-        union { __bf16 h[8]; uint4 u; } o;
-        o.h[0] = (__bf16)lo.x; o.h[1] = (__bf16)lo.y; o.h[2] = (__bf16)lo.z; o.h[3] = (__bf16)lo.w;
-        o.h[4] = (__bf16)hi.x; o.h[5] = (__bf16)hi.y; o.h[6] = (__bf16)hi.z; o.h[7] = (__bf16)hi.w;
-        d4[c] = o.u;
-      }
-    } else {
-      // quantised rows: a pass first loads up to kQuantPass 512-channel
-      // groups (eight channels per lane), then quantises them, so that many
-      // loads are in flight per wave
-      const uint4 *s4 = (const uint4 *)src;
-      uint8_t *dq = (uint8_t *)sc.xg + (size_t)pos * d;
-      for (int p0 = 0; p0 < d; p0 += 512 * kQuantPass) {
-        uint4 in[kQuantPass];
+    const float4 *s4 = (const float4 *)a.xrow[row0 + p / k];
+    uint4 *d4 = (uint4 *)((char *)sc.xg + (size_t)pos * d * 2);
+    for (int c = lane; c < d / 8; c += 64) {
+      const float4 lo = s4[2 * c], hi = s4[2 * c + 1];
+      union { __bf16 h[8]; uint4 u; } o;
+      o.h[0] = (__bf16)lo.x; o.h[1] = (__bf16)lo.y; o.h[2] = (__bf16)lo.z; o.h[3] = (__bf16)lo.w;
+      o.h[4] = (__bf16)hi.x; o.h[5] = (__bf16)hi.y; o.h[6] = (__bf16)hi.z; o.h[7] = (__bf16)hi.w;
+      d4[c] = o.u;
+    }
+  }
+}
+
+// bf16 -> MXFP8 rows (e4m3 and MXFP4 weights), one wave per batch row: the
+// row is read and quantised once and its codes and scales written to the
+// grouped row of each of its local slots (a token averages 1.3 local slots
+// on the skewed workloads, so reading per token rather than per pair saves a
+// quarter of the reads).  A pass first loads up to kQuantPass 512-channel
+// groups (eight channels per lane), then quantises them, so that many loads
+// are in flight per wave.
+__global__ __launch_bounds__(256) void k_pack_tokens(Arena a, Scratch sc, int row0, int n_rows,
+                                                     int k, int d) {
+  const int lane = threadIdx.x & 63;
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= n_rows) return;  // uniform over the wave
+  static_assert(kMaxTopK <= 64, "a row's slots fit one wave");
+  const int ps = lane < k ? sc.pos_of[(size_t)i * k + lane] : -1;
+  const uint64_t valid = __ballot(ps >= 0);
+  if (valid == 0) return;
+  const uint4 *s4 = (const uint4 *)a.xrow[row0 + i];
+  uint8_t *xs = (uint8_t *)sc.xs;
+  for (int p0 = 0; p0 < d; p0 += 512 * kQuantPass) {
+    uint4 in[kQuantPass];
 #pragma unroll
-        for (int u = 0; u < kQuantPass; ++u) {
-          const int c = p0 + u * 512 + lane * 8;
-          in[u] = c < d ? s4[c / 8] : make_uint4(0u, 0u, 0u, 0u);
-        }
+    for (int u = 0; u < kQuantPass; ++u) {
+      const int c = p0 + u * 512 + lane * 8;
+      in[u] = c < d ? s4[c / 8] : make_uint4(0u, 0u, 0u, 0u);
+    }
 #pragma unroll
-        for (int u = 0; u < kQuantPass; ++u) {
-          if (p0 + u * 512 >= d) break;  // uniform over the wave
-          const int c = p0 + u * 512 + lane * 8;
-          quant_mx8(in[u], c < d, lane, c, dq, (uint8_t *)sc.xs, pos, sc.s_ld);
-        }
+    for (int u = 0; u < kQuantPass; ++u) {
+      if (p0 + u * 512 >= d) break;  // uniform over the wave
+      const int c = p0 + u * 512 + lane * 8;
+      int code;
+      const uint2 q = quant_mx8(in[u], &code);
+      if (c >= d) continue;
+      for (uint64_t m = valid; m; m &= m - 1) {
+        const int pos = __shfl(ps, __builtin_ctzll(m));
+        *(uint2 *)((uint8_t *)sc.xg + (size_t)pos * d + c) = q;
+        if ((lane & 3) == 0) xs[mx_row_scale_offset(pos, c / kMxBlock, sc.s_ld)] = (uint8_t)code;
       }
     }
   }
@@ -767,11 +782,12 @@ hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows,
   // grouped rows: at most every pair plus one partial tile per expert
   const long long bound = ((long long)(expected_pairs + align - 1) / align + E) * align;
   const int n_pad = (int)std::min<long long>(bound, max_mpad);
-  const dim3 pgrid((n_pad + kPackRows - 1) / kPackRows);
   if (wk == kWMx || wk == kWFp8)
-    hipLaunchKernelGGL(k_pack_rows<3>, pgrid, dim3(256), 0, s, a, sc, row0, k, E, d, n_pad);
+    hipLaunchKernelGGL(k_pack_tokens, dim3((n_rows + 3) / 4), dim3(256), 0, s, a, sc, row0, n_rows,
+                       k, d);
   else if (x_dtype == 0)
-    hipLaunchKernelGGL(k_pack_rows<1>, pgrid, dim3(256), 0, s, a, sc, row0, k, E, d, n_pad);
+    hipLaunchKernelGGL(k_pack_rows, dim3((n_pad + kPackRows - 1) / kPackRows), dim3(256), 0, s, a,
+                       sc, row0, k, E, d, n_pad);
   // bf16 rows with bf16 weights: GEMM1 reads them in place
   return hipGetLastError();
 }
