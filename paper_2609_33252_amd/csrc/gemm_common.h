@@ -152,55 +152,6 @@ __device__ inline void wait_stages(int r) {
 // 4*(l/16) + r of the 256-column tile nt (lane l), so each lane holds four
 // consecutive outputs of a row.
 //
-// GEMM1: h = silu(gate) * up, quantised to MXFP8.  The wave's 64 columns are
-// 32 gate and 32 up columns (interleaved in groups of 32), so its 32 h
-// columns of a row -- one MX block -- lie in the four lanes of the row: the
-// block amax takes two cross-lane steps.  The E8M0 scale is
-// 2^(floor(log2 amax) - 8) (emax of e4m3), the codes e4m3(h / scale)
-// saturated at 448; each lane stores two runs of 4 codes.
-__device__ inline void store_h_mx(const f32x4 (&acc)[8][4], const GemmArgs &g, const Tile &t,
-                                  int nt, int wm, int wn, int lane) {
-  uint8_t *H = (uint8_t *)g.out;
-  uint8_t *Hs = (uint8_t *)g.out_s;
-  const int I = g.N / 2, hblk = nt * 4 + wn;  // this wave's MX block of h columns
-  const int r16 = lane & 15, grp = lane >> 4;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    // h columns nt*128 + wn*32 + jj*16 + 4*grp + r = silu(gate fragment jj)
-    // * up fragment jj+2
-    float h[2][4];
-    float m = 0.0f;
-#pragma unroll
-    for (int jj = 0; jj < 2; ++jj)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        h[jj][r] = silu_mul(acc[i][jj][r], acc[i][jj + 2][r]);
-        m = fmaxf(m, fabsf(h[jj][r]));
-      }
-    m = fmaxf(m, __shfl_xor(m, 16));
-    m = fmaxf(m, __shfl_xor(m, 32));
-    const int rt = wm * 128 + i * 16 + r16;
-    if (rt >= t.rows) continue;
-    const int code = max((int)((__float_as_uint(m) >> 23) & 0xff) - 8, 0);
-    const int e = 127 - code;  // h / 2^(code - 127), exact
-    uint32_t w[2];
-#pragma unroll
-    for (int jj = 0; jj < 2; ++jj) {
-      float q[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) q[r] = fminf(fmaxf(ldexpf(h[jj][r], e), -448.0f), 448.0f);
-      int v = __builtin_amdgcn_cvt_pk_fp8_f32(q[0], q[1], 0, false);
-      v = __builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], v, true);
-      w[jj] = (uint32_t)v;
-    }
-    const size_t row = (size_t)t.row0 + rt;
-    uint8_t *hrow = H + row * I + nt * 128 + wn * 32 + 4 * grp;
-    *(uint32_t *)hrow = w[0];
-    *(uint32_t *)(hrow + 16) = w[1];
-    if (grp == 0) Hs[mx_row_scale_offset((int)row, hblk, g.s_ld)] = (uint8_t)code;
-  }
-}
-
 // GEMM2: the routing coefficients of the lane's eight rows, loaded before
 // the K loop so that their latency hides behind it (loaded in the epilogue,
 // each load's wait would also wait for the stores before it).
@@ -236,6 +187,116 @@ __device__ inline void store_y_bf16(const f32x4 (&acc)[8][4], const float (&wrow
                ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[i][j][2 * r + 1] * wr)) << 16);
       *(uint2 *)(yrow + j * 16) = make_uint2(v[0], v[1]);
     }
+  }
+}
+
+// GEMM2 through LDS: the waves write their coefficient-scaled bf16 outputs
+// into the idle operand ring (512 bytes a row, 16-byte chunk c of row r at
+// slot c ^ (r & 15), so that the sixteen rows of one write instruction hit
+// distinct banks), then the workgroup stores whole rows with 16-byte stores:
+// one store instruction covers two full rows, where the accumulator layout
+// gives 64 pieces of 8 bytes.  The rows of wave row 0 go to st0, those of
+// wave row 1 to st1 (each 64 KB), or with st1 null both through st0 in turn.
+template <int NW>
+__device__ inline void store_y_bf16_staged(const f32x4 (&acc)[8][4], const float (&wrow)[8],
+                                           const GemmArgs &g, const Tile &t, int nt, int wm,
+                                           int wn, int lane, int tid, u32x4 *st0, u32x4 *st1) {
+  const int r16 = lane & 15, grp = lane >> 4;
+  constexpr int WR = NW / 4;  // wave rows of 128 tile rows
+  const int passes = st1 ? 1 : WR;
+  __bf16 *Y = (__bf16 *)g.out + (size_t)t.row0 * g.N + (size_t)nt * 256;
+  for (int pass = 0; pass < passes; ++pass) {
+    __syncthreads();  // the ring (or the previous pass's rows) is no longer read
+    if (passes == 1 || wm == pass) {
+      u32x4 *st = wm == 0 || !st1 ? st0 : st1;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int r = i * 16 + r16;  // row within the wave row
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          uint32_t v[2];
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+            v[h] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[i][j][2 * h] * wrow[i])) |
+                   ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[i][j][2 * h + 1] * wrow[i]))
+                    << 16);
+          const int c = wn * 8 + j * 2 + (grp >> 1);  // 16-byte chunk of the row
+          uint2 *dst = (uint2 *)&st[r * 32 + (c ^ r16)] + (grp & 1);
+          *dst = make_uint2(v[0], v[1]);
+        }
+      }
+    }
+    __syncthreads();
+    const int rlo = passes == 1 ? 0 : pass * 128, nrows = passes == 1 ? 128 * WR : 128;
+#pragma unroll 4
+    for (int q = tid; q < nrows * 32; q += 64 * NW) {
+      const int row = rlo + (q >> 5), c = q & 31;
+      if (row >= t.rows) break;  // q grows with the row
+      const u32x4 *src = row < 128 || !st1 ? st0 : st1;
+      const int lr = row & 127;
+      *(u32x4 *)(Y + (size_t)row * g.N + c * 8) = src[lr * 32 + (c ^ (lr & 15))];
+    }
+  }
+}
+
+// GEMM1: h = silu(gate) * up, quantised to MXFP8.  The wave's 64 columns are
+// 32 gate and 32 up columns (interleaved in groups of 32), so its 32 h
+// columns of a row -- one MX block -- lie in the four lanes of the row: the
+// block amax takes two cross-lane steps.  The E8M0 scale is
+// 2^(floor(log2 amax) - 8) (emax of e4m3), the codes e4m3(h / scale)
+// saturated at 448.
+//
+// The codes go through the idle operand ring (128 bytes a row, 16-byte chunk
+// c of row r at slot c ^ ((r >> 1) & 7): a write instruction's sixteen rows x
+// four dwords hit distinct banks), then the workgroup stores whole 128-byte
+// row segments with 16-byte stores.  st holds BM x 128 bytes.
+template <int NW>
+__device__ inline void store_h_mx_staged(const f32x4 (&acc)[8][4], const GemmArgs &g,
+                                         const Tile &t, int nt, int wm, int wn, int lane,
+                                         int tid, u32x4 *st) {
+  uint8_t *Hs = (uint8_t *)g.out_s;
+  const int I = g.N / 2, hblk = nt * 4 + wn;  // this wave's MX block of h columns
+  const int r16 = lane & 15, grp = lane >> 4;
+  __syncthreads();  // every wave's last operand reads completed: the ring is idle
+  uint32_t *st32 = (uint32_t *)st;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    float h[2][4];
+    float m = 0.0f;
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        h[jj][r] = silu_mul(acc[i][jj][r], acc[i][jj + 2][r]);
+        m = fmaxf(m, fabsf(h[jj][r]));
+      }
+    m = fmaxf(m, __shfl_xor(m, 16));
+    m = fmaxf(m, __shfl_xor(m, 32));
+    const int code = max((int)((__float_as_uint(m) >> 23) & 0xff) - 8, 0);
+    const int e = 127 - code;  // h / 2^(code - 127), exact
+    const int rt = wm * 128 + i * 16 + r16;
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+      float q[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) q[r] = fminf(fmaxf(ldexpf(h[jj][r], e), -448.0f), 448.0f);
+      int v = __builtin_amdgcn_cvt_pk_fp8_f32(q[0], q[1], 0, false);
+      v = __builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], v, true);
+      // bytes wn*32 + jj*16 + 4*grp of the row: chunk 2*wn + jj, dword grp
+      const int c = 2 * wn + jj;
+      st32[(rt * 8 + (c ^ ((rt >> 1) & 7))) * 4 + grp] = (uint32_t)v;
+    }
+    if (grp == 0 && rt < t.rows)
+      Hs[mx_row_scale_offset(t.row0 + rt, hblk, g.s_ld)] = (uint8_t)code;
+  }
+  __syncthreads();
+  uint8_t *H = (uint8_t *)g.out + (size_t)t.row0 * I + (size_t)nt * 128;
+  constexpr int BM = 128 * NW / 4;
+#pragma unroll 2
+  for (int q = tid; q < BM * 8; q += 64 * NW) {
+    const int row = q >> 3, c = q & 7;
+    if (row >= t.rows) break;  // q grows with the row
+    *(u32x4 *)(H + (size_t)row * I + c * 16) = st[row * 8 + (c ^ ((row >> 1) & 7))];
   }
 }
 

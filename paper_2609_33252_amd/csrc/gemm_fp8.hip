@@ -176,10 +176,16 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
 #undef CEP_F8_STAGE
 #undef CEP_F8_OFF
 
-  if (SWIGLU)
-    store_h_mx(acc, g, t, nt, wm, wn, lane);
+  // staging: BM x 128 code bytes; y rows of 512 bytes, 128 per wave row
+  static_assert(sizeof(sA) >= BM * 128, "the h tile fits the A ring");
+  static_assert(NW == 8 ? sizeof(sA) >= 128 * 512 && sizeof(sB) >= 128 * 512
+                        : sizeof(sB) >= 128 * 512, "y rows fit the rings");
+  if constexpr (SWIGLU)
+    store_h_mx_staged<NW>(acc, g, t, nt, wm, wn, lane, tid, &sA[0][0]);
+  else if constexpr (NW == 8)
+    store_y_bf16_staged<NW>(acc, wr, g, t, nt, wm, wn, lane, tid, &sA[0][0], &sB[0][0]);
   else
-    store_y_bf16(acc, wr, g, t, nt, wm, wn, lane);
+    store_y_bf16_staged<NW>(acc, wr, g, t, nt, wm, wn, lane, tid, &sB[0][0], nullptr);
 }
 
 }  // namespace

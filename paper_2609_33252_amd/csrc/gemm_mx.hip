@@ -168,10 +168,15 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_mx(GemmArgs g) {
   }
 #undef CEP_MX_STAGE
 
-  if (SWIGLU)
-    store_h_mx(acc, g, t, nt, wm, wn, lane);
-  else
+  // staging: BM x 128 code bytes, or 128 rows x 512 bytes of y per pass
+  static_assert(sizeof(sA) >= BM * 128, "the h tile fits the A ring");
+  if constexpr (SWIGLU) {
+    store_h_mx_staged<NW>(acc, g, t, nt, wm, wn, lane, tid, &sA[0][0]);
+  } else if constexpr (sizeof(sA) >= 128 * 512) {
+    store_y_bf16_staged<NW>(acc, wr, g, t, nt, wm, wn, lane, tid, &sA[0][0], nullptr);
+  } else {
     store_y_bf16(acc, wr, g, t, nt, wm, wn, lane);
+  }
 }
 
 }  // namespace
