@@ -61,7 +61,6 @@ __device__ inline bool work_item(int it, int n_live, int n_tiles_n, int *mt, int
 }
 
 // s_waitcnt lgkmcnt(0) alone (vmcnt and expcnt at their "do not wait" maxima)
-__device__ inline void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xF | (7 << 4) | (3 << 14)); }
 
 // One workgroup per CU of the current device, a multiple of 8 (the XCDs).
 inline int persistent_grid() {

@@ -120,6 +120,11 @@ __device__ inline void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
+// Waits for this wave's LDS (and scalar-memory) operations only; a barrier
+// after it synchronises LDS use without waiting for outstanding global
+// stores (__syncthreads() would also wait for those).
+__device__ inline void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xF | (7 << 4) | (3 << 14)); }
+
 // Waits until at most r (0 <= r <= R) groups of PER vector-memory operations
 // of this wave are outstanding.
 template <int PER, int R>
@@ -206,7 +211,10 @@ __device__ inline void store_y_bf16_staged(const f32x4 (&acc)[8][4], const float
   const int passes = st1 ? 1 : WR;
   __bf16 *Y = (__bf16 *)g.out + (size_t)t.row0 * g.N + (size_t)nt * 256;
   for (int pass = 0; pass < passes; ++pass) {
-    __syncthreads();  // the ring (or the previous pass's rows) is no longer read
+    // the ring (or the previous pass's rows) is no longer read; the previous
+    // pass's global stores may still be in flight
+    wait_lgkm0();
+    __builtin_amdgcn_s_barrier();
     if (passes == 1 || wm == pass) {
       u32x4 *st = wm == 0 || !st1 ? st0 : st1;
 #pragma unroll
@@ -226,7 +234,8 @@ __device__ inline void store_y_bf16_staged(const f32x4 (&acc)[8][4], const float
         }
       }
     }
-    __syncthreads();
+    wait_lgkm0();
+    __builtin_amdgcn_s_barrier();
     const int rlo = passes == 1 ? 0 : pass * 128, nrows = passes == 1 ? 128 * WR : 128;
 #pragma unroll 4
     for (int q = tid; q < nrows * 32; q += 64 * NW) {
@@ -259,6 +268,7 @@ __device__ inline void store_h_mx_staged(const f32x4 (&acc)[8][4], const GemmArg
   const int r16 = lane & 15, grp = lane >> 4;
   __syncthreads();  // every wave's last operand reads completed: the ring is idle
   uint32_t *st32 = (uint32_t *)st;
+  int codes[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     float h[2][4];
@@ -286,10 +296,10 @@ __device__ inline void store_h_mx_staged(const f32x4 (&acc)[8][4], const GemmArg
       const int c = 2 * wn + jj;
       st32[(rt * 8 + (c ^ ((rt >> 1) & 7))) * 4 + grp] = (uint32_t)v;
     }
-    if (grp == 0 && rt < t.rows)
-      Hs[mx_row_scale_offset(t.row0 + rt, hblk, g.s_ld)] = (uint8_t)code;
+    codes[i] = code;
   }
-  __syncthreads();
+  wait_lgkm0();
+  __builtin_amdgcn_s_barrier();
   uint8_t *H = (uint8_t *)g.out + (size_t)t.row0 * I + (size_t)nt * 128;
   constexpr int BM = 128 * NW / 4;
 #pragma unroll 2
@@ -297,6 +307,14 @@ __device__ inline void store_h_mx_staged(const f32x4 (&acc)[8][4], const GemmArg
     const int row = q >> 3, c = q & 7;
     if (row >= t.rows) break;  // q grows with the row
     *(u32x4 *)(H + (size_t)row * I + c * 16) = st[row * 8 + (c ^ ((row >> 1) & 7))];
+  }
+  // the scales last: a store before the barrier would make it wait for them
+  if (grp == 0) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int rt = wm * 128 + i * 16 + r16;
+      if (rt < t.rows) Hs[mx_row_scale_offset(t.row0 + rt, hblk, g.s_ld)] = (uint8_t)codes[i];
+    }
   }
 }
 
