@@ -177,8 +177,11 @@ struct Scratch {
   int32_t *perm;       // [max_mpad] flat pair of each grouped row or -1
   float *wrow;         // [max_mpad] routing coefficient of each grouped row
   void *xg;            // [max_mpad][d] bf16 or e4m3
-  float *xs;           // e4m3: [d/128][s_ld] activation scales, k-block major;
-                       // mx: E8M0 bytes at mx_row_scale_offset (same size)
+  float *xs;           // e4m3 and MXFP4 weights: the rows' E8M0 scales (MXFP8,
+                       // one byte per 32 channels) at mx_row_scale_offset
+  uint8_t *xs_rows;    // [max_mpad][xs_pitch] the same bytes row-major, as the
+                       // pack writes them (k_scale_layout moves them to xs)
+  int xs_pitch;        // d/32 rounded up to 16 bytes
   void *h;             // [max_mpad][I] bf16 or e4m3
   float *hs;           // scales of h, laid out like xs (K = I)
   int s_ld;            // row stride of xs / hs (= max_mpad, a multiple of 256)

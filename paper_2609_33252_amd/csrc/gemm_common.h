@@ -308,13 +308,19 @@ __device__ inline void store_h_mx_staged(const f32x4 (&acc)[8][4], const GemmArg
     if (row >= t.rows) break;  // q grows with the row
     *(u32x4 *)(H + (size_t)row * I + c * 16) = st[row * 8 + (c ^ ((row >> 1) & 7))];
   }
-  // the scales last: a store before the barrier would make it wait for them
+  // the scales last (a store before the barrier would make it wait for
+  // them): lane r16 of the wave's first sixteen holds rows r16 + 16i of a
+  // 128-row group (the tile's rows start at a multiple of 128), whose scales
+  // are one 8-byte word of the layout; padding rows' words are never read
   if (grp == 0) {
+    uint32_t lo = 0, hi = 0;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int rt = wm * 128 + i * 16 + r16;
-      if (rt < t.rows) Hs[mx_row_scale_offset(t.row0 + rt, hblk, g.s_ld)] = (uint8_t)codes[i];
+    for (int i = 0; i < 4; ++i) {
+      lo |= (uint32_t)codes[i] << (8 * i);
+      hi |= (uint32_t)codes[i + 4] << (8 * i);
     }
+    *(uint2 *)(Hs + mx_row_scale_offset(t.row0 + wm * 128 + r16, hblk, g.s_ld)) =
+        make_uint2(lo, hi);
   }
 }
 

@@ -498,7 +498,7 @@ __global__ __launch_bounds__(256) void k_pack_tokens(Arena a, Scratch sc, int ro
   const uint64_t valid = __ballot(ps >= 0);
   if (valid == 0) return;
   const uint4 *s4 = (const uint4 *)a.xrow[row0 + i];
-  uint8_t *xs = (uint8_t *)sc.xs;
+  uint8_t *xs_rows = sc.xs_rows;
   for (int p0 = 0; p0 < d; p0 += 512 * kQuantPass) {
     uint4 in[kQuantPass];
 #pragma unroll
@@ -516,9 +516,46 @@ __global__ __launch_bounds__(256) void k_pack_tokens(Arena a, Scratch sc, int ro
       for (uint64_t m = valid; m; m &= m - 1) {
         const int pos = __shfl(ps, __builtin_ctzll(m));
         *(uint2 *)((uint8_t *)sc.xg + (size_t)pos * d + c) = q;
-        if ((lane & 3) == 0) xs[mx_row_scale_offset(pos, c / kMxBlock, sc.s_ld)] = (uint8_t)code;
+        // the wave's 16 scale bytes of this pass are contiguous here
+        if ((lane & 3) == 0) xs_rows[(size_t)pos * sc.xs_pitch + c / kMxBlock] = (uint8_t)code;
       }
     }
+  }
+}
+
+// The packed rows' scale bytes, row-major in xs_rows, moved to the GEMM's
+// layout (mx_row_scale_offset): for a 128-row group and a 32-channel block
+// the 128 bytes are one contiguous run, byte (r % 16) * 8 + r / 16 for row r
+// of the group.  One block per (128-row group, 256 blocks): the rows come
+// into LDS with 16-byte loads and leave as 4-byte words of the runs.  (The
+// pack writing them there directly scatters single bytes: a position's
+// scales are 192 bytes in 192 different runs at d = 6144.)
+constexpr int kScaleCols = 256;                 // 32-channel blocks per LDS tile
+constexpr int kScaleLdsPitch = kScaleCols + 4;  // rows 16 apart fall in distinct banks
+
+__global__ __launch_bounds__(256) void k_scale_layout(Scratch sc, int nb) {
+  __shared__ uint8_t tile[128 * kScaleLdsPitch];
+  const int g = blockIdx.x, b0 = blockIdx.y * kScaleCols;
+  const int nbt = min(kScaleCols, nb - b0);            // blocks of this tile
+  const int nq = (min(b0 + kScaleCols, sc.xs_pitch) - b0) / 16;  // 16-byte chunks a row
+  const uint8_t *src = sc.xs_rows + (size_t)g * 128 * sc.xs_pitch + b0;
+  for (int q = threadIdx.x; q < 128 * nq; q += blockDim.x) {
+    const int r = q / nq, ch = q % nq;
+    const uint4 v = *(const uint4 *)(src + (size_t)r * sc.xs_pitch + ch * 16);
+    uint32_t *t = (uint32_t *)&tile[r * kScaleLdsPitch + ch * 16];
+    t[0] = v.x; t[1] = v.y; t[2] = v.z; t[3] = v.w;
+  }
+  __syncthreads();
+  uint8_t *xs = (uint8_t *)sc.xs;
+  for (int q = threadIdx.x; q < nbt * 32; q += blockDim.x) {
+    const int bl = q >> 5, w = q & 31, b = b0 + bl;
+    uint32_t word = 0;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int p = 4 * w + t, r = (p & 7) * 16 + (p >> 3);
+      word |= (uint32_t)tile[r * kScaleLdsPitch + bl] << (8 * t);
+    }
+    *(uint32_t *)(xs + mx_row_scale_offset(g * 128, b, sc.s_ld) + 4 * w) = word;
   }
 }
 
@@ -782,9 +819,13 @@ hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows,
   // grouped rows: at most every pair plus one partial tile per expert
   const long long bound = ((long long)(expected_pairs + align - 1) / align + E) * align;
   const int n_pad = (int)std::min<long long>(bound, max_mpad);
-  if (wk == kWMx || wk == kWFp8)
+  if (wk == kWMx || wk == kWFp8) {
     hipLaunchKernelGGL(k_pack_tokens, dim3((n_rows + 3) / 4), dim3(256), 0, s, a, sc, row0, n_rows,
                        k, d);
+    const int nb = d / kMxBlock;
+    hipLaunchKernelGGL(k_scale_layout, dim3((n_pad + 127) / 128, (nb + kScaleCols - 1) / kScaleCols),
+                       dim3(256), 0, s, sc, nb);
+  }
   else if (x_dtype == 0)
     hipLaunchKernelGGL(k_pack_rows, dim3((n_pad + kPackRows - 1) / kPackRows), dim3(256), 0, s, a,
                        sc, row0, k, E, d, n_pad);

@@ -499,10 +499,12 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
     if (!(c->wk == kWBf16 && cfg->x_dtype == CEP_BF16)) sc.xg = A(xes * c->max_mpad * d);
     sc.h = A(xes * c->max_mpad * I);
     sc.y = A((c->wk == kWBf16 ? 4 : 2) * (size_t)c->max_mpad * d);
-    if (c->wk != kWBf16) {  // e4m3 float scales per 128, or E8M0 bytes per 32: same size
+    if (c->wk != kWBf16) {  // E8M0 bytes per 32 channels
       sc.xs = (float *)A(sizeof(float) * c->max_mpad * (d / 128));
       sc.hs = (float *)A(sizeof(float) * c->max_mpad * (I / 128));
       sc.s_ld = c->max_mpad;
+      sc.xs_pitch = (int)align_up((size_t)d / 32, 16);
+      sc.xs_rows = (uint8_t *)A((size_t)c->max_mpad * sc.xs_pitch);
     }
   }
   if (e != hipSuccess) {
@@ -1070,6 +1072,8 @@ CEP_API int cep_ffn_noalloc(cep_ctx *c, int replica, int n_rows, int n_pairs,
       sc.xs = (float *)cv.take(sizeof(float) * (size_t)mpad * (d / 128));
       sc.hs = (float *)cv.take(sizeof(float) * (size_t)mpad * (I / 128));
       sc.s_ld = mpad;
+      sc.xs_pitch = (int)align_up((size_t)d / 32, 16);
+      sc.xs_rows = (uint8_t *)cv.take((size_t)mpad * sc.xs_pitch);
     }
     if (pass == 0) continue;
 
