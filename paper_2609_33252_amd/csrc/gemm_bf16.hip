@@ -43,39 +43,6 @@ __device__ inline void static_for(F &&f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-// Work item it of this workgroup, balanced over the XCDs as balanced_tile:
-// the live work W = n_live x N tiles is cut into 8 contiguous shares, one per
-// XCD.  A persistent grid (one workgroup per CU, gridDim.x a multiple of 8)
-// takes items j, j + gridDim.x/8, ... of its XCD's share; otherwise a
-// workgroup takes item blockIdx.x/8 only.
-template <int GM, bool PERSIST>
-__device__ inline bool work_item(int it, int n_live, int n_tiles_n, int *mt, int *nt) {
-  if (!PERSIST && it > 0) return false;
-  const int W = n_live * n_tiles_n;
-  const int C = (W + 7) / 8;
-  const int x = blockIdx.x & 7, j = (blockIdx.x >> 3) + it * (int)(gridDim.x >> 3);
-  const int L = x * C + j;
-  if (j >= C || L >= W) return false;
-  tile_of<GM>(L, n_live, n_tiles_n, mt, nt);
-  return true;
-}
-
-// s_waitcnt lgkmcnt(0) alone (vmcnt and expcnt at their "do not wait" maxima)
-
-// One workgroup per CU of the current device, a multiple of 8 (the XCDs).
-inline int persistent_grid() {
-  static int cached[64] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (!cached[dev]) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 8)
-      n = 256;
-    cached[dev] = n / 8 * 8;
-  }
-  return cached[dev];
-}
-
 // BM x BN output tile, NW waves as WGM x (NW/WGM), each wave owning a
 // (BM/WGM) x (BN/(NW/WGM)) block of 32x32 MFMA fragments (for SwiGLU a
 // wave's columns hold whole gate/up pairs of 32).  K advances in steps of BK through a ring of STAGES

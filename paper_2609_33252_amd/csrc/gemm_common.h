@@ -78,6 +78,37 @@ __device__ inline bool balanced_tile(int n_live, int n_tiles_n, int *mt, int *nt
   return true;
 }
 
+// Work item it of this workgroup, balanced over the XCDs as balanced_tile:
+// the live work W = n_live x N tiles is cut into 8 contiguous shares, one per
+// XCD.  A persistent grid (one workgroup per CU, gridDim.x a multiple of 8)
+// takes items j, j + gridDim.x/8, ... of its XCD's share; otherwise a
+// workgroup takes item blockIdx.x/8 only.
+template <int GM, bool PERSIST>
+__device__ inline bool work_item(int it, int n_live, int n_tiles_n, int *mt, int *nt) {
+  if (!PERSIST && it > 0) return false;
+  const int W = n_live * n_tiles_n;
+  const int C = (W + 7) / 8;
+  const int x = blockIdx.x & 7, j = (blockIdx.x >> 3) + it * (int)(gridDim.x >> 3);
+  const int L = x * C + j;
+  if (j >= C || L >= W) return false;
+  tile_of<GM>(L, n_live, n_tiles_n, mt, nt);
+  return true;
+}
+
+// One workgroup per CU of the current device, a multiple of 8 (the XCDs).
+inline int persistent_grid() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cached[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 8)
+      n = 256;
+    cached[dev] = n / 8 * 8;
+  }
+  return cached[dev];
+}
+
 // Grid for balanced_tile: at least the bound's work, a multiple of 8.
 inline int balanced_grid(int grid_tiles, int gm, int n_tiles_n) {
   return ((grid_tiles + gm - 1) / gm * gm * n_tiles_n + 7) / 8 * 8;
@@ -196,38 +227,43 @@ __device__ inline void store_y_bf16(const f32x4 (&acc)[8][4], const float (&wrow
 }
 
 // GEMM2 through LDS: the waves write their coefficient-scaled bf16 outputs
-// into the idle operand ring (512 bytes a row, 16-byte chunk c of row r at
-// slot c ^ (r & 15), so that the sixteen rows of one write instruction hit
-// distinct banks), then the workgroup stores whole rows with 16-byte stores:
-// one store instruction covers two full rows, where the accumulator layout
-// gives 64 pieces of 8 bytes.  The rows of wave row 0 go to st0, those of
-// wave row 1 to st1 (each 64 KB), or with st1 null both through st0 in turn.
-template <int NW>
+// into idle operand-ring buffers (512 bytes a row, 16-byte chunk c of row r
+// at slot c ^ (r & 15), so that the sixteen rows of one write instruction
+// hit distinct banks), then the workgroup stores whole rows with 16-byte
+// stores: one store instruction covers two full rows, where the accumulator
+// layout gives 64 pieces of 8 bytes.  One pass per wave row of 128 rows,
+// staged as rows 0-63 in lo and 64-127 in hi (32 KB each).  The barriers
+// wait for LDS operations only: loads and stores in flight (the previous
+// pass's stores, a persistent workgroup's prefetch of its next tile) are not
+// waited for.  FULL stores the padding rows of the tile too (never read), so
+// that every wave issues the same number of stores.  PRESCALED: acc already
+// holds the coefficient-scaled outputs (wrow unused).
+template <int NW, bool FULL = false, bool PRESCALED = false>
 __device__ inline void store_y_bf16_staged(const f32x4 (&acc)[8][4], const float (&wrow)[8],
                                            const GemmArgs &g, const Tile &t, int nt, int wm,
-                                           int wn, int lane, int tid, u32x4 *st0, u32x4 *st1) {
+                                           int wn, int lane, int tid, u32x4 *lo, u32x4 *hi) {
   const int r16 = lane & 15, grp = lane >> 4;
-  constexpr int WR = NW / 4;  // wave rows of 128 tile rows
-  const int passes = st1 ? 1 : WR;
   __bf16 *Y = (__bf16 *)g.out + (size_t)t.row0 * g.N + (size_t)nt * 256;
-  for (int pass = 0; pass < passes; ++pass) {
-    // the ring (or the previous pass's rows) is no longer read; the previous
-    // pass's global stores may still be in flight
+#pragma unroll
+  for (int pass = 0; pass < NW / 4; ++pass) {
+    // no wave still reads the buffers (ring or the previous pass's rows)
     wait_lgkm0();
     __builtin_amdgcn_s_barrier();
-    if (passes == 1 || wm == pass) {
-      u32x4 *st = wm == 0 || !st1 ? st0 : st1;
+    if (wm == pass) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const int r = i * 16 + r16;  // row within the wave row
+        u32x4 *st = i < 4 ? lo : hi;
+        const int r = (i & 3) * 16 + r16;  // row within the 64-row piece
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           uint32_t v[2];
 #pragma unroll
-          for (int h = 0; h < 2; ++h)
-            v[h] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[i][j][2 * h] * wrow[i])) |
-                   ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[i][j][2 * h + 1] * wrow[i]))
-                    << 16);
+          for (int h = 0; h < 2; ++h) {
+            const float y0 = PRESCALED ? acc[i][j][2 * h] : acc[i][j][2 * h] * wrow[i];
+            const float y1 = PRESCALED ? acc[i][j][2 * h + 1] : acc[i][j][2 * h + 1] * wrow[i];
+            v[h] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)y0) |
+                   ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)y1) << 16);
+          }
           const int c = wn * 8 + j * 2 + (grp >> 1);  // 16-byte chunk of the row
           uint2 *dst = (uint2 *)&st[r * 32 + (c ^ r16)] + (grp & 1);
           *dst = make_uint2(v[0], v[1]);
@@ -236,14 +272,13 @@ __device__ inline void store_y_bf16_staged(const f32x4 (&acc)[8][4], const float
     }
     wait_lgkm0();
     __builtin_amdgcn_s_barrier();
-    const int rlo = passes == 1 ? 0 : pass * 128, nrows = passes == 1 ? 128 * WR : 128;
 #pragma unroll 4
-    for (int q = tid; q < nrows * 32; q += 64 * NW) {
-      const int row = rlo + (q >> 5), c = q & 31;
-      if (row >= t.rows) break;  // q grows with the row
-      const u32x4 *src = row < 128 || !st1 ? st0 : st1;
-      const int lr = row & 127;
-      *(u32x4 *)(Y + (size_t)row * g.N + c * 8) = src[lr * 32 + (c ^ (lr & 15))];
+    for (int q = tid; q < 128 * 32; q += 64 * NW) {
+      const int lr = q >> 5, c = q & 31, row = pass * 128 + lr;
+      if (!FULL && row >= t.rows) break;  // q grows with the row
+      const u32x4 *src = lr < 64 ? lo : hi;
+      const int pr = lr & 63;
+      *(u32x4 *)(Y + (size_t)row * g.N + c * 8) = src[pr * 32 + (c ^ (pr & 15))];
     }
   }
 }
@@ -258,15 +293,17 @@ __device__ inline void store_y_bf16_staged(const f32x4 (&acc)[8][4], const float
 // The codes go through the idle operand ring (128 bytes a row, 16-byte chunk
 // c of row r at slot c ^ ((r >> 1) & 7): a write instruction's sixteen rows x
 // four dwords hit distinct banks), then the workgroup stores whole 128-byte
-// row segments with 16-byte stores.  st holds BM x 128 bytes.
-template <int NW>
+// row segments with 16-byte stores.  st holds BM x 128 bytes.  Barriers and
+// FULL as in store_y_bf16_staged.
+template <int NW, bool FULL = false>
 __device__ inline void store_h_mx_staged(const f32x4 (&acc)[8][4], const GemmArgs &g,
                                          const Tile &t, int nt, int wm, int wn, int lane,
                                          int tid, u32x4 *st) {
   uint8_t *Hs = (uint8_t *)g.out_s;
   const int I = g.N / 2, hblk = nt * 4 + wn;  // this wave's MX block of h columns
   const int r16 = lane & 15, grp = lane >> 4;
-  __syncthreads();  // every wave's last operand reads completed: the ring is idle
+  wait_lgkm0();  // every wave's last operand reads completed: the buffer is idle
+  __builtin_amdgcn_s_barrier();
   uint32_t *st32 = (uint32_t *)st;
   int codes[8];
 #pragma unroll
@@ -305,7 +342,7 @@ __device__ inline void store_h_mx_staged(const f32x4 (&acc)[8][4], const GemmArg
 #pragma unroll 2
   for (int q = tid; q < BM * 8; q += 64 * NW) {
     const int row = q >> 3, c = q & 7;
-    if (row >= t.rows) break;  // q grows with the row
+    if (!FULL && row >= t.rows) break;  // q grows with the row
     *(u32x4 *)(H + (size_t)row * I + c * 16) = st[row * 8 + (c ^ ((row >> 1) & 7))];
   }
   // the scales last (a store before the barrier would make it wait for

@@ -21,6 +21,8 @@
 // applies to K block g of its row or column.
 #include "gemm_common.h"
 
+#include <algorithm>
+
 namespace cep {
 namespace {
 
@@ -50,84 +52,112 @@ __device__ inline f32x4 f8_mfma(const i32x8 &w, const i32x8 &x, int ox, int sx) 
 // the BM x 4 row scales per stage).  The row-scale layout
 // (mx_row_scale_offset) gives each lane its eight row fragments' scales of
 // its K block as one 8-byte word.  The weight block scales of the tile's
-// columns go to LDS once.  An LDS row is 128 codes = eight 16-byte chunks;
-// chunk c of row r lives at slot c ^ ((r >> 1) & 7).  A lane reads chunks g
-// and g + 4 of its row (g = lane / 16): a 16-byte LDS read serves per cycle
-// the sixteen lanes of one half-wave whose quad index (lane bits 2-4) has
-// one parity, and those lanes then touch sixteen distinct slots of 256 bytes.
+// columns go to LDS once per tile.  An LDS row is 128 codes = eight 16-byte
+// chunks; chunk c of row r lives at slot c ^ ((r >> 1) & 7).  A lane reads
+// chunks g and g + 4 of its row (g = lane / 16): a 16-byte LDS read serves
+// per cycle the sixteen lanes of one half-wave whose quad index (lane bits
+// 2-4) has one parity, and those lanes then touch sixteen distinct slots of
+// 256 bytes.
 //
-// Epilogues: store_h_mx (GEMM1) and store_y_bf16 (GEMM2).
-template <int NW, int STAGES, bool SWIGLU, int OCC = 1>
+// PERSIST (8 waves, two stages): one workgroup per CU takes work items j,
+// j + grid/8, ... of its XCD's share.  After a tile's K loop it issues the
+// next tile's first stage into buffer 0 and loads the next tile's block
+// scales into registers, then runs the epilogue through buffer 1 (staged
+// stores of every row, so each wave issues a fixed number S of stores), so
+// that the next tile's first loads and its memory latency overlap the
+// epilogue; it then waits until at most those S stores are outstanding (the
+// loads issued before them have landed) and moves on.
+//
+// Epilogues: store_h_mx_staged (GEMM1) and store_y_bf16_staged (GEMM2).
+struct F8Tile {
+  Tile t;
+  int nt;
+  const char *Ag, *Bg, *Asg;
+  const float *bs;
+};
+
+template <int NW, int STAGES, bool SWIGLU, bool PERSIST, int OCC = 1>
 __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
   constexpr int BM = 128 * NW / 4, BN = 256, BK = 128, WN = BN / 4;
   constexpr int A_LD = BM * BK / 1024 / NW, B_LD = BN * BK / 1024 / NW;  // loads per wave
   constexpr int PER = A_LD + B_LD;  // per thread per step; wave 0 adds one (row scales)
   static_assert(BM * 4 <= 1024, "one load of the row scales");
+  static_assert(!PERSIST || (NW == 8 && STAGES == 2), "persistent: the 8-wave two-stage tile");
+  // uniform over the workgroup: kept in scalar registers
+  const int n_live = __builtin_amdgcn_readfirstlane(*g.n_tiles), ntn = g.N / BN;
   int mt, nt;
-  if (!balanced_tile<kGroupM>(*g.n_tiles, g.N / BN, &mt, &nt)) return;
-  const Tile t = g.tiles[mt];
+  if (!work_item<kGroupM, PERSIST>(0, n_live, ntn, &mt, &nt)) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wid >> 2, wn = wid & 3;
   const int K = g.K, nkb = K / BK;
-  const uint8_t *blob = blob_of(g.bt, t.expert);
-  const char *Ag = (const char *)(g.A + (size_t)t.row0 * K);
-  const char *Bg = (const char *)(blob + g.b_off + (size_t)nt * BN * K);
-  // row scales of K step kb: 512 bytes per 128-row group, groups contiguous
-  const char *Asg = (const char *)g.As + (size_t)(t.row0 >> 7) * 512;
-  const size_t as_step = (size_t)(g.s_ld >> 7) * 512;
-  const float *Bs = (const float *)(blob + g.bs_off);
+  const size_t as_step = (size_t)(g.s_ld >> 7) * 512;  // row scales: 512 bytes per 128-row group
+  // weight block scales of a tile's columns: 8 consecutive rows of
+  // [N/32][nkb] for GEMM1, 2 of [N/128][nkb] for GEMM2
+  const int nbs = (SWIGLU ? BN / kInterleave : BN / 128) * nkb;
 
   __shared__ u32x4 sA[STAGES][BM * 8];
   __shared__ u32x4 sB[STAGES][BN * 8];
   __shared__ u32x4 sAs[STAGES][BM / 4];
   __shared__ float sBs[8 * (kMaxDim / BK)];
+  // PERSIST GEMM2: the tile's routing coefficients, brought with its first
+  // stage (they are only needed after the K loop)
+  __shared__ float sW[PERSIST && !SWIGLU ? BM : 1];
 
+  auto tile_at = [&](int mt_, int nt_) {
+    F8Tile f;
+    mt_ = __builtin_amdgcn_readfirstlane(mt_);
+    nt_ = __builtin_amdgcn_readfirstlane(nt_);
+    f.t = g.tiles[mt_];
+    f.nt = nt_;
+    const uint8_t *blob = blob_of(g.bt, f.t.expert);
+    f.Ag = (const char *)(g.A + (size_t)f.t.row0 * K);
+    f.Bg = (const char *)(blob + g.b_off + (size_t)nt_ * BN * K);
+    f.Asg = (const char *)g.As + (size_t)(f.t.row0 >> 7) * 512;
+    f.bs = (const float *)(blob + g.bs_off) + (size_t)nt_ * nbs;
+    return f;
+  };
   // lane l of a load fills slot l of a 1 KB segment (8 rows x 8 chunks)
   const int seg_row = lane >> 3;
-#define CEP_F8_OFF(seg)                                                            \
-  ((uint32_t)((seg) * 8 + seg_row) * K +                                           \
-   (uint32_t)(((lane & 7) ^ ((((seg) * 8 + seg_row) >> 1) & 7)) * 16))
-#define CEP_F8_STAGE(kb)                                                           \
-  {                                                                                \
-    const int buf_ = (kb) % STAGES;                                                \
-    _Pragma("unroll") for (int i = 0; i < A_LD; ++i) {                             \
-      const int seg = wid * A_LD + i;                                              \
-      dma16(Ag + (size_t)(kb) * BK + CEP_F8_OFF(seg),                              \
-            __builtin_amdgcn_readfirstlane(lds_offset(&sA[buf_][seg * 64])));      \
-    }                                                                              \
-    _Pragma("unroll") for (int i = 0; i < B_LD; ++i) {                             \
-      const int seg = wid * B_LD + i;                                              \
-      dma16(Bg + (size_t)(kb) * BK + CEP_F8_OFF(seg),                              \
-            __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf_][seg * 64])));      \
-    }                                                                              \
-    if (wid == 0 && lane < BM / 4)                                                 \
-      dma16(Asg + (size_t)(kb) * as_step + lane * 16,                              \
-            __builtin_amdgcn_readfirstlane(lds_offset(&sAs[buf_][0])));            \
-  }
-
-  f32x4 acc[8][4];
+  auto lane_off = [&](int seg) {
+    const int r = seg * 8 + seg_row;
+    return (uint32_t)r * K + (uint32_t)(((lane & 7) ^ ((r >> 1) & 7)) * 16);
+  };
+  auto stage = [&](const F8Tile &f, int kb, int buf) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < A_LD; ++i) {
+      const int seg = wid * A_LD + i;
+      dma16(f.Ag + (size_t)kb * BK + lane_off(seg),
+            __builtin_amdgcn_readfirstlane(lds_offset(&sA[buf][seg * 64])));
+    }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{};
+    for (int i = 0; i < B_LD; ++i) {
+      const int seg = wid * B_LD + i;
+      dma16(f.Bg + (size_t)kb * BK + lane_off(seg),
+            __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf][seg * 64])));
+    }
+    if (wid == 0 && lane < BM / 4)
+      dma16(f.Asg + (size_t)kb * as_step + lane * 16,
+            __builtin_amdgcn_readfirstlane(lds_offset(&sAs[buf][0])));
+  };
+  // the coefficients of the tile's BM rows: one 1 KB load by wave 1 (the
+  // rows of a tile lie inside the layout's padded rows)
+  auto stage_coef = [&](const F8Tile &f) {
+    if constexpr (PERSIST && !SWIGLU) {
+      static_assert(BM * 4 == 1024, "one 1 KB load");
+      if (wid == 1)
+        dma16(g.wrow + f.t.row0 + lane * 4, __builtin_amdgcn_readfirstlane(lds_offset(&sW[0])));
+    }
+  };
 
+  F8Tile cur = tile_at(mt, nt);
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s)
-    if (s < nkb) CEP_F8_STAGE(s);
-
-  // The weight block scales of the tile's columns (8 consecutive rows of
-  // [N/32][nkb] for GEMM1, 2 of [N/128][nkb] for GEMM2) go to LDS once, so
-  // the main loop issues no vector loads besides the ring's.
-  {
-    const int nbs = (SWIGLU ? BN / kInterleave : BN / 128) * nkb;
-    const float *src = Bs + (size_t)nt * nbs;
-    for (int i = tid; i < nbs; i += 64 * NW) sBs[i] = src[i];
-  }
+    if (s < nkb) stage(cur, s, s % STAGES);
+  stage_coef(cur);
+  for (int i = tid; i < nbs; i += 64 * NW) sBs[i] = cur.bs[i];
   __syncthreads();
 
-  float wr[8];
-  if (!SWIGLU) load_row_coef(g, t, wm, lane, wr);
   const int r16 = lane & 15, grp = lane >> 4;
   const int rsw = (r16 >> 1) & 7;  // swizzle of every operand row this lane reads
   // scale rows of this wave's column blocks: GEMM1 fragments j = 0,1 (gate)
@@ -140,64 +170,141 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
     const u32x4 hi = s[row * 8 + ((grp + 4) ^ rsw)];
     return __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
   };
-  for (int kb = 0; kb < nkb; ++kb) {
-    // this wave's loads of step kb are done when at most the loads of the
-    // steps issued after it are outstanding
-    const int later = min(nkb - 1, kb + STAGES - 2) - kb;
-    if (wid == 0)
-      wait_stages<PER + 1, STAGES - 2>(later);
-    else
-      wait_stages<PER, STAGES - 2>(later);
-    // every wave's loads of step kb landed; step kb-1 fully consumed
-    __builtin_amdgcn_s_barrier();
-    if (kb + STAGES - 1 < nkb) CEP_F8_STAGE(kb + STAGES - 1);
-    const int cur = kb % STAGES;
-    const float sb0 = sb_row0[kb], sb1 = sb_row1[kb];
-    const uint2 sa = ((const uint2 *)&sAs[cur][0])[wm * 64 + grp * 16 + r16];
+  // stores each wave issues in a PERSIST epilogue (FULL staging, 512
+  // threads): GEMM1 256 x 128 code bytes in 16-byte pieces (4) and one
+  // scale word; GEMM2 two passes of 128 x 512 bytes (8 each)
+  constexpr int S_EPI = SWIGLU ? 4 : 16;
+  // block scales per thread (at most 8 or 2 rows of kMaxDim/BK per tile)
+  constexpr int NBSV = PERSIST ? (SWIGLU ? 8 : 2) * (kMaxDim / BK) / (64 * NW) : 1;
 
-    i32x8 b[4];
+  for (int it = 0;; ++it) {
+    float wr[8];
+    if (!SWIGLU && !PERSIST) load_row_coef(g, cur.t, wm, lane, wr);
+    f32x4 acc[8][4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) b[j] = read_op(sB[cur], wn * WN + j * 16 + r16);
-    // A fragments one row group ahead: the reads of group i+1 are issued
-    // before the MFMAs of group i, so LDS latency hides behind them
-    i32x8 a_next = read_op(sA[cur], wm * 128 + r16);
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const i32x8 a = a_next;
-      if (i + 1 < 8) a_next = read_op(sA[cur], wm * 128 + (i + 1) * 16 + r16);
-      const int sai = (int)(i < 4 ? sa.x : sa.y);
-      f32x4 p[4];
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{};
+
+    for (int kb = 0; kb < nkb; ++kb) {
+      // this wave's loads of step kb are done when at most the loads of the
+      // steps issued after it are outstanding (a PERSIST tile's first stage
+      // was waited for before its block scales went to LDS)
+      const int later = min(nkb - 1, kb + STAGES - 2) - kb;
+      if (!PERSIST || kb > 0) {
+        if (wid == 0)
+          wait_stages<PER + 1, STAGES - 2>(later);
+        else
+          wait_stages<PER, STAGES - 2>(later);
+      }
+      // every wave's loads of step kb landed; step kb-1 fully consumed
+      __builtin_amdgcn_s_barrier();
+      if (kb + STAGES - 1 < nkb) stage(cur, kb + STAGES - 1, (kb + STAGES - 1) % STAGES);
+      const int buf = kb % STAGES;
+      const float sb0 = sb_row0[kb], sb1 = sb_row1[kb];
+      const uint2 sa = ((const uint2 *)&sAs[buf][0])[wm * 64 + grp * 16 + r16];
+
+      i32x8 b[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) p[j] = f8_mfma(b[j], a, i & 3, sai);
+      for (int j = 0; j < 4; ++j) b[j] = read_op(sB[buf], wn * WN + j * 16 + r16);
+      // A fragments one row group ahead: the reads of group i+1 are issued
+      // before the MFMAs of group i, so LDS latency hides behind them
+      i32x8 a_next = read_op(sA[buf], wm * 128 + r16);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] += p[j] * (j < 2 ? sb0 : sb1);
+      for (int i = 0; i < 8; ++i) {
+        const i32x8 a = a_next;
+        if (i + 1 < 8) a_next = read_op(sA[buf], wm * 128 + (i + 1) * 16 + r16);
+        const int sai = (int)(i < 4 ? sa.x : sa.y);
+        f32x4 p[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) p[j] = f8_mfma(b[j], a, i & 3, sai);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] += p[j] * (j < 2 ? sb0 : sb1);
+      }
+    }
+
+    if constexpr (!PERSIST) {
+      // staging: BM x 128 code bytes; y rows of 512 bytes, 64 per 32 KB piece
+      static_assert(sizeof(sA) >= BM * 128, "the h tile fits the A ring");
+      static_assert(sizeof(sB[0]) >= 64 * 512 && (NW == 4 || sizeof(sA[0]) >= 64 * 512),
+                    "y rows fit the ring");
+      if constexpr (SWIGLU)
+        store_h_mx_staged<NW>(acc, g, cur.t, cur.nt, wm, wn, lane, tid, &sA[0][0]);
+      else if constexpr (NW == 8)
+        store_y_bf16_staged<NW>(acc, wr, g, cur.t, cur.nt, wm, wn, lane, tid, &sA[0][0],
+                                &sA[1][0]);
+      else
+        store_y_bf16_staged<NW>(acc, wr, g, cur.t, cur.nt, wm, wn, lane, tid, &sB[0][0],
+                                &sB[1][0]);
+      return;
+    } else {
+      // GEMM2's coefficients (in LDS since the tile's first step) go into
+      // the accumulators before the next tile's coefficients overwrite them
+      if constexpr (!SWIGLU) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const float w = sW[wm * 128 + i * 16 + r16];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[i][j] *= w;
+        }
+      }
+      int mt2, nt2;
+      const bool more = work_item<kGroupM, true>(it + 1, n_live, ntn, &mt2, &nt2);
+      F8Tile nxt;
+      float sbv[NBSV];
+      if (more) {
+        // every wave's operand reads of the last step completed (it may
+        // have used buffer 0): the next tile's first stage may fill it
+        wait_lgkm0();
+        __builtin_amdgcn_s_barrier();
+        nxt = tile_at(mt2, nt2);
+        stage(nxt, 0, 0);
+        stage_coef(nxt);
+#pragma unroll
+        for (int v = 0; v < NBSV; ++v) {
+          const int i = tid + v * 64 * NW;
+          sbv[v] = i < nbs ? nxt.bs[i] : 0.0f;
+        }
+      }
+      // epilogue through buffer 1 (sA[1], sB[1]: 32 KB each)
+      static_assert(sizeof(sA[1]) >= BM * 128 && sizeof(sA[1]) >= 64 * 512 &&
+                        sizeof(sB[1]) >= 64 * 512, "staging fits buffer 1");
+      if constexpr (SWIGLU)
+        store_h_mx_staged<NW, true>(acc, g, cur.t, cur.nt, wm, wn, lane, tid, &sA[1][0]);
+      else
+        store_y_bf16_staged<NW, true, true>(acc, wr, g, cur.t, cur.nt, wm, wn, lane, tid,
+                                            &sA[1][0], &sB[1][0]);
+      if (!more) return;
+      // the next tile's first stage and block scales landed once at most the
+      // epilogue's stores are outstanding
+      wait_vmcnt<S_EPI>();
+#pragma unroll
+      for (int v = 0; v < NBSV; ++v) {
+        const int i = tid + v * 64 * NW;
+        if (i < nbs) sBs[i] = sbv[v];
+      }
+      wait_lgkm0();  // the block scales are in LDS before the K loop's barrier
+      cur = nxt;
     }
   }
-#undef CEP_F8_STAGE
-#undef CEP_F8_OFF
-
-  // staging: BM x 128 code bytes; y rows of 512 bytes, 128 per wave row
-  static_assert(sizeof(sA) >= BM * 128, "the h tile fits the A ring");
-  static_assert(NW == 8 ? sizeof(sA) >= 128 * 512 && sizeof(sB) >= 128 * 512
-                        : sizeof(sB) >= 128 * 512, "y rows fit the rings");
-  if constexpr (SWIGLU)
-    store_h_mx_staged<NW>(acc, g, t, nt, wm, wn, lane, tid, &sA[0][0]);
-  else if constexpr (NW == 8)
-    store_y_bf16_staged<NW>(acc, wr, g, t, nt, wm, wn, lane, tid, &sA[0][0], &sB[0][0]);
-  else
-    store_y_bf16_staged<NW>(acc, wr, g, t, nt, wm, wn, lane, tid, &sB[0][0], nullptr);
 }
 
 }  // namespace
+
+// persistent 8-wave tiles for GEMM2 ([0]) and GEMM1 ([1])
+constexpr bool kFp8Persist[2] = {true, true};
 
 template <bool SWIGLU>
 hipError_t launch_fp8(const GemmArgs &g, int grid_tiles, int align, hipStream_t s) {
   if (g.N % 256 || g.K % 128 || g.K > kMaxDim || g.s_ld % 256) return hipErrorInvalidValue;
   const int grid = balanced_grid(grid_tiles, kGroupM, g.N / 256);
   if (align == kFp8TileM)
-    hipLaunchKernelGGL((k_gemm_fp8<4, 3, SWIGLU>), dim3(grid), dim3(256), 0, s, g);
+    hipLaunchKernelGGL((k_gemm_fp8<4, 3, SWIGLU, false>), dim3(grid), dim3(256), 0, s, g);
+  else if (align == kFp8LargeTileM && kFp8Persist[SWIGLU])
+    hipLaunchKernelGGL((k_gemm_fp8<8, 2, SWIGLU, true>), dim3(std::min(grid, persistent_grid())),
+                       dim3(512), 0, s, g);
   else if (align == kFp8LargeTileM)
-    hipLaunchKernelGGL((k_gemm_fp8<8, 2, SWIGLU>), dim3(grid), dim3(512), 0, s, g);
+    hipLaunchKernelGGL((k_gemm_fp8<8, 2, SWIGLU, false>), dim3(grid), dim3(512), 0, s, g);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

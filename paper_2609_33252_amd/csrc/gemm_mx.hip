@@ -168,12 +168,12 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_mx(GemmArgs g) {
   }
 #undef CEP_MX_STAGE
 
-  // staging: BM x 128 code bytes, or 128 rows x 512 bytes of y per pass
+  // staging: BM x 128 code bytes, or y rows of 512 bytes, 64 per A stage
   static_assert(sizeof(sA) >= BM * 128, "the h tile fits the A ring");
   if constexpr (SWIGLU) {
     store_h_mx_staged<NW>(acc, g, t, nt, wm, wn, lane, tid, &sA[0][0]);
-  } else if constexpr (sizeof(sA) >= 128 * 512) {
-    store_y_bf16_staged<NW>(acc, wr, g, t, nt, wm, wn, lane, tid, &sA[0][0], nullptr);
+  } else if constexpr (sizeof(sA[0]) >= 64 * 512) {
+    store_y_bf16_staged<NW>(acc, wr, g, t, nt, wm, wn, lane, tid, &sA[0][0], &sA[1][0]);
   } else {
     store_y_bf16(acc, wr, g, t, nt, wm, wn, lane);
   }
