@@ -62,10 +62,10 @@ GEMM_SOURCES = {
     "mxfp4": ["paper_2609_33252_amd/csrc/gemm_mx.hip", "paper_2609_33252_amd/csrc/gemm_common.h"],
 }
 TRAFFIC_BYTES = {  # workload -> (GEMM family, sha1 prefix of its sources, bytes per launch)
-    "fp8_fetch_d6144": ("fp8", "7dc7cabc759f", 2175150482),
-    "sync_d4096": ("bf16", "1009e8ba0d48", 504210999),
-    "zipf_imbalanced_d7168/per_chunk": ("bf16", "1009e8ba0d48", 473461898),
-    "mxfp4_dsv4flash_d4096": ("mxfp4", "a5632d261183", 1369028571),
+    "fp8_fetch_d6144": ("fp8", "8cd1162a8696", 2204963054),
+    "sync_d4096": ("bf16", "be1536a05110", 504211803),
+    "zipf_imbalanced_d7168/per_chunk": ("bf16", "be1536a05110", 473388711),
+    "mxfp4_dsv4flash_d4096": ("mxfp4", "31b1a1017063", 1368926427),
 }
 
 
