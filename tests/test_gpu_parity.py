@@ -452,6 +452,34 @@ def test_all_remote_chunk_launches_nothing():
     run.close()
 
 
+def test_fp8_persistent_tiles_odd_k_steps_all_rows():
+    # The persistent 8-wave e4m3 tiles over more tiles than workgroups (each
+    # workgroup runs several, prefetching the next one's first stage during
+    # the epilogue) with an odd number of K steps in GEMM2 (I = 640: five),
+    # so that a tile's last step uses ring buffer 0, the buffer the next
+    # tile's first stage fills: every row against the oracle, and bitwise
+    # equal to per-chunk batches on the 4-wave 128-row tile.
+    wl = W.generate("fp8_fetch_d6144", 11, d=1024, I=640, E=4, Eg=16, R=4, T=4096, cpr=64)
+    E, k = wl.cfg["E"], wl.cfg["k"]
+    run = harness.Runner(wl, n_streams=1, record_routing=True, use_fetch=False)
+    run.run(policy=cep.CEP_WAIT_ALL)
+    a = _out(run)
+    m = cep.cep_get_batch_routing(run.ctx, 0, E, k)
+    assert m["align"] == 256
+    m_tiles = int(sum((c + 255) // 256 for c in m["cnt"]))
+    assert m_tiles * (wl.cfg["d"] // 256) > 256, m["cnt"]  # GEMM2 tiles > workgroups
+    mx, rel = U.check(wl, a)
+    run.out.zero_()
+    run.run(policy=cep.CEP_PER_CHUNK)
+    b = _out(run)
+    aligns = {cep.cep_get_batch_routing(run.ctx, i, E, k)["align"]
+              for i in range(cep.cep_get_batch_count(run.ctx))}
+    run.close()
+    assert aligns == {128}
+    assert np.array_equal(a, b)
+    print(f"fp8 persistent tiles, odd K steps: pairs={wl.n_pairs} max_abs={mx:.3e} rel={rel:.3e}")
+
+
 def test_fp8_large_tile_all_rows_and_small_tile_bitwise():
     # The e4m3 8-wave 256-row tile (the large-batch tile of the e4m3
     # workload) over every row against the oracle: four experts of 1757 to
