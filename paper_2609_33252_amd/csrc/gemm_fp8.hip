@@ -156,6 +156,11 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
     if (s < nkb) stage(cur, s, s % STAGES);
   stage_coef(cur);
   for (int i = tid; i < nbs; i += 64 * NW) sBs[i] = cur.bs[i];
+  // a PERSIST tile's K loop starts without a wait: its first stage (and the
+  // coefficients) must have landed for every wave here.  The direct loads
+  // are invisible to the compiler, so __syncthreads() alone would not wait
+  // for them in the waves that load no block scale.
+  if constexpr (PERSIST) wait_vmcnt<0>();
   __syncthreads();
 
   const int r16 = lane & 15, grp = lane >> 4;
