@@ -19,7 +19,9 @@
  *      re-quantised to MXFP8)
  *   5. grouped down GEMM, scaled by the routing coefficient
  *   6. combine: each source token's local contributions summed in slot order
- *      and written to its (replica, token) row of the output
+ *      and written to its (replica, token) row of the output (e4m3 / MXFP4
+ *      weights: step 5 writes the row of a token with one local pair itself,
+ *      with the same value)
  *   (steps 1-6: Appendix C, "Grouped FFN invocations" and "Output return and
  *   combine").
  *
@@ -136,7 +138,11 @@ int cep_pack_experts(const cep_config *cfg, const cep_weights *w, int first, int
 
 /* Create a context: validates cfg, allocates every scratch buffer, the chunk
  * arena and the fetch buffer, creates the streams, and packs the weights of
- * resident experts into library-owned memory.  These are the expert weights
+ * resident experts into library-owned memory.  Each library stream has a
+ * hardware queue of its own (a CU-masked stream naming every CU), so a batch
+ * waiting for a late chunk holds back no other stream; like any stream
+ * created without hipStreamNonBlocking, these streams synchronise with the
+ * legacy default (NULL) stream.  These are the expert weights
  * every grouped invocation reads (Appendix C, "Grouped FFN invocations"),
  * and the preallocated temporary weight buffer of a helper (Appendix C,
  * "One-shot weight fetching": its capacity bounds the fetch byte budget).

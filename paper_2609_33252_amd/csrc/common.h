@@ -160,6 +160,8 @@ struct Arena {
   int32_t *ids;        // [cap][k] local expert id or -1
   float *w;            // [cap][k] routing coefficient
   int32_t *dst;        // [cap] output row (replica * T_max + token) or -1
+  int32_t *solo;       // [cap] the output row of a row with exactly one local
+                       // pair, else -1
   const void **xrow;   // [cap] pointer to the row's input
 };
 
@@ -176,6 +178,9 @@ struct Scratch {
   int32_t *pos_of;     // [max_rows * k] grouped row of each flat pair or -1
   int32_t *perm;       // [max_mpad] flat pair of each grouped row or -1
   float *wrow;         // [max_mpad] routing coefficient of each grouped row
+  int32_t *ydst;       // [max_mpad] output row of a grouped row that is its
+                       // token's only local pair (GEMM2 writes that token's
+                       // output row itself), else -1
   void *xg;            // [max_mpad][d] bf16 or e4m3
   float *xs;           // e4m3 and MXFP4 weights: the rows' E8M0 scales (MXFP8,
                        // one byte per 32 channels) at mx_row_scale_offset
@@ -234,9 +239,11 @@ hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows,
                         int align, int expected_pairs, int max_mpad, int max_tiles,
                         uint64_t fetched_mask, int x_dtype, int wk, int d, int split_cu,
                         int n_tiles_n, bool var, uint32_t *err, hipStream_t s);
-// y_f32: the grouped outputs are float32 (bf16 weights), else bf16
+// y_f32: the grouped outputs are float32 (bf16 weights), else bf16.
+// skip_solo: the batch's GEMM2 wrote the output rows of tokens with one
+// local pair (gemm2_writes_solo); the combine leaves them alone.
 hipError_t launch_combine(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int d,
-                          bool y_f32, float *out, hipStream_t s);
+                          bool y_f32, bool skip_solo, float *out, hipStream_t s);
 
 // grouped GEMMs over the tile lists of `which` (0 resident, 1 fetched) of a
 // scratch whose lists hold list_cap tiles each; the grid covers grid_tiles
@@ -249,8 +256,14 @@ hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_til
                         int split_tiles, int align, bool var, const BlobTable &bt,
                         const BlobLayout &L, int wk, int d, int I, const Arena *gather, int row0,
                         int k, hipStream_t s);
+// out (may be null): with gemm2_writes_solo(wk), a grouped row whose token
+// has no other local pair (Scratch::ydst) is written to that token's output
+// row [d] float32 as the combine would write it, instead of to y.
 hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles,
                         int split_tiles, int align, bool var, const BlobTable &bt,
-                        const BlobLayout &L, int wk, int d, int I, hipStream_t s);
+                        const BlobLayout &L, int wk, int d, int I, float *out, hipStream_t s);
+// GEMM2 of e4m3 and MXFP4 weights (bf16 grouped outputs, staged epilogues)
+// writes single-pair tokens' output rows itself.
+inline bool gemm2_writes_solo(int wk) { return wk != kWBf16; }
 
 }  // namespace cep

@@ -70,9 +70,13 @@ hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_til
 
 hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles,
                         int split_tiles, int align, bool var, const BlobTable &bt,
-                        const BlobLayout &L, int wk, int d, int I, hipStream_t s) {
+                        const BlobLayout &L, int wk, int d, int I, float *out, hipStream_t s) {
   if (grid_tiles <= 0) return hipSuccess;
   GemmArgs g = base_args(sc, 2 * which, list_cap, grid_tiles, bt);
+  if (out && gemm2_writes_solo(wk)) {
+    g.yout = out;
+    g.ydst = sc.ydst;
+  }
   g.A = (const uint8_t *)sc.h;
   g.As = sc.hs;
   g.K = I;

@@ -33,6 +33,11 @@ struct GemmArgs {
                           // with bf16 weights, bf16 with e4m3 / MXFP4 weights)
   float *out_s;           // quantised GEMM1: h scales (layout of As, K = N/2)
   const float *wrow;      // GEMM2: routing coefficient per grouped row
+  // GEMM2 (e4m3, MXFP4): ydst[r] >= 0 sends grouped row r to row ydst[r] of
+  // yout ([.][N] float32), the output row of its token's only local pair;
+  // null: every row goes to out
+  float *yout;
+  const int32_t *ydst;
   // bf16 GEMM1 with A == nullptr: grouped row r is the batch's input row
   // xrow[arow0 + perm[r] / k] (padding rows, perm -1, read row arow0)
   const void *const *xrow;
@@ -138,6 +143,21 @@ __device__ inline void dma16(const void *gptr, uint32_t lds_seg) {
       : "memory");
 }
 
+// dma16 from a wave-uniform base address (scalar registers) plus a per-lane
+// 32-bit byte offset: only the offset occupies a vector register.
+__device__ inline void dma16_s(const void *sbase, uint32_t voff, uint32_t lds_seg) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(voff), "s"(sbase), "s"(lds_seg)
+      : "memory");
+}
+
 __device__ inline uint32_t lds_offset(const void *p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
 }
@@ -149,6 +169,22 @@ template <int N>
 __device__ inline void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Waits until at most n (wave-uniform, LO <= n) vector-memory operations of
+// this wave are outstanding; n above HI waits for HI.  A binary search over
+// the immediate of s_waitcnt.
+template <int LO, int HI>
+__device__ inline void wait_vmcnt_upto(int n) {
+  if constexpr (LO >= HI) {
+    wait_vmcnt<HI>();
+  } else {
+    constexpr int MID = (LO + HI) / 2;
+    if (n <= MID)
+      wait_vmcnt_upto<LO, MID>(n);
+    else
+      wait_vmcnt_upto<MID + 1, HI>(n);
+  }
 }
 
 // Waits for this wave's LDS (and scalar-memory) operations only; a barrier
@@ -200,11 +236,37 @@ __device__ inline void load_row_coef(const GemmArgs &g, const Tile &t, int wm, i
   }
 }
 
+// GEMM2: the output rows of the lane's eight rows for a direct write
+// (GemmArgs::ydst), -1 for a grouped output row; loaded with the
+// coefficients.
+__device__ inline void load_row_dst(const GemmArgs &g, const Tile &t, int wm, int lane,
+                                    int (&yd)[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int rt = wm * 128 + i * 16 + (lane & 15);
+    yd[i] = g.ydst && rt < t.rows ? g.ydst[(size_t)t.row0 + rt] : -1;
+  }
+}
+
+// The bits of +0.0f + x for the float with bits x: -0 becomes +0.  A token's
+// only grouped output, written as its output row, gets the bits the combine's
+// float32 sum from +0 would give it.
+__device__ inline uint32_t plus_zero(uint32_t x) { return x == 0x80000000u ? 0u : x; }
+
+// Eight bf16 (a 16-byte piece of a y row) widened to float32, +0 for -0.
+__device__ inline void widen_bf16x8(const u32x4 &v, u32x4 &lo, u32x4 &hi) {
+  lo = u32x4{plus_zero(v.x << 16), plus_zero(v.x & 0xffff0000u), plus_zero(v.y << 16),
+             plus_zero(v.y & 0xffff0000u)};
+  hi = u32x4{plus_zero(v.z << 16), plus_zero(v.z & 0xffff0000u), plus_zero(v.w << 16),
+             plus_zero(v.w & 0xffff0000u)};
+}
+
 // GEMM2: y = coefficient * acc in bf16, four consecutive columns (8 bytes)
-// per lane and row.
+// per lane and row; a row with yd[i] >= 0 goes to that output row as float32
+// (16 bytes).
 __device__ inline void store_y_bf16(const f32x4 (&acc)[8][4], const float (&wrow)[8],
-                                    const GemmArgs &g, const Tile &t, int nt, int wm, int wn,
-                                    int lane) {
+                                    const int (&yd)[8], const GemmArgs &g, const Tile &t, int nt,
+                                    int wm, int wn, int lane) {
   __bf16 *Y = (__bf16 *)g.out;
   const int r16 = lane & 15, grp = lane >> 4;
 #pragma unroll
@@ -213,7 +275,9 @@ __device__ inline void store_y_bf16(const f32x4 (&acc)[8][4], const float (&wrow
     if (rt >= t.rows) continue;
     const size_t row = (size_t)t.row0 + rt;
     const float wr = wrow[i];
-    __bf16 *yrow = Y + row * g.N + nt * 256 + wn * 64 + 4 * grp;
+    const size_t col = (size_t)nt * 256 + wn * 64 + 4 * grp;
+    __bf16 *yrow = Y + row * g.N + col;
+    uint32_t *orow = yd[i] >= 0 ? (uint32_t *)g.yout + (size_t)yd[i] * g.N + col : nullptr;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       uint32_t v[2];
@@ -221,12 +285,33 @@ __device__ inline void store_y_bf16(const f32x4 (&acc)[8][4], const float (&wrow
       for (int r = 0; r < 2; ++r)
         v[r] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[i][j][2 * r] * wr)) |
                ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[i][j][2 * r + 1] * wr)) << 16);
-      *(uint2 *)(yrow + j * 16) = make_uint2(v[0], v[1]);
+      if (orow)
+        *(u32x4 *)(orow + j * 16) = u32x4{plus_zero(v[0] << 16), plus_zero(v[0] & 0xffff0000u),
+                                          plus_zero(v[1] << 16), plus_zero(v[1] & 0xffff0000u)};
+      else
+        *(uint2 *)(yrow + j * 16) = make_uint2(v[0], v[1]);
     }
   }
 }
 
-// GEMM2 through LDS: the waves write their coefficient-scaled bf16 outputs
+// GEMM2 outputs y = coefficient * acc of a wave's 8 x 4 fragments, rounded
+// to bf16: two consecutive columns per word.  Packed as soon as the
+// accumulators are final, they take half the registers.
+__device__ inline void pack_y_bf16(const f32x4 (&acc)[8][4], const float (&wrow)[8],
+                                   uint32_t (&yb)[8][4][2]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        yb[i][j][h] =
+            (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[i][j][2 * h] * wrow[i])) |
+            ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[i][j][2 * h + 1] * wrow[i]))
+             << 16);
+}
+
+// GEMM2 through LDS: the waves write their packed bf16 outputs (pack_y_bf16)
 // into idle operand-ring buffers (512 bytes a row, 16-byte chunk c of row r
 // at slot c ^ (r & 15), so that the sixteen rows of one write instruction
 // hit distinct banks), then the workgroup stores whole rows with 16-byte
@@ -236,13 +321,17 @@ __device__ inline void store_y_bf16(const f32x4 (&acc)[8][4], const float (&wrow
 // wait for LDS operations only: loads and stores in flight (the previous
 // pass's stores, a persistent workgroup's prefetch of its next tile) are not
 // waited for.  FULL stores the padding rows of the tile too (never read), so
-// that every wave issues the same number of stores.  PRESCALED: acc already
-// holds the coefficient-scaled outputs (wrow unused).
-template <int NW, bool FULL = false, bool PRESCALED = false>
-__device__ inline void store_y_bf16_staged(const f32x4 (&acc)[8][4], const float (&wrow)[8],
-                                           const GemmArgs &g, const Tile &t, int nt, int wm,
-                                           int wn, int lane, int tid, u32x4 *lo, u32x4 *hi) {
+// that every wave issues at least a fixed number of stores.  sD (LDS) holds
+// the tile rows' GemmArgs::ydst: a row with sD[row] >= 0 goes to that output
+// row as float32 (two 16-byte stores per piece), padding rows have -1.
+// Returns a lower bound of the store instructions the wave issued (FULL): a
+// piece's store instructions run only for lanes that take their branch.
+template <int NW, bool FULL = false>
+__device__ inline int store_y_bf16_staged(const uint32_t (&yb)[8][4][2], const GemmArgs &g,
+                                          const Tile &t, int nt, int wm, int wn, int lane,
+                                          int tid, u32x4 *lo, u32x4 *hi, const int *sD) {
   const int r16 = lane & 15, grp = lane >> 4;
+  int n_st = 0;
   __bf16 *Y = (__bf16 *)g.out + (size_t)t.row0 * g.N + (size_t)nt * 256;
 #pragma unroll
   for (int pass = 0; pass < NW / 4; ++pass) {
@@ -256,17 +345,9 @@ __device__ inline void store_y_bf16_staged(const f32x4 (&acc)[8][4], const float
         const int r = (i & 3) * 16 + r16;  // row within the 64-row piece
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          uint32_t v[2];
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const float y0 = PRESCALED ? acc[i][j][2 * h] : acc[i][j][2 * h] * wrow[i];
-            const float y1 = PRESCALED ? acc[i][j][2 * h + 1] : acc[i][j][2 * h + 1] * wrow[i];
-            v[h] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)y0) |
-                   ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)y1) << 16);
-          }
-          const int c = wn * 8 + j * 2 + (grp >> 1);  // 16-byte chunk of the row
+      const int c = wn * 8 + j * 2 + (grp >> 1);  // 16-byte chunk of the row
           uint2 *dst = (uint2 *)&st[r * 32 + (c ^ r16)] + (grp & 1);
-          *dst = make_uint2(v[0], v[1]);
+          *dst = make_uint2(yb[i][j][0], yb[i][j][1]);
         }
       }
     }
@@ -278,9 +359,21 @@ __device__ inline void store_y_bf16_staged(const f32x4 (&acc)[8][4], const float
       if (!FULL && row >= t.rows) break;  // q grows with the row
       const u32x4 *src = lr < 64 ? lo : hi;
       const int pr = lr & 63;
-      *(u32x4 *)(Y + (size_t)row * g.N + c * 8) = src[pr * 32 + (c ^ (pr & 15))];
+      const u32x4 v = src[pr * 32 + (c ^ (pr & 15))];
+      const int od = sD[row];
+      n_st += (__ballot(od >= 0) ? 2 : 0) + (__ballot(od < 0) ? 1 : 0);
+      if (od >= 0) {
+        u32x4 f0, f1;
+        widen_bf16x8(v, f0, f1);
+        u32x4 *o = (u32x4 *)(g.yout + (size_t)od * g.N + (size_t)nt * 256 + c * 8);
+        o[0] = f0;
+        o[1] = f1;
+      } else {
+        *(u32x4 *)(Y + (size_t)row * g.N + c * 8) = v;
+      }
     }
   }
+  return __builtin_amdgcn_readfirstlane(n_st);
 }
 
 // GEMM1: h = silu(gate) * up, quantised to MXFP8.  The wave's 64 columns are

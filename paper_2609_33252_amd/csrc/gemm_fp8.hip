@@ -103,6 +103,9 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
   // PERSIST GEMM2: the tile's routing coefficients, brought with its first
   // stage (they are only needed after the K loop)
   __shared__ float sW[PERSIST && !SWIGLU ? BM : 1];
+  // GEMM2: the tile rows' output rows for direct writes (GemmArgs::ydst);
+  // PERSIST: two buffers, the next tile's loads beside the current epilogue
+  __shared__ int sD[SWIGLU ? 1 : (PERSIST ? 2 : 1)][SWIGLU ? 1 : BM];
 
   auto tile_at = [&](int mt_, int nt_) {
     F8Tile f;
@@ -140,13 +143,21 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
       dma16(f.Asg + (size_t)kb * as_step + lane * 16,
             __builtin_amdgcn_readfirstlane(lds_offset(&sAs[buf][0])));
   };
-  // the coefficients of the tile's BM rows: one 1 KB load by wave 1 (the
-  // rows of a tile lie inside the layout's padded rows)
-  auto stage_coef = [&](const F8Tile &f) {
+  // the coefficients and output rows of the tile's BM rows: one 1 KB load
+  // each, by waves 1 and 2 (the rows of a tile lie inside the layout's
+  // padded rows)
+  auto stage_coef = [&](const F8Tile &f, int db) {
     if constexpr (PERSIST && !SWIGLU) {
       static_assert(BM * 4 == 1024, "one 1 KB load");
       if (wid == 1)
-        dma16(g.wrow + f.t.row0 + lane * 4, __builtin_amdgcn_readfirstlane(lds_offset(&sW[0])));
+        dma16_s(g.wrow + f.t.row0, lane * 16, __builtin_amdgcn_readfirstlane(lds_offset(&sW[0])));
+      if (g.ydst) {
+        if (wid == 2)
+          dma16_s(g.ydst + f.t.row0, lane * 16,
+                  __builtin_amdgcn_readfirstlane(lds_offset(&sD[db][0])));
+      } else if (tid < BM) {
+        sD[db][tid] = -1;
+      }
     }
   };
 
@@ -154,7 +165,8 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s)
     if (s < nkb) stage(cur, s, s % STAGES);
-  stage_coef(cur);
+  int db = 0;  // PERSIST GEMM2: sD buffer of the current tile
+  stage_coef(cur, db);
   for (int i = tid; i < nbs; i += 64 * NW) sBs[i] = cur.bs[i];
   // a PERSIST tile's K loop starts without a wait: its first stage (and the
   // coefficients) must have landed for every wave here.  The direct loads
@@ -175,16 +187,21 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
     const u32x4 hi = s[row * 8 + ((grp + 4) ^ rsw)];
     return __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
   };
-  // stores each wave issues in a PERSIST epilogue (FULL staging, 512
-  // threads): GEMM1 256 x 128 code bytes in 16-byte pieces (4) and one
-  // scale word; GEMM2 two passes of 128 x 512 bytes (8 each)
+  // stores each wave issues at least in a PERSIST epilogue (FULL staging,
+  // 512 threads): GEMM1 256 x 128 code bytes in 16-byte pieces (4) and one
+  // scale word; GEMM2 two passes of 128 x 512 bytes (8 each; the staging
+  // counts its direct float32 rows' extra stores)
   constexpr int S_EPI = SWIGLU ? 4 : 16;
   // block scales per thread (at most 8 or 2 rows of kMaxDim/BK per tile)
   constexpr int NBSV = PERSIST ? (SWIGLU ? 8 : 2) * (kMaxDim / BK) / (64 * NW) : 1;
 
   for (int it = 0;; ++it) {
     float wr[8];
-    if (!SWIGLU && !PERSIST) load_row_coef(g, cur.t, wm, lane, wr);
+    int ydv = -1;  // non-PERSIST GEMM2: row tid's output row, to sD after the K loop
+    if (!SWIGLU && !PERSIST) {
+      load_row_coef(g, cur.t, wm, lane, wr);
+      if (g.ydst && tid < BM) ydv = g.ydst[(size_t)cur.t.row0 + tid];
+    }
     f32x4 acc[8][4];
 #pragma unroll
     for (int i = 0; i < 8; ++i)
@@ -233,25 +250,32 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
       static_assert(sizeof(sA) >= BM * 128, "the h tile fits the A ring");
       static_assert(sizeof(sB[0]) >= 64 * 512 && (NW == 4 || sizeof(sA[0]) >= 64 * 512),
                     "y rows fit the ring");
-      if constexpr (SWIGLU)
+      if constexpr (!SWIGLU) {
+        // read after the epilogue's first barrier
+        if (tid < BM) sD[0][tid] = ydv;
+      }
+      if constexpr (SWIGLU) {
         store_h_mx_staged<NW>(acc, g, cur.t, cur.nt, wm, wn, lane, tid, &sA[0][0]);
-      else if constexpr (NW == 8)
-        store_y_bf16_staged<NW>(acc, wr, g, cur.t, cur.nt, wm, wn, lane, tid, &sA[0][0],
-                                &sA[1][0]);
-      else
-        store_y_bf16_staged<NW>(acc, wr, g, cur.t, cur.nt, wm, wn, lane, tid, &sB[0][0],
-                                &sB[1][0]);
+      } else {
+        uint32_t yb[8][4][2];
+        pack_y_bf16(acc, wr, yb);
+        if constexpr (NW == 8)
+          store_y_bf16_staged<NW>(yb, g, cur.t, cur.nt, wm, wn, lane, tid, &sA[0][0], &sA[1][0],
+                                  &sD[0][0]);
+        else
+          store_y_bf16_staged<NW>(yb, g, cur.t, cur.nt, wm, wn, lane, tid, &sB[0][0], &sB[1][0],
+                                  &sD[0][0]);
+      }
       return;
     } else {
-      // GEMM2's coefficients (in LDS since the tile's first step) go into
-      // the accumulators before the next tile's coefficients overwrite them
+      // GEMM2: the outputs are scaled by the coefficients (in LDS since the
+      // tile's first step) and packed to bf16 before the next tile's
+      // coefficients overwrite them
+      uint32_t yb[SWIGLU ? 1 : 8][4][2];
       if constexpr (!SWIGLU) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const float w = sW[wm * 128 + i * 16 + r16];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) acc[i][j] *= w;
-        }
+        for (int i = 0; i < 8; ++i) wr[i] = sW[wm * 128 + i * 16 + r16];
+        pack_y_bf16(acc, wr, yb);
       }
       int mt2, nt2;
       const bool more = work_item<kGroupM, true>(it + 1, n_live, ntn, &mt2, &nt2);
@@ -264,7 +288,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
         __builtin_amdgcn_s_barrier();
         nxt = tile_at(mt2, nt2);
         stage(nxt, 0, 0);
-        stage_coef(nxt);
+        stage_coef(nxt, db ^ 1);
 #pragma unroll
         for (int v = 0; v < NBSV; ++v) {
           const int i = tid + v * 64 * NW;
@@ -274,15 +298,19 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
       // epilogue through buffer 1 (sA[1], sB[1]: 32 KB each)
       static_assert(sizeof(sA[1]) >= BM * 128 && sizeof(sA[1]) >= 64 * 512 &&
                         sizeof(sB[1]) >= 64 * 512, "staging fits buffer 1");
+      int n_st = S_EPI;
       if constexpr (SWIGLU)
         store_h_mx_staged<NW, true>(acc, g, cur.t, cur.nt, wm, wn, lane, tid, &sA[1][0]);
       else
-        store_y_bf16_staged<NW, true, true>(acc, wr, g, cur.t, cur.nt, wm, wn, lane, tid,
-                                            &sA[1][0], &sB[1][0]);
+        n_st = store_y_bf16_staged<NW, true>(yb, g, cur.t, cur.nt, wm, wn, lane, tid, &sA[1][0],
+                                             &sB[1][0], &sD[db][0]);
       if (!more) return;
       // the next tile's first stage and block scales landed once at most the
       // epilogue's stores are outstanding
-      wait_vmcnt<S_EPI>();
+      if constexpr (SWIGLU)
+        wait_vmcnt<S_EPI>();
+      else
+        wait_vmcnt_upto<0, 63>(n_st);
 #pragma unroll
       for (int v = 0; v < NBSV; ++v) {
         const int i = tid + v * 64 * NW;
@@ -290,6 +318,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
       }
       wait_lgkm0();  // the block scales are in LDS before the K loop's barrier
       cur = nxt;
+      db ^= 1;
     }
   }
 }

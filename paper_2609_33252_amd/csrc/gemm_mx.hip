@@ -86,6 +86,9 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_mx(GemmArgs g) {
   __shared__ u32x4 sB[STAGES][BN * 4];
   __shared__ u32x4 sAs[STAGES][BM / 4];
   __shared__ u32x4 sBs[STAGES][64];
+  // GEMM2 staged epilogue: the tile rows' output rows for direct writes
+  // (GemmArgs::ydst)
+  __shared__ int sD[SWIGLU || NW != 8 ? 1 : BM];
 
   const int a_row = lane >> 3, b_row = lane >> 2;
 #define CEP_MX_STAGE(kb)                                                            \
@@ -120,7 +123,16 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_mx(GemmArgs g) {
     if (s < nkb) CEP_MX_STAGE(s);
 
   float wr[8];
-  if (!SWIGLU) load_row_coef(g, t, wm, lane, wr);
+  int yd[8];     // GEMM2 with 8-byte stores: output rows of the lane's rows
+  int ydv = -1;  // GEMM2 staged: row tid's output row, to sD after the K loop
+  if constexpr (!SWIGLU) {
+    load_row_coef(g, t, wm, lane, wr);
+    if constexpr (sizeof(sA[0]) >= 64 * 512) {
+      if (g.ydst && tid < BM) ydv = g.ydst[(size_t)t.row0 + tid];
+    } else {
+      load_row_dst(g, t, wm, lane, yd);
+    }
+  }
   const int r16 = lane & 15, grp = lane >> 4;
   const int asw = (r16 >> 1) & 7;  // A swizzle of every row this lane reads
   const int bsw = bsw_of(r16);     // B swizzle of every row this lane reads
@@ -173,9 +185,13 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_mx(GemmArgs g) {
   if constexpr (SWIGLU) {
     store_h_mx_staged<NW>(acc, g, t, nt, wm, wn, lane, tid, &sA[0][0]);
   } else if constexpr (sizeof(sA[0]) >= 64 * 512) {
-    store_y_bf16_staged<NW>(acc, wr, g, t, nt, wm, wn, lane, tid, &sA[0][0], &sA[1][0]);
+    static_assert(NW == 8, "the staged y epilogue is the 8-wave tile's");
+    if (tid < BM) sD[tid] = ydv;  // read after the epilogue's first barrier
+    uint32_t yb[8][4][2];
+    pack_y_bf16(acc, wr, yb);
+    store_y_bf16_staged<NW>(yb, g, t, nt, wm, wn, lane, tid, &sA[0][0], &sA[1][0], sD);
   } else {
-    store_y_bf16(acc, wr, g, t, nt, wm, wn, lane);
+    store_y_bf16(acc, wr, yd, g, t, nt, wm, wn, lane);
   }
 }
 

@@ -67,6 +67,7 @@ __global__ __launch_bounds__(256) void k_ingest(Arena a, IngestGroup grp, int k,
   else bad |= kErrBadToken;
   a.dst[row] = dst;
   a.xrow[row] = (const char *)c.x + (size_t)i * x_row_bytes;
+  int n_local = 0;
 #pragma unroll
   for (int s = 0; s < kMaxTopK; ++s) {
     if (s < k) {
@@ -76,10 +77,12 @@ __global__ __launch_bounds__(256) void k_ingest(Arena a, IngestGroup grp, int k,
         id = -1;
       }
       if (dst < 0) id = -1;
+      n_local += id >= 0;
       a.ids[(size_t)row * k + s] = id;
       a.w[(size_t)row * k + s] = wv[s];
     }
   }
+  a.solo[row] = n_local == 1 ? dst : -1;
   if (bad) atomicOr(err, bad);
 }
 
@@ -193,7 +196,10 @@ __device__ void plan_batch(const Scratch &sc, PlanLds &L, const PlanArgs &a, int
   // padding rows of each expert's last tile carry no pair
   for (int i = tid; i < E * align; i += nthr) {
     const int x = i / align, r = L.pad[x] + L.cnt[x] + i % align;
-    if (r < L.pad[x + 1] && r < a.max_mpad) sc.perm[r] = -1;
+    if (r < L.pad[x + 1] && r < a.max_mpad) {
+      sc.perm[r] = -1;
+      sc.ydst[r] = -1;
+    }
   }
   if (tid < E) {
     const int which = (int)((a.fetched_mask >> tid) & 1);
@@ -296,6 +302,7 @@ __global__ __launch_bounds__(64 * kFusedWaves) void k_route_fused(Arena a, Scrat
       if (pos >= 0) {
         sc.perm[pos] = p;
         sc.wrow[pos] = a.w[(size_t)row0 * k + p];  // the row's routing coefficient
+        sc.ydst[pos] = a.solo[row0 + p / k];
       }
     }
   }
@@ -408,6 +415,7 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_scan_scatter(Arena a, S
     if (pos >= 0) {
       sc.perm[pos] = p;
       sc.wrow[pos] = a.w[(size_t)row0 * k + p];  // the row's routing coefficient
+      sc.ydst[pos] = a.solo[row0 + p / k];
     }
   }
 }
@@ -562,14 +570,16 @@ __global__ __launch_bounds__(256) void k_scale_layout(Scratch sc, int nb) {
 // --------------------------------------------------------------- combine
 // One block per batch row: out[dst] = sum over its valid slots, in slot
 // order, of the grouped output rows (already scaled by their coefficient;
-// float32, or bf16 with YF32 false), accumulated in float32.
+// float32, or bf16 with YF32 false), accumulated in float32 from +0.
 // The row's valid slot positions are gathered once into LDS; each thread
 // then issues the loads of all its columns before summing, slot by slot.
+// skip_solo: GEMM2 has written the rows with exactly one local pair itself
+// (the same value: +0 plus the one grouped output); they are skipped.
 constexpr int kCombineCols = 4;  // float4 columns per thread per pass
 
 template <bool YF32>
 __global__ __launch_bounds__(256) void k_combine(Arena a, Scratch sc, int row0, int k, int d,
-                                                 float *__restrict__ out) {
+                                                 bool skip_solo, float *__restrict__ out) {
   __shared__ int s_pos[kMaxTopK];
   __shared__ int s_n;
   const int i = blockIdx.x;
@@ -580,6 +590,7 @@ __global__ __launch_bounds__(256) void k_combine(Arena a, Scratch sc, int row0, 
   int ps = -1;
   if (threadIdx.x < k) ps = sc.pos_of[(size_t)i * k + threadIdx.x];
   const int dst = a.dst[row0 + i];
+  const int solo = skip_solo ? a.solo[row0 + i] : -1;
   if (dst < 0) return;  // the same for the whole block
   if (threadIdx.x < 64) {
     const uint64_t m = __ballot(ps >= 0);
@@ -588,6 +599,8 @@ __global__ __launch_bounds__(256) void k_combine(Arena a, Scratch sc, int row0, 
   }
   __syncthreads();
   const int n = s_n, d4 = d / 4;
+  // a row whose one local pair has a grouped row: GEMM2 wrote it
+  if (solo >= 0 && n == 1) return;
   float4 *o = (float4 *)(out + (size_t)dst * d);
   for (int c0 = threadIdx.x; c0 < d4; c0 += blockDim.x * kCombineCols) {
     float4 acc[kCombineCols];
@@ -834,12 +847,14 @@ hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows,
 }
 
 hipError_t launch_combine(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int d,
-                          bool y_f32, float *out, hipStream_t s) {
+                          bool y_f32, bool skip_solo, float *out, hipStream_t s) {
   if (n_rows <= 0) return hipSuccess;
   if (y_f32)
-    hipLaunchKernelGGL(k_combine<true>, dim3(n_rows), dim3(256), 0, s, a, sc, row0, k, d, out);
+    hipLaunchKernelGGL(k_combine<true>, dim3(n_rows), dim3(256), 0, s, a, sc, row0, k, d,
+                       skip_solo, out);
   else
-    hipLaunchKernelGGL(k_combine<false>, dim3(n_rows), dim3(256), 0, s, a, sc, row0, k, d, out);
+    hipLaunchKernelGGL(k_combine<false>, dim3(n_rows), dim3(256), 0, s, a, sc, row0, k, d,
+                       skip_solo, out);
   return hipGetLastError();
 }
 

@@ -186,6 +186,23 @@ void *dalloc(cep_ctx *c, size_t bytes, hipError_t *e) {
   return p;
 }
 
+// A stream on a hardware queue that no other stream shares.  HIP runs a
+// process's streams on at most GPU_MAX_HW_QUEUES hardware queues (4 by
+// default), and streams that share a queue run its packets in order: a batch
+// stream waiting for a late chunk's arrival event would hold back every
+// stream on its queue -- another stream slot, the staging stream, the weight
+// copy -- and the application's own streams could hold back the library's.
+// A stream created with a CU mask gets a queue of its own; the mask names
+// every compute unit.  (Such a stream also synchronises with the legacy
+// default stream, as any stream created without hipStreamNonBlocking does.)
+constexpr int kMaxCUs = 1024;
+hipError_t own_queue_stream(hipStream_t *s, int n_cu) {
+  uint32_t mask[(kMaxCUs + 31) / 32] = {};
+  if (n_cu < 1 || n_cu > kMaxCUs) return hipErrorInvalidValue;
+  for (int i = 0; i < n_cu; ++i) mask[i / 32] |= 1u << (i % 32);
+  return hipExtStreamCreateWithCUMask(s, (uint32_t)((n_cu + 31) / 32), mask);
+}
+
 // Timing events from per-layer pools.  Phase markers only measure time, so
 // they skip the system-scope fence (an L2 writeback and invalidate between
 // the phases); a batch's end event keeps it, because the host reads the
@@ -331,7 +348,8 @@ int launch_pending(cep_ctx *c) {
   HIPCHK(c, launch_gemm1(sc, 0, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
                          gather, b.row0, k, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[1], s));
-  HIPCHK(c, launch_gemm2(sc, 0, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I, s));
+  HIPCHK(c, launch_gemm2(sc, 0, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
+                         c->out, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[2], s));
   // fetched experts' tiles (the scan's second tile lists) run after the
   // resident experts' GEMMs, once their weights are in: the copy overlaps
@@ -343,10 +361,12 @@ int launch_pending(cep_ctx *c) {
     HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
                            gather, b.row0, k, s));
     if (b.phases) HIPCHK(c, hipEventRecord(b.ev_fphase[1], s));
-    HIPCHK(c, launch_gemm2(sc, 1, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I, s));
+    HIPCHK(c, launch_gemm2(sc, 1, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
+                           c->out, s));
     if (b.phases) HIPCHK(c, hipEventRecord(b.ev_fphase[2], s));
   }
-  HIPCHK(c, launch_combine(c->arena, sc, b.row0, b.n_rows, k, d, c->wk == kWBf16, c->out, s));
+  HIPCHK(c, launch_combine(c->arena, sc, b.row0, b.n_rows, k, d, c->wk == kWBf16,
+                           gemm2_writes_solo(c->wk), c->out, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[3], s));
 
   if (cfg.record_routing) {
@@ -481,6 +501,7 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
   c->arena.ids = (int32_t *)A(sizeof(int32_t) * c->arena_cap * k);
   c->arena.w = (float *)A(sizeof(float) * c->arena_cap * k);
   c->arena.dst = (int32_t *)A(sizeof(int32_t) * c->arena_cap);
+  c->arena.solo = (int32_t *)A(sizeof(int32_t) * c->arena_cap);
   c->arena.xrow = (const void **)A(sizeof(void *) * c->arena_cap);
   c->d_err = (uint32_t *)A(sizeof(uint32_t));
   const size_t xes = c->wk != kWBf16 ? 1 : 2;
@@ -495,6 +516,7 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
     sc.pos_of = (int32_t *)A(sizeof(int32_t) * (size_t)c->max_rows * k);
     sc.perm = (int32_t *)A(sizeof(int32_t) * c->max_mpad);
     sc.wrow = (float *)A(sizeof(float) * c->max_mpad);
+    sc.ydst = (int32_t *)A(sizeof(int32_t) * c->max_mpad);
     // bf16 rows with bf16 weights are read in place by GEMM1 (no packed copy)
     if (!(c->wk == kWBf16 && cfg->x_dtype == CEP_BF16)) sc.xg = A(xes * c->max_mpad * d);
     sc.h = A(xes * c->max_mpad * I);
@@ -512,14 +534,14 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
     return fail(nullptr, CEP_ENOMEM, "cep_init_experts: device allocation failed: %s",
                 hipGetErrorString(e));
   }
-  // streams at default priority; events for ordering only skip timing
-  bool ok = hipStreamCreateWithFlags(&c->ingest, hipStreamNonBlocking) == hipSuccess;
+  // streams at default priority, each on a hardware queue of its own;
+  // events for ordering only skip timing
+  bool ok = own_queue_stream(&c->ingest, c->n_cu) == hipSuccess;
   for (int i = 0; i < cfg->n_streams && ok; ++i) {
-    ok = hipStreamCreateWithFlags(&c->st[i], hipStreamNonBlocking) == hipSuccess &&
+    ok = own_queue_stream(&c->st[i], c->n_cu) == hipSuccess &&
          hipEventCreateWithFlags(&c->ev_ingest[i], kDepEvent) == hipSuccess;
   }
-  if (ok && cfg->fetch_buffer_bytes)
-    ok = hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking) == hipSuccess;
+  if (ok && cfg->fetch_buffer_bytes) ok = own_queue_stream(&c->copy, c->n_cu) == hipSuccess;
   ok = ok && hipEventCreateWithFlags(&c->ev_origin, hipEventDisableSystemFence) == hipSuccess &&
        hipEventCreateWithFlags(&c->ev_fetch_start, hipEventDisableSystemFence) == hipSuccess &&
        hipEventCreate(&c->ev_fetch_ready) == hipSuccess &&
@@ -1054,6 +1076,7 @@ CEP_API int cep_ffn_noalloc(cep_ctx *c, int replica, int n_rows, int n_pairs,
     a.ids = (int32_t *)cv.take(sizeof(int32_t) * (size_t)n_rows * k);
     a.w = (float *)cv.take(sizeof(float) * (size_t)n_rows * k);
     a.dst = (int32_t *)cv.take(sizeof(int32_t) * (size_t)n_rows);
+    a.solo = (int32_t *)cv.take(sizeof(int32_t) * (size_t)n_rows);
     a.xrow = (const void **)cv.take(sizeof(void *) * (size_t)n_rows);
     Scratch sc{};
     sc.blk_cnt = (int32_t *)cv.take(sizeof(int32_t) * (size_t)blocks * E);
@@ -1065,6 +1088,7 @@ CEP_API int cep_ffn_noalloc(cep_ctx *c, int replica, int n_rows, int n_pairs,
     sc.pos_of = (int32_t *)cv.take(sizeof(int32_t) * (size_t)n_rows * k);
     sc.perm = (int32_t *)cv.take(sizeof(int32_t) * (size_t)mpad);
     sc.wrow = (float *)cv.take(sizeof(float) * (size_t)mpad);
+    sc.ydst = (int32_t *)cv.take(sizeof(int32_t) * (size_t)mpad);
     if (packed) sc.xg = cv.take(xes * (size_t)mpad * d);
     sc.h = cv.take(xes * (size_t)mpad * I);
     sc.y = cv.take((c->wk == kWBf16 ? 4 : 2) * (size_t)mpad * d);
@@ -1094,8 +1118,10 @@ CEP_API int cep_ffn_noalloc(cep_ctx *c, int replica, int n_rows, int n_pairs,
     const Arena *gather = packed ? nullptr : &a;
     HIPCHK(c, launch_gemm1(sc, 0, tiles_cap, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
                            gather, 0, k, s));
-    HIPCHK(c, launch_gemm2(sc, 0, tiles_cap, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I, s));
-    HIPCHK(c, launch_combine(a, sc, 0, n_rows, k, d, c->wk == kWBf16, out, s));
+    HIPCHK(c, launch_gemm2(sc, 0, tiles_cap, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
+                           out, s));
+    HIPCHK(c, launch_combine(a, sc, 0, n_rows, k, d, c->wk == kWBf16, gemm2_writes_solo(c->wk),
+                             out, s));
   }
   return CEP_OK;
 }

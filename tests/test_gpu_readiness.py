@@ -10,6 +10,8 @@ arrived, each with its own event.  The library must read every chunk only
 after its event: the output then equals the run on resident inputs, bit for
 bit, under every policy and stream count.
 """
+import ctypes
+
 import numpy as np
 import pytest
 import torch
@@ -150,6 +152,21 @@ def test_missing_waits_would_read_poison():
     assert failed or not np.array_equal(got, ref)
 
 
+def _own_stream():
+    """A stream on a hardware queue of its own.  HIP runs a process's
+    streams on a bounded set of hardware queues, and streams that share one
+    run its packets in order: a long kernel on a torch pool stream may hold
+    back a library stream on the same queue.  A stream with a CU mask (here
+    every CU) gets a queue that no other stream shares."""
+    hip = ctypes.CDLL("libamdhip64.so.7")  # the runtime torch already loaded
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    words = (n_cu + 31) // 32
+    mask = (ctypes.c_uint32 * words)(*([0xFFFFFFFF] * words))
+    h = ctypes.c_void_p()
+    assert hip.hipExtStreamCreateWithCUMask(ctypes.byref(h), words, mask) == 0
+    return hip, h, torch.cuda.ExternalStream(h.value)
+
+
 def test_late_chunk_blocks_only_its_own_batch():
     # chunk 0 arrives long after all others; per-chunk batches on two
     # streams: batch 0 (chunk 0) waits on stream slot 0, batches on slot 1
@@ -163,7 +180,7 @@ def test_late_chunk_blocks_only_its_own_batch():
     late.poison()
     run.out.zero_()
     n = len(run.chunks)
-    slow = torch.cuda.Stream()
+    hip, h, slow = _own_stream()
     events = late.deliver(range(1, n), delay=0)
     with torch.cuda.stream(slow):
         torch.cuda._sleep(20 * DELAY)
@@ -180,6 +197,10 @@ def test_late_chunk_blocks_only_its_own_batch():
     assert nonempty[0]["first_chunk"] == 0 and nonempty[0]["slot"] == 0
     early = [b for b in nonempty if b["slot"] == 1]
     assert early, "per-chunk batches on the second stream slot"
+    timeline = [(b["slot"], b["first_chunk"], round(b["start_ms"], 3), round(b["end_ms"], 3))
+                for b in nonempty]
     for b in early:
-        assert b["end_ms"] < a0, (b, a0)
+        assert b["end_ms"] < a0, (a0, timeline)
     run.close()
+    torch.cuda.synchronize()
+    assert hip.hipStreamDestroy(h) == 0
