@@ -138,11 +138,13 @@ int cep_pack_experts(const cep_config *cfg, const cep_weights *w, int first, int
 
 /* Create a context: validates cfg, allocates every scratch buffer, the chunk
  * arena and the fetch buffer, creates the streams, and packs the weights of
- * resident experts into library-owned memory.  Each library stream has a
- * hardware queue of its own (a CU-masked stream naming every CU), so a batch
- * waiting for a late chunk holds back no other stream; like any stream
- * created without hipStreamNonBlocking, these streams synchronise with the
- * legacy default (NULL) stream.  These are the expert weights
+ * resident experts into library-owned memory.  The library's streams are
+ * non-blocking streams at default priority.  HIP runs a process's streams on
+ * at most GPU_MAX_HW_QUEUES hardware queues (4 by default) and streams that
+ * share a queue run its packets in order: a batch waiting for a late chunk
+ * then also holds back the other streams on its queue.  A process with more
+ * streams in use than that should raise GPU_MAX_HW_QUEUES (it is read when
+ * HIP initialises).  These are the expert weights
  * every grouped invocation reads (Appendix C, "Grouped FFN invocations"),
  * and the preallocated temporary weight buffer of a helper (Appendix C,
  * "One-shot weight fetching": its capacity bounds the fetch byte budget).

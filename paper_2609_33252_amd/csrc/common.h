@@ -256,14 +256,14 @@ hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_til
                         int split_tiles, int align, bool var, const BlobTable &bt,
                         const BlobLayout &L, int wk, int d, int I, const Arena *gather, int row0,
                         int k, hipStream_t s);
-// out (may be null): with gemm2_writes_solo(wk), a grouped row whose token
+// out (may be null): with gemm2_writes_solo, a grouped row whose token
 // has no other local pair (Scratch::ydst) is written to that token's output
 // row [d] float32 as the combine would write it, instead of to y.
 hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles,
                         int split_tiles, int align, bool var, const BlobTable &bt,
                         const BlobLayout &L, int wk, int d, int I, float *out, hipStream_t s);
-// GEMM2 of e4m3 and MXFP4 weights (bf16 grouped outputs, staged epilogues)
-// writes single-pair tokens' output rows itself.
-inline bool gemm2_writes_solo(int wk) { return wk != kWBf16; }
+// GEMM2 writes single-pair tokens' output rows itself, except in the 256-row
+// bf16 tiles (batches of row alignment kBf16TileM, and their remainders).
+inline bool gemm2_writes_solo(int wk, int align) { return wk != kWBf16 || align != kBf16TileM; }
 
 }  // namespace cep

@@ -73,7 +73,7 @@ hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_til
                         const BlobLayout &L, int wk, int d, int I, float *out, hipStream_t s) {
   if (grid_tiles <= 0) return hipSuccess;
   GemmArgs g = base_args(sc, 2 * which, list_cap, grid_tiles, bt);
-  if (out && gemm2_writes_solo(wk)) {
+  if (out && gemm2_writes_solo(wk, align)) {
     g.yout = out;
     g.ydst = sc.ydst;
   }

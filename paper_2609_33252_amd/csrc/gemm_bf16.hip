@@ -101,6 +101,9 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
 
   __shared__ u32x4 sA[AS][BM * CH];
   __shared__ u32x4 sB[STAGES][BN * CH];
+  // GEMM2 of the non-PIPE tiles: direct output rows (GemmArgs::ydst; the
+  // 256-row tile's epilogue has no registers to spare and gets none)
+  const bool direct = !SWIGLU && !PIPE && g.ydst;
 
   // Lane l of a load fills slot l of a 1 KB segment (RPS rows x CH chunks):
   // row seg*RPS + l/CH, slot l%CH, which holds chunk (l%CH) ^ swz(row).  The
@@ -504,12 +507,28 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
     }
     return;
   }
+  // GEMM2: direct output rows of the lane's 16 rows of group i (ydst), -1
+  // for a grouped output row; rotated with the coefficients
+  auto dst16 = [&](int i, int(&o)[16]) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int lr = frow(i) + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      o[r] = direct && lr < t.rows ? g.ydst[(size_t)t.row0 + lr] : -1;
+    }
+  };
   float wc[16], wx[16];
-  if (!SWIGLU) coef16(0, wc);
+  int dc[16], dx[16];
+  if (!SWIGLU) {
+    coef16(0, wc);
+    dst16(0, dc);
+  }
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
     if (half && i > 0) break;
-    if (!SWIGLU && i + 1 < FM && !half) coef16(i + 1, wx);
+    if (!SWIGLU && i + 1 < FM && !half) {
+      coef16(i + 1, wx);
+      dst16(i + 1, dx);
+    }
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int rt = frow(i) + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
@@ -524,15 +543,22 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
         for (int j2 = 0; j2 < FN / 2; ++j2)
           H[hbase + j2 * 32] = (__bf16)silu_mul(acc[i][2 * j2][r], acc[i][2 * j2 + 1][r]);
       } else {
-        float *Y = (float *)g.out;
-        const size_t ybase = row * g.N + nt * BN + wn * WN + (lane & 31);
+        // a row with dc >= 0 goes to that output row (+0 for -0)
+        const size_t col = (size_t)nt * BN + wn * WN + (lane & 31);
+        float *yr = (dc[r] >= 0 ? g.yout + (size_t)dc[r] * g.N : (float *)g.out + row * g.N) + col;
 #pragma unroll
-        for (int j = 0; j < FN; ++j) Y[ybase + j * 32] = acc[i][j][r] * wc[r];
+        for (int j = 0; j < FN; ++j) {
+          const float v = acc[i][j][r] * wc[r];
+          yr[j * 32] = dc[r] >= 0 ? __uint_as_float(plus_zero(__float_as_uint(v))) : v;
+        }
       }
     }
     if (!SWIGLU) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) wc[r] = wx[r];
+      for (int r = 0; r < 16; ++r) {
+        wc[r] = wx[r];
+        dc[r] = dx[r];
+      }
     }
   }
   }  // work items

@@ -186,23 +186,6 @@ void *dalloc(cep_ctx *c, size_t bytes, hipError_t *e) {
   return p;
 }
 
-// A stream on a hardware queue that no other stream shares.  HIP runs a
-// process's streams on at most GPU_MAX_HW_QUEUES hardware queues (4 by
-// default), and streams that share a queue run its packets in order: a batch
-// stream waiting for a late chunk's arrival event would hold back every
-// stream on its queue -- another stream slot, the staging stream, the weight
-// copy -- and the application's own streams could hold back the library's.
-// A stream created with a CU mask gets a queue of its own; the mask names
-// every compute unit.  (Such a stream also synchronises with the legacy
-// default stream, as any stream created without hipStreamNonBlocking does.)
-constexpr int kMaxCUs = 1024;
-hipError_t own_queue_stream(hipStream_t *s, int n_cu) {
-  uint32_t mask[(kMaxCUs + 31) / 32] = {};
-  if (n_cu < 1 || n_cu > kMaxCUs) return hipErrorInvalidValue;
-  for (int i = 0; i < n_cu; ++i) mask[i / 32] |= 1u << (i % 32);
-  return hipExtStreamCreateWithCUMask(s, (uint32_t)((n_cu + 31) / 32), mask);
-}
-
 // Timing events from per-layer pools.  Phase markers only measure time, so
 // they skip the system-scope fence (an L2 writeback and invalidate between
 // the phases); a batch's end event keeps it, because the host reads the
@@ -366,7 +349,7 @@ int launch_pending(cep_ctx *c) {
     if (b.phases) HIPCHK(c, hipEventRecord(b.ev_fphase[2], s));
   }
   HIPCHK(c, launch_combine(c->arena, sc, b.row0, b.n_rows, k, d, c->wk == kWBf16,
-                           gemm2_writes_solo(c->wk), c->out, s));
+                           gemm2_writes_solo(c->wk, A), c->out, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[3], s));
 
   if (cfg.record_routing) {
@@ -534,14 +517,14 @@ CEP_API int cep_init_experts(cep_ctx **out, const cep_config *cfg, const cep_wei
     return fail(nullptr, CEP_ENOMEM, "cep_init_experts: device allocation failed: %s",
                 hipGetErrorString(e));
   }
-  // streams at default priority, each on a hardware queue of its own;
-  // events for ordering only skip timing
-  bool ok = own_queue_stream(&c->ingest, c->n_cu) == hipSuccess;
+  // streams at default priority; events for ordering only skip timing
+  bool ok = hipStreamCreateWithFlags(&c->ingest, hipStreamNonBlocking) == hipSuccess;
   for (int i = 0; i < cfg->n_streams && ok; ++i) {
-    ok = own_queue_stream(&c->st[i], c->n_cu) == hipSuccess &&
+    ok = hipStreamCreateWithFlags(&c->st[i], hipStreamNonBlocking) == hipSuccess &&
          hipEventCreateWithFlags(&c->ev_ingest[i], kDepEvent) == hipSuccess;
   }
-  if (ok && cfg->fetch_buffer_bytes) ok = own_queue_stream(&c->copy, c->n_cu) == hipSuccess;
+  if (ok && cfg->fetch_buffer_bytes)
+    ok = hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking) == hipSuccess;
   ok = ok && hipEventCreateWithFlags(&c->ev_origin, hipEventDisableSystemFence) == hipSuccess &&
        hipEventCreateWithFlags(&c->ev_fetch_start, hipEventDisableSystemFence) == hipSuccess &&
        hipEventCreate(&c->ev_fetch_ready) == hipSuccess &&
@@ -1120,7 +1103,7 @@ CEP_API int cep_ffn_noalloc(cep_ctx *c, int replica, int n_rows, int n_pairs,
                            gather, 0, k, s));
     HIPCHK(c, launch_gemm2(sc, 0, tiles_cap, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
                            out, s));
-    HIPCHK(c, launch_combine(a, sc, 0, n_rows, k, d, c->wk == kWBf16, gemm2_writes_solo(c->wk),
+    HIPCHK(c, launch_combine(a, sc, 0, n_rows, k, d, c->wk == kWBf16, gemm2_writes_solo(c->wk, A),
                              out, s));
   }
   return CEP_OK;

@@ -11,6 +11,10 @@ after its event: the output then equals the run on resident inputs, bit for
 bit, under every policy and stream count.
 """
 import ctypes
+import json
+import os
+import subprocess
+import sys
 
 import numpy as np
 import pytest
@@ -167,11 +171,10 @@ def _own_stream():
     return hip, h, torch.cuda.ExternalStream(h.value)
 
 
-def test_late_chunk_blocks_only_its_own_batch():
-    # chunk 0 arrives long after all others; per-chunk batches on two
-    # streams: batch 0 (chunk 0) waits on stream slot 0, batches on slot 1
-    # run as soon as their own chunks are in, so they end before chunk 0
-    # arrives (no head-of-line blocking behind another replica's lane)
+def _late_chunk_scenario():
+    """Chunk 0 arrives long after all others; per-chunk batches on two
+    stream slots.  Returns (output equals the resident run, chunk 0's
+    arrival ms, [(slot, first chunk, start ms, end ms)] per batch)."""
     wl = _workload()
     run = harness.Runner(wl, n_streams=2)
     run.run(policy=cep.CEP_WAIT_ALL)
@@ -189,18 +192,42 @@ def test_late_chunk_blocks_only_its_own_batch():
     late.dispatch = keep
     _layer(run, events, cep.CEP_PER_CHUNK, 1, 2)
     got = _out(run)
-    assert np.array_equal(got, ref)
     st = run.stats()
-    a0 = st["chunks"][0]["arrival_ms"]
-    assert a0 > 0
-    nonempty = [b for b in st["batches"]]
-    assert nonempty[0]["first_chunk"] == 0 and nonempty[0]["slot"] == 0
-    early = [b for b in nonempty if b["slot"] == 1]
-    assert early, "per-chunk batches on the second stream slot"
-    timeline = [(b["slot"], b["first_chunk"], round(b["start_ms"], 3), round(b["end_ms"], 3))
-                for b in nonempty]
-    for b in early:
-        assert b["end_ms"] < a0, (a0, timeline)
+    timeline = [(b["slot"], b["first_chunk"], b["start_ms"], b["end_ms"]) for b in st["batches"]]
+    result = (bool(np.array_equal(got, ref)), st["chunks"][0]["arrival_ms"], timeline)
     run.close()
     torch.cuda.synchronize()
     assert hip.hipStreamDestroy(h) == 0
+    return result
+
+
+def _late_chunk_child():
+    torch.cuda.set_device(0)
+    cep.lib()
+    print(json.dumps(_late_chunk_scenario()), flush=True)
+
+
+def test_late_chunk_blocks_only_its_own_batch():
+    # batch 0 (chunk 0) waits on stream slot 0; the batches on slot 1 run as
+    # soon as their own chunks are in, so they end before chunk 0 arrives (no
+    # head-of-line blocking behind another replica's lane).  HIP runs a
+    # process's streams on a bounded set of hardware queues, and which
+    # streams share a queue depends on every stream the process has created
+    # (torch's stream pool, earlier contexts); streams on one queue run its
+    # packets in order.  The scenario therefore runs in a fresh child process,
+    # whose few streams get distinct queues.
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, "-c",
+                        "from tests.test_gpu_readiness import _late_chunk_child; "
+                        "_late_chunk_child()"],
+                       cwd=root, capture_output=True, text=True, timeout=240)
+    assert r.returncode == 0, r.stderr[-3000:]
+    equal, a0, timeline = json.loads(r.stdout.strip().splitlines()[-1])
+    assert equal
+    assert a0 > 0
+    assert timeline[0][0] == 0 and timeline[0][1] == 0
+    early = [b for b in timeline if b[0] == 1]
+    assert early, "per-chunk batches on the second stream slot"
+    for b in early:
+        assert b[3] < a0, (a0, timeline)
+
