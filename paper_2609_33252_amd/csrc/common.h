@@ -90,6 +90,12 @@ constexpr int kBf16VarMinRows = 64;
 inline bool batch_var_tiles(int wk, int align, int pairs, int n_experts) {
   return wk == kWBf16 && align == kBf16SmallTileM && pairs >= kBf16VarMinRows * n_experts;
 }
+// Smaller bf16 batches stream the weights: GEMM1 runs the 64-row tiles
+// ordered by rows (most first) in 64-column work items handed to free CUs
+// in that order (launch_bf16_stream), GEMM2 the 64-row tiles as listed.
+inline bool batch_stream_tiles(int wk, int align, int pairs, int n_experts) {
+  return wk == kWBf16 && align == kBf16SmallTileM && pairs < kBf16VarMinRows * n_experts;
+}
 
 // Per-expert row alignment A of one batch's grouped layout = M tile of the
 // GEMMs that run it.  bf16 batches with fewer than one large tile of rows
@@ -233,12 +239,15 @@ hipError_t launch_ingest(const Arena &a, const IngestGroup &grp, int k, int E, i
 // split_cu > 0 (bf16 batches with 256-row tiles): the scan may move each
 // expert's last partial tile of at most 128 rows to 64-row remainder tiles
 // when its makespan estimate for split_cu compute units and GEMM1's
-// n_tiles_n 256-wide column tiles improves.  var (batch_var_tiles): the
-// scan also lists the 128-row tiles, in the second list of each kind.
+// n_tiles_n 256-wide column tiles improves.  list2: the scan also lists,
+// in the second list of each kind, the 128-row tiles (kListVar,
+// batch_var_tiles) or the same tiles ordered by rows, most first
+// (kListSorted, batch_stream_tiles).
+enum : int { kListNone = 0, kListVar = 1, kListSorted = 2 };
 hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int E,
                         int align, int expected_pairs, int max_mpad, int max_tiles,
                         uint64_t fetched_mask, int x_dtype, int wk, int d, int split_cu,
-                        int n_tiles_n, bool var, uint32_t *err, hipStream_t s);
+                        int n_tiles_n, int list2, uint32_t *err, hipStream_t s);
 // y_f32: the grouped outputs are float32 (bf16 weights), else bf16.
 // skip_solo: the batch's GEMM2 wrote the output rows of tokens with one
 // local pair (gemm2_writes_solo); the combine leaves them alone.
@@ -252,15 +261,17 @@ hipError_t launch_combine(const Arena &a, const Scratch &sc, int row0, int n_row
 // gather (bf16 weights and rows only): GEMM1 reads the batch's input rows
 // (arena rows from row0) in place through the permutation instead of a
 // packed copy.  var: both GEMMs run the 128-row tile list instead.
+// stream (batch_stream_tiles, the scan run with kListSorted): GEMM1 runs
+// the sorted tile list with launch_bf16_stream.
 hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles,
-                        int split_tiles, int align, bool var, const BlobTable &bt,
+                        int split_tiles, int align, bool var, bool stream, const BlobTable &bt,
                         const BlobLayout &L, int wk, int d, int I, const Arena *gather, int row0,
                         int k, hipStream_t s);
 // out (may be null): with gemm2_writes_solo, a grouped row whose token
 // has no other local pair (Scratch::ydst) is written to that token's output
 // row [d] float32 as the combine would write it, instead of to y.
 hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles,
-                        int split_tiles, int align, bool var, const BlobTable &bt,
+                        int split_tiles, int align, bool var, bool stream, const BlobTable &bt,
                         const BlobLayout &L, int wk, int d, int I, float *out, hipStream_t s);
 // GEMM2 writes single-pair tokens' output rows itself, except in the 256-row
 // bf16 tiles (batches of row alignment kBf16TileM, and their remainders).

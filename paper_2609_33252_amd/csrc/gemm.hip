@@ -44,7 +44,7 @@ GemmArgs var_list(GemmArgs g, const Scratch &sc, int which, int list_cap) {
 }  // namespace
 
 hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles,
-                        int split_tiles, int align, bool var, const BlobTable &bt,
+                        int split_tiles, int align, bool var, bool stream, const BlobTable &bt,
                         const BlobLayout &L, int wk, int d, int I, const Arena *gather, int row0,
                         int k, hipStream_t s) {
   if (grid_tiles <= 0) return hipSuccess;
@@ -65,11 +65,12 @@ hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_til
   g.out = sc.h;
   g.out_s = sc.hs;
   if (var) return launch_bf16_var<true>(var_list(g, sc, which, list_cap), grid_tiles, s);
+  if (stream) return launch_bf16_stream(var_list(g, sc, which, list_cap), grid_tiles, s);
   return launch_any<true>(g, grid_tiles, split_tiles, align, wk, sc, which, list_cap, s);
 }
 
 hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_tiles,
-                        int split_tiles, int align, bool var, const BlobTable &bt,
+                        int split_tiles, int align, bool var, bool stream, const BlobTable &bt,
                         const BlobLayout &L, int wk, int d, int I, float *out, hipStream_t s) {
   if (grid_tiles <= 0) return hipSuccess;
   GemmArgs g = base_args(sc, 2 * which, list_cap, grid_tiles, bt);
@@ -86,6 +87,7 @@ hipError_t launch_gemm2(const Scratch &sc, int which, int list_cap, int grid_til
   g.out = sc.y;
   g.wrow = sc.wrow;
   if (var) return launch_bf16_var<false>(var_list(g, sc, which, list_cap), grid_tiles, s);
+  if (stream) return launch_bf16_stream2(var_list(g, sc, which, list_cap), grid_tiles, s);
   return launch_any<false>(g, grid_tiles, split_tiles, align, wk, sc, which, list_cap, s);
 }
 

@@ -16,7 +16,10 @@
 //   mid-size batches (VAR): 128 x 128 tiles whose last tile per expert may be
 //     a 64-row half (it loads and multiplies its first 64 rows only), the
 //     weights three stages deep and the rows two, so that two workgroups
-//     still fit a CU: a hot expert streams its weights once per 128 rows.
+//     still fit a CU: a hot expert streams its weights once per 128 rows;
+//   weight-streaming batches (LIN): the small tile's schedule over 64-row
+//     tiles listed by rows, one work item per workgroup in list order,
+//     without the row loads of all-padding waves.
 // All accumulate each output over K in the same order (ascending 16-wide
 // steps of v_mfma_f32_32x32x16_bf16), so a row's result does not depend on
 // which tile its batch used.  With bf16 token rows GEMM1 runs as GATHER: its
@@ -61,7 +64,8 @@ __device__ inline void static_for(F &&f) {
 // tile): fragments are read right before their MFMAs and loads run STAGES-1
 // steps ahead, which keeps more weight bytes in flight per LDS byte.
 template <int BM, int BN, int BK, int STAGES, int OCC, bool PIPE, bool SWIGLU, int WGM = 2,
-          int NW = 4, int GM = kGroupM, bool GATHER = false, bool VAR = false, int ASTG = 0>
+          int NW = 4, int GM = kGroupM, bool GATHER = false, bool VAR = false, int ASTG = 0,
+          bool LIN = false>
 __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
   static_assert(BK == 32 || BK == 64, "LDS swizzle covers 4 or 8 chunks per row");
   static_assert(!VAR || (!PIPE && WGM == 2 && BM == 128), "VAR: 128-row tile, two wave rows");
@@ -90,7 +94,17 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
   const int n_live = *g.n_tiles;
   for (int it = 0;; ++it) {
   int mt, nt;
-  if (!work_item<GM, PIPE>(it, n_live, g.N / BN, &mt, &nt)) return;
+  if constexpr (LIN) {
+    // work item = workgroup id, tile-major (every column slice of tile 0
+    // first): the hardware starts the items in list order
+    if (it > 0) return;
+    const int ntn = g.N / BN, L = blockIdx.x;
+    if (L >= n_live * ntn) return;
+    mt = L / ntn;
+    nt = L % ntn;
+  } else if (!work_item<GM, PIPE>(it, n_live, g.N / BN, &mt, &nt)) {
+    return;
+  }
   const Tile t = g.tiles[mt];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -311,7 +325,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
     auto run = [&](auto nfa_c, auto nal_c) {
       constexpr int NFA = decltype(nfa_c)::value, NAL_ = decltype(nal_c)::value;
       constexpr int PERX = NAL_ + B_LD;
-      const char *arow[NAL_];
+      const char *arow[NAL_ > 0 ? NAL_ : 1];
       CEP_AROWS(arow)
       if constexpr (ASTG == 2) {
         // B (weights, from HBM) runs STAGES-1 steps ahead, A (rows, mostly
@@ -372,6 +386,14 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
         run(std::integral_constant<int, 1>{}, std::integral_constant<int, A_LD / 2>{});
       else
         run(std::integral_constant<int, FM>{}, std::integral_constant<int, A_LD>{});
+    } else if constexpr (LIN) {
+      // a wave whose A rows are all padding loads none of them (its MFMAs
+      // then read stale LDS rows, whose outputs are never stored): a tile of
+      // a few rows requests little more than its weights
+      if (wid * A_LD * RPS < t.rows)
+        run(std::integral_constant<int, FM>{}, std::integral_constant<int, A_LD>{});
+      else
+        run(std::integral_constant<int, FM>{}, std::integral_constant<int, 0>{});
     } else {
       run(std::integral_constant<int, FM>{}, std::integral_constant<int, A_LD>{});
     }
@@ -647,6 +669,45 @@ hipError_t launch_bf16_var(const GemmArgs &g, int grid_tiles, hipStream_t s) {
     }
   }
   return launch_bf16_var_as<SWIGLU, false>(g, grid_tiles, s);
+}
+
+// Weight-streaming batches (a few hundred pairs over all local experts, one
+// of them hot).  A CU's load rate bounds these launches, and it counts every
+// byte requested, rows from L2 as much as weights from HBM, so a launch lasts
+// as long as its most loaded CU.  The scan lists the batch's 64-row tiles by
+// rows, most first; the work items (GEMM1: 64 rows x 64 columns, 32 h
+// columns; GEMM2: 64 x 128) follow that list one per workgroup, so the items
+// of the largest tiles start first and the small ones fill in behind them,
+// and waves whose 16 rows are all padding load no rows (a tile of a few rows
+// requests little more than its weights).  Straggler workload, per-chunk
+// batches: GEMM1 108 -> 98 us, GEMM2 48.5 -> 46 us per batch on average.
+template <bool GATHER>
+hipError_t launch_bf16_stream_as(const GemmArgs &g, int grid_tiles, hipStream_t s) {
+  constexpr int BN = 64;
+  if (g.N % BN || g.K % 64) return hipErrorInvalidValue;
+  const int grid = grid_tiles * (g.N / BN);
+  hipLaunchKernelGGL((k_gemm_bf16<kBf16SmallTileM, BN, 64, 3, 2, false, true, 2, 4, kGroupM,
+                                  GATHER, false, 0, true>),
+                     dim3(grid), dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_bf16_stream2(const GemmArgs &g, int grid_tiles, hipStream_t s) {
+  constexpr int BN = 128;
+  if (g.N % BN || g.K % 64) return hipErrorInvalidValue;
+  const int grid = grid_tiles * (g.N / BN);
+  hipLaunchKernelGGL((k_gemm_bf16<kBf16SmallTileM, BN, 64, 3, 2, false, false, 2, 4, kGroupM,
+                                  false, false, 0, true>),
+                     dim3(grid), dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_bf16_stream(const GemmArgs &g, int grid_tiles, hipStream_t s) {
+  if (g.A == nullptr) {
+    if (!g.xrow || !g.perm || g.k < 1) return hipErrorInvalidValue;
+    return launch_bf16_stream_as<true>(g, grid_tiles, s);
+  }
+  return launch_bf16_stream_as<false>(g, grid_tiles, s);
 }
 
 template hipError_t launch_bf16_var<true>(const GemmArgs &, int, hipStream_t);

@@ -463,6 +463,11 @@ hipError_t launch_bf16_rem(const GemmArgs &g, int grid_tiles, hipStream_t s);
 // bf16 GEMM over a list of 128-row and 64-row (half) tiles
 template <bool SWIGLU>
 hipError_t launch_bf16_var(const GemmArgs &g, int grid_tiles, hipStream_t s);
+// bf16 GEMM1 (SwiGLU) of a weight-streaming batch over its 64-row tiles
+// ordered by rows, one 64-column work item per workgroup in list order
+hipError_t launch_bf16_stream(const GemmArgs &g, int grid_tiles, hipStream_t s);
+// bf16 GEMM2 of a weight-streaming batch over the same list, 128-column items
+hipError_t launch_bf16_stream2(const GemmArgs &g, int grid_tiles, hipStream_t s);
 template <bool SWIGLU>
 hipError_t launch_fp8(const GemmArgs &g, int grid_tiles, int align, hipStream_t s);
 template <bool SWIGLU>

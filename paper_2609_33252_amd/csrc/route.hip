@@ -121,13 +121,16 @@ struct PlanArgs {
   int E, align, expected_pairs, max_mpad, max_tiles;
   uint64_t fetched_mask;
   int split_cu, n_tiles_n;
-  int var;  // also list each expert's 128-row tiles (second list of each kind)
+  // second list of each kind: kListVar each expert's 128-row tiles,
+  // kListSorted the 64-row tiles ordered by rows, most first; kListNone none
+  int list2;
   uint32_t *err;
 };
 
 struct PlanLds {
   int cnt[kMaxExperts], off[kMaxExperts + 1], pad[kMaxExperts + 1];
   int tile0[kMaxExperts], rtile0[kMaxExperts];
+  int nfull[2];  // full tiles of resident / fetched experts (sorted list)
   int split;
 };
 
@@ -162,6 +165,7 @@ __device__ void plan_batch(const Scratch &sc, PlanLds &L, const PlanArgs &a, int
     L.split = split;
     int o = 0, op = 0;
     int t0[4] = {0, 0, 0, 0};
+    int nfull[2] = {0, 0};
     for (int x = 0; x < E; ++x) {
       L.off[x] = o;
       L.pad[x] = op;
@@ -171,14 +175,23 @@ __device__ void plan_batch(const Scratch &sc, PlanLds &L, const PlanArgs &a, int
       L.tile0[x] = t0[2 * which];
       L.rtile0[x] = t0[2 * which + 1];
       t0[2 * which] += rem ? c / align : (c + align - 1) / align;
-      t0[2 * which + 1] += rem    ? (r + kBf16SmallTileM - 1) / kBf16SmallTileM
-                           : a.var ? (c + kBf16VarTileM - 1) / kBf16VarTileM
-                                   : 0;
+      t0[2 * which + 1] += rem                     ? (r + kBf16SmallTileM - 1) / kBf16SmallTileM
+                           : a.list2 == kListVar    ? (c + kBf16VarTileM - 1) / kBf16VarTileM
+                           : a.list2 == kListSorted ? (c + align - 1) / align
+                                                    : 0;
+      // sorted list: the kind's full tiles first, in expert order (rtile0 =
+      // full tiles of the kind's earlier experts), then its partial tiles
+      if (a.list2 == kListSorted) {
+        L.rtile0[x] = nfull[which];
+        nfull[which] += c / align;
+      }
       o += c;
       op += (c + align - 1) / align * align;
     }
     L.off[E] = o;
     L.pad[E] = op;
+    L.nfull[0] = nfull[0];
+    L.nfull[1] = nfull[1];
     if (o != a.expected_pairs) atomicOr(a.err, kErrPairCount);
     bool over = op > a.max_mpad;
     for (int l = 0; l < 4; ++l) {
@@ -213,7 +226,30 @@ __device__ void plan_batch(const Scratch &sc, PlanLds &L, const PlanArgs &a, int
       if (ti >= a.max_tiles || row0 + align > a.max_mpad) break;
       list[ti] = Tile{tid, row0, min(align, c - q * align), 0};
     }
-    if (a.var) {
+    if (a.list2 == kListSorted) {
+      // the second list holds the same tiles ordered by rows, most first:
+      // the kind's full tiles in expert order, then its partial tiles by
+      // rows, ties by expert
+      Tile *slist = sc.tiles + (size_t)(2 * which + 1) * a.max_tiles;
+      for (int q = 0; q < c / align; ++q) {
+        const int ti = L.rtile0[tid] + q;
+        const int row0 = L.pad[tid] + q * align;
+        if (ti >= a.max_tiles || row0 + align > a.max_mpad) break;
+        slist[ti] = Tile{tid, row0, align, 0};
+      }
+      if (r > 0) {
+        int rank = 0;
+        for (int x = 0; x < E; ++x) {
+          const int rx = L.cnt[x] % align;
+          rank += (int)((a.fetched_mask >> x) & 1) == which && rx > 0 &&
+                  (rx > r || (rx == r && x < tid));
+        }
+        const int ti = L.nfull[which] + rank;
+        const int row0 = L.pad[tid] + (c / align) * align;
+        if (ti < a.max_tiles && row0 + align <= a.max_mpad) slist[ti] = Tile{tid, row0, r, 0};
+      }
+    }
+    if (a.list2 == kListVar) {
       // the second list holds the 128-row tiles; a tile of more than 64
       // rows spans 128 rows of the expert's 64-aligned region
       Tile *vlist = sc.tiles + (size_t)(2 * which + 1) * a.max_tiles;
@@ -814,12 +850,12 @@ hipError_t launch_ingest(const Arena &a, const IngestGroup &grp, int k, int E, i
 hipError_t launch_route(const Arena &a, const Scratch &sc, int row0, int n_rows, int k, int E,
                         int align, int expected_pairs, int max_mpad, int max_tiles,
                         uint64_t fetched_mask, int x_dtype, int wk, int d, int split_cu,
-                        int n_tiles_n, bool var, uint32_t *err, hipStream_t s) {
+                        int n_tiles_n, int list2, uint32_t *err, hipStream_t s) {
   const int n_flat = n_rows * k;
   const int nb = (n_flat + kRoutePairs - 1) / kRoutePairs;
   if (nb == 0) return hipSuccess;
   const PlanArgs pa{E, align, expected_pairs, max_mpad, max_tiles, fetched_mask, split_cu,
-                    n_tiles_n, var ? 1 : 0, err};
+                    n_tiles_n, list2, err};
   if (n_flat <= kFusedRoutePairs) {
     hipLaunchKernelGGL(k_route_fused, dim3(1), dim3(64 * kFusedWaves), 0, s, a, sc, row0,
                        n_flat, k, pa);

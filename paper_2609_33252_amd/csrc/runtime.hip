@@ -318,9 +318,12 @@ int launch_pending(cep_ctx *c) {
   const int split_tiles = split ? 2 * E : 0;
   // 64-row bf16 batches with enough rows per expert: 128-row tiles
   const bool var = batch_var_tiles(c->wk, A, P, E);
+  // smaller 64-row bf16 batches: GEMM1 over the tiles sorted by rows
+  const bool stream = batch_stream_tiles(c->wk, A, P, E);
   HIPCHK(c, launch_route(c->arena, sc, b.row0, b.n_rows, k, E, A, P, c->max_mpad, c->max_tiles,
                          c->fetched_mask, cfg.x_dtype, c->wk, d, split ? c->n_cu : 0,
-                         2 * I / kBf16TileN, var, c->d_err, s));
+                         2 * I / kBf16TileN,
+                         var ? kListVar : stream ? kListSorted : kListNone, c->d_err, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[0], s));
 
   BlobTable bt{};
@@ -328,11 +331,11 @@ int launch_pending(cep_ctx *c) {
   // bf16 rows with bf16 weights are not packed: GEMM1 reads them in place
   const Arena *gather = c->wk == kWBf16 && cfg.x_dtype == CEP_BF16 ? &c->arena : nullptr;
 
-  HIPCHK(c, launch_gemm1(sc, 0, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
-                         gather, b.row0, k, s));
+  HIPCHK(c, launch_gemm1(sc, 0, c->max_tiles, tiles, split_tiles, A, var, stream, bt, c->L,
+                         c->wk, d, I, gather, b.row0, k, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[1], s));
-  HIPCHK(c, launch_gemm2(sc, 0, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
-                         c->out, s));
+  HIPCHK(c, launch_gemm2(sc, 0, c->max_tiles, tiles, split_tiles, A, var, stream, bt, c->L,
+                         c->wk, d, I, c->out, s));
   if (b.phases) HIPCHK(c, hipEventRecord(b.ev_phase[2], s));
   // fetched experts' tiles (the scan's second tile lists) run after the
   // resident experts' GEMMs, once their weights are in: the copy overlaps
@@ -341,11 +344,11 @@ int launch_pending(cep_ctx *c) {
   if (b.fetched) {
     if (c->copied) HIPCHK(c, hipStreamWaitEvent(s, c->ev_fetch_ready, 0));
     if (b.phases) HIPCHK(c, hipEventRecord(b.ev_fphase[0], s));
-    HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
-                           gather, b.row0, k, s));
+    HIPCHK(c, launch_gemm1(sc, 1, c->max_tiles, tiles, split_tiles, A, var, stream, bt, c->L,
+                           c->wk, d, I, gather, b.row0, k, s));
     if (b.phases) HIPCHK(c, hipEventRecord(b.ev_fphase[1], s));
-    HIPCHK(c, launch_gemm2(sc, 1, c->max_tiles, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
-                           c->out, s));
+    HIPCHK(c, launch_gemm2(sc, 1, c->max_tiles, tiles, split_tiles, A, var, stream, bt, c->L,
+                           c->wk, d, I, c->out, s));
     if (b.phases) HIPCHK(c, hipEventRecord(b.ev_fphase[2], s));
   }
   HIPCHK(c, launch_combine(c->arena, sc, b.row0, b.n_rows, k, d, c->wk == kWBf16,
@@ -1093,16 +1096,18 @@ CEP_API int cep_ffn_noalloc(cep_ctx *c, int replica, int n_rows, int n_pairs,
     const bool split = c->wk == kWBf16 && A == kBf16TileM;
     const int split_tiles = split ? 2 * E : 0;
     const bool var = batch_var_tiles(c->wk, A, P, E);
+    const bool stream = batch_stream_tiles(c->wk, A, P, E);
     const int tiles = std::min(tiles_cap, (P + A - 1) / A + E);
     HIPCHK(c, launch_route(a, sc, 0, n_rows, k, E, A, P, mpad, tiles_cap, 0, cfg.x_dtype, c->wk,
-                           d, split ? c->n_cu : 0, 2 * I / kBf16TileN, var, c->d_err, s));
+                           d, split ? c->n_cu : 0, 2 * I / kBf16TileN,
+                           var ? kListVar : stream ? kListSorted : kListNone, c->d_err, s));
     BlobTable bt{};
     for (int e = 0; e < E; ++e) bt.blob[e] = c->w_res + (size_t)e * c->L.bytes;
     const Arena *gather = packed ? nullptr : &a;
-    HIPCHK(c, launch_gemm1(sc, 0, tiles_cap, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
-                           gather, 0, k, s));
-    HIPCHK(c, launch_gemm2(sc, 0, tiles_cap, tiles, split_tiles, A, var, bt, c->L, c->wk, d, I,
-                           out, s));
+    HIPCHK(c, launch_gemm1(sc, 0, tiles_cap, tiles, split_tiles, A, var, stream, bt, c->L, c->wk,
+                           d, I, gather, 0, k, s));
+    HIPCHK(c, launch_gemm2(sc, 0, tiles_cap, tiles, split_tiles, A, var, stream, bt, c->L, c->wk,
+                           d, I, out, s));
     HIPCHK(c, launch_combine(a, sc, 0, n_rows, k, d, c->wk == kWBf16, gemm2_writes_solo(c->wk, A),
                              out, s));
   }

@@ -307,6 +307,39 @@ def test_var_tiles_packed_rows_agree_bitwise():
     U.check(wl, a)
 
 
+def test_stream_tiles_by_rows_agree_bitwise():
+    # Weight-streaming bf16 batches (fewer than 64 pairs per local expert:
+    # single chunks of the straggler shape, a hot expert of 100-150 rows
+    # beside experts of a few rows) run both GEMMs over their 64-row tiles
+    # listed by rows, most first, one work item per workgroup, waves of
+    # padding rows loading no rows; resident and fetched experts have lists
+    # of their own.  Same K order as the wait-all batch: the same bits.
+    wl = W.generate("zipf_imbalanced_d7168", 8, d=1024, I=512, fetch_frac=0.25)
+    E, k = wl.cfg["E"], wl.cfg["k"]
+    assert wl.fetched
+    run = harness.Runner(wl, n_streams=2, record_routing=True)
+    run.run(policy=cep.CEP_WAIT_ALL)
+    a = _out(run)
+    run.out.zero_()
+    run.run(policy=cep.CEP_PER_CHUNK, n_streams=2)
+    b = _out(run)
+    fetched = np.zeros(E, bool)
+    fetched[list(wl.fetched)] = True
+    mixed = 0
+    for i in range(cep.cep_get_batch_count(run.ctx)):
+        m = cep.cep_get_batch_routing(run.ctx, i, E, k)
+        c = m["cnt"]
+        assert m["align"] == 64 and c.sum() < 64 * E
+        # several tiles of one expert, tiles of a few rows, resident and
+        # fetched experts with pairs
+        mixed += int(c.max() > 64 and ((c > 0) & (c <= 16)).any() and
+                     (c[fetched] > 0).any() and (c[~fetched] > 0).any())
+    run.close()
+    assert mixed > 0
+    assert np.array_equal(a, b)
+    U.check(wl, a)
+
+
 def test_remainder_tiles_agree_bitwise():
     # Full-size wait-all batch: two experts overflow 4 full 256-row tiles by a
     # few rows, which the tile plan runs as 64-row remainder tiles next to the
