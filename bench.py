@@ -605,8 +605,13 @@ def full_bench(args):
     run = harness.Runner(wl4, n_streams=2)
     f4 = 6.0 * c4["d"] * c4["I"] * run.n_pairs
     res = {}
+    # wait-all, theta(0.9), and the smaller launch thresholds of the
+    # comparison (per-chunk batches and theta 1024 / 4096 pairs per launch)
     for name, pol, theta, ns in (("wait_all", cep.CEP_WAIT_ALL, 1, 1),
-                                 (f"theta_{THETA_09}", cep.CEP_THRESHOLD, THETA_09, 2)):
+                                 (f"theta_{THETA_09}", cep.CEP_THRESHOLD, THETA_09, 2),
+                                 ("theta_4096", cep.CEP_THRESHOLD, 4096, 2),
+                                 ("theta_1024", cep.CEP_THRESHOLD, 1024, 2),
+                                 ("per_chunk", cep.CEP_PER_CHUNK, 1, 2)):
         ms_ = []
         for i in range(1 + args.timed_layers):
             run.run(policy=pol, theta=theta, n_streams=ns, timed=True)

@@ -18,8 +18,8 @@
 //     weights three stages deep and the rows two, so that two workgroups
 //     still fit a CU: a hot expert streams its weights once per 128 rows;
 //   weight-streaming batches (LIN): the small tile's schedule over 64-row
-//     tiles listed by rows, one work item per workgroup in list order,
-//     without the row loads of all-padding waves.
+//     tiles listed by rows, one work item per workgroup in list order, each
+//     wave loading only its 8-row segments that hold rows.
 // All accumulate each output over K in the same order (ascending 16-wide
 // steps of v_mfma_f32_32x32x16_bf16), so a row's result does not depend on
 // which tile its batch used.  With bf16 token rows GEMM1 runs as GATHER: its
@@ -142,7 +142,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
 #define CEP_AROWS(arow_)                                                            \
   if constexpr (GATHER) {                                                           \
     _Pragma("unroll") for (int i = 0; i < NAL_; ++i) {                              \
-      const int r = (wid * NAL_ + i) * RPS + seg_row;                               \
+      const int r = (wid * SEGW_ + i) * RPS + seg_row;                              \
       const int p = g.perm[t.row0 + r];                                             \
       arow_[i] = (const char *)g.xrow[g.arow0 + (p >= 0 ? p / g.k : 0)] +           \
                  ((lane % CH) ^ ((r >> SH) & (CH - 1))) * 16;                       \
@@ -152,7 +152,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
   {                                                                                 \
     const int buf_ = (kt) % AS;                                                     \
     _Pragma("unroll") for (int i = 0; i < NAL_; ++i) {                              \
-      const int seg = wid * NAL_ + i;                                               \
+      const int seg = wid * SEGW_ + i;                                              \
       dma16(GATHER ? arow[i] + (size_t)(kt) * BK * 2                                \
                    : Ag + (size_t)(kt) * BK * 2 + CEP_LANE_OFF(seg),                \
             __builtin_amdgcn_readfirstlane(lds_offset(&sA[buf_][seg * 64])));       \
@@ -195,7 +195,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
   // a VAR tile of at most BM/2 rows loads and multiplies its first half only
   const bool half = VAR && t.rows <= BM / 2;
   if constexpr (PIPE) {
-    constexpr int NAL_ = A_LD;
+    constexpr int NAL_ = A_LD, SEGW_ = A_LD;
     const char *arow[NAL_];
     CEP_AROWS(arow)
     // Stage s is issued at the barrier of step s - STAGES + 1 (the prologue
@@ -318,12 +318,13 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
     // the tail's reloads must land before the workgroup's LDS is released
     wait_vmcnt<0>();
   } else {
-    // NFA A fragments per wave and NAL_ A loads per wave and step (all of
-    // them, or for a VAR half tile those of its first BM/2 rows); every wave
-    // issues the same number of loads per step, so the vmcnt waits count
-    // whole steps.
-    auto run = [&](auto nfa_c, auto nal_c) {
+    // NFA A fragments per wave and NAL_ A loads per wave and step, the
+    // first NAL_ of the wave's SEGW_ load segments (wave w loads segments
+    // w*SEGW_ ..: all of them, or for a VAR half tile those of its first
+    // BM/2 rows); the wave's vmcnt waits count its own loads per step.
+    auto run = [&](auto nfa_c, auto nal_c, auto segw_c) {
       constexpr int NFA = decltype(nfa_c)::value, NAL_ = decltype(nal_c)::value;
+      constexpr int SEGW_ = decltype(segw_c)::value;
       constexpr int PERX = NAL_ + B_LD;
       const char *arow[NAL_ > 0 ? NAL_ : 1];
       CEP_AROWS(arow)
@@ -381,21 +382,28 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_bf16(GemmArgs g) {
         }
       }
     };
+    // LIN: a wave loads only those of its load segments (RPS rows each)
+    // that hold rows of the tile (its MFMAs then read stale LDS rows for the
+    // rest, whose outputs are never stored): a tile of a few rows requests
+    // little more than its weights
+    auto run_rows = [&](auto nfa_c, auto segw_c) {
+      constexpr int SEGW = decltype(segw_c)::value;
+      if constexpr (LIN) {
+        const int n = min(SEGW, max(0, (t.rows - wid * SEGW * RPS + RPS - 1) / RPS));
+        static_for<SEGW + 1>([&](auto k) {
+          if (n == decltype(k)::value) run(nfa_c, k, segw_c);
+        });
+      } else {
+        run(nfa_c, segw_c, segw_c);
+      }
+    };
     if constexpr (VAR) {
       if (half)
-        run(std::integral_constant<int, 1>{}, std::integral_constant<int, A_LD / 2>{});
+        run_rows(ic<1>{}, ic<A_LD / 2>{});
       else
-        run(std::integral_constant<int, FM>{}, std::integral_constant<int, A_LD>{});
-    } else if constexpr (LIN) {
-      // a wave whose A rows are all padding loads none of them (its MFMAs
-      // then read stale LDS rows, whose outputs are never stored): a tile of
-      // a few rows requests little more than its weights
-      if (wid * A_LD * RPS < t.rows)
-        run(std::integral_constant<int, FM>{}, std::integral_constant<int, A_LD>{});
-      else
-        run(std::integral_constant<int, FM>{}, std::integral_constant<int, 0>{});
+        run_rows(ic<FM>{}, ic<A_LD>{});
     } else {
-      run(std::integral_constant<int, FM>{}, std::integral_constant<int, A_LD>{});
+      run_rows(ic<FM>{}, ic<A_LD>{});
     }
   }
 #undef CEP_LOAD_FRAG
@@ -678,9 +686,10 @@ hipError_t launch_bf16_var(const GemmArgs &g, int grid_tiles, hipStream_t s) {
 // rows, most first; the work items (GEMM1: 64 rows x 64 columns, 32 h
 // columns; GEMM2: 64 x 128) follow that list one per workgroup, so the items
 // of the largest tiles start first and the small ones fill in behind them,
-// and waves whose 16 rows are all padding load no rows (a tile of a few rows
-// requests little more than its weights).  Straggler workload, per-chunk
-// batches: GEMM1 108 -> 98 us, GEMM2 48.5 -> 46 us per batch on average.
+// and each wave loads only its 8-row segments that hold rows (a tile of a
+// few rows requests little more than its weights).  Straggler workload,
+// per-chunk batches: GEMM1 108 -> 98 us, GEMM2 48.5 -> 46 us per batch on
+// average.
 template <bool GATHER>
 hipError_t launch_bf16_stream_as(const GemmArgs &g, int grid_tiles, hipStream_t s) {
   constexpr int BN = 64;
