@@ -62,10 +62,10 @@ GEMM_SOURCES = {
     "mxfp4": ["paper_2609_33252_amd/csrc/gemm_mx.hip", "paper_2609_33252_amd/csrc/gemm_common.h"],
 }
 TRAFFIC_BYTES = {  # workload -> (GEMM family, sha1 prefix of its sources, bytes per launch)
-    "fp8_fetch_d6144": ("fp8", "8cd1162a8696", 2204963054),
-    "sync_d4096": ("bf16", "be1536a05110", 504211803),
-    "zipf_imbalanced_d7168/per_chunk": ("bf16", "be1536a05110", 473388711),
-    "mxfp4_dsv4flash_d4096": ("mxfp4", "31b1a1017063", 1368926427),
+    "fp8_fetch_d6144": ("fp8", "de8dba9173a6", 2220125504),
+    "sync_d4096": ("bf16", "2b7aa1606aba", 504196498),
+    "zipf_imbalanced_d7168/per_chunk": ("bf16", "2b7aa1606aba", 507441708),
+    "mxfp4_dsv4flash_d4096": ("mxfp4", "f8862a9a89ad", 1369589413),
 }
 
 
