@@ -123,6 +123,37 @@ inline int balanced_grid(int grid_tiles, int gm, int n_tiles_n) {
 // eight, at equal or better speed (measured on the bf16 and MXFP4 GEMM1 of
 // the DeepSeek-V4-Flash-shaped and 4096-wide workloads).
 constexpr int kGroupM = 4;
+// M tiles per group when whole groups go to one XCD (work_item_xg): eight,
+// so that 32 workgroups run an 8 x 4 block (as few distinct panels as 4 x 8)
+// and groups of 20 or 24 column tiles are a whole number of rounds.
+constexpr int kGroupXcd = 8;
+
+// Persistent work item it of this workgroup, whole tile groups per XCD when
+// that costs no round: group g (GM consecutive M tiles x all N tiles, M
+// fastest) belongs to XCD g % 8, whose gridDim.x/8 workgroups take items j,
+// j + gridDim.x/8, ... of its groups in order.  When a group's items are a
+// whole number of rounds, every round of an XCD's workgroups is then one
+// GM x (32/GM) block of a single group (work_item's contiguous shares start
+// mid-group, so some of its rounds span two groups and share less in L2:
+// e4m3 GEMM1 L2 hit rate 73 -> 78 %).  Otherwise, or when whole groups would
+// leave the busiest XCD more rounds than contiguous shares, work_item.
+template <int GM>
+__device__ inline bool work_item_xg(int it, int n_live, int n_tiles_n, int *mt, int *nt) {
+  const int wpx = (int)(gridDim.x >> 3);  // workgroups per XCD
+  const int per = GM * n_tiles_n;         // items of a full group
+  const int ngroups = (n_live + GM - 1) / GM;
+  const int r_xg = ((ngroups + 7) / 8 * per + wpx - 1) / wpx;
+  const int r_bal = ((n_live * n_tiles_n + 7) / 8 + wpx - 1) / wpx;
+  if (per % wpx != 0 || r_xg > r_bal) return work_item<kGroupM, true>(it, n_live, n_tiles_n, mt, nt);
+  const int x = blockIdx.x & 7, j = (blockIdx.x >> 3) + it * wpx;
+  const int g = x + 8 * (j / per), w = j % per;
+  if (g >= ngroups) return false;
+  const int gm = min(GM, n_live - g * GM);  // M tiles of this group
+  if (w >= gm * n_tiles_n) return false;    // past the last (partial) group
+  *mt = g * GM + w % gm;
+  *nt = w / gm;
+  return true;
+}
 
 // One direct global->LDS load of 16 bytes per lane: lane l's bytes land at
 // LDS byte offset lds_seg + 16*l.  Issued as inline assembly so that the

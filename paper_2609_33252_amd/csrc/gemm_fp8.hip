@@ -86,7 +86,9 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
   // uniform over the workgroup: kept in scalar registers
   const int n_live = __builtin_amdgcn_readfirstlane(*g.n_tiles), ntn = g.N / BN;
   int mt, nt;
-  if (!work_item<kGroupM, PERSIST>(0, n_live, ntn, &mt, &nt)) return;
+  if (!(PERSIST ? work_item_xg<kGroupXcd>(0, n_live, ntn, &mt, &nt)
+                : work_item<kGroupM, false>(0, n_live, ntn, &mt, &nt)))
+    return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wid >> 2, wn = wid & 3;
@@ -278,7 +280,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
         pack_y_bf16(acc, wr, yb);
       }
       int mt2, nt2;
-      const bool more = work_item<kGroupM, true>(it + 1, n_live, ntn, &mt2, &nt2);
+      const bool more = work_item_xg<kGroupXcd>(it + 1, n_live, ntn, &mt2, &nt2);
       F8Tile nxt;
       float sbv[NBSV];
       if (more) {
