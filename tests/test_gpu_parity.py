@@ -513,6 +513,30 @@ def test_fp8_persistent_tiles_odd_k_steps_all_rows():
     print(f"fp8 persistent tiles, odd K steps: pairs={wl.n_pairs} max_abs={mx:.3e} rel={rel:.3e}")
 
 
+def test_fp8_whole_groups_per_xcd_all_rows():
+    # 141 M tiles of 256 rows with 4 column tiles in GEMM1: eighteen groups of
+    # eight M tiles, the last partial, so that the persistent GEMM1 gives each
+    # XCD whole groups (two or three) instead of contiguous shares.  Every
+    # row against the oracle; the two per-replica batches (about 71 M tiles
+    # each) bitwise equal to the wait-all batch.
+    wl = W.generate("fp8_fetch_d6144", 5, d=512, I=512, E=4, Eg=8, k=4, R=2, T=8192, cpr=1)
+    E, k = wl.cfg["E"], wl.cfg["k"]
+    run = harness.Runner(wl, n_streams=2, record_routing=True, use_fetch=False)
+    run.run(policy=cep.CEP_WAIT_ALL)
+    a = _out(run)
+    m = cep.cep_get_batch_routing(run.ctx, 0, E, k)
+    assert m["align"] == 256
+    m_tiles = int(sum((c + 255) // 256 for c in m["cnt"]))
+    assert m_tiles > 16 * 8 and m_tiles % 8, m["cnt"]
+    mx, rel = U.check(wl, a)
+    run.out.zero_()
+    run.run(policy=cep.CEP_PER_CHUNK, n_streams=2)
+    b = _out(run)
+    run.close()
+    assert np.array_equal(a, b)
+    print(f"fp8 whole groups per XCD: pairs={wl.n_pairs} M tiles={m_tiles} rel={rel:.3e}")
+
+
 def test_fp8_large_tile_all_rows_and_small_tile_bitwise():
     # The e4m3 8-wave 256-row tile (the large-batch tile of the e4m3
     # workload) over every row against the oracle: four experts of 1757 to
