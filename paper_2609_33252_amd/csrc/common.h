@@ -261,8 +261,8 @@ hipError_t launch_combine(const Arena &a, const Scratch &sc, int row0, int n_row
 // gather (bf16 weights and rows only): GEMM1 reads the batch's input rows
 // (arena rows from row0) in place through the permutation instead of a
 // packed copy.  var: both GEMMs run the 128-row tile list instead.
-// stream (batch_stream_tiles, the scan run with kListSorted): GEMM1 runs
-// the sorted tile list with launch_bf16_stream.
+// stream (batch_stream_tiles, the scan run with kListSorted): both GEMMs
+// run the sorted tile list (launch_bf16_stream, launch_bf16_stream2).
 hipError_t launch_gemm1(const Scratch &sc, int which, int list_cap, int grid_tiles,
                         int split_tiles, int align, bool var, bool stream, const BlobTable &bt,
                         const BlobLayout &L, int wk, int d, int I, const Arena *gather, int row0,

@@ -34,7 +34,8 @@ hipError_t launch_any(const GemmArgs &g, int grid_tiles, int split_tiles, int al
   return launch_bf16_rem<SWIGLU>(r, split_tiles, s);
 }
 
-// the scan's second list of `which`: the batch's 128-row tiles
+// the scan's second list of `which`: the batch's 128-row tiles (kListVar)
+// or its 64-row tiles ordered by rows (kListSorted)
 GemmArgs var_list(GemmArgs g, const Scratch &sc, int which, int list_cap) {
   g.tiles = sc.tiles + (size_t)(2 * which + 1) * list_cap;
   g.n_tiles = sc.n_tiles + 2 * which + 1;
