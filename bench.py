@@ -599,33 +599,47 @@ def full_bench(args):
     del run
     print(json.dumps({"progress": "sync_d4096"}), file=sys.stderr, flush=True)
 
-    # ---- straggler workload on timed arrivals: wait-all vs theta(0.9)
+    # ---- timed arrivals: wait-all against theta(0.9) and the smaller launch
+    # thresholds of the comparison (theta 1024 / 4096 pairs per launch and
+    # per-chunk batches)
+    def timed_policies(run, flop, policies):
+        res = {}
+        for name, pol, theta, ns in policies:
+            ms_ = []
+            for i in range(1 + args.timed_layers):
+                run.run(policy=pol, theta=theta, n_streams=ns, timed=True)
+                torch.cuda.synchronize()
+                if i:
+                    ms_.append(streaming.layer_metrics(run.stats(), flop))
+            m = streaming.mean_metrics(ms_)
+            res[name] = {"batches": m["batches"],
+                         "time_to_last_chunk_done_ms": round(m["time_to_last_chunk_done_ms"], 4),
+                         "last_arrival_ms": round(m["last_arrival_ms"], 4),
+                         "exposed_tail_ms": round(m["exposed_tail_ms"], 4),
+                         "chunk_latency_p50_ms": round(m["chunk_latency_ms"]["p50"], 4),
+                         "chunk_latency_p95_ms": round(m["chunk_latency_ms"]["p95"], 4),
+                         "busy_tflops": round(m["busy_tflops"], 2)}
+        return res
+    WA = ("wait_all", cep.CEP_WAIT_ALL, 1, 1)
+    TH = (f"theta_{THETA_09}", cep.CEP_THRESHOLD, THETA_09, 2)
+    PC = ("per_chunk", cep.CEP_PER_CHUNK, 1, 2)
+
+    # the lognormal-arrival workload without a straggler (each replica's
+    # eight chunks arrive with lognormal gaps)
+    wl3 = W.generate("zipf_stream_d7168", 0)
+    run = harness.Runner(wl3, n_streams=2)
+    res3 = timed_policies(run, 6.0 * wl3.cfg["d"] * wl3.cfg["I"] * run.n_pairs, (WA, TH, PC))
+    cep.cep_get_status(run.ctx)
+    run.close()
+    del run
+
+    # the straggler workload
     wl4 = W.generate("zipf_imbalanced_d7168", 0)
     c4 = wl4.cfg
     run = harness.Runner(wl4, n_streams=2)
     f4 = 6.0 * c4["d"] * c4["I"] * run.n_pairs
-    res = {}
-    # wait-all, theta(0.9), and the smaller launch thresholds of the
-    # comparison (per-chunk batches and theta 1024 / 4096 pairs per launch)
-    for name, pol, theta, ns in (("wait_all", cep.CEP_WAIT_ALL, 1, 1),
-                                 (f"theta_{THETA_09}", cep.CEP_THRESHOLD, THETA_09, 2),
-                                 ("theta_4096", cep.CEP_THRESHOLD, 4096, 2),
-                                 ("theta_1024", cep.CEP_THRESHOLD, 1024, 2),
-                                 ("per_chunk", cep.CEP_PER_CHUNK, 1, 2)):
-        ms_ = []
-        for i in range(1 + args.timed_layers):
-            run.run(policy=pol, theta=theta, n_streams=ns, timed=True)
-            torch.cuda.synchronize()
-            if i:
-                ms_.append(streaming.layer_metrics(run.stats(), f4))
-        m = streaming.mean_metrics(ms_)
-        res[name] = {"batches": m["batches"],
-                     "time_to_last_chunk_done_ms": round(m["time_to_last_chunk_done_ms"], 4),
-                     "last_arrival_ms": round(m["last_arrival_ms"], 4),
-                     "exposed_tail_ms": round(m["exposed_tail_ms"], 4),
-                     "chunk_latency_p50_ms": round(m["chunk_latency_ms"]["p50"], 4),
-                     "chunk_latency_p95_ms": round(m["chunk_latency_ms"]["p95"], 4),
-                     "busy_tflops": round(m["busy_tflops"], 2)}
+    res = timed_policies(run, f4, (WA, TH, ("theta_4096", cep.CEP_THRESHOLD, 4096, 2),
+                                   ("theta_1024", cep.CEP_THRESHOLD, 1024, 2), PC))
     # matched work (the same layer, inputs resident, no arrival timing):
     # wait-all on one stream against theta(0.9) on two streams and per-chunk
     # batches, wait-all timed before and after the others; then the
@@ -671,6 +685,13 @@ def full_bench(args):
         "layers": args.timed_layers, **res,
         "exposed_tail_ratio": round(th["exposed_tail_ms"] / wa["exposed_tail_ms"], 4),
         "busy_tflops_ratio": round(th["busy_tflops"] / wa["busy_tflops"], 4)}
+    wa3, th3 = res3["wait_all"], res3[f"theta_{THETA_09}"]
+    line["time_to_last_chunk_done_no_straggler"] = {
+        "workload": describe(wl3.cfg, "zipf_stream_d7168"), "local_pairs": wl3.n_pairs,
+        "arrivals": "timed: lognormal(0, 0.5) ms gaps, no straggler",
+        "layers": args.timed_layers, **res3,
+        "exposed_tail_ratio": round(th3["exposed_tail_ms"] / wa3["exposed_tail_ms"], 4),
+        "busy_tflops_ratio": round(th3["busy_tflops"] / wa3["busy_tflops"], 4)}
     print(json.dumps({"progress": "straggler"}), file=sys.stderr, flush=True)
 
     # ---- targets of the path, as measured here
@@ -678,12 +699,14 @@ def full_bench(args):
         "bf16_gemm1_mfma_frac_ge_0.60": line["sync_d4096"]["roofline"]["frac"] >= 0.60,
         "fp8_gemm1_mfma_frac": roof["frac"],
         "streaming_hbm_frac_ge_0.70": line["streaming_roofline"]["frac"] >= 0.70,
-        "streaming_lowers_exposed_tail": th["exposed_tail_ms"] < wa["exposed_tail_ms"]}
+        "streaming_lowers_exposed_tail": (th["exposed_tail_ms"] < wa["exposed_tail_ms"] and
+                                          th3["exposed_tail_ms"] < wa3["exposed_tail_ms"])}
 
     # ---- the CPU oracle
     if not args.no_cpu:
         per = {}
-        gens = {HEADLINE: wl, "sync_d4096": wl2, "zipf_imbalanced_d7168": wl4}
+        gens = {HEADLINE: wl, "sync_d4096": wl2, "zipf_stream_d7168": wl3,
+                "zipf_imbalanced_d7168": wl4}
         for name in W.CONFIG_ORDER:
             w_ = gens.get(name) or W.generate(name, 0)
             per[name] = {"all_threads": cpu_oracle_rate(w_, args.cpu_budget),
