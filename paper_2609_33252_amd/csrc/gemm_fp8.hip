@@ -132,14 +132,14 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
 #pragma unroll
     for (int i = 0; i < A_LD; ++i) {
       const int seg = wid * A_LD + i;
-      dma16(f.Ag + (size_t)kb * BK + lane_off(seg),
-            __builtin_amdgcn_readfirstlane(lds_offset(&sA[buf][seg * 64])));
+      dma16_s(f.Ag + (size_t)kb * BK, lane_off(seg),
+              __builtin_amdgcn_readfirstlane(lds_offset(&sA[buf][seg * 64])));
     }
 #pragma unroll
     for (int i = 0; i < B_LD; ++i) {
       const int seg = wid * B_LD + i;
-      dma16(f.Bg + (size_t)kb * BK + lane_off(seg),
-            __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf][seg * 64])));
+      dma16_s(f.Bg + (size_t)kb * BK, lane_off(seg),
+              __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf][seg * 64])));
     }
     if (wid == 0 && lane < BM / 4)
       dma16(f.Asg + (size_t)kb * as_step + lane * 16,
