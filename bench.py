@@ -62,7 +62,7 @@ GEMM_SOURCES = {
     "mxfp4": ["paper_2609_33252_amd/csrc/gemm_mx.hip", "paper_2609_33252_amd/csrc/gemm_common.h"],
 }
 TRAFFIC_BYTES = {  # workload -> (GEMM family, sha1 prefix of its sources, bytes per launch)
-    "fp8_fetch_d6144": ("fp8", "34953a9e3e50", 1837411365),
+    "fp8_fetch_d6144": ("fp8", "406c1e479798", 1833503223),
     "sync_d4096": ("bf16", "c12c043df95d", 504261285),
     "zipf_imbalanced_d7168/per_chunk": ("bf16", "c12c043df95d", 507424984),
     "mxfp4_dsv4flash_d4096": ("mxfp4", "918ca6de742c", 1370523849),
