@@ -17,6 +17,8 @@
 // LDS reads below follow this so that hardware K equals data K.
 #include "gemm_common.h"
 
+#include <algorithm>
+
 namespace cep {
 namespace {
 
@@ -55,7 +57,9 @@ __device__ inline f32x4 mx_mfma(const i32x8 &w, const i32x8 &x, const f32x4 &c, 
 // with SQ_LDS_BANK_CONFLICT); with these swizzles each such group reads
 // sixteen distinct 16-byte slots of 256 bytes in both operand reads.
 //
-// Epilogues: store_h_mx (GEMM1) and store_y_bf16 (GEMM2).
+// Epilogues: store_h_mx_staged (GEMM1) and store_y_bf16 (GEMM2).  The
+// 256-row tiles run as the persistent 8-wave kernel below (same stage, LDS
+// layout and MFMA order, so both tile heights give bitwise equal outputs).
 __device__ inline int bsw_of(int r) { return (r & 1) | ((r >> 1) & 2); }
 
 
@@ -86,9 +90,6 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_mx(GemmArgs g) {
   __shared__ u32x4 sB[STAGES][BN * 4];
   __shared__ u32x4 sAs[STAGES][BM / 4];
   __shared__ u32x4 sBs[STAGES][64];
-  // GEMM2 staged epilogue: the tile rows' output rows for direct writes
-  // (GemmArgs::ydst)
-  __shared__ int sD[SWIGLU || NW != 8 ? 1 : BM];
 
   const int a_row = lane >> 3, b_row = lane >> 2;
 #define CEP_MX_STAGE(kb)                                                            \
@@ -123,15 +124,10 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_mx(GemmArgs g) {
     if (s < nkb) CEP_MX_STAGE(s);
 
   float wr[8];
-  int yd[8];     // GEMM2 with 8-byte stores: output rows of the lane's rows
-  int ydv = -1;  // GEMM2 staged: row tid's output row, to sD after the K loop
+  int yd[8];  // GEMM2: output rows of the lane's rows (GemmArgs::ydst)
   if constexpr (!SWIGLU) {
     load_row_coef(g, t, wm, lane, wr);
-    if constexpr (sizeof(sA[0]) >= 64 * 512) {
-      if (g.ydst && tid < BM) ydv = g.ydst[(size_t)t.row0 + tid];
-    } else {
-      load_row_dst(g, t, wm, lane, yd);
-    }
+    load_row_dst(g, t, wm, lane, yd);
   }
   const int r16 = lane & 15, grp = lane >> 4;
   const int asw = (r16 >> 1) & 7;  // A swizzle of every row this lane reads
@@ -180,18 +176,206 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_mx(GemmArgs g) {
   }
 #undef CEP_MX_STAGE
 
-  // staging: BM x 128 code bytes, or y rows of 512 bytes, 64 per A stage
+  // GEMM1 stages BM x 128 code bytes through the A ring
   static_assert(sizeof(sA) >= BM * 128, "the h tile fits the A ring");
   if constexpr (SWIGLU) {
     store_h_mx_staged<NW>(acc, g, t, nt, wm, wn, lane, tid, &sA[0][0]);
-  } else if constexpr (sizeof(sA[0]) >= 64 * 512) {
-    static_assert(NW == 8, "the staged y epilogue is the 8-wave tile's");
-    if (tid < BM) sD[tid] = ydv;  // read after the epilogue's first barrier
-    uint32_t yb[8][4][2];
-    pack_y_bf16(acc, wr, yb);
-    store_y_bf16_staged<NW>(yb, g, t, nt, wm, wn, lane, tid, &sA[0][0], &sA[1][0], sD);
   } else {
     store_y_bf16(acc, wr, yd, g, t, nt, wm, wn, lane);
+  }
+}
+
+
+// Persistent 8-wave tiles, as the e4m3 GEMMs': one workgroup per CU walks
+// its XCD's share of the tile order (work_item_xg).  After a tile's K loop
+// it issues the next tile's first stage into ring buffer 0 (and, for
+// GEMM2, the next tile's routing coefficients and output rows into LDS),
+// then runs the epilogue through buffer 1 (GEMM2's y rows 64-127 of a pass
+// through sY), storing every row so that each wave issues a fixed number of
+// stores, and waits until at most those stores are outstanding: the next
+// tile's loads have landed, the stores may still drain.
+struct MxTile {
+  Tile t;
+  int nt;
+  const char *Ag, *Bt, *Asg, *Bsg;
+};
+
+template <bool SWIGLU>
+__global__ __launch_bounds__(512, 1) void k_gemm_mx_persist(GemmArgs g) {
+  constexpr int NW = 8, BM = 256, BN = 256, BK = 128;
+  constexpr int A_LD = BM * BK / 1024 / NW, B_LD = BN * (BK / 2) / 1024 / NW;
+  const int n_live = __builtin_amdgcn_readfirstlane(*g.n_tiles), ntn = g.N / BN;
+  int mt, nt;
+  if (!work_item_xg<kGroupXcd>(0, n_live, ntn, &mt, &nt)) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wid >> 2, wn = wid & 3;
+  const int K = g.K, nkb = K / BK, KB = K / 2;  // KB: bytes of one packed weight row
+  const size_t as_step = (size_t)(g.s_ld >> 7) * 512;
+
+  __shared__ u32x4 sA[2][BM * 8];
+  __shared__ u32x4 sB[2][BN * 4];
+  __shared__ u32x4 sAs[2][BM / 4];
+  __shared__ u32x4 sBs[2][64];
+  // GEMM2: the second 32 KB of a staged pass of y rows, the tile's routing
+  // coefficients and (two buffers: the next tile's beside the current
+  // epilogue) its rows' output rows
+  __shared__ u32x4 sY[SWIGLU ? 1 : 64 * 32];
+  __shared__ float sW[SWIGLU ? 1 : BM];
+  __shared__ int sD[SWIGLU ? 1 : 2][SWIGLU ? 1 : BM];
+
+  auto tile_at = [&](int mt_, int nt_) {
+    MxTile f;
+    mt_ = __builtin_amdgcn_readfirstlane(mt_);
+    nt_ = __builtin_amdgcn_readfirstlane(nt_);
+    f.t = g.tiles[mt_];
+    f.nt = nt_;
+    const uint8_t *blob = blob_of(g.bt, f.t.expert);
+    f.Ag = (const char *)(g.A + (size_t)f.t.row0 * K);
+    // the tile's 16 blocks of 16 weight rows (mx_block_index): K step kb
+    // 1 KB further into each
+    f.Bt = (const char *)(blob + g.b_off) + (size_t)nt_ * (BN / 16) * (KB >> 6) * 1024;
+    f.Asg = (const char *)g.As + (size_t)(f.t.row0 >> 7) * 512;
+    f.Bsg = (const char *)(blob + g.bs_off) + (size_t)nt_ * nkb * 1024;
+    return f;
+  };
+  const int a_row = lane >> 3, b_row = lane >> 2;
+  auto stage = [&](const MxTile &f, int kb, int buf) {
+#pragma unroll
+    for (int i = 0; i < A_LD; ++i) {
+      const int seg = wid * A_LD + i, r = seg * 8 + a_row;
+      dma16(f.Ag + (size_t)kb * BK + (size_t)r * K + (((lane & 7) ^ ((r >> 1) & 7)) * 16),
+            __builtin_amdgcn_readfirstlane(lds_offset(&sA[buf][seg * 64])));
+    }
+#pragma unroll
+    for (int i = 0; i < B_LD; ++i) {
+      const int seg = wid * B_LD + i, r = seg * 16 + b_row;
+      dma16(f.Bt + (size_t)kb * 1024 + mx_block_index(r, ((lane & 3) ^ bsw_of(r)) * 16, KB),
+            __builtin_amdgcn_readfirstlane(lds_offset(&sB[buf][seg * 64])));
+    }
+    if (wid == 0)
+      dma16(f.Asg + (size_t)kb * as_step + lane * 16,
+            __builtin_amdgcn_readfirstlane(lds_offset(&sAs[buf][0])));
+    if (wid == 1)
+      dma16(f.Bsg + (size_t)kb * 1024 + lane * 16,
+            __builtin_amdgcn_readfirstlane(lds_offset(&sBs[buf][0])));
+  };
+  // GEMM2: the coefficients and output rows of the tile's BM rows, one 1 KB
+  // load each by waves 2 and 3 (the rows of a tile lie inside the layout's
+  // padded rows)
+  auto stage_coef = [&](const MxTile &f, int db) {
+    if constexpr (!SWIGLU) {
+      if (wid == 2)
+        dma16_s(g.wrow + f.t.row0, lane * 16, __builtin_amdgcn_readfirstlane(lds_offset(&sW[0])));
+      if (g.ydst) {
+        if (wid == 3)
+          dma16_s(g.ydst + f.t.row0, lane * 16,
+                  __builtin_amdgcn_readfirstlane(lds_offset(&sD[db][0])));
+      } else if (tid < BM) {
+        sD[db][tid] = -1;
+      }
+    }
+  };
+
+  MxTile cur = tile_at(mt, nt);
+  stage(cur, 0, 0);
+  int db = 0;
+  stage_coef(cur, db);
+  // the direct loads are invisible to the compiler: __syncthreads() alone
+  // would not wait for them
+  wait_vmcnt<0>();
+  __syncthreads();
+
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int asw = (r16 >> 1) & 7;  // A swizzle of every row this lane reads
+  const int bsw = bsw_of(r16);     // B swizzle of every row this lane reads
+  // stores each wave issues at least in a GEMM1 epilogue: BM x 128 code
+  // bytes in 16-byte pieces by 512 threads (4), and one scale word
+  constexpr int S_EPI = 4;
+  for (int it = 0;; ++it) {
+    f32x4 acc[8][4];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{};
+    for (int kb = 0; kb < nkb; ++kb) {
+      // this wave's loads of step kb are its only ones outstanding (a
+      // tile's first stage was waited for before its K loop)
+      if (kb > 0) wait_vmcnt<0>();
+      // every wave's loads of step kb landed; step kb-1 fully consumed
+      __builtin_amdgcn_s_barrier();
+      if (kb + 1 < nkb) stage(cur, kb + 1, (kb + 1) & 1);
+      const int buf = kb & 1;
+      const uint32_t sb = ((const uint32_t *)&sBs[buf][0])[(wn * 4 + grp) * 16 + r16];
+      const uint2 sa = ((const uint2 *)&sAs[buf][0])[wm * 64 + grp * 16 + r16];
+      i32x8 b[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int row = wn * 64 + j * 16 + r16;
+        const u32x4 v = sB[buf][row * 4 + (grp ^ bsw)];
+        b[j] = __builtin_bit_cast(i32x8, __builtin_shufflevector(v, v, 0, 1, 2, 3, -1, -1, -1, -1));
+      }
+      auto read_a = [&](int i) {
+        const int row = wm * 128 + i * 16 + r16;
+        const u32x4 lo = sA[buf][row * 8 + (grp ^ asw)];
+        const u32x4 hi = sA[buf][row * 8 + ((grp + 4) ^ asw)];
+        return __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      };
+      i32x8 a_next = read_a(0);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const i32x8 a = a_next;
+        if (i + 1 < 8) a_next = read_a(i + 1);
+        __builtin_amdgcn_sched_barrier(0);
+        const int sai = (int)(i < 4 ? sa.x : sa.y);
+        acc[i][0] = mx_mfma<0>(b[0], a, acc[i][0], i & 3, sai, (int)sb);
+        acc[i][1] = mx_mfma<1>(b[1], a, acc[i][1], i & 3, sai, (int)sb);
+        acc[i][2] = mx_mfma<2>(b[2], a, acc[i][2], i & 3, sai, (int)sb);
+        acc[i][3] = mx_mfma<3>(b[3], a, acc[i][3], i & 3, sai, (int)sb);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    // GEMM2: outputs scaled by the coefficients and packed to bf16 before
+    // the next tile's coefficients overwrite them
+    uint32_t yb[SWIGLU ? 1 : 8][4][2];
+    if constexpr (!SWIGLU) {
+      float wr[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) wr[i] = sW[wm * 128 + i * 16 + r16];
+      pack_y_bf16(acc, wr, yb);
+    }
+    int mt2, nt2;
+    const bool more = work_item_xg<kGroupXcd>(it + 1, n_live, ntn, &mt2, &nt2);
+    MxTile nxt;
+    if (more) {
+      // every wave's reads of the last step (and of sW) completed: buffer
+      // 0 and sW may be refilled
+      wait_lgkm0();
+      __builtin_amdgcn_s_barrier();
+      nxt = tile_at(mt2, nt2);
+      stage(nxt, 0, 0);
+      stage_coef(nxt, db ^ 1);
+    }
+    static_assert(sizeof(sA[1]) >= BM * 128 && sizeof(sA[1]) >= 64 * 512 &&
+                      sizeof(sY) >= (SWIGLU ? 16 : 64 * 512),
+                  "staging fits buffer 1 and sY");
+    int n_st = S_EPI;
+    if constexpr (SWIGLU)
+      store_h_mx_staged<NW, true>(acc, g, cur.t, cur.nt, wm, wn, lane, tid, &sA[1][0]);
+    else
+      n_st = store_y_bf16_staged<NW, true>(yb, g, cur.t, cur.nt, wm, wn, lane, tid, &sA[1][0],
+                                           &sY[0], &sD[db][0]);
+    if (!more) return;
+    // the next tile's first stage (and coefficients) landed once at most the
+    // epilogue's stores are outstanding; this wave's staging reads are done
+    // before the next barrier lets stage 1 refill buffer 1
+    if constexpr (SWIGLU)
+      wait_vmcnt<S_EPI>();
+    else
+      wait_vmcnt_upto<0, 63>(n_st);
+    wait_lgkm0();
+    cur = nxt;
+    db ^= 1;
   }
 }
 
@@ -208,7 +392,8 @@ hipError_t launch_mx(const GemmArgs &g, int grid_tiles, int align, hipStream_t s
   if (align == kFp8TileM)
     hipLaunchKernelGGL((k_gemm_mx<4, 2, SWIGLU, 2>), dim3(grid), dim3(256), 0, s, g);
   else if (align == kFp8LargeTileM)
-    hipLaunchKernelGGL((k_gemm_mx<8, 2, SWIGLU>), dim3(grid), dim3(512), 0, s, g);
+    hipLaunchKernelGGL((k_gemm_mx_persist<SWIGLU>), dim3(std::min(grid, persistent_grid())),
+                       dim3(512), 0, s, g);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
