@@ -7,6 +7,8 @@ quantisations); outputs are held to the e4m3 relative-RMS bound.
 * full-size workload on sampled tokens, hottest and coldest experts included
 * 128-row and 256-row M tiles give the same bits; a fetched expert equals a
   resident one; a zero-gate expert gives exact zeros
+* the persistent 256-row tiles over more tiles than workgroups, with an odd
+  number of GEMM2 K steps, on every row and bitwise equal to 128-row tiles
 """
 import numpy as np
 import pytest
@@ -116,3 +118,31 @@ def test_mxfp4_zero_gate_codes_give_exact_zero():
     run.close()
     assert wl.n_pairs > 0
     assert not got.any()
+
+
+def test_mxfp4_persistent_tiles_odd_k_steps_all_rows():
+    # The persistent 8-wave MXFP4 tiles over more tiles than workgroups (each
+    # workgroup runs several, loading the next one's first stage and GEMM2
+    # coefficients during the epilogue) with an odd number of GEMM2 K steps
+    # (I = 640: five), so that a tile's last step uses ring buffer 0, the
+    # buffer the next tile's first stage fills: every row against the oracle,
+    # and bitwise equal to per-chunk batches on the 4-wave 128-row tile.
+    wl = W.generate(NAME, 12, d=1024, I=640, E=4, Eg=16, R=4, T=4096, cpr=64)
+    E, k = wl.cfg["E"], wl.cfg["k"]
+    run = harness.Runner(wl, n_streams=1, record_routing=True, use_fetch=False)
+    run.run(policy=cep.CEP_WAIT_ALL)
+    a = _out(run)
+    m = cep.cep_get_batch_routing(run.ctx, 0, E, k)
+    assert m["align"] == 256
+    m_tiles = int(sum((c + 255) // 256 for c in m["cnt"]))
+    assert m_tiles * (wl.cfg["d"] // 256) > 256, m["cnt"]  # GEMM2 tiles > workgroups
+    mx, rel = U.check(wl, a)
+    run.out.zero_()
+    run.run(policy=cep.CEP_PER_CHUNK)
+    b = _out(run)
+    aligns = {cep.cep_get_batch_routing(run.ctx, i, E, k)["align"]
+              for i in range(cep.cep_get_batch_count(run.ctx))}
+    run.close()
+    assert aligns == {128}
+    assert np.array_equal(a, b)
+    print(f"mxfp4 persistent tiles, odd K steps: pairs={wl.n_pairs} max_abs={mx:.3e} rel={rel:.3e}")
