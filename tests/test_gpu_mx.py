@@ -8,7 +8,9 @@ quantisations); outputs are held to the e4m3 relative-RMS bound.
 * 128-row and 256-row M tiles give the same bits; a fetched expert equals a
   resident one; a zero-gate expert gives exact zeros
 * the persistent 256-row tiles over more tiles than workgroups, with an odd
-  number of GEMM2 K steps, on every row and bitwise equal to 128-row tiles
+  number of GEMM2 K steps, on every row and bitwise equal to 128-row tiles;
+  with fetched experts (their own persistent launches) bitwise equal to the
+  all-resident layer
 """
 import numpy as np
 import pytest
@@ -146,3 +148,25 @@ def test_mxfp4_persistent_tiles_odd_k_steps_all_rows():
     assert aligns == {128}
     assert np.array_equal(a, b)
     print(f"mxfp4 persistent tiles, odd K steps: pairs={wl.n_pairs} max_abs={mx:.3e} rel={rel:.3e}")
+
+
+def test_mxfp4_persistent_tiles_fetched_equal_resident_bitwise():
+    # 256-row batches with fetched experts: the resident and the fetched
+    # experts' tiles run as two persistent launches per GEMM (the fetched
+    # ones behind the copy); bitwise equal to every expert resident.
+    wl = W.generate(NAME, 13, d=1024, I=640, E=8, Eg=32, R=4, T=4096, cpr=64, fetch_frac=0.25)
+    assert wl.fetched
+    E, k = wl.cfg["E"], wl.cfg["k"]
+    a = harness.Runner(wl, n_streams=1, record_routing=True, use_fetch=True)
+    a.run(policy=cep.CEP_WAIT_ALL)
+    ga = _out(a)
+    assert cep.cep_get_batch_routing(a.ctx, 0, E, k)["align"] == 256
+    assert all(b["fetched"] for b in a.stats()["batches"])
+    a.close()
+    b = harness.Runner(wl, n_streams=1, use_fetch=False)
+    b.run(policy=cep.CEP_WAIT_ALL)
+    gb = _out(b)
+    b.close()
+    assert np.array_equal(ga, gb)
+    mx, rel = U.check(wl, gb)
+    print(f"mxfp4 persistent tiles with fetched experts: pairs={wl.n_pairs} rel={rel:.3e}")
