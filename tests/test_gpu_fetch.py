@@ -124,3 +124,28 @@ def test_fetch_buffer_reused_across_layers():
         run.run(policy=cep.CEP_THRESHOLD, theta=200 + 300 * i, n_streams=1 + i % 3)
         assert np.array_equal(_out(run), ref), i
     run.close()
+
+
+@pytest.mark.parametrize("name", ["fp8_fetch_d6144", "mxfp4_dsv4flash_d4096",
+                                  "zipf_stream_d7168"])
+def test_every_expert_fetched_large_tiles(name):
+    # Every local expert fetched, batches of 256-row tiles: the resident
+    # experts' launches have no tile (the persistent workgroups leave at
+    # once) and the fetched experts' launches do all the work.  Every row
+    # against the oracle, and bitwise equal to the all-resident layer.
+    wl = W.generate(name, 31, d=512, I=256, E=4, Eg=8, k=4, R=2, T=4096, cpr=1, fetch_frac=1.0)
+    assert len(wl.fetched) == wl.cfg["E"]
+    E, k = wl.cfg["E"], wl.cfg["k"]
+    print(f"case {name} pairs={wl.n_pairs}", flush=True)
+    a = harness.Runner(wl, n_streams=1, record_routing=True, use_fetch=True)
+    a.run(policy=cep.CEP_WAIT_ALL)
+    ga = _out(a)
+    assert cep.cep_get_batch_routing(a.ctx, 0, E, k)["align"] == 256
+    assert all(b["fetched"] for b in a.stats()["batches"])
+    a.close()
+    b = harness.Runner(wl, n_streams=1, use_fetch=False)
+    b.run(policy=cep.CEP_WAIT_ALL)
+    gb = _out(b)
+    b.close()
+    assert np.array_equal(ga, gb)
+    U.check(wl, ga)
