@@ -45,6 +45,14 @@ CASES = [
                                        fetch_frac=0.2), "threshold", 0.3, 2),
     ("mxfp4_dsv4flash_d4096", 29, dict(d=512, I=256, E=4, Eg=8, k=4, R=2, T=4096, cpr=2),
      "per_chunk", 0, 2),
+    # top-1: every token has one pair (the e4m3 and MXFP4 GEMM2 write every
+    # output row themselves)
+    ("sync_d4096", 41, dict(d=512, I=256, E=4, Eg=8, k=1, R=2, T=8192, cpr=2), "threshold",
+     0.5, 2),
+    ("fp8_fetch_d6144", 41, dict(d=512, I=256, E=4, Eg=8, k=1, R=2, T=8192, cpr=2),
+     "threshold", 0.5, 2),
+    ("mxfp4_dsv4flash_d4096", 41, dict(d=512, I=256, E=4, Eg=8, k=1, R=2, T=8192, cpr=2),
+     "threshold", 0.5, 2),
 ]
 
 
