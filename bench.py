@@ -62,7 +62,7 @@ GEMM_SOURCES = {
     "mxfp4": ["paper_2609_33252_amd/csrc/gemm_mx.hip", "paper_2609_33252_amd/csrc/gemm_common.h"],
 }
 TRAFFIC_BYTES = {  # workload -> (GEMM family, sha1 prefix of its sources, bytes per launch)
-    "fp8_fetch_d6144": ("fp8", "406c1e479798", 1833503223),
+    "fp8_fetch_d6144": ("fp8", "41923e0288b7", 1833528987),
     "sync_d4096": ("bf16", "c12c043df95d", 504261285),
     "zipf_imbalanced_d7168/per_chunk": ("bf16", "c12c043df95d", 507424984),
     "mxfp4_dsv4flash_d4096": ("mxfp4", "a63161e27ae7", 1375766455),

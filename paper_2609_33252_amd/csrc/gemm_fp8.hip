@@ -82,7 +82,8 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
   constexpr int A_LD = BM * BK / 1024 / NW, B_LD = BN * BK / 1024 / NW;  // loads per wave
   constexpr int PER = A_LD + B_LD;  // per thread per step; wave 0 adds one (row scales)
   static_assert(BM * 4 <= 1024, "one load of the row scales");
-  static_assert(!PERSIST || (NW == 8 && STAGES == 2), "persistent: the 8-wave two-stage tile");
+  static_assert(PERSIST == (NW == 8) && (!PERSIST || STAGES == 2),
+                "the 8-wave tiles are the persistent two-stage ones");
   // uniform over the workgroup: kept in scalar registers
   const int n_live = __builtin_amdgcn_readfirstlane(*g.n_tiles), ntn = g.N / BN;
   int mt, nt;
@@ -250,8 +251,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
     if constexpr (!PERSIST) {
       // staging: BM x 128 code bytes; y rows of 512 bytes, 64 per 32 KB piece
       static_assert(sizeof(sA) >= BM * 128, "the h tile fits the A ring");
-      static_assert(sizeof(sB[0]) >= 64 * 512 && (NW == 4 || sizeof(sA[0]) >= 64 * 512),
-                    "y rows fit the ring");
+      static_assert(sizeof(sB[0]) >= 64 * 512, "y rows fit the ring");
       if constexpr (!SWIGLU) {
         // read after the epilogue's first barrier
         if (tid < BM) sD[0][tid] = ydv;
@@ -261,12 +261,8 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
       } else {
         uint32_t yb[8][4][2];
         pack_y_bf16(acc, wr, yb);
-        if constexpr (NW == 8)
-          store_y_bf16_staged<NW>(yb, g, cur.t, cur.nt, wm, wn, lane, tid, &sA[0][0], &sA[1][0],
-                                  &sD[0][0]);
-        else
-          store_y_bf16_staged<NW>(yb, g, cur.t, cur.nt, wm, wn, lane, tid, &sB[0][0], &sB[1][0],
-                                  &sD[0][0]);
+        store_y_bf16_staged<NW>(yb, g, cur.t, cur.nt, wm, wn, lane, tid, &sB[0][0], &sB[1][0],
+                                &sD[0][0]);
       }
       return;
     } else {
@@ -327,20 +323,15 @@ __global__ __launch_bounds__(64 * NW, OCC) void k_gemm_fp8(GemmArgs g) {
 
 }  // namespace
 
-// persistent 8-wave tiles for GEMM2 ([0]) and GEMM1 ([1])
-constexpr bool kFp8Persist[2] = {true, true};
-
 template <bool SWIGLU>
 hipError_t launch_fp8(const GemmArgs &g, int grid_tiles, int align, hipStream_t s) {
   if (g.N % 256 || g.K % 128 || g.K > kMaxDim || g.s_ld % 256) return hipErrorInvalidValue;
   const int grid = balanced_grid(grid_tiles, kGroupM, g.N / 256);
   if (align == kFp8TileM)
     hipLaunchKernelGGL((k_gemm_fp8<4, 3, SWIGLU, false>), dim3(grid), dim3(256), 0, s, g);
-  else if (align == kFp8LargeTileM && kFp8Persist[SWIGLU])
+  else if (align == kFp8LargeTileM)
     hipLaunchKernelGGL((k_gemm_fp8<8, 2, SWIGLU, true>), dim3(std::min(grid, persistent_grid())),
                        dim3(512), 0, s, g);
-  else if (align == kFp8LargeTileM)
-    hipLaunchKernelGGL((k_gemm_fp8<8, 2, SWIGLU, false>), dim3(grid), dim3(512), 0, s, g);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
